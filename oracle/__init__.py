@@ -1,0 +1,15 @@
+"""fp64 CPU oracle of the batched row softmax and checks of its slice schedules.
+
+TEST INFRASTRUCTURE ONLY. Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline
+leg may import this package. It shares no code with the HIP library
+(paper_2002_07062_amd), and neither imports the other; inputs for both come from the
+stand-alone seeded generators in workloads.py.
+
+Pins (what checks the oracle against something other than itself) live in
+tests/test_oracle.py and tests/test_plan_checks.py; every function here has at least one.
+"""
+
+from . import plan_checks
+from .softmax import DTYPE_CODE, build, softmax, softmax_rows
+
+__all__ = ["DTYPE_CODE", "build", "plan_checks", "softmax", "softmax_rows"]
