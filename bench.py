@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Batched row-softmax bench on one MI355X.
+
+A step is one pass of the whole hot path (plan lookup is built once, then every step launches
+the persistent softmax kernel over the full batch: row loads, max, exp and sum, normalise,
+store) over one batch of seeded synthetic input already resident in HBM. The headline workload
+is BERT's attention-score shape: 384 slices of 512 x 512 fp32 packed as 196608 x 512.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2] [--schedule xcd]
+
+Prints ONE JSON line. `value` is achieved HBM GB/s with algorithmic bytes (every element read
+once and written once) over the timed region; `roofline` reports the kernel's average launch
+duration (HIP events on the launch stream) against the 8 TB/s HBM peak; `cpu_baseline` is the
+fp64 oracle timed on this host's cores on the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "batched-softmax HBM GB/s (% of MI355X peak) at 384×512×512 fp32"
+PEAK_HBM_GBS = 8000.0   # MI355X published HBM3E bandwidth
+MALL_BYTES = 256 << 20  # last-level Infinity Cache; rotation keeps reuse distance above it
+
+
+def _to_device(w):
+    import numpy as np
+    import torch
+
+    if w.dtype == "f32":
+        return torch.from_numpy(w.x).cuda()
+    return torch.from_numpy(w.x.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _rotation(footprint: int) -> int:
+    """Buffer pairs to rotate so the data a step touches was last used > 1 GB of traffic ago."""
+    return max(2, math.ceil((4 * MALL_BYTES) / max(footprint, 1)) + 1)
+
+
+def time_plan(plan, xs, outs, steps, warmup):
+    """Returns (whole-region ms, list of per-launch ms) for `steps` launches after `warmup`."""
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    n = len(xs)
+    for i in range(warmup):
+        bsm.bsm_plan_execute(plan, xs[i % n], outs[i % n])
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(steps):
+        ev[i][0].record(stream)
+        bsm.bsm_plan_execute(plan, xs[i % n], outs[i % n])
+        ev[i][1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1), [a.elapsed_time(b) for a, b in ev]
+
+
+def time_copy(xs, outs, nbytes, steps, warmup):
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    n = len(xs)
+    for i in range(warmup):
+        bsm.bsm_copy(xs[i % n], outs[i % n], nbytes)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        bsm.bsm_copy(xs[i % n], outs[i % n], nbytes)
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def run_workload(name, schedule, steps, warmup, rotate=None, w=None):
+    """Bench one (workload, schedule). Returns a dict of measurements."""
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    w = w or workloads.generate(name)
+    nbytes = w.algorithmic_bytes
+    n_pairs = rotate or _rotation(nbytes)
+    x0 = _to_device(w)
+    xs = [x0] + [x0.clone() for _ in range(n_pairs - 1)]
+    outs = [torch.empty_like(x0) for _ in range(n_pairs)]
+    t_plan = time.perf_counter()
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule=schedule, device=0)
+    plan_ms = (time.perf_counter() - t_plan) * 1e3
+    st = bsm.bsm_plan_describe(plan)
+    region_ms, launch_ms = time_plan(plan, xs, outs, steps, warmup)
+    plan.destroy()
+    ms_step = region_ms / steps
+    avg_launch = statistics.fmean(launch_ms)
+    res = dict(
+        workload=w.name, schedule=schedule, batch=w.batch, dtype=w.dtype,
+        algorithmic_bytes=nbytes, ms_per_step=ms_step, gbs=nbytes / (ms_step * 1e-3) / 1e9,
+        launch_ms_avg=avg_launch, launch_ms_median=statistics.median(launch_ms),
+        launch_ms_p10=sorted(launch_ms)[max(0, len(launch_ms) // 10 - 1)],
+        launch_ms_p90=sorted(launch_ms)[min(len(launch_ms) - 1, (9 * len(launch_ms)) // 10)],
+        launch_gbs=nbytes / (avg_launch * 1e-3) / 1e9,
+        slices_per_s=w.batch / (ms_step * 1e-3), plan_build_ms=plan_ms,
+        n_wg=st["n_wg"], wg_threads=st["wg_threads"], n_items=st["n_items"],
+        kernel_class=st["kernel_class"], max_over_mean_wg_cost=st["max_wg_cost"] / max(st["mean_wg_cost"], 1e-9),
+        moved_bytes=st["moved_bytes"], buffers_rotated=n_pairs)
+    del xs, outs, x0
+    torch.cuda.empty_cache()
+    return res, w
+
+
+def cpu_baseline(w):
+    import oracle
+
+    threads = min(16, len(os.sched_getaffinity(0)))
+    t0 = time.perf_counter()
+    oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(w.algorithmic_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"all {w.batch} slices of {w.name} once (fp64 reference, {threads} threads, "
+                      "bytes counted as the fp32 read-once + write-once of the GPU path)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--schedule", default="xcd", choices=["rr", "balanced", "xcd"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="headline line only")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not "
+              "supported: the batched softmax needs no exchange between GPUs and this build "
+              "runs on a single MI355X", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    bsm.load()
+    info = bsm.bsm_device_info(0)
+
+    head, w = run_workload(args.workload, args.schedule, args.steps, args.warmup)
+
+    # Copy ceiling on the same bytes (read n/2, write n/2), same rotation.
+    import numpy as np  # noqa: F401
+
+    x0 = _to_device(w)
+    n_pairs = head["buffers_rotated"]
+    xs = [x0] + [x0.clone() for _ in range(n_pairs - 1)]
+    outs = [torch.empty_like(x0) for _ in range(n_pairs)]
+    half = w.algorithmic_bytes // 2
+    copy_ms = time_copy(xs, outs, half, args.steps, args.warmup)
+    del xs, outs, x0
+    torch.cuda.empty_cache()
+    copy_gbs = w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9
+
+    extra = {}
+    if not args.no_extra:
+        for sch in ("rr", "balanced", "xcd"):
+            if sch == args.schedule:
+                continue
+            r, _ = run_workload(args.workload, sch, args.steps, args.warmup, w=w)
+            extra[f"{args.workload}_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_wg_cost")}
+        w5 = None
+        for sch in ("rr", "balanced", "xcd"):
+            r, w5 = run_workload("c5", sch, args.steps, args.warmup, w=w5)
+            extra[f"c5_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_wg_cost", "moved_bytes")}
+        del w5
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
+    achieved = head["launch_gbs"]
+    line = {
+        "metric": METRIC,
+        "value": round(head["gbs"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": head["workload"], "batch": head["batch"],
+                   "rows": int(w.rows[0]) if w.uniform else "ragged",
+                   "cols": int(w.cols[0]) if w.uniform else "ragged",
+                   "schedule": args.schedule, "n_wg": head["n_wg"],
+                   "wg_threads": head["wg_threads"], "buffers_rotated": head["buffers_rotated"]},
+        "pct_of_peak": round(100.0 * head["gbs"] / PEAK_HBM_GBS, 2),
+        "slices_per_s": round(head["slices_per_s"], 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "bsm_softmax_kernel", "launch_us_avg": round(head["launch_ms_avg"] * 1e3, 2),
+                     "launch_us_median": round(head["launch_ms_median"] * 1e3, 2),
+                     "launch_us_p10": round(head["launch_ms_p10"] * 1e3, 2),
+                     "launch_us_p90": round(head["launch_ms_p90"] * 1e3, 2),
+                     "bytes_per_launch": head["algorithmic_bytes"]},
+        "copy_ceiling": {"gbs": round(copy_gbs, 2), "us": round(copy_ms * 1e3, 2),
+                         "softmax_pct_of_copy": round(100.0 * head["gbs"] / copy_gbs, 2)},
+        "cpu_baseline": cpu,
+        "device": {"arch": info["arch"], "n_cu": info["n_cu"], "n_xcd": info["n_xcd"]},
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

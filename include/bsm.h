@@ -1,0 +1,212 @@
+/*
+ * bsm.h -- batched row softmax over packed 2-D slices, with slice-to-workgroup scheduling,
+ *          for AMD Instinct MI355X (gfx950).  Plain C ABI of libbsm.so.
+ *
+ * The operation (the paper's problem statement, Section 2): B small slices, slice s being an
+ * R_s x C_s row-major matrix, are packed into one buffer (for BERT, 384 attention-score slices
+ * of 512 x 512 stacked along rows as a 196608 x 512 tensor).  Softmax runs on every row of
+ * every slice:
+ *
+ *     y[s][r][j] = exp(x[s][r][j] - m) / sum_k exp(x[s][r][k] - m),   m = max_k x[s][r][k]
+ *
+ * and the library decides which persistent workgroup processes which rows (Sections 3 to 5 of
+ * the paper: round-robin batch-to-core scheduling as the prior solution; cluster beamforming
+ * plus load balancing, with a MINIMAX objective, as the proposed one).  On MI355X a
+ * "cluster/core" is a persistent workgroup and a "memory bank" is an XCD with its own L2.
+ *
+ * Common conventions
+ *   - Ownership: the caller owns every input, output and metadata buffer; the library owns
+ *     plans, the plan cache and the device copies of work tables.
+ *   - Pointers: `in` / `out` / `trace` are DEVICE pointers on the plan's device; every other
+ *     pointer is HOST memory, read (or written) before the call returns.
+ *   - Asynchrony: compute calls enqueue on `stream` (a hipStream_t passed as void*, NULL = the
+ *     null stream) and return without synchronising.
+ *   - Aliasing: in == out (in place) is allowed; any other overlap of the two extents is
+ *     rejected with BSM_ERR_ALIAS.
+ *   - Errors: every call returns a bsm_status; nothing is thrown, printed or aborted.  After a
+ *     failure bsm_last_error() gives a thread-local description.  A failed call leaves its
+ *     outputs untouched (no kernel is launched).
+ *   - Element values: fp32, or bf16 (stored as raw 16-bit patterns); input and output share
+ *     the type; arithmetic is fp32.  A row of all -inf (fully masked) yields zeros; a NaN or
+ *     +inf entry makes its whole row NaN.
+ */
+#ifndef BSM_H
+#define BSM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BSM_ABI_VERSION 1
+#define BSM_MAX_XCD 16
+
+typedef enum bsm_status {
+    BSM_OK = 0,
+    BSM_ERR_INVALID_ARG = 1, /* bad pointer, size, enum, geometry or overlapping slices */
+    BSM_ERR_UNSUPPORTED = 2, /* valid request this build cannot serve (e.g. host-only plan) */
+    BSM_ERR_ALIAS = 3,       /* in and out overlap without being equal */
+    BSM_ERR_OOM = 4,         /* host or device allocation failed */
+    BSM_ERR_HIP = 5          /* a HIP runtime call failed; bsm_last_error() has its string */
+} bsm_status;
+
+typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1 } bsm_dtype;
+
+/* Which workgroup processes which rows.
+ *   RR        Section 3's prior solution: whole slice s goes to workgroup (s mod n_wg).
+ *   BALANCED  Section 4.2 at core granularity: the rows of all slices, in slice order, are cut
+ *             into n_wg contiguous ranges of equal planner cost (within one row's cost of the
+ *             MINIMAX optimum for this cost model).
+ *   XCD       Sections 4.1 + 4.2: each slice gets a home XCD (the virtual bank holding the
+ *             largest share of its elements, ties to the lowest index, or the caller's
+ *             home_xcd[]); the load balancer moves the fewest rows it must from XCDs above
+ *             their share to XCDs below it; each XCD's rows are then cut into equal-cost
+ *             ranges over that XCD's workgroups (workgroup w runs on XCD w mod n_xcd). */
+typedef enum bsm_schedule {
+    BSM_SCHED_RR = 0,
+    BSM_SCHED_BALANCED = 1,
+    BSM_SCHED_XCD = 2
+} bsm_schedule;
+
+/* Launch geometry and cost model used by the planner.  Zero-filled fields take defaults. */
+typedef struct bsm_topology {
+    int32_t n_cu;       /* compute units (MI355X: 256) */
+    int32_t n_xcd;      /* XCDs (MI355X: 8); workgroup w is taken to run on XCD w mod n_xcd */
+    int32_t wg_per_cu;  /* persistent workgroups per CU; the grid has n_cu * wg_per_cu */
+    int32_t wg_threads; /* threads per workgroup, a multiple of 64 in [64, 1024] */
+    float item_cost;    /* planner cost of one work item, in byte equivalents (<= 0: default) */
+    float row_cost;     /* planner cost of one row on top of its bytes (<= 0: default) */
+} bsm_topology;
+
+/* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): a
+ * contiguous range of rows of one slice. */
+typedef struct bsm_item {
+    int64_t elem_offset; /* element offset of the item's first row in in/out */
+    int32_t cols;        /* row length C_s, which is also the row stride */
+    int32_t nrows;       /* rows in the item */
+    int32_t slice;       /* slice index s */
+    int32_t row_begin;   /* index of the item's first row within slice s */
+} bsm_item;
+
+typedef struct bsm_plan_stats {
+    int64_t batch;             /* slices */
+    int64_t n_items;           /* entries of the work table */
+    int64_t total_rows;        /* rows over all slices */
+    int64_t algorithmic_bytes; /* every element read once plus written once */
+    int64_t extent_elems;      /* elements from 0 to the end of the furthest slice */
+    int64_t moved_bytes;       /* XCD: algorithmic bytes of rows run off their home XCD */
+    int64_t trace_bytes;       /* size a trace buffer passed to bsm_plan_execute must have */
+    int32_t n_wg;              /* persistent workgroups in the grid */
+    int32_t n_xcd;
+    int32_t wg_threads;
+    int32_t schedule;          /* bsm_schedule */
+    int32_t dtype;             /* bsm_dtype */
+    int32_t n_overlap;         /* XCD: slices straddling two or more virtual banks */
+    int32_t max_cols;          /* longest row */
+    int32_t kernel_class;      /* which kernel instance the plan launches (internal) */
+    double max_wg_cost;        /* planner cost of the most loaded workgroup */
+    double mean_wg_cost;       /* total planner cost / n_wg */
+    double max_row_cost;       /* planner cost of the most expensive single row */
+    double moved_cost;         /* XCD: planner cost of the rows run off their home XCD */
+    double min_moved_cost;     /* XCD: sum over XCDs of (home load - fair share)+, the least
+                                  any rebalancing must move */
+    double build_us;           /* host time spent building the table */
+    int64_t xcd_bytes[BSM_MAX_XCD];  /* algorithmic bytes run by each XCD's workgroups */
+    int64_t bank_touch[BSM_MAX_XCD]; /* XCD: N_x, slices with elements in bank x */
+    int64_t bank_home[BSM_MAX_XCD];  /* XCD: L_x, slices homed on bank x */
+} bsm_plan_stats;
+
+/* One record per wave when a trace buffer is passed to bsm_plan_execute (32 bytes). */
+typedef struct bsm_trace_rec {
+    uint32_t wg;      /* workgroup index in the grid */
+    uint32_t xcc_id;  /* XCD the wave ran on, from the hardware XCC_ID register */
+    uint32_t hw_id;   /* raw hardware HW_ID register (wave, SIMD, CU, shader engine) */
+    uint32_t rows;    /* rows this wave processed */
+    uint64_t t_start; /* constant-rate (100 MHz) real-time counter when the wave started */
+    uint64_t t_end;   /* ... when it finished its last row */
+} bsm_trace_rec;
+
+typedef struct bsm_device_props {
+    int32_t n_cu;
+    int32_t n_xcd;
+    int32_t wave_size;
+    int32_t max_threads_per_cu;
+    int64_t lds_bytes_per_cu;
+    int64_t l2_bytes;          /* as reported by the runtime */
+    int64_t hbm_bytes;
+    int64_t wall_clock_hz;     /* rate of the counter in bsm_trace_rec */
+    double peak_hbm_gbs;       /* from memory clock and bus width, as reported */
+    int32_t clock_khz;
+    char arch[64];             /* e.g. "gfx950:sramecc+:xnack-" */
+} bsm_device_props;
+
+typedef struct bsm_plan_s* bsm_plan;
+
+/* One-shot batched row softmax.
+ *   in, out        device buffers of `dtype` elements
+ *   slice_offsets  NULL for uniform slices: then rows[0] = R and cols[0] = C for every slice
+ *                  and slice s starts at element s*R*C.  Otherwise [batch] element offsets:
+ *                  slice s occupies elements [slice_offsets[s], slice_offsets[s] + R_s*C_s).
+ *                  Slices may sit in any order with gaps between them, but must not overlap;
+ *                  gaps are never read or written.
+ *   rows, cols     [batch] (or [1] when uniform), each >= 0; an empty slice is skipped
+ *   schedule       see bsm_schedule
+ *   stream         hipStream_t as void*
+ * Plans are built on first use of a geometry (host work plus a synchronous table upload) and
+ * cached per device; later calls with the same geometry only launch the kernel.
+ * batch == 0, or only empty slices, returns BSM_OK without touching the GPU. */
+bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets,
+                       const int32_t* rows, const int32_t* cols, int64_t batch,
+                       bsm_dtype dtype, bsm_schedule schedule, void* stream);
+
+/* Build a reusable plan: the work table of the HW batch scheduler of Section 5, built once
+ * up front and reused for every execution.
+ *   home_xcd   optional [batch] home XCD per slice in [0, n_xcd) for the XCD schedule (the
+ *              bank each slice was created on); NULL = virtual banks, i.e. n_xcd equal
+ *              contiguous element ranges over the span of the slices.  Ignored by RR and
+ *              BALANCED.
+ *   topology   NULL = the device's defaults (bsm_default_topology).
+ *   device     HIP device ordinal; -1 builds a host-only plan (topology required) that can
+ *              be described and exported but not executed; it touches no GPU. */
+bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets,
+                           const int32_t* rows, const int32_t* cols, int64_t batch,
+                           bsm_dtype dtype, bsm_schedule schedule, const int8_t* home_xcd,
+                           const bsm_topology* topology, int device);
+
+/* Run a plan: out = row softmax of in, on `stream`.  `trace` is NULL or a device buffer of
+ * stats.trace_bytes bytes that receives one bsm_trace_rec per wave. */
+bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace);
+
+bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats);
+
+/* Copy the host work table out: wg_ptr [n_wg + 1] (CSR row pointer), items [n_items], and,
+ * when non-NULL, home [batch] (home XCD per slice after overlap resolution, -1 where the
+ * schedule has none) and overlap [batch] (1 if the slice spans two or more virtual banks). */
+bsm_status bsm_plan_export(bsm_plan plan, int32_t* wg_ptr, bsm_item* items, int8_t* home,
+                           uint8_t* overlap);
+
+/* Free a plan.  Waits for the plan's last enqueued execution to finish first. */
+bsm_status bsm_plan_destroy(bsm_plan plan);
+
+bsm_status bsm_device_info(int device, bsm_device_props* info);
+
+/* The topology bsm_plan_create uses for `device` when none is given. */
+bsm_status bsm_default_topology(int device, bsm_topology* topology);
+
+/* Plain device-to-device copy kernel of `bytes` bytes (128-bit accesses where aligned), the
+ * streaming reference the softmax bandwidth is compared with.  src and dst must not overlap. */
+bsm_status bsm_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
+/* Drop every cached one-shot plan (waits for their last use). */
+bsm_status bsm_cache_clear(void);
+
+const char* bsm_status_string(bsm_status status);
+const char* bsm_last_error(void);
+int32_t bsm_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BSM_H */

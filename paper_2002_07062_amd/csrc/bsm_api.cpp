@@ -1,0 +1,445 @@
+// C-ABI of libbsm.so: argument checks, plans (host table + device copy), the one-shot plan
+// cache, device queries and the copy reference.  Every failure is a status code plus a
+// thread-local message; nothing is thrown across the ABI.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <list>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "bsm.h"
+#include "bsm_launch.hpp"
+#include "bsm_plan.hpp"
+
+struct bsm_plan_s {
+    int device = -1;  // -1: host-only plan
+    bsm_dtype dtype = BSM_F32;
+    bsm_schedule schedule = BSM_SCHED_RR;
+    bsm::Topology topo;
+    bsm::Geometry geo;
+    bsm::Table table;
+    int kernel_class = 0;
+    void* d_table = nullptr;  // device copy: wg_ptr, then items (16-byte aligned)
+    const int32_t* d_wg_ptr = nullptr;
+    const bsm_item* d_items = nullptr;
+    hipEvent_t last_use = nullptr;
+    bool used = false;
+};
+
+namespace {
+
+thread_local std::string g_error;
+
+bsm_status fail(bsm_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+bsm_status hip_fail(hipError_t e, const char* what) {
+    return fail(BSM_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
+}
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+    int prev = -1;
+    bool switched = false;
+    hipError_t enter(int device) {
+        hipError_t e = hipGetDevice(&prev);
+        if (e != hipSuccess) return e;
+        if (prev != device) {
+            e = hipSetDevice(device);
+            if (e != hipSuccess) return e;
+            switched = true;
+        }
+        return hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (switched) (void)hipSetDevice(prev);
+    }
+};
+
+int elem_bytes_of(bsm_dtype d) { return d == BSM_BF16 ? 2 : 4; }
+
+bool valid_dtype(int d) { return d == BSM_F32 || d == BSM_BF16; }
+bool valid_schedule(int s) { return s == BSM_SCHED_RR || s == BSM_SCHED_BALANCED || s == BSM_SCHED_XCD; }
+
+// Defaults for a device: all CUs, the runtime's XCD count, 256-thread workgroups.  wg_per_cu
+// is left 0 ("as many as stay resident"): a plan fills it from the occupancy of the kernel
+// instance it launches, so the persistent grid is fully resident and the static table is
+// what actually runs.
+bsm_status default_topology(int device, bsm_topology* t) {
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    int n_xcd = 1;
+    e = hipDeviceGetAttribute(&n_xcd, hipDeviceAttributeNumberOfXccs, device);
+    if (e != hipSuccess || n_xcd < 1) n_xcd = 1;
+    if (n_xcd > BSM_MAX_XCD) n_xcd = BSM_MAX_XCD;
+    std::memset(t, 0, sizeof *t);
+    t->n_cu = prop.multiProcessorCount;
+    t->n_xcd = n_xcd;
+    t->wg_threads = 256;
+    t->wg_per_cu = 0;
+    t->item_cost = 4096.0f;
+    t->row_cost = 128.0f;
+    return BSM_OK;
+}
+
+constexpr int kMaxWgPerCu = 8;
+
+bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtype, int kclass,
+                            bsm::Topology* out) {
+    bsm_topology t;
+    if (device >= 0) {
+        bsm_status st = default_topology(device, &t);
+        if (st != BSM_OK) return st;
+    } else {
+        std::memset(&t, 0, sizeof t);
+        t.n_cu = 256;
+        t.n_xcd = 8;
+        t.wg_threads = 256;
+        t.wg_per_cu = 8;
+        t.item_cost = 4096.0f;
+        t.row_cost = 128.0f;
+    }
+    if (user) {
+        if (user->n_cu > 0) t.n_cu = user->n_cu;
+        if (user->n_xcd > 0) t.n_xcd = user->n_xcd;
+        if (user->wg_per_cu > 0) t.wg_per_cu = user->wg_per_cu;
+        if (user->wg_threads > 0) t.wg_threads = user->wg_threads;
+        if (user->item_cost > 0.0f) t.item_cost = user->item_cost;
+        if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
+    }
+    if (t.wg_per_cu <= 0) {
+        t.wg_per_cu = kMaxWgPerCu;
+        if (device >= 0 && t.wg_threads >= 64 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
+            int n = 0;
+            DeviceGuard g;
+            hipError_t e = g.enter(device);
+            if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, &n);
+            if (e != hipSuccess) return hip_fail(e, "occupancy query");
+            t.wg_per_cu = std::max(1, std::min(kMaxWgPerCu, n));
+        }
+    }
+    out->n_cu = t.n_cu;
+    out->n_xcd = t.n_xcd;
+    out->wg_per_cu = t.wg_per_cu;
+    out->wg_threads = t.wg_threads;
+    out->item_cost = t.item_cost;
+    out->row_cost = t.row_cost;
+    std::string err = bsm::check_topology(*out);
+    if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "topology: %s", err.c_str());
+    return BSM_OK;
+}
+
+void free_device(bsm_plan p) {
+    if (p->device < 0) return;
+    DeviceGuard g;
+    if (g.enter(p->device) != hipSuccess) return;
+    if (p->last_use) {
+        if (p->used) (void)hipEventSynchronize(p->last_use);
+        (void)hipEventDestroy(p->last_use);
+        p->last_use = nullptr;
+    }
+    if (p->d_table) {
+        (void)hipFree(p->d_table);
+        p->d_table = nullptr;
+    }
+}
+
+bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* rows,
+                       const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
+                       const int8_t* home_xcd, const bsm_topology* topology, int device) {
+    if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
+    if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
+    if (device < -1) return fail(BSM_ERR_INVALID_ARG, "device %d", device);
+    if (device == -1 && !topology) return fail(BSM_ERR_INVALID_ARG, "a host-only plan (device -1) needs a topology");
+    if (device >= 0) {
+        int n = 0;
+        hipError_t e = hipGetDeviceCount(&n);
+        if (e != hipSuccess) return hip_fail(e, "hipGetDeviceCount");
+        if (device >= n) return fail(BSM_ERR_INVALID_ARG, "device %d of %d", device, n);
+    }
+    std::unique_ptr<bsm_plan_s> p(new (std::nothrow) bsm_plan_s);
+    if (!p) return fail(BSM_ERR_OOM, "plan allocation failed");
+    try {
+        std::string err = bsm::make_geometry(offs, rows, cols, batch, elem_bytes_of(dtype), &p->geo);
+        if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
+        p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
+        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
+        if (st != BSM_OK) return st;
+        err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, &p->table);
+        if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "plan: %s", err.c_str());
+    } catch (const std::bad_alloc&) {
+        return fail(BSM_ERR_OOM, "host allocation failed while planning");
+    }
+    p->device = device;
+    p->dtype = dtype;
+    p->schedule = schedule;
+    p->table.stats.dtype = dtype;
+    p->table.stats.kernel_class = p->kernel_class;
+
+    if (device >= 0) {
+        DeviceGuard g;
+        hipError_t e = g.enter(device);
+        if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+        const size_t ptr_bytes = p->table.wg_ptr.size() * sizeof(int32_t);
+        const size_t items_at = (ptr_bytes + 255) & ~static_cast<size_t>(255);
+        const size_t bytes = items_at + std::max<size_t>(p->table.items.size(), 1) * sizeof(bsm_item);
+        e = hipMalloc(&p->d_table, bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            p->d_table = nullptr;
+            return fail(e == hipErrorOutOfMemory ? BSM_ERR_OOM : BSM_ERR_HIP,
+                        "hipMalloc(%zu) for the work table: %s", bytes, hipGetErrorString(e));
+        }
+        char* base = static_cast<char*>(p->d_table);
+        e = hipMemcpy(base, p->table.wg_ptr.data(), ptr_bytes, hipMemcpyHostToDevice);
+        if (e == hipSuccess && !p->table.items.empty())
+            e = hipMemcpy(base + items_at, p->table.items.data(),
+                          p->table.items.size() * sizeof(bsm_item), hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->last_use, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            bsm_status st = hip_fail(e, "uploading the work table");
+            free_device(p.get());
+            return st;
+        }
+        p->d_wg_ptr = reinterpret_cast<const int32_t*>(base);
+        p->d_items = reinterpret_cast<const bsm_item*>(base + items_at);
+    }
+    *out_plan = p.release();
+    return BSM_OK;
+}
+
+bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, void* trace) {
+    if (!p) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    if (p->device < 0) return fail(BSM_ERR_UNSUPPORTED, "host-only plan (device -1) cannot execute");
+    const int64_t extent_bytes = p->geo.extent * elem_bytes_of(p->dtype);
+    if (p->geo.total_elems == 0) return BSM_OK;
+    if (!in || !out) return fail(BSM_ERR_INVALID_ARG, "in or out is NULL");
+    const uintptr_t a = reinterpret_cast<uintptr_t>(in), b = reinterpret_cast<uintptr_t>(out);
+    if (a != b && a < b + static_cast<uintptr_t>(extent_bytes) && b < a + static_cast<uintptr_t>(extent_bytes))
+        return fail(BSM_ERR_ALIAS, "in and out overlap without being equal (extent %lld bytes)",
+                    static_cast<long long>(extent_bytes));
+    if ((a % elem_bytes_of(p->dtype)) != 0 || (b % elem_bytes_of(p->dtype)) != 0)
+        return fail(BSM_ERR_INVALID_ARG, "in/out not aligned to the element size");
+    DeviceGuard g;
+    hipError_t e = g.enter(p->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_wg_ptr, p->d_items,
+                            p->topo.n_wg(), p->topo.wg_threads, trace, s);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    e = hipEventRecord(p->last_use, s);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    p->used = true;
+    return BSM_OK;
+}
+
+// ---------------------------------------------------------------------------- plan cache
+struct CacheKey {
+    int device;
+    int dtype;
+    int schedule;
+    bool uniform;
+    int64_t batch;
+    std::vector<int64_t> off;
+    std::vector<int32_t> R, C;
+    bool operator==(const CacheKey& o) const {
+        return device == o.device && dtype == o.dtype && schedule == o.schedule &&
+               uniform == o.uniform && batch == o.batch && off == o.off && R == o.R && C == o.C;
+    }
+};
+
+struct CacheEntry {
+    CacheKey key;
+    bsm_plan plan;
+};
+
+std::mutex g_cache_mu;
+std::list<CacheEntry> g_cache;  // most recently used first
+constexpr size_t kCacheMax = 32;
+
+void destroy_plan(bsm_plan p) {
+    if (!p) return;
+    free_device(p);
+    delete p;
+}
+
+}  // namespace
+
+extern "C" {
+
+bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets, const int32_t* rows,
+                           const int32_t* cols, int64_t batch, bsm_dtype dtype,
+                           bsm_schedule schedule, const int8_t* home_xcd,
+                           const bsm_topology* topology, int device) {
+    return create_plan(out_plan, slice_offsets, rows, cols, batch, dtype, schedule, home_xcd,
+                       topology, device);
+}
+
+bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace) {
+    return execute_plan(plan, in, out, stream, trace);
+}
+
+bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats) {
+    if (!plan || !stats) return fail(BSM_ERR_INVALID_ARG, "plan or stats is NULL");
+    *stats = plan->table.stats;
+    return BSM_OK;
+}
+
+bsm_status bsm_plan_export(bsm_plan plan, int32_t* wg_ptr, bsm_item* items, int8_t* home,
+                           uint8_t* overlap) {
+    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    const bsm::Table& t = plan->table;
+    if (wg_ptr) std::memcpy(wg_ptr, t.wg_ptr.data(), t.wg_ptr.size() * sizeof(int32_t));
+    if (items && !t.items.empty()) std::memcpy(items, t.items.data(), t.items.size() * sizeof(bsm_item));
+    if (home && !t.home.empty()) std::memcpy(home, t.home.data(), t.home.size());
+    if (overlap && !t.overlap.empty()) std::memcpy(overlap, t.overlap.data(), t.overlap.size());
+    return BSM_OK;
+}
+
+bsm_status bsm_plan_destroy(bsm_plan plan) {
+    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    destroy_plan(plan);
+    return BSM_OK;
+}
+
+bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, const int32_t* rows,
+                       const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
+                       void* stream) {
+    if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
+    if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
+    // Validate the geometry before any HIP call (also decides the no-op cases).
+    bsm::Geometry geo;
+    std::string err;
+    try {
+        err = bsm::make_geometry(slice_offsets, rows, cols, batch, elem_bytes_of(dtype), &geo);
+    } catch (const std::bad_alloc&) {
+        return fail(BSM_ERR_OOM, "host allocation failed");
+    }
+    if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
+    if (geo.total_elems == 0) return BSM_OK;
+    if (!in || !out) return fail(BSM_ERR_INVALID_ARG, "in or out is NULL");
+    const int64_t extent_bytes = geo.extent * elem_bytes_of(dtype);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(in), b = reinterpret_cast<uintptr_t>(out);
+    if (a != b && a < b + static_cast<uintptr_t>(extent_bytes) && b < a + static_cast<uintptr_t>(extent_bytes))
+        return fail(BSM_ERR_ALIAS, "in and out overlap without being equal");
+
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    CacheKey key{device, dtype, schedule, slice_offsets == nullptr, batch, {}, {}, {}};
+    if (slice_offsets) {
+        key.off.assign(slice_offsets, slice_offsets + batch);
+        key.R.assign(rows, rows + batch);
+        key.C.assign(cols, cols + batch);
+    } else {
+        key.R.assign(rows, rows + 1);
+        key.C.assign(cols, cols + 1);
+    }
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    bsm_plan plan = nullptr;
+    for (auto it = g_cache.begin(); it != g_cache.end(); ++it) {
+        if (it->key == key) {
+            plan = it->plan;
+            g_cache.splice(g_cache.begin(), g_cache, it);
+            break;
+        }
+    }
+    if (!plan) {
+        bsm_status st = create_plan(&plan, slice_offsets, rows, cols, batch, dtype, schedule,
+                                    nullptr, nullptr, device);
+        if (st != BSM_OK) return st;
+        g_cache.push_front(CacheEntry{std::move(key), plan});
+        while (g_cache.size() > kCacheMax) {
+            destroy_plan(g_cache.back().plan);
+            g_cache.pop_back();
+        }
+    }
+    return execute_plan(plan, in, out, stream, nullptr);
+}
+
+bsm_status bsm_cache_clear(void) {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    for (auto& ent : g_cache) destroy_plan(ent.plan);
+    g_cache.clear();
+    return BSM_OK;
+}
+
+bsm_status bsm_device_info(int device, bsm_device_props* info) {
+    if (!info) return fail(BSM_ERR_INVALID_ARG, "info is NULL");
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    std::memset(info, 0, sizeof *info);
+    int n_xcd = 1;
+    if (hipDeviceGetAttribute(&n_xcd, hipDeviceAttributeNumberOfXccs, device) != hipSuccess) n_xcd = 1;
+    int wall = 0;
+    if (hipDeviceGetAttribute(&wall, hipDeviceAttributeWallClockRate, device) != hipSuccess) wall = 0;
+    info->n_cu = prop.multiProcessorCount;
+    info->n_xcd = n_xcd;
+    info->wave_size = prop.warpSize;
+    info->max_threads_per_cu = prop.maxThreadsPerMultiProcessor;
+    info->lds_bytes_per_cu = static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor);
+    info->l2_bytes = prop.l2CacheSize;
+    info->hbm_bytes = static_cast<int64_t>(prop.totalGlobalMem);
+    info->wall_clock_hz = static_cast<int64_t>(wall) * 1000;  // attribute is in kHz
+    info->clock_khz = prop.clockRate;
+    info->peak_hbm_gbs = 2.0 * static_cast<double>(prop.memoryClockRate) * 1e3 *
+                         (static_cast<double>(prop.memoryBusWidth) / 8.0) / 1e9;
+    std::snprintf(info->arch, sizeof info->arch, "%s", prop.gcnArchName);
+    return BSM_OK;
+}
+
+bsm_status bsm_default_topology(int device, bsm_topology* topology) {
+    if (!topology) return fail(BSM_ERR_INVALID_ARG, "topology is NULL");
+    return default_topology(device, topology);
+}
+
+bsm_status bsm_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+    if (bytes < 0) return fail(BSM_ERR_INVALID_ARG, "bytes is negative");
+    if (bytes == 0) return BSM_OK;
+    if (!src || !dst) return fail(BSM_ERR_INVALID_ARG, "src or dst is NULL");
+    const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);
+    if (a < b + static_cast<uintptr_t>(bytes) && b < a + static_cast<uintptr_t>(bytes))
+        return fail(BSM_ERR_ALIAS, "src and dst overlap");
+    int device = 0, n_cu = 256;
+    if (hipGetDevice(&device) == hipSuccess)
+        (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, device);
+    hipError_t e = bsm::launch_copy(src, dst, bytes, n_cu, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "copy kernel launch");
+    return BSM_OK;
+}
+
+const char* bsm_status_string(bsm_status status) {
+    switch (status) {
+        case BSM_OK: return "BSM_OK";
+        case BSM_ERR_INVALID_ARG: return "BSM_ERR_INVALID_ARG";
+        case BSM_ERR_UNSUPPORTED: return "BSM_ERR_UNSUPPORTED";
+        case BSM_ERR_ALIAS: return "BSM_ERR_ALIAS";
+        case BSM_ERR_OOM: return "BSM_ERR_OOM";
+        case BSM_ERR_HIP: return "BSM_ERR_HIP";
+    }
+    return "BSM_ERR_UNKNOWN";
+}
+
+const char* bsm_last_error(void) { return g_error.c_str(); }
+
+int32_t bsm_abi_version(void) { return BSM_ABI_VERSION; }
+
+}  // extern "C"

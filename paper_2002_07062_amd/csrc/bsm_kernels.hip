@@ -1,0 +1,455 @@
+// Persistent batched row-softmax kernels for gfx950 (CDNA4, wave64).
+//
+// One launch runs a grid of n_wg persistent workgroups.  Workgroup w walks the items
+// [wg_ptr[w], wg_ptr[w+1]) of the host-built work table (the paper's Patch<->Cluster mapping
+// table, Section 5: geometry is read per item, the instructions are the same for every patch).
+// Inside an item, rows are spread over the workgroup's waves; no barrier is ever needed
+// because every row is owned by one group of lanes of one wave.
+//
+// Per row (softmax over the row, the operation of the problem statement, Section 2):
+//   128-bit loads (fp32 or bf16 -> fp32 registers)  -> lane max -> group max (DPP, permlane)
+//   -> e = 2^((x - m) * log2 e) (v_exp_f32)          -> lane sum (pairwise) -> group sum
+//   -> y = e * (1/S)                                 -> RNE to bf16 if needed -> 128-bit stores
+// Reductions combine each lane with a partner that combines the same two values in the other
+// order; IEEE max and add are commutative, so every lane of a group ends with the same bits,
+// and a row's result depends only on its values and length, never on the schedule.
+//
+// A group of G lanes (16, 32 or 64) owns one row and holds V 16-byte vectors per lane, so a
+// wave covers 64/G rows at a time.  Rows longer than the register tile of the kernel class
+// use a two-pass online max/sum (reads the row twice).  Rows whose start or length is not
+// 16-byte aligned use element loads with the same lane layout while they fit one vector's
+// worth of elements per lane, and the two-pass path beyond that.  This is bandwidth-bound
+// work: no MFMA, no LDS.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "bsm.h"
+#include "bsm_launch.hpp"
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ float bits_f(unsigned v) { return __builtin_bit_cast(float, v); }
+__device__ __forceinline__ unsigned f_bits(float v) { return __builtin_bit_cast(unsigned, v); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+struct OpMax {
+    __device__ __forceinline__ static float f(float a, float b) { return __builtin_fmaxf(a, b); }
+};
+struct OpAdd {
+    __device__ __forceinline__ static float f(float a, float b) { return a + b; }
+};
+
+// Reduction over aligned groups of G lanes; all lanes of a group end with identical bits.
+template <int G, class Op>
+__device__ __forceinline__ float group_reduce(float v) {
+    static_assert(G == 16 || G == 32 || G == 64, "group size");
+    v = Op::f(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]: partner lane ^ 1
+    v = Op::f(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]: partner lane ^ 2
+    v = Op::f(v, dpp<0x141>(v));  // row_half_mirror: partner in the other quad of 8
+    v = Op::f(v, dpp<0x140>(v));  // row_mirror: partner in the other half of the 16-lane row
+    if constexpr (G >= 32) {      // rows 2k and 2k+1 meet
+        auto p = __builtin_amdgcn_permlane16_swap(f_bits(v), f_bits(v), false, false);
+        v = Op::f(bits_f(p[0]), bits_f(p[1]));
+    }
+    if constexpr (G == 64) {      // the two 32-lane halves meet
+        auto p = __builtin_amdgcn_permlane32_swap(f_bits(v), f_bits(v), false, false);
+        v = Op::f(bits_f(p[0]), bits_f(p[1]));
+    }
+    return v;
+}
+
+// In-lane pairwise reduction of K values (K a power of two).
+template <int K, class Op>
+__device__ __forceinline__ float lane_reduce(const float* x) {
+    if constexpr (K == 1) {
+        return x[0];
+    } else {
+        float t[K / 2];
+#pragma unroll
+        for (int i = 0; i < K / 2; ++i) t[i] = Op::f(x[2 * i], x[2 * i + 1]);
+        return lane_reduce<K / 2, Op>(t);
+    }
+}
+
+struct F32 {
+    using T = float;
+    static constexpr int kBytes = 4;
+    static constexpr int kEPV = 4;  // elements per 16-byte vector
+    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+        x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+    }
+    __device__ __forceinline__ static void store_vec(T* p, const float* y) {
+        *reinterpret_cast<f32x4*>(p) = f32x4{y[0], y[1], y[2], y[3]};
+    }
+    __device__ __forceinline__ static float load1(const T* p) { return *p; }
+    __device__ __forceinline__ static void store1(T* p, float y) { *p = y; }
+};
+
+struct BF16 {
+    using T = uint16_t;  // raw bf16 bit pattern
+    static constexpr int kBytes = 2;
+    static constexpr int kEPV = 8;
+    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] = bits_f(v[i] << 16);
+            x[2 * i + 1] = bits_f(v[i] & 0xFFFF0000u);
+        }
+    }
+    __device__ __forceinline__ static unsigned pack(float a, float b) {
+        // round to nearest even, NaN stays NaN (v_cvt_pk_bf16_f32)
+        return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
+    }
+    __device__ __forceinline__ static void store_vec(T* p, const float* y) {
+        *reinterpret_cast<u32x4*>(p) =
+            u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])};
+    }
+    __device__ __forceinline__ static float load1(const T* p) {
+        return bits_f(static_cast<unsigned>(*p) << 16);
+    }
+    __device__ __forceinline__ static void store1(T* p, float y) {
+        *p = __builtin_bit_cast(uint16_t, static_cast<__bf16>(y));
+    }
+};
+
+// Softmax of U rows per group, all loads first (U rows x V vectors in flight per lane).
+//   row r of the item starts at element base + r * cols; rows r0, r0 + step, ...
+template <class E, int G, int V, int U, bool VEC>
+__device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* out, int64_t base,
+                                       int cols, int nrows, int r0, int step, int lane) {
+    constexpr int EPV = E::kEPV;
+    constexpr int K = V * EPV;
+    float x[U][K];
+    bool act[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = r0 + u * step;
+        act[u] = r < nrows;
+        const typename E::T* src = in + base + static_cast<int64_t>(r) * cols;
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const int vi = lane + v * G;
+                if (act[u] && vi < nvec) {
+                    E::load_vec(src + vi * EPV, &x[u][v * EPV]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < EPV; ++i) x[u][v * EPV + i] = kNegInf;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = lane + k * G;
+                x[u][k] = (act[u] && j < cols) ? E::load1(src + j) : kNegInf;
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float m = group_reduce<G, OpMax>(lane_reduce<K, OpMax>(x[u]));
+        const float ms = (m == kNegInf) ? 0.0f : m;  // fully masked row: every e is 0
+#pragma unroll
+        for (int k = 0; k < K; ++k) x[u][k] = __builtin_amdgcn_exp2f((x[u][k] - ms) * kLog2e);
+        const float s = group_reduce<G, OpAdd>(lane_reduce<K, OpAdd>(x[u]));
+        const float inv = (s == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(s);
+#pragma unroll
+        for (int k = 0; k < K; ++k) x[u][k] *= inv;
+        const int r = r0 + u * step;
+        typename E::T* dst = out + base + static_cast<int64_t>(r) * cols;
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const int vi = lane + v * G;
+                if (act[u] && vi < nvec) E::store_vec(dst + vi * EPV, &x[u][v * EPV]);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = lane + k * G;
+                if (act[u] && j < cols) E::store1(dst + j, x[u][k]);
+            }
+        }
+    }
+}
+
+// One item with G lanes per row.  The wave's rows are wave*RPW + sub + k*step, k = 0, 1, ...
+// (RPW = 64/G rows per wave, step = rows covered by the whole workgroup at once); the loop
+// trip count depends on the wave only, so lanes never diverge across iterations.
+template <class E, int G, int V, bool VEC>
+__device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E::T* out,
+                                             int64_t base, int cols, int nrows, int wave,
+                                             int nwaves, int lane64) {
+    constexpr int RPW = 64 / G;
+    // Rows in flight per group: about 16 values per lane for aligned rows; one row for the
+    // element-wise path, whose per-element addresses cost registers.
+    constexpr int K = V * E::kEPV;
+    constexpr int U = (!VEC || K >= 16) ? 1 : 16 / K;
+    const int sub = lane64 / G;
+    const int lane = lane64 % G;
+    const int step = nwaves * RPW;
+    uint32_t done = 0;
+    for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
+        rows_u<E, G, V, U, VEC>(in, out, base, cols, nrows, r0 + sub, step, lane);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int left = nrows - (r0 + u * step);
+            done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+        }
+    }
+    return done;
+}
+
+// Rows longer than the register tile: one wave per row, two passes.  Pass 1 keeps a per-lane
+// running max and a sum rescaled whenever the max grows; the lanes' pairs are then merged.
+// Pass 2 re-reads the row and writes e * (1/S).
+template <class E, bool VEC>
+__device__ __forceinline__ void long_row(const typename E::T* src, typename E::T* dst, int cols,
+                                      int lane) {
+    constexpr int EPV = E::kEPV;
+    float m = kNegInf, s = 0.0f;
+    if constexpr (VEC) {
+        const int nvec = cols / EPV;
+        for (int vi = lane; vi < nvec; vi += 64) {
+            float x[EPV];
+            E::load_vec(src + vi * EPV, x);
+            const float cm = lane_reduce<EPV, OpMax>(x);
+            if (cm > m) {
+                s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
+                m = cm;
+            }
+            if (m != kNegInf) {
+#pragma unroll
+                for (int i = 0; i < EPV; ++i) x[i] = __builtin_amdgcn_exp2f((x[i] - m) * kLog2e);
+                s += lane_reduce<EPV, OpAdd>(x);
+            }
+        }
+    } else {
+        for (int j = lane; j < cols; j += 64) {
+            const float x = E::load1(src + j);
+            if (x > m) {
+                s *= __builtin_amdgcn_exp2f((m - x) * kLog2e);
+                m = x;
+            }
+            if (m != kNegInf) s += __builtin_amdgcn_exp2f((x - m) * kLog2e);
+        }
+    }
+    const float M = group_reduce<64, OpMax>(m);
+    const float Ms = (M == kNegInf) ? 0.0f : M;
+    const float scale = (m == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f((m - Ms) * kLog2e);
+    const float S = group_reduce<64, OpAdd>(s * scale);
+    const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
+    if constexpr (VEC) {
+        const int nvec = cols / EPV;
+        for (int vi = lane; vi < nvec; vi += 64) {
+            float x[EPV];
+            E::load_vec(src + vi * EPV, x);
+#pragma unroll
+            for (int i = 0; i < EPV; ++i) x[i] = __builtin_amdgcn_exp2f((x[i] - Ms) * kLog2e) * inv;
+            E::store_vec(dst + vi * EPV, x);
+        }
+    } else {
+        for (int j = lane; j < cols; j += 64)
+            E::store1(dst + j, __builtin_amdgcn_exp2f((E::load1(src + j) - Ms) * kLog2e) * inv);
+    }
+}
+
+template <class E, int KCLASS, bool VEC>
+__device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
+                                                  int64_t base, int cols, int nrows, int wave,
+                                                  int nwaves, int lane64) {
+    const int nvec = (cols + E::kEPV - 1) / E::kEPV;
+    if (nvec <= 16) return run_item<E, 16, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    if (nvec <= 32) return run_item<E, 32, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    if (nvec <= 64) return run_item<E, 64, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    // Larger register tiles only for aligned rows; unaligned longer rows take the two-pass path.
+    if constexpr (VEC && KCLASS >= 1) {
+        if (nvec <= 128) return run_item<E, 64, 2, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    }
+    if constexpr (VEC && KCLASS >= 2) {
+        if (nvec <= 256) return run_item<E, 64, 4, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    }
+    if constexpr (VEC && KCLASS >= 3) {
+        if (nvec <= 512) return run_item<E, 64, 8, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    }
+    if constexpr (!VEC || KCLASS >= 4) {
+        uint32_t done = 0;
+        for (int r = wave; r < nrows; r += nwaves) {
+            const int64_t o = base + static_cast<int64_t>(r) * cols;
+            long_row<E, VEC>(in + o, out + o, cols, lane64);
+            ++done;
+        }
+        return done;
+    }
+    return 0;  // unreachable: the host picks a class that covers the plan's longest row
+}
+
+template <class E, int KCLASS>
+__global__ void __launch_bounds__(1024)
+bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ wg_ptr,
+                   const bsm_item* __restrict__ items, int base_aligned,
+                   bsm_trace_rec* __restrict__ trace) {
+    const int w = blockIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int nwaves = static_cast<int>(blockDim.x) >> 6;
+    const int lane64 = static_cast<int>(threadIdx.x) & 63;
+    const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
+    uint32_t rows = 0;
+    const int i0 = wg_ptr[w];
+    const int i1 = wg_ptr[w + 1];
+    for (int i = i0; i < i1; ++i) {
+        const int64_t base = items[i].elem_offset;
+        const int cols = items[i].cols;
+        const int nrows = items[i].nrows;
+        const bool vec = base_aligned && ((base * E::kBytes) & 15) == 0 &&
+                         ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
+        if (vec)
+            rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, wave, nwaves, lane64);
+        else
+            rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, wave, nwaves, lane64);
+    }
+    if (trace && lane64 == 0) {
+        bsm_trace_rec rec;
+        rec.wg = static_cast<uint32_t>(w);
+        // XCC_ID register (id 20), bits [3:0]; HW_ID register (id 4), all 32 bits
+        rec.xcc_id = __builtin_amdgcn_s_getreg(20 | (0 << 6) | ((4 - 1) << 11)) & 0xF;
+        rec.hw_id = __builtin_amdgcn_s_getreg(4 | (0 << 6) | ((32 - 1) << 11));
+        rec.rows = rows;
+        rec.t_start = t0;
+        rec.t_end = __builtin_amdgcn_s_memrealtime();
+        trace[static_cast<int64_t>(w) * nwaves + wave] = rec;
+    }
+}
+
+// Streaming copy, the bandwidth reference: 4 independent 16-byte accesses per thread in
+// flight, grid-stride over the buffer; a byte loop handles an unaligned remainder.
+__global__ void __launch_bounds__(256) bsm_copy_kernel(const u32x4* __restrict__ src,
+                                                       u32x4* __restrict__ dst, int64_t n_vec) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    for (; i + 3 * stride < n_vec; i += 4 * stride) {
+        const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        dst[i] = a;
+        dst[i + stride] = b;
+        dst[i + 2 * stride] = c;
+        dst[i + 3 * stride] = d;
+    }
+    for (; i < n_vec; i += stride) dst[i] = src[i];
+}
+
+__global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char* __restrict__ src,
+                                                             unsigned char* __restrict__ dst,
+                                                             int64_t n) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += stride)
+        dst[i] = src[i];
+}
+
+template <class E, int KCLASS>
+hipError_t launch_t(const void* in, void* out, const int32_t* wg_ptr, const bsm_item* items,
+                    int n_wg, int wg_threads, int aligned, void* trace, hipStream_t stream) {
+    hipLaunchKernelGGL((bsm_softmax_kernel<E, KCLASS>), dim3(n_wg), dim3(wg_threads), 0, stream,
+                       static_cast<const typename E::T*>(in), static_cast<typename E::T*>(out),
+                       wg_ptr, items, aligned, static_cast<bsm_trace_rec*>(trace));
+    return hipGetLastError();
+}
+
+template <class E>
+hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* wg_ptr,
+                        const bsm_item* items, int n_wg, int wg_threads, int aligned, void* trace,
+                        hipStream_t stream) {
+    switch (kclass) {
+        case 0: return launch_t<E, 0>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+        case 1: return launch_t<E, 1>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+        case 2: return launch_t<E, 2>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+        case 3: return launch_t<E, 3>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+        default: return launch_t<E, 4>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+    }
+}
+
+}  // namespace
+
+namespace bsm {
+
+int kernel_class_for(int32_t max_cols, int elem_bytes) {
+    const int64_t nvec = (static_cast<int64_t>(max_cols) * elem_bytes + 15) / 16;
+    if (nvec <= 64) return 0;
+    if (nvec <= 128) return 1;
+    if (nvec <= 256) return 2;
+    if (nvec <= 512) return 3;
+    return 4;
+}
+
+hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
+                          const int32_t* d_wg_ptr, const bsm_item* d_items, int n_wg,
+                          int wg_threads, void* trace, hipStream_t stream) {
+    const int aligned = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+    (void)hipGetLastError();  // start from a clean error state
+    if (dtype == BSM_BF16)
+        return launch_dtype<BF16>(kernel_class, in, out, d_wg_ptr, d_items, n_wg, wg_threads, aligned, trace, stream);
+    return launch_dtype<F32>(kernel_class, in, out, d_wg_ptr, d_items, n_wg, wg_threads, aligned, trace, stream);
+}
+
+hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads, int* n) {
+    const void* fn = nullptr;
+    if (dtype == BSM_BF16) {
+        switch (kernel_class) {
+            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 0>); break;
+            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 1>); break;
+            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 2>); break;
+            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 3>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 4>); break;
+        }
+    } else {
+        switch (kernel_class) {
+            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 0>); break;
+            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 1>); break;
+            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 2>); break;
+            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 3>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 4>); break;
+        }
+    }
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(n, fn, wg_threads, 0);
+}
+
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipStream_t stream) {
+    (void)hipGetLastError();
+    const bool aligned = ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
+    const int64_t n_vec = aligned ? bytes / 16 : 0;
+    const int64_t max_grid = static_cast<int64_t>(n_cu > 0 ? n_cu : 256) * 8;
+    if (n_vec > 0) {
+        int64_t grid = (n_vec + 1023) / 1024;
+        if (grid > max_grid) grid = max_grid;
+        hipLaunchKernelGGL(bsm_copy_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, stream,
+                           static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), n_vec);
+    }
+    const int64_t rest = bytes - n_vec * 16;
+    if (rest > 0) {
+        int64_t grid = (rest + 255) / 256;
+        if (grid > max_grid) grid = max_grid;
+        hipLaunchKernelGGL(bsm_copy_bytes_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                           stream, static_cast<const unsigned char*>(src) + n_vec * 16,
+                           static_cast<unsigned char*>(dst) + n_vec * 16, rest);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace bsm

@@ -1,0 +1,30 @@
+// Launch wrappers exported by bsm_kernels.hip to the C-ABI layer (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "bsm.h"
+
+namespace bsm {
+
+// Kernel classes: the longest row decides how large a register tile the kernel instance
+// carries (a bigger tile costs registers, hence occupancy, for every row).
+//   0: rows of <= 64 16-byte vectors   (fp32 C <= 256,  bf16 C <= 512)
+//   1: <= 128 vectors                  (fp32 C <= 512,  bf16 C <= 1024)
+//   2: <= 256 vectors                  (fp32 C <= 1024, bf16 C <= 2048)
+//   3: <= 512 vectors                  (fp32 C <= 2048, bf16 C <= 4096)
+//   4: any length (longer rows take a two-pass online path)
+int kernel_class_for(int32_t max_cols, int elem_bytes);
+
+hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
+                          const int32_t* d_wg_ptr, const bsm_item* d_items, int n_wg,
+                          int wg_threads, void* trace, hipStream_t stream);
+
+// Workgroups of the kernel instance that fit on one CU at once (registers decide).
+hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads, int* n);
+
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipStream_t stream);
+
+}  // namespace bsm

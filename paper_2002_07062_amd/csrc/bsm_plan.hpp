@@ -1,0 +1,54 @@
+// Host planner: slice geometry -> per-workgroup work table (CSR), for the three schedules.
+// Pure C++17; no HIP.  The paper's HW batch scheduler (Section 5) built in software.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "bsm.h"
+
+namespace bsm {
+
+struct Geometry {
+    int64_t batch = 0;
+    std::vector<int64_t> off;  // [batch] element offset of slice s
+    std::vector<int32_t> R;    // [batch]
+    std::vector<int32_t> C;    // [batch]
+    int elem_bytes = 4;        // in and out share the element type
+    int64_t extent = 0;        // max over slices of off + R*C (0 if all empty)
+    int64_t total_rows = 0;
+    int64_t total_elems = 0;
+    int32_t max_cols = 0;
+};
+
+struct Topology {
+    int32_t n_cu = 256;
+    int32_t n_xcd = 8;
+    int32_t wg_per_cu = 8;
+    int32_t wg_threads = 256;
+    double item_cost = 4096.0;  // byte equivalents
+    double row_cost = 128.0;    // byte equivalents on top of the row's bytes
+    int32_t n_wg() const { return n_cu * wg_per_cu; }
+};
+
+struct Table {
+    std::vector<int32_t> wg_ptr;  // [n_wg + 1]
+    std::vector<bsm_item> items;
+    std::vector<int8_t> home;     // [batch]; -1 where the schedule assigns no home
+    std::vector<uint8_t> overlap; // [batch]
+    bsm_plan_stats stats{};
+};
+
+// Checks the geometry (sizes, overflow, slices not overlapping) and fills `g`.  Returns an
+// empty string on success, else what is wrong.
+std::string make_geometry(const int64_t* slice_offsets, const int32_t* rows,
+                          const int32_t* cols, int64_t batch, int elem_bytes, Geometry* g);
+
+std::string check_topology(const Topology& t);
+
+// Builds the table for `schedule`.  home_xcd may be null.  Returns "" or an error message.
+std::string build_table(const Geometry& g, bsm_schedule schedule, const Topology& t,
+                        const int8_t* home_xcd, Table* out);
+
+}  // namespace bsm

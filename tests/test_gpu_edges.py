@@ -1,0 +1,192 @@
+"""GPU edge cases: ragged geometry with gaps, unaligned bases, odd row lengths, rows beyond the
+register tile, special values, in-place runs, indexing exactness, empty slices, aliasing,
+determinism, the per-wave trace and the copy reference. Oracle: the fp64 CPU reference."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2002_07062_amd as bsm
+import workloads
+from gpu_util import (SENTINEL_BF16, SENTINEL_F32, compare, covered_mask, run_plan,
+                      sentinel_like, to_device, to_host_bits)
+
+pytestmark = pytest.mark.gpu
+
+SCHEDULES = ("rr", "balanced", "xcd")
+ODD_COLS = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 31, 33, 63, 64, 65, 100, 127, 128, 129, 255, 256,
+            257, 511, 512, 513, 1000, 1023, 1024, 1025, 2047, 2048, 2049]
+
+
+def _check_ragged(w, schedule, topology=None):
+    n = int(w.offsets[-1])
+    out, st = run_plan(w, schedule, topology=topology)
+    bits = to_host_bits(out)
+    ref = oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols)
+    mask = covered_mask(w.offsets[: w.batch], w.rows, w.cols, n)
+    compare(bits, ref, w.dtype, mask)
+    sentinel = SENTINEL_F32 if w.dtype == "f32" else SENTINEL_BF16
+    assert np.all(bits[~mask] == sentinel), "a byte outside every slice was written"
+    return bits, st
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_ragged_odd_cols_with_gaps(dtype, schedule):
+    rng = np.random.default_rng(7)
+    cols = ODD_COLS
+    rows = [int(r) for r in rng.integers(1, 40, size=len(cols))]
+    w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=8, gap=3, base=5)
+    print(f"[ragged {dtype} {schedule}] {len(cols)} slices", flush=True)
+    _check_ragged(w, schedule)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_long_rows_two_pass_path(dtype):
+    cols = [2049, 4095, 4096, 4100, 8192, 10000, 40000, 100003]
+    rows = [3, 2, 2, 3, 2, 2, 1, 1]
+    w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=9, gap=8)
+    print(f"[long {dtype}]", flush=True)
+    bits, st = _check_ragged(w, "balanced")
+    assert st["kernel_class"] == 4
+
+
+@pytest.mark.parametrize("shift", [1, 2, 3])
+def test_unaligned_base_pointer(shift):
+    """Input and output start a few elements past a 16-byte boundary: the element-wise path."""
+    w = workloads.custom([7, 5, 9, 4], [64, 512, 1000, 3000], sigma=2.0, seed=10)
+    n = int(w.offsets[-1])
+    buf = torch.zeros(n + shift, device="cuda")
+    buf[shift:] = to_device(w.x, "f32")
+    x = buf[shift:]
+    assert x.data_ptr() % 16 != 0
+    outb = sentinel_like(n + shift, "f32")
+    out = outb[shift:]
+    out_t, _ = run_plan(w, "xcd", x=x, out=out)
+    ref = oracle.softmax(w.x, "f32", w.offsets[:-1], w.rows, w.cols)
+    compare(to_host_bits(out_t), ref, "f32")
+
+
+def test_in_place_equals_out_of_place():
+    w = workloads.generate("c5", batch=40)
+    x = to_device(w.x, w.dtype)
+    out, _ = run_plan(w, "xcd", x=x)
+    y = x.clone()
+    run_plan(w, "xcd", x=y, out=y)
+    assert torch.equal(y.view(torch.int32), out.view(torch.int32))
+
+
+def test_repeat_runs_are_bitwise_identical():
+    w = workloads.generate("c2", batch=48)
+    x = to_device(w.x, w.dtype)
+    a, _ = run_plan(w, "balanced", x=x)
+    b, _ = run_plan(w, "balanced", x=x)
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+@pytest.mark.parametrize("C", [37, 64, 128, 512, 1000])
+def test_one_hot_argmax_exact(C):
+    B, R = 5, 33
+    x = np.zeros((B, R, C), np.float32)
+    for s in range(B):
+        for r in range(R):
+            x[s, r, (131 * s + 17 * r) % C] = 30.0
+    w = workloads.Workload("onehot", "f32", x.reshape(-1),
+                           np.arange(B + 1, dtype=np.int64) * R * C,
+                           np.full(B, R, np.int32), np.full(B, C, np.int32), True)
+    out, _ = run_plan(w, "xcd")
+    y = out.cpu().numpy().reshape(B, R, C)
+    for s in range(B):
+        for r in range(R):
+            assert int(np.argmax(y[s, r])) == (131 * s + 17 * r) % C
+    hot = math.exp(30.0) / (math.exp(30.0) + C - 1)
+    assert np.max(np.abs(y.max(axis=2) - hot)) <= 2e-6
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_special_values(dtype):
+    """Fully masked rows give zeros; a NaN or +inf entry makes its whole row NaN; partially
+    masked rows ignore the masked entries."""
+    C = 96
+    rows = np.random.default_rng(3).standard_normal((6, C)).astype(np.float32)
+    rows[0, :] = -np.inf
+    rows[1, 10] = np.nan
+    rows[2, 50] = np.inf
+    rows[3, 40:] = -np.inf
+    rows[4, :] = 0.0
+    x = rows.reshape(-1)
+    if dtype == "bf16":
+        x = workloads._to_bf16_bits(x)
+    w = workloads.Workload("special", dtype, x, np.array([0, 6 * C], np.int64),
+                           np.array([6], np.int32), np.array([C], np.int32), True)
+    out, _ = run_plan(w, "rr")
+    bits = to_host_bits(out)
+    ref = oracle.softmax(w.x, dtype, [0], [6], [C])
+    compare(bits, ref, dtype)
+    assert np.all(bits[:C] == 0)  # +0 for a fully masked row
+
+
+def test_empty_slices_and_noops():
+    w = workloads.custom([0, 4, 3, 0, 2], [9, 0, 17, 5, 33], sigma=1.0, seed=4, gap=2)
+    _check_ragged(w, "balanced")
+    x = torch.zeros(16, device="cuda")
+    out = torch.full_like(x, 7.0)
+    bsm.bsm_softmax(x, out, 4, 4, batch=0)  # batch 0: no-op
+    bsm.bsm_softmax(x, out, 0, 4, batch=4)  # empty slices: no-op
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+
+
+def test_partial_alias_is_rejected():
+    x = torch.zeros(4 * 64 + 8, device="cuda")
+    with pytest.raises(bsm.BsmError) as e:
+        bsm.bsm_softmax(x[:256], x[4:260], 4, 64, batch=1)
+    assert e.value.status == bsm.BSM_ERR_ALIAS
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_trace_xcd_mapping_and_row_counts(schedule):
+    w = workloads.generate("c5", batch=64)
+    info = bsm.bsm_device_info(0)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[:-1], dtype="f32", schedule=schedule)
+    st = bsm.bsm_plan_describe(plan)
+    trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
+    x = to_device(w.x, "f32")
+    out = torch.empty_like(x)
+    bsm.bsm_plan_execute(plan, x, out, trace=trace)
+    torch.cuda.synchronize()
+    rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+    waves = st["wg_threads"] // 64
+    assert len(rec) == st["n_wg"] * waves
+    assert np.array_equal(rec["wg"], np.repeat(np.arange(st["n_wg"]), waves))
+    assert int(rec["rows"].sum()) == int(w.rows.sum())
+    assert np.all(rec["t_end"] >= rec["t_start"])
+    print(f"n_xcd={info['n_xcd']} xcc ids seen: {sorted(set(rec['xcc_id'].tolist()))}", flush=True)
+    if info["n_xcd"] > 1:
+        # dispatch places workgroup w on XCD w mod n_xcd; the XCD schedule relies on it
+        assert np.array_equal(rec["xcc_id"], rec["wg"] % info["n_xcd"])
+    plan.destroy()
+
+
+def test_copy_kernel():
+    for n in (1, 15, 16, 1000, 1 << 20, (1 << 20) + 7):
+        src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+        dst = torch.zeros_like(src)
+        bsm.bsm_copy(src, dst)
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)
+    a = torch.randn(1 << 20, device="cuda")
+    b = torch.zeros((1 << 20) + 1, device="cuda")[1:]  # unaligned destination
+    bsm.bsm_copy(a, b, a.numel() * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_device_info():
+    d = bsm.bsm_device_info(0)
+    print(d, flush=True)
+    assert d["n_cu"] > 0 and d["wave_size"] == 64
+    assert "gfx950" in d["arch"]
