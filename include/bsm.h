@@ -53,16 +53,19 @@ typedef enum bsm_status {
 
 typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1 } bsm_dtype;
 
-/* Which workgroup processes which rows.
- *   RR        Section 3's prior solution: whole slice s goes to workgroup (s mod n_wg).
- *   BALANCED  Section 4.2 at core granularity: the rows of all slices, in slice order, are cut
- *             into n_wg contiguous ranges of equal planner cost (within one row's cost of the
- *             MINIMAX optimum for this cost model).
+/* Which worker processes which rows.
+ *   RR        Section 3's prior solution: whole slice s goes to workgroup (s mod n_wg), whose
+ *             waves share its rows.  Workers are workgroups.
+ *   BALANCED  Section 4.2's load balancing at core granularity, with every wave a worker: the
+ *             rows of all slices, in slice order, are cut into rounds of equal cost and every
+ *             round into one piece per worker (pieces matched to the least-loaded workers), so
+ *             each worker's total is within about one piece-granule of the MINIMAX optimum for
+ *             this cost model and all workers sweep the tensor together.
  *   XCD       Sections 4.1 + 4.2: each slice gets a home XCD (the virtual bank holding the
  *             largest share of its elements, ties to the lowest index, or the caller's
  *             home_xcd[]); the load balancer moves the fewest rows it must from XCDs above
- *             their share to XCDs below it; each XCD's rows are then cut into equal-cost
- *             ranges over that XCD's workgroups (workgroup w runs on XCD w mod n_xcd). */
+ *             their share to XCDs below it; each XCD's rows are then cut into rounds over the
+ *             waves of that XCD's workgroups (workgroup w runs on XCD w mod n_xcd). */
 typedef enum bsm_schedule {
     BSM_SCHED_RR = 0,
     BSM_SCHED_BALANCED = 1,
@@ -71,22 +74,28 @@ typedef enum bsm_schedule {
 
 /* Launch geometry and cost model used by the planner.  Zero-filled fields take defaults. */
 typedef struct bsm_topology {
-    int32_t n_cu;       /* compute units (MI355X: 256) */
-    int32_t n_xcd;      /* XCDs (MI355X: 8); workgroup w is taken to run on XCD w mod n_xcd */
-    int32_t wg_per_cu;  /* persistent workgroups per CU; the grid has n_cu * wg_per_cu */
-    int32_t wg_threads; /* threads per workgroup, a multiple of 64 in [64, 1024] */
-    float item_cost;    /* planner cost of one work item, in byte equivalents (<= 0: default) */
-    float row_cost;     /* planner cost of one row on top of its bytes (<= 0: default) */
+    int32_t n_cu;        /* compute units (MI355X: 256) */
+    int32_t n_xcd;       /* XCDs (MI355X: 8); workgroup w is taken to run on XCD w mod n_xcd */
+    int32_t wg_per_cu;   /* persistent workgroups per CU; the grid has n_cu * wg_per_cu */
+    int32_t wg_threads;  /* threads per workgroup, a multiple of 64 in [64, 1024] */
+    int32_t piece_bytes; /* BALANCED / XCD: traffic of one worker's piece of a round */
+    float item_cost;     /* planner cost of one work item, in byte equivalents (<= 0: default) */
+    float row_cost;      /* planner cost of one row on top of its bytes (<= 0: default) */
+    int32_t reserved;    /* must be 0 */
 } bsm_topology;
 
-/* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): a
- * contiguous range of rows of one slice. */
+/* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): `reps`
+ * ranges of `nrows` rows each; range k starts at element elem_offset + k*rep_stride*cols.
+ * Every row lies inside a slice of row length `cols` (a range may run on into the next slice
+ * when the two are adjacent in memory and share the row length). */
 typedef struct bsm_item {
-    int64_t elem_offset; /* element offset of the item's first row in in/out */
-    int32_t cols;        /* row length C_s, which is also the row stride */
-    int32_t nrows;       /* rows in the item */
-    int32_t slice;       /* slice index s */
-    int32_t row_begin;   /* index of the item's first row within slice s */
+    int64_t elem_offset; /* element offset of the first row of the first range */
+    int32_t cols;        /* row length C, which is also the row stride */
+    int32_t nrows;       /* rows per range */
+    int32_t reps;        /* ranges (>= 1) */
+    int32_t rep_stride;  /* rows from the start of one range to the start of the next */
+    int32_t slice;       /* slice holding the item's first row */
+    int32_t row_begin;   /* index of that row within its slice */
 } bsm_item;
 
 typedef struct bsm_plan_stats {
@@ -97,6 +106,9 @@ typedef struct bsm_plan_stats {
     int64_t extent_elems;      /* elements from 0 to the end of the furthest slice */
     int64_t moved_bytes;       /* XCD: algorithmic bytes of rows run off their home XCD */
     int64_t trace_bytes;       /* size a trace buffer passed to bsm_plan_execute must have */
+    int64_t n_rounds;          /* BALANCED / XCD: rounds the largest team's stream was cut into */
+    int32_t n_workers;         /* entries of the work table's row pointer minus one */
+    int32_t per_wave;          /* 1: workers are waves (w * waves_per_wg + wave); 0: workgroups */
     int32_t n_wg;              /* persistent workgroups in the grid */
     int32_t n_xcd;
     int32_t wg_threads;
@@ -105,8 +117,8 @@ typedef struct bsm_plan_stats {
     int32_t n_overlap;         /* XCD: slices straddling two or more virtual banks */
     int32_t max_cols;          /* longest row */
     int32_t kernel_class;      /* which kernel instance the plan launches (internal) */
-    double max_wg_cost;        /* planner cost of the most loaded workgroup */
-    double mean_wg_cost;       /* total planner cost / n_wg */
+    double max_worker_cost;    /* planner cost of the most loaded worker */
+    double mean_worker_cost;   /* total planner cost / n_workers */
     double max_row_cost;       /* planner cost of the most expensive single row */
     double moved_cost;         /* XCD: planner cost of the rows run off their home XCD */
     double min_moved_cost;     /* XCD: sum over XCDs of (home load - fair share)+, the least
@@ -180,10 +192,11 @@ bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stre
 
 bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats);
 
-/* Copy the host work table out: wg_ptr [n_wg + 1] (CSR row pointer), items [n_items], and,
- * when non-NULL, home [batch] (home XCD per slice after overlap resolution, -1 where the
- * schedule has none) and overlap [batch] (1 if the slice spans two or more virtual banks). */
-bsm_status bsm_plan_export(bsm_plan plan, int32_t* wg_ptr, bsm_item* items, int8_t* home,
+/* Copy the host work table out: worker_ptr [n_workers + 1] (CSR row pointer: worker v owns
+ * items [worker_ptr[v], worker_ptr[v+1])), items [n_items], and, when non-NULL, home [batch]
+ * (home XCD per slice after overlap resolution, -1 where the schedule has none) and overlap
+ * [batch] (1 if the slice spans two or more virtual banks). */
+bsm_status bsm_plan_export(bsm_plan plan, int32_t* worker_ptr, bsm_item* items, int8_t* home,
                            uint8_t* overlap);
 
 /* Free a plan.  Waits for the plan's last enqueued execution to finish first. */

@@ -3,8 +3,8 @@
 TEST INFRASTRUCTURE ONLY. Everything here is brute force or a direct definition, written for
 clarity rather than speed, and shares no code with the library's host planner:
 
-* exactly-once coverage of every (slice, row) by a work table (the mapping table of
-  Section 5 must schedule every patch, and no patch twice);
+* exactly-once coverage of every row of every slice by a work table (the mapping table of
+  Section 5 must schedule every patch, and no patch twice), with the slice's row length;
 * the batch-to-bank table of Section 4.1, computed by counting the elements of each slice that
   fall in each bank (OVERLAP flag, the counts N_x with overlaps, the max-proportion home with
   ties to the lowest bank, the counts L_x after resolution);
@@ -22,58 +22,89 @@ import numpy as np
 
 
 # ----------------------------------------------------------------------------- work tables
+#
+# A work table is a CSR row pointer over workers plus items; item i covers `reps` ranges of
+# `nrows` rows of row length `cols`, range k starting at element
+# elem_offset + k * rep_stride * cols (the library's documented table format).
 
-def table_rows(wg_ptr, items):
-    """Expand a CSR work table into (wg, slice, row) triples, one per scheduled row.
 
-    `items` is a structured array or a sequence of dicts with fields slice, row_begin, nrows.
-    """
-    out = []
-    n_wg = len(wg_ptr) - 1
-    for w in range(n_wg):
-        for i in range(int(wg_ptr[w]), int(wg_ptr[w + 1])):
+def slice_row_starts(offsets, rows, cols):
+    """Every row of every slice: arrays (start element, slice, row, cols), in slice order."""
+    starts, sl, rr, cc = [], [], [], []
+    for s in range(len(rows)):
+        R, C = int(rows[s]), int(cols[s])
+        if R == 0 or C == 0:
+            continue
+        r = np.arange(R, dtype=np.int64)
+        starts.append(int(offsets[s]) + r * C)
+        sl.append(np.full(R, s, np.int64))
+        rr.append(r)
+        cc.append(np.full(R, C, np.int64))
+    if not starts:
+        z = np.zeros(0, np.int64)
+        return z, z, z, z
+    return (np.concatenate(starts), np.concatenate(sl), np.concatenate(rr), np.concatenate(cc))
+
+
+def table_row_starts(worker_ptr, items):
+    """Every row a table schedules: arrays (worker, start element, cols)."""
+    ws, st, cc = [], [], []
+    for v in range(len(worker_ptr) - 1):
+        for i in range(int(worker_ptr[v]), int(worker_ptr[v + 1])):
             it = items[i]
-            s, r0, n = int(it["slice"]), int(it["row_begin"]), int(it["nrows"])
-            for r in range(r0, r0 + n):
-                out.append((w, s, r))
-    return out
+            e0, C = int(it["elem_offset"]), int(it["cols"])
+            n, reps, stride = int(it["nrows"]), int(it["reps"]), int(it["rep_stride"])
+            for k in range(reps):
+                first = e0 + k * stride * C
+                st.append(first + np.arange(n, dtype=np.int64) * C)
+                ws.append(np.full(n, v, np.int64))
+                cc.append(np.full(n, C, np.int64))
+    if not st:
+        z = np.zeros(0, np.int64)
+        return z, z, z
+    return np.concatenate(ws), np.concatenate(st), np.concatenate(cc)
 
 
-def check_exactly_once(wg_ptr, items, rows):
+def check_exactly_once(worker_ptr, items, offsets, rows, cols):
     """Return a list of problems (empty when every row of every slice is scheduled exactly
-    once and nothing else is)."""
+    once, with its slice's row length, and nothing else is)."""
     problems = []
-    if int(wg_ptr[0]) != 0:
-        problems.append("wg_ptr[0] != 0")
-    if any(int(wg_ptr[w + 1]) < int(wg_ptr[w]) for w in range(len(wg_ptr) - 1)):
-        problems.append("wg_ptr not monotone")
-    if int(wg_ptr[-1]) != len(items):
-        problems.append(f"wg_ptr[-1]={int(wg_ptr[-1])} but {len(items)} items")
+    if int(worker_ptr[0]) != 0:
+        problems.append("worker_ptr[0] != 0")
+    if any(int(worker_ptr[w + 1]) < int(worker_ptr[w]) for w in range(len(worker_ptr) - 1)):
+        problems.append("worker_ptr not monotone")
+    if int(worker_ptr[-1]) != len(items):
+        problems.append(f"worker_ptr[-1]={int(worker_ptr[-1])} but {len(items)} items")
+    for i in range(len(items)):
+        if int(items[i]["reps"]) < 1 or int(items[i]["nrows"]) < 1:
+            problems.append(f"item {i} has reps {int(items[i]['reps'])}, nrows {int(items[i]['nrows'])}")
     if problems:
         return problems
-    seen = {}
-    for w, s, r in table_rows(wg_ptr, items):
-        if not 0 <= s < len(rows) or not 0 <= r < int(rows[s]):
-            problems.append(f"row ({s},{r}) does not exist (wg {w})")
-            continue
-        seen[(s, r)] = seen.get((s, r), 0) + 1
-    for (s, r), k in seen.items():
-        if k != 1:
-            problems.append(f"row ({s},{r}) scheduled {k} times")
-    expected = int(sum(int(R) for R in rows))
-    if len(seen) != expected:
-        problems.append(f"{len(seen)} distinct rows scheduled, {expected} exist")
+    want, _, _, want_c = slice_row_starts(offsets, rows, cols)
+    _, got, got_c = table_row_starts(worker_ptr, items)
+    order_w, order_g = np.argsort(want, kind="stable"), np.argsort(got, kind="stable")
+    if len(got) != len(want):
+        problems.append(f"{len(got)} rows scheduled, {len(want)} exist")
+        return problems
+    if not np.array_equal(want[order_w], got[order_g]):
+        dup = np.unique(got[order_g][1:][np.diff(got[order_g]) == 0])
+        problems.append(f"scheduled row starts differ from the slices' rows "
+                        f"(duplicates: {dup[:5].tolist()})")
+        return problems
+    if not np.array_equal(want_c[order_w], got_c[order_g]):
+        problems.append("a row is scheduled with the wrong row length")
     return problems
 
 
-def wg_loads(wg_ptr, items, row_cost, item_cost=0.0):
-    """Cost per workgroup: item_cost per item plus row_cost(slice) per row."""
-    n_wg = len(wg_ptr) - 1
-    loads = np.zeros(n_wg, dtype=np.float64)
-    for w in range(n_wg):
-        for i in range(int(wg_ptr[w]), int(wg_ptr[w + 1])):
+def worker_loads(worker_ptr, items, row_cost, item_cost=0.0):
+    """Cost per worker: item_cost per item plus row_cost(cols) per row."""
+    n = len(worker_ptr) - 1
+    loads = np.zeros(n, dtype=np.float64)
+    for v in range(n):
+        for i in range(int(worker_ptr[v]), int(worker_ptr[v + 1])):
             it = items[i]
-            loads[w] += item_cost + int(it["nrows"]) * row_cost(int(it["slice"]))
+            nr = int(it["nrows"]) * int(it["reps"])
+            loads[v] += item_cost + nr * row_cost(int(it["cols"]))
     return loads
 
 

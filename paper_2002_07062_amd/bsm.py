@@ -41,17 +41,20 @@ _STATUS_NAMES = {0: "BSM_OK", 1: "BSM_ERR_INVALID_ARG", 2: "BSM_ERR_UNSUPPORTED"
 class bsm_topology(ctypes.Structure):
     _fields_ = [("n_cu", ctypes.c_int32), ("n_xcd", ctypes.c_int32),
                 ("wg_per_cu", ctypes.c_int32), ("wg_threads", ctypes.c_int32),
-                ("item_cost", ctypes.c_float), ("row_cost", ctypes.c_float)]
+                ("piece_bytes", ctypes.c_int32), ("item_cost", ctypes.c_float),
+                ("row_cost", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
 class bsm_item(ctypes.Structure):
     _fields_ = [("elem_offset", ctypes.c_int64), ("cols", ctypes.c_int32),
-                ("nrows", ctypes.c_int32), ("slice", ctypes.c_int32),
+                ("nrows", ctypes.c_int32), ("reps", ctypes.c_int32),
+                ("rep_stride", ctypes.c_int32), ("slice", ctypes.c_int32),
                 ("row_begin", ctypes.c_int32)]
 
 
 ITEM_DTYPE = np.dtype([("elem_offset", "<i8"), ("cols", "<i4"), ("nrows", "<i4"),
-                       ("slice", "<i4"), ("row_begin", "<i4")])
+                       ("reps", "<i4"), ("rep_stride", "<i4"), ("slice", "<i4"),
+                       ("row_begin", "<i4")])
 TRACE_DTYPE = np.dtype([("wg", "<u4"), ("xcc_id", "<u4"), ("hw_id", "<u4"), ("rows", "<u4"),
                         ("t_start", "<u8"), ("t_end", "<u8")])
 
@@ -60,12 +63,13 @@ class bsm_plan_stats(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int64), ("n_items", ctypes.c_int64),
                 ("total_rows", ctypes.c_int64), ("algorithmic_bytes", ctypes.c_int64),
                 ("extent_elems", ctypes.c_int64), ("moved_bytes", ctypes.c_int64),
-                ("trace_bytes", ctypes.c_int64),
+                ("trace_bytes", ctypes.c_int64), ("n_rounds", ctypes.c_int64),
+                ("n_workers", ctypes.c_int32), ("per_wave", ctypes.c_int32),
                 ("n_wg", ctypes.c_int32), ("n_xcd", ctypes.c_int32),
                 ("wg_threads", ctypes.c_int32), ("schedule", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("n_overlap", ctypes.c_int32),
                 ("max_cols", ctypes.c_int32), ("kernel_class", ctypes.c_int32),
-                ("max_wg_cost", ctypes.c_double), ("mean_wg_cost", ctypes.c_double),
+                ("max_worker_cost", ctypes.c_double), ("mean_worker_cost", ctypes.c_double),
                 ("max_row_cost", ctypes.c_double), ("moved_cost", ctypes.c_double),
                 ("min_moved_cost", ctypes.c_double), ("build_us", ctypes.c_double),
                 ("xcd_bytes", ctypes.c_int64 * BSM_MAX_XCD),
@@ -136,6 +140,8 @@ def _arr(a, dtype):
 def _dtype_code(d) -> int:
     if isinstance(d, str):
         return DTYPES[d]
+    if isinstance(d, (int, np.integer)):
+        return int(d)  # raw bsm_dtype code: the library validates it
     if d == torch.float32:
         return BSM_F32
     if d == torch.bfloat16:
@@ -291,10 +297,10 @@ def bsm_plan_describe(plan: Plan) -> dict:
 
 
 def bsm_plan_export(plan: Plan):
-    """Returns (wg_ptr int32[n_wg+1], items ITEM_DTYPE[n_items], home int8[batch],
+    """Returns (worker_ptr int32[n_workers+1], items ITEM_DTYPE[n_items], home int8[batch],
     overlap uint8[batch])."""
     d = bsm_plan_describe(plan)
-    wg_ptr = np.zeros(d["n_wg"] + 1, np.int32)
+    wg_ptr = np.zeros(d["n_workers"] + 1, np.int32)
     items = np.zeros(d["n_items"], ITEM_DTYPE)
     home = np.zeros(plan.batch, np.int8)
     overlap = np.zeros(plan.batch, np.uint8)

@@ -26,8 +26,8 @@ struct bsm_plan_s {
     bsm::Geometry geo;
     bsm::Table table;
     int kernel_class = 0;
-    void* d_table = nullptr;  // device copy: wg_ptr, then items (16-byte aligned)
-    const int32_t* d_wg_ptr = nullptr;
+    void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
+    const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
     hipEvent_t last_use = nullptr;
     bool used = false;
@@ -70,15 +70,21 @@ struct DeviceGuard {
     }
 };
 
+constexpr int kDefaultWgPerCu = 2;
+constexpr int kDefaultPieceBytes = 8192;
+constexpr float kDefaultItemCost = 1024.0f;
+constexpr float kDefaultRowCost = 64.0f;
+
 int elem_bytes_of(bsm_dtype d) { return d == BSM_BF16 ? 2 : 4; }
 
 bool valid_dtype(int d) { return d == BSM_F32 || d == BSM_BF16; }
 bool valid_schedule(int s) { return s == BSM_SCHED_RR || s == BSM_SCHED_BALANCED || s == BSM_SCHED_XCD; }
 
 // Defaults for a device: all CUs, the runtime's XCD count, 256-thread workgroups.  wg_per_cu
-// is left 0 ("as many as stay resident"): a plan fills it from the occupancy of the kernel
-// instance it launches, so the persistent grid is fully resident and the static table is
-// what actually runs.
+// is left 0: a plan uses kDefaultWgPerCu, capped by the occupancy of the kernel instance it
+// launches, so the persistent grid is always fully resident and the static table is what
+// actually runs.  Two 4-wave workgroups per CU (8 waves) measured fastest for streaming rows
+// on MI355X: more waves only add DRAM page conflicts.
 bsm_status default_topology(int device, bsm_topology* t) {
     hipDeviceProp_t prop;
     hipError_t e = hipGetDeviceProperties(&prop, device);
@@ -92,12 +98,11 @@ bsm_status default_topology(int device, bsm_topology* t) {
     t->n_xcd = n_xcd;
     t->wg_threads = 256;
     t->wg_per_cu = 0;
-    t->item_cost = 4096.0f;
-    t->row_cost = 128.0f;
+    t->piece_bytes = kDefaultPieceBytes;
+    t->item_cost = kDefaultItemCost;
+    t->row_cost = kDefaultRowCost;
     return BSM_OK;
 }
-
-constexpr int kMaxWgPerCu = 8;
 
 bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtype, int kclass,
                             bsm::Topology* out) {
@@ -110,33 +115,39 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         t.n_cu = 256;
         t.n_xcd = 8;
         t.wg_threads = 256;
-        t.wg_per_cu = 8;
-        t.item_cost = 4096.0f;
-        t.row_cost = 128.0f;
+        t.piece_bytes = kDefaultPieceBytes;
+        t.item_cost = kDefaultItemCost;
+        t.row_cost = kDefaultRowCost;
     }
     if (user) {
+        if (user->reserved != 0) return fail(BSM_ERR_INVALID_ARG, "topology.reserved must be 0");
+        if (user->n_cu < 0 || user->n_xcd < 0 || user->wg_per_cu < 0 || user->wg_threads < 0 ||
+            user->piece_bytes < 0)
+            return fail(BSM_ERR_INVALID_ARG, "topology fields must be >= 0 (0 = default)");
         if (user->n_cu > 0) t.n_cu = user->n_cu;
         if (user->n_xcd > 0) t.n_xcd = user->n_xcd;
         if (user->wg_per_cu > 0) t.wg_per_cu = user->wg_per_cu;
         if (user->wg_threads > 0) t.wg_threads = user->wg_threads;
+        if (user->piece_bytes > 0) t.piece_bytes = user->piece_bytes;
         if (user->item_cost > 0.0f) t.item_cost = user->item_cost;
         if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
     }
     if (t.wg_per_cu <= 0) {
-        t.wg_per_cu = kMaxWgPerCu;
+        t.wg_per_cu = kDefaultWgPerCu;
         if (device >= 0 && t.wg_threads >= 64 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
             int n = 0;
             DeviceGuard g;
             hipError_t e = g.enter(device);
             if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, &n);
             if (e != hipSuccess) return hip_fail(e, "occupancy query");
-            t.wg_per_cu = std::max(1, std::min(kMaxWgPerCu, n));
+            t.wg_per_cu = std::max(1, std::min(kDefaultWgPerCu, n));
         }
     }
     out->n_cu = t.n_cu;
     out->n_xcd = t.n_xcd;
     out->wg_per_cu = t.wg_per_cu;
     out->wg_threads = t.wg_threads;
+    out->piece_bytes = t.piece_bytes;
     out->item_cost = t.item_cost;
     out->row_cost = t.row_cost;
     std::string err = bsm::check_topology(*out);
@@ -182,7 +193,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
         bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
         if (st != BSM_OK) return st;
-        err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, &p->table);
+        err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, p->kernel_class, &p->table);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "plan: %s", err.c_str());
     } catch (const std::bad_alloc&) {
         return fail(BSM_ERR_OOM, "host allocation failed while planning");
@@ -197,7 +208,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         DeviceGuard g;
         hipError_t e = g.enter(device);
         if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
-        const size_t ptr_bytes = p->table.wg_ptr.size() * sizeof(int32_t);
+        const size_t ptr_bytes = p->table.worker_ptr.size() * sizeof(int32_t);
         const size_t items_at = (ptr_bytes + 255) & ~static_cast<size_t>(255);
         const size_t bytes = items_at + std::max<size_t>(p->table.items.size(), 1) * sizeof(bsm_item);
         e = hipMalloc(&p->d_table, bytes);
@@ -208,7 +219,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
                         "hipMalloc(%zu) for the work table: %s", bytes, hipGetErrorString(e));
         }
         char* base = static_cast<char*>(p->d_table);
-        e = hipMemcpy(base, p->table.wg_ptr.data(), ptr_bytes, hipMemcpyHostToDevice);
+        e = hipMemcpy(base, p->table.worker_ptr.data(), ptr_bytes, hipMemcpyHostToDevice);
         if (e == hipSuccess && !p->table.items.empty())
             e = hipMemcpy(base + items_at, p->table.items.data(),
                           p->table.items.size() * sizeof(bsm_item), hipMemcpyHostToDevice);
@@ -218,7 +229,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             free_device(p.get());
             return st;
         }
-        p->d_wg_ptr = reinterpret_cast<const int32_t*>(base);
+        p->d_worker_ptr = reinterpret_cast<const int32_t*>(base);
         p->d_items = reinterpret_cast<const bsm_item*>(base + items_at);
     }
     *out_plan = p.release();
@@ -241,8 +252,8 @@ bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, voi
     hipError_t e = g.enter(p->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_wg_ptr, p->d_items,
-                            p->topo.n_wg(), p->topo.wg_threads, trace, s);
+    e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_worker_ptr, p->d_items,
+                            p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     e = hipEventRecord(p->last_use, s);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -302,11 +313,11 @@ bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats) {
     return BSM_OK;
 }
 
-bsm_status bsm_plan_export(bsm_plan plan, int32_t* wg_ptr, bsm_item* items, int8_t* home,
+bsm_status bsm_plan_export(bsm_plan plan, int32_t* worker_ptr, bsm_item* items, int8_t* home,
                            uint8_t* overlap) {
     if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
     const bsm::Table& t = plan->table;
-    if (wg_ptr) std::memcpy(wg_ptr, t.wg_ptr.data(), t.wg_ptr.size() * sizeof(int32_t));
+    if (worker_ptr) std::memcpy(worker_ptr, t.worker_ptr.data(), t.worker_ptr.size() * sizeof(int32_t));
     if (items && !t.items.empty()) std::memcpy(items, t.items.data(), t.items.size() * sizeof(bsm_item));
     if (home && !t.home.empty()) std::memcpy(home, t.home.data(), t.home.size());
     if (overlap && !t.overlap.empty()) std::memcpy(overlap, t.overlap.data(), t.overlap.size());

@@ -26,6 +26,7 @@
 
 #include "bsm.h"
 #include "bsm_launch.hpp"
+#include "bsm_tile.hpp"
 
 namespace {
 
@@ -90,11 +91,11 @@ struct F32 {
     static constexpr int kBytes = 4;
     static constexpr int kEPV = 4;  // elements per 16-byte vector
     __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+        const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
         x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
     }
     __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        *reinterpret_cast<f32x4*>(p) = f32x4{y[0], y[1], y[2], y[3]};
+        __builtin_nontemporal_store(f32x4{y[0], y[1], y[2], y[3]}, reinterpret_cast<f32x4*>(p));
     }
     __device__ __forceinline__ static float load1(const T* p) { return *p; }
     __device__ __forceinline__ static void store1(T* p, float y) { *p = y; }
@@ -105,7 +106,7 @@ struct BF16 {
     static constexpr int kBytes = 2;
     static constexpr int kEPV = 8;
     __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             x[2 * i] = bits_f(v[i] << 16);
@@ -117,8 +118,9 @@ struct BF16 {
         return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
     }
     __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        *reinterpret_cast<u32x4*>(p) =
-            u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])};
+        __builtin_nontemporal_store(
+            u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])},
+            reinterpret_cast<u32x4*>(p));
     }
     __device__ __forceinline__ static float load1(const T* p) {
         return bits_f(static_cast<unsigned>(*p) << 16);
@@ -191,28 +193,32 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
     }
 }
 
-// One item with G lanes per row.  The wave's rows are wave*RPW + sub + k*step, k = 0, 1, ...
-// (RPW = 64/G rows per wave, step = rows covered by the whole workgroup at once); the loop
-// trip count depends on the wave only, so lanes never diverge across iterations.
+// One item with G lanes per row: `reps` ranges of `nrows` rows, range k starting at element
+// base + k * stride.  Within a range the worker's rows are wave*RPW + sub + j*step, j = 0, 1,
+// ... (RPW = 64/G rows per wave, step = rows covered by all the worker's waves at once); loop
+// trip counts depend on the wave only, so lanes never diverge across iterations.
 template <class E, int G, int V, bool VEC>
 __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E::T* out,
-                                             int64_t base, int cols, int nrows, int wave,
-                                             int nwaves, int lane64) {
+                                             int64_t base, int cols, int nrows, int reps,
+                                             int64_t stride, int wave, int nwaves, int lane64) {
     constexpr int RPW = 64 / G;
-    // Rows in flight per group: about 16 values per lane for aligned rows; one row for the
-    // element-wise path, whose per-element addresses cost registers.
+    // Rows in flight per group: about kValuesInFlight values per lane for aligned rows; one
+    // row for the element-wise path, whose per-element addresses cost registers.
     constexpr int K = V * E::kEPV;
-    constexpr int U = (!VEC || K >= 16) ? 1 : 16 / K;
+    constexpr int U = (!VEC || K >= bsm::kValuesInFlight) ? 1 : bsm::kValuesInFlight / K;
     const int sub = lane64 / G;
     const int lane = lane64 % G;
     const int step = nwaves * RPW;
     uint32_t done = 0;
-    for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
-        rows_u<E, G, V, U, VEC>(in, out, base, cols, nrows, r0 + sub, step, lane);
+    for (int k = 0; k < reps; ++k) {
+        const int64_t b = base + k * stride;
+        for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
+            rows_u<E, G, V, U, VEC>(in, out, b, cols, nrows, r0 + sub, step, lane);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int left = nrows - (r0 + u * step);
-            done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+            for (int u = 0; u < U; ++u) {
+                const int left = nrows - (r0 + u * step);
+                done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+            }
         }
     }
     return done;
@@ -272,59 +278,74 @@ __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T
     }
 }
 
+// Register-tile choice per item (wave-uniform branch); the thresholds are bsm::tile_for's.
 template <class E, int KCLASS, bool VEC>
 __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
-                                                  int64_t base, int cols, int nrows, int wave,
-                                                  int nwaves, int lane64) {
+                                                  int64_t base, int cols, int nrows, int reps,
+                                                  int64_t stride, int wave, int nwaves,
+                                                  int lane64) {
     const int nvec = (cols + E::kEPV - 1) / E::kEPV;
-    if (nvec <= 16) return run_item<E, 16, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
-    if (nvec <= 32) return run_item<E, 32, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
-    if (nvec <= 64) return run_item<E, 64, 1, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+#define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    if (nvec <= 16) return BSM_RUN(16, 1);
+    if (nvec <= 32) return BSM_RUN(32, 1);
+    if (nvec <= 64) return BSM_RUN(64, 1);
     // Larger register tiles only for aligned rows; unaligned longer rows take the two-pass path.
     if constexpr (VEC && KCLASS >= 1) {
-        if (nvec <= 128) return run_item<E, 64, 2, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+        if (nvec <= 128) return BSM_RUN(64, 2);
     }
     if constexpr (VEC && KCLASS >= 2) {
-        if (nvec <= 256) return run_item<E, 64, 4, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+        if (nvec <= 256) return BSM_RUN(64, 4);
     }
     if constexpr (VEC && KCLASS >= 3) {
-        if (nvec <= 512) return run_item<E, 64, 8, VEC>(in, out, base, cols, nrows, wave, nwaves, lane64);
+        if (nvec <= 512) return BSM_RUN(64, 8);
     }
+#undef BSM_RUN
     if constexpr (!VEC || KCLASS >= 4) {
         uint32_t done = 0;
-        for (int r = wave; r < nrows; r += nwaves) {
-            const int64_t o = base + static_cast<int64_t>(r) * cols;
-            long_row<E, VEC>(in + o, out + o, cols, lane64);
-            ++done;
+        for (int k = 0; k < reps; ++k) {
+            for (int r = wave; r < nrows; r += nwaves) {
+                const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
+                long_row<E, VEC>(in + o, out + o, cols, lane64);
+                ++done;
+            }
         }
         return done;
     }
     return 0;  // unreachable: the host picks a class that covers the plan's longest row
 }
 
+// Worker w of the table is workgroup w (all its waves share each item) or, when per_wave is
+// set, wave (w * waves_per_workgroup + wave), which then runs its own items alone.
 template <class E, int KCLASS>
 __global__ void __launch_bounds__(1024)
-bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ wg_ptr,
-                   const bsm_item* __restrict__ items, int base_aligned,
+bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
+                   const bsm_item* __restrict__ items, int base_aligned, int per_wave,
                    bsm_trace_rec* __restrict__ trace) {
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int nwaves = static_cast<int>(blockDim.x) >> 6;
     const int lane64 = static_cast<int>(threadIdx.x) & 63;
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
+    const int worker = per_wave ? w * nwaves + wave : w;
+    const int my_wave = per_wave ? 0 : wave;
+    const int my_nwaves = per_wave ? 1 : nwaves;
     uint32_t rows = 0;
-    const int i0 = wg_ptr[w];
-    const int i1 = wg_ptr[w + 1];
+    const int i0 = worker_ptr[worker];
+    const int i1 = worker_ptr[worker + 1];
     for (int i = i0; i < i1; ++i) {
         const int64_t base = items[i].elem_offset;
         const int cols = items[i].cols;
         const int nrows = items[i].nrows;
+        const int reps = items[i].reps;
+        const int64_t stride = static_cast<int64_t>(items[i].rep_stride) * cols;
         const bool vec = base_aligned && ((base * E::kBytes) & 15) == 0 &&
                          ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
         if (vec)
-            rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, wave, nwaves, lane64);
+            rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, reps, stride,
+                                                   my_wave, my_nwaves, lane64);
         else
-            rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, wave, nwaves, lane64);
+            rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, reps, stride,
+                                                    my_wave, my_nwaves, lane64);
     }
     if (trace && lane64 == 0) {
         bsm_trace_rec rec;
@@ -339,20 +360,14 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
     }
 }
 
-// Streaming copy, the bandwidth reference: 4 independent 16-byte accesses per thread in
-// flight, grid-stride over the buffer; a byte loop handles an unaligned remainder.
+// Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the
+// whole grid sweeps one compact window (the fastest copy layout measured on MI355X); a byte
+// loop handles an unaligned remainder.
 __global__ void __launch_bounds__(256) bsm_copy_kernel(const u32x4* __restrict__ src,
                                                        u32x4* __restrict__ dst, int64_t n_vec) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
-    int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    for (; i + 3 * stride < n_vec; i += 4 * stride) {
-        const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
-        dst[i] = a;
-        dst[i + stride] = b;
-        dst[i + 2 * stride] = c;
-        dst[i + 3 * stride] = d;
-    }
-    for (; i < n_vec; i += stride) dst[i] = src[i];
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n_vec; i += stride)
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
 __global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char* __restrict__ src,
@@ -364,25 +379,28 @@ __global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char
 }
 
 template <class E, int KCLASS>
-hipError_t launch_t(const void* in, void* out, const int32_t* wg_ptr, const bsm_item* items,
-                    int n_wg, int wg_threads, int aligned, void* trace, hipStream_t stream) {
+hipError_t launch_t(const void* in, void* out, const int32_t* worker_ptr, const bsm_item* items,
+                    int n_wg, int wg_threads, int aligned, int per_wave, void* trace,
+                    hipStream_t stream) {
     hipLaunchKernelGGL((bsm_softmax_kernel<E, KCLASS>), dim3(n_wg), dim3(wg_threads), 0, stream,
                        static_cast<const typename E::T*>(in), static_cast<typename E::T*>(out),
-                       wg_ptr, items, aligned, static_cast<bsm_trace_rec*>(trace));
+                       worker_ptr, items, aligned, per_wave, static_cast<bsm_trace_rec*>(trace));
     return hipGetLastError();
 }
 
 template <class E>
-hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* wg_ptr,
-                        const bsm_item* items, int n_wg, int wg_threads, int aligned, void* trace,
-                        hipStream_t stream) {
+hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* worker_ptr,
+                        const bsm_item* items, int n_wg, int wg_threads, int aligned, int per_wave,
+                        void* trace, hipStream_t stream) {
+#define BSM_LAUNCH(K) launch_t<E, K>(in, out, worker_ptr, items, n_wg, wg_threads, aligned, per_wave, trace, stream)
     switch (kclass) {
-        case 0: return launch_t<E, 0>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
-        case 1: return launch_t<E, 1>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
-        case 2: return launch_t<E, 2>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
-        case 3: return launch_t<E, 3>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
-        default: return launch_t<E, 4>(in, out, wg_ptr, items, n_wg, wg_threads, aligned, trace, stream);
+        case 0: return BSM_LAUNCH(0);
+        case 1: return BSM_LAUNCH(1);
+        case 2: return BSM_LAUNCH(2);
+        case 3: return BSM_LAUNCH(3);
+        default: return BSM_LAUNCH(4);
     }
+#undef BSM_LAUNCH
 }
 
 }  // namespace
@@ -390,7 +408,7 @@ hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* wg
 namespace bsm {
 
 int kernel_class_for(int32_t max_cols, int elem_bytes) {
-    const int64_t nvec = (static_cast<int64_t>(max_cols) * elem_bytes + 15) / 16;
+    const int64_t nvec = (static_cast<int64_t>(max_cols) * elem_bytes + kVecBytes - 1) / kVecBytes;
     if (nvec <= 64) return 0;
     if (nvec <= 128) return 1;
     if (nvec <= 256) return 2;
@@ -399,13 +417,15 @@ int kernel_class_for(int32_t max_cols, int elem_bytes) {
 }
 
 hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
-                          const int32_t* d_wg_ptr, const bsm_item* d_items, int n_wg,
-                          int wg_threads, void* trace, hipStream_t stream) {
+                          const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg,
+                          int wg_threads, int per_wave, void* trace, hipStream_t stream) {
     const int aligned = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
     (void)hipGetLastError();  // start from a clean error state
     if (dtype == BSM_BF16)
-        return launch_dtype<BF16>(kernel_class, in, out, d_wg_ptr, d_items, n_wg, wg_threads, aligned, trace, stream);
-    return launch_dtype<F32>(kernel_class, in, out, d_wg_ptr, d_items, n_wg, wg_threads, aligned, trace, stream);
+        return launch_dtype<BF16>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
+                                  aligned, per_wave, trace, stream);
+    return launch_dtype<F32>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
+                             aligned, per_wave, trace, stream);
 }
 
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads, int* n) {
@@ -434,9 +454,9 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipS
     (void)hipGetLastError();
     const bool aligned = ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
     const int64_t n_vec = aligned ? bytes / 16 : 0;
-    const int64_t max_grid = static_cast<int64_t>(n_cu > 0 ? n_cu : 256) * 8;
+    const int64_t max_grid = static_cast<int64_t>(n_cu > 0 ? n_cu : 256) * 4;
     if (n_vec > 0) {
-        int64_t grid = (n_vec + 1023) / 1024;
+        int64_t grid = (n_vec + 255) / 256;
         if (grid > max_grid) grid = max_grid;
         hipLaunchKernelGGL(bsm_copy_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, stream,
                            static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), n_vec);

@@ -1,18 +1,27 @@
-// Host planner for the batched row softmax: builds the per-workgroup work table.
+// Host planner for the batched row softmax: builds the per-worker work table.
 //
-// The paper's scheduler (Sections 3-5) maps patches (slices) to compute clusters.  Here a
-// cluster is a persistent workgroup, the table is a CSR list of row ranges per workgroup, and
-// it is built once per geometry on the host (the paper's "constructed upfront" table).
+// The paper's scheduler (Sections 3-5) maps patches (slices) to compute clusters and builds the
+// mapping table once, up front.  Here the table is a CSR list of row ranges per worker, built
+// on the host once per geometry.  A worker is a workgroup (RR) or a single wave (BALANCED and
+// XCD).
 //
-// Cost model (Section 4.2's E_t, for a bandwidth-bound kernel): a row of C elements costs
-// row_cost + 2*C*elem_bytes (read once, write once) byte equivalents; every work item adds
-// item_cost.  All cuts are made at row boundaries with exact integer arithmetic.
+// Cost model (Section 4.2's execution time E_t, for a bandwidth-bound kernel): a row of C
+// elements costs row_cost + 2*C*elem_bytes byte equivalents (read once, written once); each
+// work item adds item_cost (reported, not balanced).  Cuts use exact integer arithmetic.
+//
+// BALANCED and XCD cut a team's row stream into rounds, and every round into one piece per
+// worker.  All workers of a team then sweep the stream together, so at any moment the team
+// touches one compact window of memory (DRAM rows stay open; measured on MI355X to be worth
+// ~20% over one contiguous chunk per worker), while each worker's total stays balanced.
 #include "bsm_plan.hpp"
 
 #include <algorithm>
 #include <chrono>
 #include <cmath>
 #include <limits>
+#include <numeric>
+
+#include "bsm_tile.hpp"
 
 namespace bsm {
 namespace {
@@ -20,92 +29,162 @@ namespace {
 using i128 = __int128;
 
 constexpr int64_t kMaxElems = int64_t(1) << 60;
+constexpr int64_t kMaxBins = int64_t(1) << 26;
 
-struct Piece {
-    int32_t slice;
-    int32_t row_begin;
+// Rows [0, nrows) of row length `cols`; row r starts at element off + r * cols.
+struct Span {
+    int64_t off;
+    int32_t cols;
     int32_t nrows;
 };
 
-int64_t row_cost_of(const Geometry& g, const Topology& t, int32_t s) {
-    return static_cast<int64_t>(std::llround(t.row_cost)) +
-           static_cast<int64_t>(g.C[s]) * 2 * g.elem_bytes;
+int64_t row_cost_of(const Topology& t, int elem_bytes, int32_t cols) {
+    return static_cast<int64_t>(std::llround(t.row_cost)) + static_cast<int64_t>(cols) * 2 * elem_bytes;
 }
 
-void push_merged(std::vector<Piece>* bin, Piece p) {
-    if (p.nrows <= 0) return;
-    if (!bin->empty()) {
-        Piece& last = bin->back();
-        if (last.slice == p.slice && last.row_begin + last.nrows == p.row_begin) {
-            last.nrows += p.nrows;
+// Appends a span, merging it into the previous one when it continues it in memory with the
+// same row length (adjacent slices of equal C form one longer run of rows).
+void push_span(std::vector<Span>* v, Span s) {
+    if (s.nrows <= 0) return;
+    if (!v->empty()) {
+        Span& b = v->back();
+        if (b.cols == s.cols && b.off + static_cast<int64_t>(b.nrows) * b.cols == s.off &&
+            static_cast<int64_t>(b.nrows) + s.nrows <= std::numeric_limits<int32_t>::max()) {
+            b.nrows += s.nrows;
             return;
         }
     }
-    bin->push_back(p);
+    v->push_back(s);
 }
 
-// Cuts the row stream `pieces` (rows taken in order) into K consecutive ranges whose costs are
-// proportional to `weights` (all equal when `weights` is empty).  A row occupying cost
-// interval [a, a + c) of the stream's total T goes to the bin whose cumulative-weight interval
-// contains its midpoint scaled to the weights: bin j with cw[j] <= W(a + c/2)/T < cw[j+1].
-// Each bin's cost is then within one row's cost of its share.  Zero-weight bins get nothing.
-void cut_stream(const Geometry& g, const Topology& t, const std::vector<Piece>& pieces,
-                const std::vector<int64_t>& weights, int K, std::vector<std::vector<Piece>>* bins) {
+// A stream segment of n_units equal units of unit_rows rows, each costing unit_cost.
+struct Segment {
+    int64_t off;
+    int32_t cols;
+    int32_t unit_rows;
+    int64_t n_units;
+    int64_t unit_cost;
+};
+
+std::vector<Segment> segments_of(const std::vector<Span>& stream, const Topology& t, int es,
+                                 int kernel_class, bool whole_steps) {
+    std::vector<Segment> segs;
+    for (const Span& s : stream) {
+        const int64_t rc = row_cost_of(t, es, s.cols);
+        const int32_t unit = whole_steps ? std::max(1, wave_step_rows(s.cols, es, kernel_class)) : 1;
+        const int64_t full = s.nrows / unit, tail = s.nrows % unit;
+        if (full > 0) segs.push_back(Segment{s.off, s.cols, unit, full, unit * rc});
+        if (tail > 0)
+            segs.push_back(Segment{s.off + full * unit * static_cast<int64_t>(s.cols), s.cols,
+                                   static_cast<int32_t>(tail), 1, tail * rc});
+    }
+    return segs;
+}
+
+// Cuts the stream into K consecutive bins with costs proportional to `weights` (all equal when
+// empty), at unit boundaries.  A unit occupying cost interval [a, a + c) of the total T goes to
+// the bin whose cumulative-weight interval holds its scaled midpoint: the largest j with
+// cw[j] <= W (a + c/2) / T.  Every bin is then within one unit's cost of its share; bins of
+// zero weight get nothing.
+void cut_stream(const std::vector<Segment>& segs, const std::vector<int64_t>& weights, int64_t K,
+                std::vector<std::vector<Span>>* bins) {
     bins->assign(static_cast<size_t>(K), {});
     if (K <= 0) return;
     std::vector<i128> cw(static_cast<size_t>(K) + 1, 0);
-    for (int j = 0; j < K; ++j)
+    for (int64_t j = 0; j < K; ++j)
         cw[j + 1] = cw[j] + (weights.empty() ? 1 : std::max<int64_t>(0, weights[j]));
     const i128 W = cw[K];
     i128 T = 0;
-    for (const Piece& p : pieces) T += static_cast<i128>(p.nrows) * row_cost_of(g, t, p.slice);
+    for (const Segment& s : segs) T += static_cast<i128>(s.n_units) * s.unit_cost;
     if (T == 0 || W == 0) return;
 
-    i128 A0 = 0;  // stream cost before the current piece
-    for (const Piece& p : pieces) {
-        const i128 c = row_cost_of(g, t, p.slice);
-        // Row rr's midpoint scaled by 2W: pos(rr) = W*(2*A0 + (2rr+1)c); it belongs to the
-        // largest bin j with 2T*cw[j] <= pos(rr).
-        auto bin_of = [&](int64_t rr) -> int {
-            const i128 pos = W * (2 * A0 + (2 * static_cast<i128>(rr) + 1) * c);
-            // largest j with 2T*cw[j] <= pos
-            int lo = 0, hi = K - 1;
+    i128 A0 = 0;  // stream cost before the current segment
+    for (const Segment& s : segs) {
+        const i128 c = s.unit_cost;
+        // Unit u's midpoint scaled by 2W: pos(u) = W (2 A0 + (2u + 1) c); its bin is the
+        // largest j with 2 T cw[j] <= pos(u).
+        auto bin_of = [&](int64_t u) -> int64_t {
+            const i128 pos = W * (2 * A0 + (2 * static_cast<i128>(u) + 1) * c);
+            int64_t lo = 0, hi = K - 1;
             while (lo < hi) {
-                const int mid = (lo + hi + 1) / 2;
+                const int64_t mid = (lo + hi + 1) / 2;
                 if (2 * T * cw[mid] <= pos) lo = mid; else hi = mid - 1;
             }
             return lo;
         };
-        int64_t r = 0;
-        while (r < p.nrows) {
-            const int b = bin_of(r);
-            int64_t r_end = p.nrows;
+        int64_t u = 0;
+        while (u < s.n_units) {
+            const int64_t b = bin_of(u);
+            int64_t u_end = s.n_units;
             if (b + 1 < K) {
-                // first row rr with W*(2*A0 + (2rr+1)c) >= 2T*cw[b+1]
+                // first unit v with W (2 A0 + (2v + 1) c) >= 2 T cw[b+1]
                 const i128 need = 2 * T * cw[b + 1] - W * (2 * A0 + c);
                 const i128 den = 2 * W * c;
-                i128 rr = need <= 0 ? 0 : (need + den - 1) / den;
-                if (rr < r + 1) rr = r + 1;
-                if (rr < r_end) r_end = static_cast<int64_t>(rr);
+                i128 v = need <= 0 ? 0 : (need + den - 1) / den;
+                if (v < u + 1) v = u + 1;
+                if (v < u_end) u_end = static_cast<int64_t>(v);
             }
-            push_merged(&(*bins)[b], Piece{p.slice, p.row_begin + static_cast<int32_t>(r),
-                                           static_cast<int32_t>(r_end - r)});
-            r = r_end;
+            const int64_t r0 = u * s.unit_rows;
+            const int64_t nr = (u_end - u) * s.unit_rows;
+            push_span(&(*bins)[b], Span{s.off + r0 * s.cols, s.cols, static_cast<int32_t>(nr)});
+            u = u_end;
         }
-        A0 += static_cast<i128>(p.nrows) * c;
+        A0 += static_cast<i128>(s.n_units) * c;
     }
 }
 
-std::vector<Piece> whole_slices(const Geometry& g) {
-    std::vector<Piece> v;
-    for (int64_t s = 0; s < g.batch; ++s)
-        if (g.R[s] > 0 && g.C[s] > 0) v.push_back(Piece{static_cast<int32_t>(s), 0, g.R[s]});
-    return v;
+i128 span_cost(const Span& s, const Topology& t, int es) {
+    return static_cast<i128>(s.nrows) * row_cost_of(t, es, s.cols);
+}
+
+// Rounds for one team: the stream is cut into n_rounds * W bins of equal cost (whole tile
+// steps of the kernel where possible); in each round the largest pieces go to the workers
+// with the least accumulated cost (ties to the lower worker), which keeps every worker's total
+// within about one piece-granule of the others.
+int64_t assign_rounds(const std::vector<Span>& stream, const std::vector<int32_t>& workers,
+                      const Topology& t, int es, int kernel_class,
+                      std::vector<std::vector<Span>>* per_worker) {
+    const int64_t W = static_cast<int64_t>(workers.size());
+    if (W == 0 || stream.empty()) return 0;
+    i128 total = 0;
+    for (const Span& s : stream) total += span_cost(s, t, es);
+    const std::vector<Segment> segs = segments_of(stream, t, es, kernel_class, true);
+    int64_t n_units = 0;
+    for (const Segment& s : segs) n_units += s.n_units;
+    // Rounds of about W * piece_bytes each, but never so many that a piece falls below one
+    // tile step of the kernel.
+    const double per_round = static_cast<double>(W) * std::max(1, t.piece_bytes);
+    int64_t n_rounds = static_cast<int64_t>(std::llround(static_cast<double>(total) / per_round));
+    n_rounds = std::min<int64_t>(n_rounds, n_units / W);
+    n_rounds = std::max<int64_t>(1, std::min<int64_t>(n_rounds, kMaxBins / W));
+    std::vector<std::vector<Span>> bins;
+    cut_stream(segs, {}, n_rounds * W, &bins);
+
+    std::vector<i128> acc(static_cast<size_t>(W), 0);
+    std::vector<i128> cost(static_cast<size_t>(W));
+    std::vector<int64_t> ob(static_cast<size_t>(W)), ow(static_cast<size_t>(W));
+    for (int64_t r = 0; r < n_rounds; ++r) {
+        for (int64_t k = 0; k < W; ++k) {
+            i128 c = 0;
+            for (const Span& s : bins[r * W + k]) c += span_cost(s, t, es);
+            cost[k] = c;
+        }
+        std::iota(ob.begin(), ob.end(), 0);
+        std::iota(ow.begin(), ow.end(), 0);
+        std::stable_sort(ob.begin(), ob.end(), [&](int64_t a, int64_t b) { return cost[a] > cost[b]; });
+        std::stable_sort(ow.begin(), ow.end(), [&](int64_t a, int64_t b) { return acc[a] < acc[b]; });
+        for (int64_t k = 0; k < W; ++k) {
+            const int64_t slot = ow[k], bin = ob[k];
+            acc[slot] += cost[bin];
+            for (const Span& s : bins[r * W + bin]) push_span(&(*per_worker)[workers[slot]], s);
+        }
+    }
+    return n_rounds;
 }
 
 // Homes of Section 4.1.  Virtual banks: n equal contiguous element ranges over the span of the
 // non-empty slices; a slice's home is the bank holding its largest share (lowest index on a
-// tie), OVERLAP is set when it has elements in two or more banks.
+// tie), and OVERLAP is set when it has elements in two or more banks.
 void assign_homes(const Geometry& g, int n, const int8_t* user, Table* tab) {
     const int64_t B = g.batch;
     tab->home.assign(static_cast<size_t>(B), -1);
@@ -134,9 +213,8 @@ void assign_homes(const Geometry& g, int n, const int8_t* user, Table* tab) {
     for (int64_t s = 0; s < B; ++s) {
         const int64_t o = g.off[s], e = o + static_cast<int64_t>(g.R[s]) * g.C[s];
         if (e == o) continue;
-        // first bank whose end is past o
-        int b0 = static_cast<int>(std::upper_bound(bound.begin() + 1, bound.end(), o) -
-                                  (bound.begin() + 1));
+        const int b0 = static_cast<int>(std::upper_bound(bound.begin() + 1, bound.end(), o) -
+                                        (bound.begin() + 1));
         int best = -1, touched = 0;
         int64_t best_share = -1;
         for (int b = b0; b < n && bound[b] < e; ++b) {
@@ -156,14 +234,21 @@ void assign_homes(const Geometry& g, int n, const int8_t* user, Table* tab) {
     }
 }
 
-// Schedule XCD: homes, then load balancing across XCDs, then equal-cost cuts per XCD.
-void plan_xcd(const Geometry& g, const Topology& t, const int8_t* user_home, Table* tab,
-              std::vector<std::vector<Piece>>* bins) {
+struct Piece {  // rows [row_begin, row_begin + nrows) of slice `slice`
+    int32_t slice;
+    int32_t row_begin;
+    int32_t nrows;
+};
+
+// XCD schedule, steps 1 and 2: homes, then the load balancer.  Returns each XCD's row stream.
+std::vector<std::vector<Span>> xcd_streams(const Geometry& g, const Topology& t,
+                                           const int8_t* user_home, Table* tab) {
     const int n = t.n_xcd;
     const int P = t.n_wg();
+    const int es = g.elem_bytes;
     assign_homes(g, n, user_home, tab);
 
-    std::vector<int> Px(static_cast<size_t>(n), 0);
+    std::vector<int64_t> Px(static_cast<size_t>(n), 0);
     for (int w = 0; w < P; ++w) Px[w % n] += 1;
 
     std::vector<std::vector<Piece>> own(static_cast<size_t>(n));
@@ -173,77 +258,129 @@ void plan_xcd(const Geometry& g, const Topology& t, const int8_t* user_home, Tab
         if (g.R[s] == 0 || g.C[s] == 0) continue;
         const int x = tab->home[s];
         own[x].push_back(Piece{static_cast<int32_t>(s), 0, g.R[s]});
-        const i128 c = static_cast<i128>(g.R[s]) * row_cost_of(g, t, static_cast<int32_t>(s));
+        const i128 c = static_cast<i128>(g.R[s]) * row_cost_of(t, es, g.C[s]);
         load[x] += c;
         total += c;
     }
     // Fair share of XCD x: total * Px / P (XCDs differ only in how many workgroups they run).
     std::vector<i128> share(static_cast<size_t>(n));
     for (int x = 0; x < n; ++x) share[x] = total * Px[x] / P;
-
     double min_moved = 0.0;
     for (int x = 0; x < n; ++x)
         if (load[x] > share[x]) min_moved += static_cast<double>(load[x] - share[x]);
     tab->stats.min_moved_cost = min_moved;
 
-    // Over-loaded XCDs keep rows whose midpoint lies within their share; the rest join a pool.
-    std::vector<std::vector<Piece>> stream(static_cast<size_t>(n));
+    // Over-loaded XCDs keep the rows whose cost midpoint lies within their share; the rest
+    // joins a pool that goes to the under-loaded XCDs in proportion to their deficits.
+    std::vector<std::vector<Piece>> kept(static_cast<size_t>(n));
     std::vector<Piece> pool;
     for (int x = 0; x < n; ++x) {
         if (load[x] <= share[x]) {
-            stream[x] = own[x];
+            kept[x] = own[x];
             continue;
         }
         i128 A0 = 0;
         for (const Piece& p : own[x]) {
-            const i128 c = row_cost_of(g, t, p.slice);
-            // rows rr with 2*(A0 + rr*c) + c <= 2*share are kept
-            const i128 num = 2 * share[x] - 2 * A0 - c;
+            const i128 c = row_cost_of(t, es, g.C[p.slice]);
+            const i128 num = 2 * share[x] - 2 * A0 - c;  // rows rr with 2(A0 + rr c) + c <= 2 share
             int64_t keep = 0;
             if (num >= 0) keep = static_cast<int64_t>(std::min<i128>(num / (2 * c) + 1, p.nrows));
-            if (keep > 0) push_merged(&stream[x], Piece{p.slice, p.row_begin, static_cast<int32_t>(keep)});
+            if (keep > 0) kept[x].push_back(Piece{p.slice, p.row_begin, static_cast<int32_t>(keep)});
             if (keep < p.nrows)
                 pool.push_back(Piece{p.slice, p.row_begin + static_cast<int32_t>(keep),
                                      static_cast<int32_t>(p.nrows - keep)});
             A0 += static_cast<i128>(p.nrows) * c;
         }
     }
-    // The pool is split over the under-loaded XCDs in proportion to their deficits.
-    std::vector<int64_t> deficit(static_cast<size_t>(n), 0);
-    bool any = false;
-    for (int x = 0; x < n; ++x) {
-        if (load[x] < share[x]) {
-            deficit[x] = static_cast<int64_t>(share[x] - load[x]);
-            any = any || deficit[x] > 0;
-        }
-    }
+    std::vector<std::vector<Span>> stream(static_cast<size_t>(n));
+    auto to_span = [&](const Piece& p) {
+        return Span{g.off[p.slice] + static_cast<int64_t>(p.row_begin) * g.C[p.slice], g.C[p.slice], p.nrows};
+    };
+    for (int x = 0; x < n; ++x)
+        for (const Piece& p : kept[x]) push_span(&stream[x], to_span(p));
     if (!pool.empty()) {
-        if (!any) {  // rounding left no deficit: give the pool to the least loaded XCD with WGs
+        std::vector<int64_t> deficit(static_cast<size_t>(n), 0);
+        bool any = false;
+        for (int x = 0; x < n; ++x) {
+            if (load[x] < share[x]) {
+                deficit[x] = static_cast<int64_t>(share[x] - load[x]);
+                any = any || deficit[x] > 0;
+            }
+        }
+        if (!any) {  // rounding left no deficit: the least loaded XCD (per workgroup) takes it
             int best = -1;
             for (int x = 0; x < n; ++x)
                 if (Px[x] > 0 && (best < 0 || load[x] * Px[best] < load[best] * Px[x])) best = x;
             deficit[best] = 1;
         }
-        std::vector<std::vector<Piece>> recv;
-        cut_stream(g, t, pool, deficit, n, &recv);
-        for (int x = 0; x < n; ++x)
-            for (const Piece& p : recv[x]) push_merged(&stream[x], p);
+        std::vector<Span> pool_spans;
         double moved_cost = 0.0;
         int64_t moved_bytes = 0;
         for (const Piece& p : pool) {
-            moved_cost += static_cast<double>(p.nrows) * row_cost_of(g, t, p.slice);
-            moved_bytes += static_cast<int64_t>(p.nrows) * g.C[p.slice] * 2 * g.elem_bytes;
+            pool_spans.push_back(to_span(p));  // unmerged: each piece keeps its own cost
+            moved_cost += static_cast<double>(p.nrows) * row_cost_of(t, es, g.C[p.slice]);
+            moved_bytes += static_cast<int64_t>(p.nrows) * g.C[p.slice] * 2 * es;
         }
+        std::vector<std::vector<Span>> recv;
+        cut_stream(segments_of(pool_spans, t, es, 0, false), deficit, n, &recv);
+        for (int x = 0; x < n; ++x)
+            for (const Span& s : recv[x]) push_span(&stream[x], s);
         tab->stats.moved_cost = moved_cost;
         tab->stats.moved_bytes = moved_bytes;
     }
-    // Within each XCD, equal-cost cut over its workgroups w = x, x + n, x + 2n, ...
-    bins->assign(static_cast<size_t>(P), {});
-    for (int x = 0; x < n; ++x) {
-        if (Px[x] == 0) continue;
-        std::vector<std::vector<Piece>> local;
-        cut_stream(g, t, stream[x], {}, Px[x], &local);
-        for (int l = 0; l < Px[x]; ++l) (*bins)[static_cast<size_t>(x) + static_cast<size_t>(l) * n] = std::move(local[l]);
+    return stream;
+}
+
+// Locates the slice holding element `e` (which lies inside some non-empty slice).
+struct SliceIndex {
+    std::vector<std::pair<int64_t, int32_t>> starts;  // (offset, slice), non-empty slices
+    explicit SliceIndex(const Geometry& g) {
+        for (int64_t s = 0; s < g.batch; ++s)
+            if (g.R[s] > 0 && g.C[s] > 0) starts.emplace_back(g.off[s], static_cast<int32_t>(s));
+        std::sort(starts.begin(), starts.end());
+    }
+    int32_t find(int64_t e) const {
+        auto it = std::upper_bound(starts.begin(), starts.end(),
+                                   std::make_pair(e, std::numeric_limits<int32_t>::max()));
+        return (it == starts.begin()) ? -1 : std::prev(it)->second;
+    }
+};
+
+// Turns a worker's spans into items, folding runs of equal-length, equally spaced spans into
+// one strided item.
+void emit_items(const Geometry& g, const SliceIndex& idx, const std::vector<Span>& spans,
+                std::vector<bsm_item>* items) {
+    size_t i = 0;
+    while (i < spans.size()) {
+        const Span& a = spans[i];
+        int64_t reps = 1, stride = 0;
+        if (i + 1 < spans.size()) {
+            const Span& b = spans[i + 1];
+            const int64_t d = b.off - a.off;
+            if (b.cols == a.cols && b.nrows == a.nrows && d > 0 && d % a.cols == 0 &&
+                d / a.cols <= std::numeric_limits<int32_t>::max()) {
+                stride = d / a.cols;
+                reps = 2;
+                while (i + reps < spans.size()) {
+                    const Span& c = spans[i + reps];
+                    const Span& p = spans[i + reps - 1];
+                    if (c.cols != a.cols || c.nrows != a.nrows || c.off - p.off != d ||
+                        reps >= std::numeric_limits<int32_t>::max())
+                        break;
+                    ++reps;
+                }
+            }
+        }
+        bsm_item it;
+        it.elem_offset = a.off;
+        it.cols = a.cols;
+        it.nrows = a.nrows;
+        it.reps = static_cast<int32_t>(reps);
+        it.rep_stride = static_cast<int32_t>(stride);
+        it.slice = idx.find(a.off);
+        it.row_begin = it.slice >= 0 ? static_cast<int32_t>((a.off - g.off[it.slice]) / g.C[it.slice]) : 0;
+        items->push_back(it);
+        i += static_cast<size_t>(reps);
     }
 }
 
@@ -306,9 +443,11 @@ std::string check_topology(const Topology& t) {
     if (t.n_cu < 1 || t.n_cu > 65536) return "n_cu out of range";
     if (t.n_xcd < 1 || t.n_xcd > BSM_MAX_XCD) return "n_xcd out of range [1, 16]";
     if (t.wg_per_cu < 1 || t.wg_per_cu > 64) return "wg_per_cu out of range [1, 64]";
-    if (static_cast<int64_t>(t.n_cu) * t.wg_per_cu > (1 << 22)) return "too many workgroups";
     if (t.wg_threads < 64 || t.wg_threads > 1024 || t.wg_threads % 64 != 0)
         return "wg_threads must be a multiple of 64 in [64, 1024]";
+    if (static_cast<int64_t>(t.n_cu) * t.wg_per_cu * (t.wg_threads / 64) > (1 << 22))
+        return "too many waves";
+    if (t.piece_bytes < 1 || t.piece_bytes > (1 << 30)) return "piece_bytes out of range";
     if (!(t.item_cost >= 0.0) || !(t.row_cost >= 0.0) || !std::isfinite(t.item_cost) ||
         !std::isfinite(t.row_cost) || t.row_cost > 1e12 || t.item_cost > 1e12)
         return "cost model values must be finite and >= 0";
@@ -316,82 +455,104 @@ std::string check_topology(const Topology& t) {
 }
 
 std::string build_table(const Geometry& g, bsm_schedule schedule, const Topology& t,
-                        const int8_t* home_xcd, Table* tab) {
+                        const int8_t* home_xcd, int kernel_class, Table* tab) {
     const auto t0 = std::chrono::steady_clock::now();
     const int P = t.n_wg();
+    const int nw = t.waves_per_wg();
+    const int es = g.elem_bytes;
     *tab = Table{};
     bsm_plan_stats& st = tab->stats;
-    std::vector<std::vector<Piece>> bins;
-
     if (home_xcd && schedule == BSM_SCHED_XCD) {
         for (int64_t s = 0; s < g.batch; ++s)
             if (home_xcd[s] < 0 || home_xcd[s] >= t.n_xcd)
                 return "home_xcd[" + std::to_string(s) + "] outside [0, n_xcd)";
     }
+    std::vector<std::vector<Span>> per_worker;
+    int64_t rounds = 0;
     switch (schedule) {
         case BSM_SCHED_RR: {
-            bins.assign(static_cast<size_t>(P), {});
-            for (const Piece& p : whole_slices(g)) bins[static_cast<size_t>(p.slice % P)].push_back(p);
+            tab->per_wave = false;
+            per_worker.assign(static_cast<size_t>(P), {});
+            for (int64_t s = 0; s < g.batch; ++s)
+                if (g.R[s] > 0 && g.C[s] > 0)
+                    per_worker[static_cast<size_t>(s % P)].push_back(Span{g.off[s], g.C[s], g.R[s]});
             tab->home.assign(static_cast<size_t>(g.batch), -1);
             tab->overlap.assign(static_cast<size_t>(g.batch), 0);
             break;
         }
         case BSM_SCHED_BALANCED: {
-            cut_stream(g, t, whole_slices(g), {}, P, &bins);
+            tab->per_wave = true;
+            per_worker.assign(static_cast<size_t>(P) * nw, {});
+            std::vector<Span> stream;
+            for (int64_t s = 0; s < g.batch; ++s)
+                if (g.R[s] > 0 && g.C[s] > 0) push_span(&stream, Span{g.off[s], g.C[s], g.R[s]});
+            std::vector<int32_t> workers(static_cast<size_t>(P) * nw);
+            std::iota(workers.begin(), workers.end(), 0);
+            rounds = assign_rounds(stream, workers, t, es, kernel_class, &per_worker);
             tab->home.assign(static_cast<size_t>(g.batch), -1);
             tab->overlap.assign(static_cast<size_t>(g.batch), 0);
             break;
         }
-        case BSM_SCHED_XCD:
-            plan_xcd(g, t, home_xcd, tab, &bins);
+        case BSM_SCHED_XCD: {
+            tab->per_wave = true;
+            per_worker.assign(static_cast<size_t>(P) * nw, {});
+            const std::vector<std::vector<Span>> streams = xcd_streams(g, t, home_xcd, tab);
+            for (int x = 0; x < t.n_xcd; ++x) {
+                std::vector<int32_t> workers;
+                for (int w = x; w < P; w += t.n_xcd)
+                    for (int k = 0; k < nw; ++k) workers.push_back(w * nw + k);
+                rounds = std::max(rounds, assign_rounds(streams[x], workers, t, es, kernel_class, &per_worker));
+            }
             break;
+        }
         default:
             return "unknown schedule";
     }
 
     // CSR pack + statistics.
-    int64_t n_items = 0;
-    for (const auto& b : bins) n_items += static_cast<int64_t>(b.size());
-    if (n_items > std::numeric_limits<int32_t>::max()) return "work table exceeds 2^31 items";
-    tab->wg_ptr.assign(static_cast<size_t>(P) + 1, 0);
-    tab->items.reserve(static_cast<size_t>(n_items));
+    const SliceIndex idx(g);
+    const int64_t n_workers = static_cast<int64_t>(per_worker.size());
+    tab->worker_ptr.assign(static_cast<size_t>(n_workers) + 1, 0);
     double max_cost = 0.0, sum_cost = 0.0;
-    for (int w = 0; w < P; ++w) {
+    for (int64_t v = 0; v < n_workers; ++v) {
+        const size_t first = tab->items.size();
+        emit_items(g, idx, per_worker[v], &tab->items);
+        if (tab->items.size() > static_cast<size_t>(std::numeric_limits<int32_t>::max()))
+            return "work table exceeds 2^31 items";
         double cost = 0.0;
-        for (const Piece& p : bins[w]) {
-            bsm_item it;
-            it.elem_offset = g.off[p.slice] + static_cast<int64_t>(p.row_begin) * g.C[p.slice];
-            it.cols = g.C[p.slice];
-            it.nrows = p.nrows;
-            it.slice = p.slice;
-            it.row_begin = p.row_begin;
-            tab->items.push_back(it);
-            cost += t.item_cost + static_cast<double>(p.nrows) * row_cost_of(g, t, p.slice);
-            st.xcd_bytes[w % t.n_xcd] += static_cast<int64_t>(p.nrows) * g.C[p.slice] * 2 * g.elem_bytes;
+        const int x = static_cast<int>((tab->per_wave ? v / nw : v) % t.n_xcd);
+        for (size_t i = first; i < tab->items.size(); ++i) {
+            const bsm_item& it = tab->items[i];
+            const int64_t rows = static_cast<int64_t>(it.nrows) * it.reps;
+            cost += t.item_cost + static_cast<double>(rows) * row_cost_of(t, es, it.cols);
+            st.xcd_bytes[x] += rows * it.cols * 2 * es;
         }
-        tab->wg_ptr[w + 1] = static_cast<int32_t>(tab->items.size());
+        tab->worker_ptr[v + 1] = static_cast<int32_t>(tab->items.size());
         max_cost = std::max(max_cost, cost);
         sum_cost += cost;
     }
     double max_row = 0.0;
     for (int64_t s = 0; s < g.batch; ++s)
         if (g.R[s] > 0 && g.C[s] > 0)
-            max_row = std::max(max_row, static_cast<double>(row_cost_of(g, t, static_cast<int32_t>(s))));
+            max_row = std::max(max_row, static_cast<double>(row_cost_of(t, es, g.C[s])));
 
     st.batch = g.batch;
-    st.n_items = n_items;
+    st.n_items = static_cast<int64_t>(tab->items.size());
     st.total_rows = g.total_rows;
-    st.algorithmic_bytes = g.total_elems * 2 * g.elem_bytes;
+    st.algorithmic_bytes = g.total_elems * 2 * es;
     st.extent_elems = g.extent;
+    st.n_rounds = rounds;
+    st.n_workers = static_cast<int32_t>(n_workers);
+    st.per_wave = tab->per_wave ? 1 : 0;
     st.n_wg = P;
     st.n_xcd = t.n_xcd;
     st.wg_threads = t.wg_threads;
     st.schedule = schedule;
     st.max_cols = g.max_cols;
-    st.max_wg_cost = max_cost;
-    st.mean_wg_cost = P ? sum_cost / P : 0.0;
+    st.max_worker_cost = max_cost;
+    st.mean_worker_cost = n_workers ? sum_cost / static_cast<double>(n_workers) : 0.0;
     st.max_row_cost = max_row;
-    st.trace_bytes = static_cast<int64_t>(P) * (t.wg_threads / 64) * static_cast<int64_t>(sizeof(bsm_trace_rec));
+    st.trace_bytes = static_cast<int64_t>(P) * nw * static_cast<int64_t>(sizeof(bsm_trace_rec));
     st.build_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
     return "";
 }

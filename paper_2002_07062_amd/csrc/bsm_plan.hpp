@@ -1,5 +1,5 @@
-// Host planner: slice geometry -> per-workgroup work table (CSR), for the three schedules.
-// Pure C++17; no HIP.  The paper's HW batch scheduler (Section 5) built in software.
+// Host planner: slice geometry -> per-worker work table (CSR), for the three schedules.
+// Pure C++17, no HIP runtime calls.  The paper's HW batch scheduler (Section 5) in software.
 #pragma once
 
 #include <cstdint>
@@ -25,18 +25,21 @@ struct Geometry {
 struct Topology {
     int32_t n_cu = 256;
     int32_t n_xcd = 8;
-    int32_t wg_per_cu = 8;
+    int32_t wg_per_cu = 2;
     int32_t wg_threads = 256;
-    double item_cost = 4096.0;  // byte equivalents
-    double row_cost = 128.0;    // byte equivalents on top of the row's bytes
+    int32_t piece_bytes = 8192;  // traffic per worker piece in one round
+    double item_cost = 1024.0;   // byte equivalents
+    double row_cost = 64.0;      // byte equivalents on top of the row's bytes
     int32_t n_wg() const { return n_cu * wg_per_cu; }
+    int32_t waves_per_wg() const { return wg_threads / 64; }
 };
 
 struct Table {
-    std::vector<int32_t> wg_ptr;  // [n_wg + 1]
+    std::vector<int32_t> worker_ptr;  // [n_workers + 1]
     std::vector<bsm_item> items;
-    std::vector<int8_t> home;     // [batch]; -1 where the schedule assigns no home
-    std::vector<uint8_t> overlap; // [batch]
+    std::vector<int8_t> home;         // [batch]; -1 where the schedule assigns no home
+    std::vector<uint8_t> overlap;     // [batch]
+    bool per_wave = false;
     bsm_plan_stats stats{};
 };
 
@@ -47,8 +50,10 @@ std::string make_geometry(const int64_t* slice_offsets, const int32_t* rows,
 
 std::string check_topology(const Topology& t);
 
-// Builds the table for `schedule`.  home_xcd may be null.  Returns "" or an error message.
+// Builds the table for `schedule`.  home_xcd may be null.  kernel_class is the register-tile
+// class of the kernel that will run the table (pieces are sized in whole tile steps).
+// Returns "" or an error message.
 std::string build_table(const Geometry& g, bsm_schedule schedule, const Topology& t,
-                        const int8_t* home_xcd, Table* out);
+                        const int8_t* home_xcd, int kernel_class, Table* out);
 
 }  // namespace bsm

@@ -1,0 +1,49 @@
+// Register-tile rule shared by the kernel (which executes it) and the planner (which sizes
+// work pieces to whole tile steps).  constexpr functions are usable from host and device.
+#pragma once
+
+#include <cstdint>
+
+namespace bsm {
+
+constexpr int kWave = 64;
+constexpr int kVecBytes = 16;          // one 128-bit access
+constexpr int kValuesInFlight = 16;    // fp32 values per lane a wave keeps in flight
+
+// Lanes per row G and 16-byte vectors per lane V for a row of `nvec` vectors.  Rows beyond
+// 64 * max_v vectors take the two-pass path (G = 64, V = 0).
+struct Tile {
+    int G;
+    int V;
+};
+
+constexpr Tile tile_for(int64_t nvec, int max_v) {
+    if (nvec <= 16) return Tile{16, 1};
+    if (nvec <= 32) return Tile{32, 1};
+    if (nvec <= 64) return Tile{64, 1};
+    if (max_v >= 2 && nvec <= 128) return Tile{64, 2};
+    if (max_v >= 4 && nvec <= 256) return Tile{64, 4};
+    if (max_v >= 8 && nvec <= 512) return Tile{64, 8};
+    return Tile{64, 0};
+}
+
+// Rows a wave keeps in flight per step: U rows per group of G lanes, 64/G groups per wave.
+constexpr int rows_in_flight(int G, int V, int elems_per_vec, bool vec_path) {
+    const int k = V * elems_per_vec;
+    const int u = (!vec_path || V == 0 || k >= kValuesInFlight) ? 1 : kValuesInFlight / k;
+    return (kWave / G) * u;
+}
+
+// Largest register tile (vectors per lane) a kernel class carries.
+constexpr int max_v_of_class(int kernel_class) {
+    return kernel_class <= 0 ? 1 : kernel_class == 1 ? 2 : kernel_class == 2 ? 4 : 8;
+}
+
+// Rows one wave finishes per step for a row of `cols` elements (aligned rows).
+constexpr int wave_step_rows(int64_t cols, int elem_bytes, int kernel_class) {
+    const int64_t nvec = (cols * elem_bytes + kVecBytes - 1) / kVecBytes;
+    const Tile t = tile_for(nvec, max_v_of_class(kernel_class));
+    return rows_in_flight(t.G, t.V, kVecBytes / elem_bytes, true);
+}
+
+}  // namespace bsm

@@ -1,0 +1,138 @@
+"""The C ABI without a GPU: the library loads, exports every function include/bsm.h declares,
+and rejects bad arguments with the documented status before any HIP call."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2002_07062_amd as bsm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bsm.h")
+TOPO = dict(n_cu=256, n_xcd=8, wg_per_cu=2, wg_threads=256)
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\*?\s+\**(bsm_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert len(names) >= 12, names
+    lib = ctypes.CDLL(bsm.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in bsm.h but not exported"
+
+
+def test_abi_version_and_status_strings():
+    assert bsm.bsm_abi_version() == 1
+    for code, name in enumerate(["BSM_OK", "BSM_ERR_INVALID_ARG", "BSM_ERR_UNSUPPORTED",
+                                 "BSM_ERR_ALIAS", "BSM_ERR_OOM", "BSM_ERR_HIP"]):
+        assert bsm.bsm_status_string(code) == name
+    assert bsm.bsm_status_string(99) == "BSM_ERR_UNKNOWN"
+
+
+def _status(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except bsm.BsmError as e:
+        return e.status, e.message
+    return bsm.BSM_OK, ""
+
+
+@pytest.mark.parametrize("kwargs,msg", [
+    (dict(rows=[4, -1], cols=[4, 4], slice_offsets=[0, 100]), "negative"),
+    (dict(rows=[4, 4], cols=[4, 4], slice_offsets=[0, 10]), "overlap"),
+    (dict(rows=[4, 4], cols=[4, 4], slice_offsets=[0, -16]), "negative"),
+    (dict(rows=[1 << 30], cols=[1 << 31 - 1], slice_offsets=[1 << 59]), "2^60"),
+    (dict(rows=[4], cols=[4], slice_offsets=[0], schedule=7), "schedule"),
+    (dict(rows=[4], cols=[4], slice_offsets=[0], dtype=9), "dtype"),
+    (dict(rows=[4, 4], cols=[4, 4], slice_offsets=[0, 16], schedule="xcd",
+          home_xcd=[0, 8]), "home_xcd"),
+])
+def test_plan_create_rejects_bad_geometry(kwargs, msg):
+    args = dict(dtype="f32", schedule="balanced", topology=TOPO, device=-1)
+    args.update(kwargs)
+    if isinstance(args["dtype"], int):
+        args["dtype"] = args["dtype"]
+    st, m = _status(bsm.bsm_plan_create, **args)
+    assert st == bsm.BSM_ERR_INVALID_ARG, m
+    assert msg in m
+
+
+@pytest.mark.parametrize("topo", [
+    dict(n_cu=-1), dict(wg_threads=100), dict(wg_threads=2048), dict(n_xcd=17),
+    dict(wg_per_cu=65), dict(reserved=1), dict(piece_bytes=-5),
+])
+def test_plan_create_rejects_bad_topology(topo):
+    t = dict(TOPO)
+    t.update(topo)
+    st, m = _status(bsm.bsm_plan_create, [4], [4], [0], dtype="f32", topology=t, device=-1)
+    assert st == bsm.BSM_ERR_INVALID_ARG, m
+
+
+def test_host_only_plan_needs_topology_and_cannot_execute():
+    st, m = _status(bsm.bsm_plan_create, [4], [4], [0], dtype="f32", device=-1)
+    assert st == bsm.BSM_ERR_INVALID_ARG and "topology" in m
+    p = bsm.bsm_plan_create([4], [4], [0], dtype="f32", topology=TOPO, device=-1)
+    lib = bsm.load()
+    rc = lib.bsm_plan_execute(p.handle, ctypes.c_void_p(16), ctypes.c_void_p(4096), None, None)
+    assert rc == bsm.BSM_ERR_UNSUPPORTED
+    p.destroy()
+
+
+def test_null_and_handle_errors():
+    lib = bsm.load()
+    assert lib.bsm_plan_destroy(None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_plan_describe(None, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_plan_create(None, None, None, None, 0, 0, 0, None, None, -1) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_copy(None, None, -1, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_copy(None, None, 0, None) == bsm.BSM_OK
+    assert "NULL" in bsm.bsm_last_error() or "negative" in bsm.bsm_last_error()
+
+
+def _c_arrays(rows, cols, offs=None):
+    r = np.asarray(rows, np.int32)
+    c = np.asarray(cols, np.int32)
+    o = None if offs is None else np.asarray(offs, np.int64)
+    P = ctypes.POINTER
+    return (r, c, o, r.ctypes.data_as(P(ctypes.c_int32)), c.ctypes.data_as(P(ctypes.c_int32)),
+            None if o is None else o.ctypes.data_as(P(ctypes.c_int64)))
+
+
+def test_one_shot_validation_happens_before_any_gpu_call():
+    lib = bsm.load()
+    r, c, o, rp, cp, op = _c_arrays([4, 4], [64, 64], [0, 256])
+    # nothing to do: OK without touching a GPU (pointers are never dereferenced)
+    assert lib.bsm_softmax(None, None, None, rp, cp, 0, 0, 0, None) == bsm.BSM_OK
+    r0, c0, _, rp0, cp0, _ = _c_arrays([0], [64])
+    assert lib.bsm_softmax(None, None, None, rp0, cp0, 5, 0, 0, None) == bsm.BSM_OK
+    # work but NULL buffers
+    assert lib.bsm_softmax(None, None, op, rp, cp, 2, 0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    # partial overlap of in and out (fake addresses, never dereferenced)
+    assert lib.bsm_softmax(ctypes.c_void_p(1 << 20), ctypes.c_void_p((1 << 20) + 64), op, rp, cp, 2,
+                           0, 0, None) == bsm.BSM_ERR_ALIAS
+    # bad enums and geometry
+    assert lib.bsm_softmax(ctypes.c_void_p(16), ctypes.c_void_p(16), op, rp, cp, 2, 5, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_softmax(ctypes.c_void_p(16), ctypes.c_void_p(16), op, rp, cp, 2, 0, 9, None) == bsm.BSM_ERR_INVALID_ARG
+    r2, c2, o2, rp2, cp2, op2 = _c_arrays([4, 4], [64, 64], [0, 100])
+    assert lib.bsm_softmax(ctypes.c_void_p(16), ctypes.c_void_p(16), op2, rp2, cp2, 2, 0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_softmax(ctypes.c_void_p(16), ctypes.c_void_p(16), None, rp, cp, -1, 0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+
+
+def test_describe_reports_the_plan():
+    p = bsm.bsm_plan_create([3, 5], [1000, 64], [0, 3000], dtype="bf16", schedule="xcd",
+                            topology=TOPO, device=-1)
+    d = bsm.bsm_plan_describe(p)
+    p.destroy()
+    assert d["batch"] == 2 and d["total_rows"] == 8
+    assert d["algorithmic_bytes"] == 2 * 2 * (3000 + 320)
+    assert d["extent_elems"] == 3320
+    assert d["max_cols"] == 1000 and d["dtype"] == bsm.BSM_BF16
+    assert d["kernel_class"] == 1  # 1000 bf16 = 125 vectors
+    assert d["schedule"] == bsm.BSM_SCHED_XCD

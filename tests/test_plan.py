@@ -1,0 +1,264 @@
+"""The library's host planner, checked on the CPU (host-only plans, device -1) against the plain
+checks in oracle/plan_checks.py: exactly-once coverage, balance bounds, the Section 4.1 bank
+table and overlap rule, the Section 4.2 load balancer, MINIMAX on tiny instances, RR's rule,
+and determinism. Topologies: MI355X-like (256 CUs / 8 XCDs), an MI300X-like part (304 / 8),
+a single XCD, and odd sizes."""
+
+import numpy as np
+import pytest
+
+import paper_2002_07062_amd as bsm
+import workloads
+from golden_io import paper_bank_table
+from oracle import plan_checks as pc
+
+MI355X = dict(n_cu=256, n_xcd=8, wg_per_cu=2, wg_threads=256)
+TOPOLOGIES = {
+    "mi355x": MI355X,
+    "mi300x_like": dict(n_cu=304, n_xcd=8, wg_per_cu=2, wg_threads=256),
+    "one_xcd": dict(n_cu=32, n_xcd=1, wg_per_cu=3, wg_threads=128),
+    "odd": dict(n_cu=7, n_xcd=3, wg_per_cu=1, wg_threads=192),
+}
+ROW_COST = 64  # the library's default per-row overhead in byte equivalents
+
+
+def _plan(w, schedule, topo, home=None, kclass_cols=None):
+    p = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                            schedule=schedule, topology=topo, home_xcd=home, device=-1)
+    d = bsm.bsm_plan_describe(p)
+    ptr, items, home_out, ov = bsm.bsm_plan_export(p)
+    p.destroy()
+    return d, ptr, items, home_out, ov
+
+
+def _row_cost(es):
+    return lambda c: ROW_COST + 2 * es * c
+
+
+def _workloads():
+    return {
+        "c1": workloads.generate("c1"),
+        "c2": workloads.generate("c2", batch=96),
+        "c3": workloads.generate("c3", batch=64),
+        "c4": workloads.generate("c4", batch=1024),
+        "c5": workloads.generate("c5"),
+        "ragged_gaps": workloads.custom([3, 0, 17, 1, 250, 9, 64], [5, 7, 1000, 2049, 64, 8, 33],
+                                        gap=11, base=3),
+    }
+
+
+WL = _workloads()
+
+
+@pytest.mark.parametrize("topo", TOPOLOGIES, ids=list(TOPOLOGIES))
+@pytest.mark.parametrize("schedule", ["rr", "balanced", "xcd"])
+@pytest.mark.parametrize("name", list(WL))
+def test_every_row_scheduled_exactly_once(name, schedule, topo):
+    w = WL[name]
+    d, ptr, items, _, _ = _plan(w, schedule, TOPOLOGIES[topo])
+    assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == []
+    t = TOPOLOGIES[topo]
+    n_wg = t["n_cu"] * t["wg_per_cu"]
+    assert d["n_wg"] == n_wg
+    assert d["n_workers"] == (n_wg if schedule == "rr" else n_wg * t["wg_threads"] // 64)
+    assert d["per_wave"] == (0 if schedule == "rr" else 1)
+    assert d["total_rows"] == int(w.rows.sum())
+    assert d["algorithmic_bytes"] == w.algorithmic_bytes
+    assert d["trace_bytes"] == n_wg * (t["wg_threads"] // 64) * 32
+
+
+@pytest.mark.parametrize("name", list(WL))
+def test_rr_gives_whole_slice_s_to_workgroup_s_mod_p(name):
+    w = WL[name]
+    d, ptr, items, _, _ = _plan(w, "rr", MI355X)
+    ws, starts, _ = pc.table_row_starts(ptr, items)
+    want, sl, rr, _ = pc.slice_row_starts(w.offsets[: w.batch], w.rows, w.cols)
+    owner = dict(zip(starts.tolist(), ws.tolist()))
+    for e, s in zip(want.tolist(), sl.tolist()):
+        assert owner[e] == s % d["n_wg"]
+
+
+def _unit_cost_bound(w):
+    # largest cost of one tile step of the kernel: at most 16 fp32 values per lane in flight,
+    # i.e. <= 64 lanes * 16 values * 2 (read + write) * 4 bytes plus its rows' overheads
+    return 64 * 16 * 2 * 4 + 16 * ROW_COST + 2 * 2 * w.elem_size * int(w.cols.max())
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5", "ragged_gaps"])
+@pytest.mark.parametrize("schedule", ["balanced", "xcd"])
+def test_balanced_workers_within_two_steps_of_each_other(name, schedule):
+    w = WL[name]
+    d, ptr, items, _, _ = _plan(w, schedule, MI355X)
+    loads = pc.worker_loads(ptr, items, _row_cost(w.elem_size))
+    lb = loads.sum() / len(loads)
+    biggest_row = ROW_COST + 2 * w.elem_size * int(w.cols.max())
+    if loads.sum() / len(loads) < 4 * _unit_cost_bound(w):
+        pytest.skip("fewer tile steps than workers: balance is not the limit")
+    assert loads.max() <= lb + 2 * _unit_cost_bound(w) + biggest_row, (loads.max(), lb)
+
+
+def test_balanced_beats_rr_on_ragged_c5():
+    w = WL["c5"]
+    _, p_rr, i_rr, _, _ = _plan(w, "rr", MI355X)
+    _, p_b, i_b, _, _ = _plan(w, "balanced", MI355X)
+    rc = _row_cost(4)
+    rr = pc.worker_loads(p_rr, i_rr, rc)
+    # RR runs a whole workgroup (4 waves) per slice: compare per-wave makespans
+    rr_wave = rr.max() / 4
+    bal = pc.worker_loads(p_b, i_b, rc).max()
+    assert bal < rr_wave / 2
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tiny_instances_against_bruteforce_minimax(seed):
+    """Two workers; whole-slice MINIMAX optimum by enumeration. BALANCED may split slices at
+    tile steps, so its makespan must not exceed the whole-slice optimum by more than one step;
+    RR can never beat the optimum."""
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 7))
+    rows = rng.integers(1, 40, size=B)
+    cols = rng.choice([8, 64, 200, 512], size=B)
+    w = workloads.custom(rows, cols, seed=seed)
+    topo = dict(n_cu=1, n_xcd=1, wg_per_cu=2, wg_threads=64)
+    rc = _row_cost(4)
+    costs = [int(r) * rc(int(c)) for r, c in zip(rows, cols)]
+    opt, _ = pc.minimax_bruteforce(costs, 2)
+    _, p_b, i_b, _, _ = _plan(w, "balanced", topo)
+    bal = pc.worker_loads(p_b, i_b, rc).max()
+    step = max(16 * rc(int(c)) for c in cols)  # a tile step is at most 16 rows
+    assert bal <= opt + step
+    assert bal >= sum(costs) / 2 - 1e-9
+    _, p_r, i_r, _, _ = _plan(w, "rr", topo)
+    assert pc.worker_loads(p_r, i_r, rc).max() >= opt
+
+
+def test_paper_bank_table_through_the_library():
+    """Section 4.1's table, reproduced by the XCD schedule with four virtual banks."""
+    banks, rows = paper_bank_table()
+    off = np.array([r["offset"] for r in rows], np.int64)
+    R = np.array([r["R"] for r in rows], np.int32)
+    C = np.array([r["C"] for r in rows], np.int32)
+    p = bsm.bsm_plan_create(R, C, off, dtype="f32", schedule="xcd", device=-1,
+                            topology=dict(n_cu=4, n_xcd=banks, wg_per_cu=1, wg_threads=64))
+    d = bsm.bsm_plan_describe(p)
+    _, _, home, ov = bsm.bsm_plan_export(p)
+    p.destroy()
+    assert ov.tolist() == [r["overlap"] for r in rows]
+    flags = np.array([r["flags"] for r in rows])
+    assert d["bank_touch"] == flags.sum(axis=0).tolist()  # N_x with overlaps
+    assert sum(d["bank_touch"]) > len(rows)
+    assert sum(d["bank_home"]) == len(rows)                 # L_x sums to N
+    assert home.tolist() == [2, 0, 1, 1, 3]
+    assert d["n_overlap"] == 1
+
+
+@pytest.mark.parametrize("name", ["c1", "c5", "ragged_gaps"])
+@pytest.mark.parametrize("n_xcd", [2, 3, 8])
+def test_homes_match_bruteforce_bank_table(name, n_xcd):
+    w = WL[name]
+    if w.n_elements > 2_000_000:
+        w = workloads.generate("c5", batch=40)
+    topo = dict(n_cu=8 * n_xcd, n_xcd=n_xcd, wg_per_cu=1, wg_threads=64)
+    d, ptr, items, home, ov = _plan(w, "xcd", topo)
+    t = pc.bank_table(w.offsets[: w.batch], w.rows, w.cols, n_xcd)
+    assert home.tolist() == t["home"].tolist()
+    assert ov.tolist() == t["overlap"].tolist()
+    assert d["bank_touch"] == t["N"].tolist()
+    assert d["bank_home"] == t["L"].tolist()
+
+
+def _xcd_loads(w, d, ptr, items, topo, home):
+    """Per-XCD cost, and the cost of rows run off their home XCD."""
+    nw = topo["wg_threads"] // 64
+    rc = _row_cost(w.elem_size)
+    ws, starts, cols = pc.table_row_starts(ptr, items)
+    want, sl, _, _ = pc.slice_row_starts(w.offsets[: w.batch], w.rows, w.cols)
+    slice_of = dict(zip(want.tolist(), sl.tolist()))
+    per_xcd = np.zeros(topo["n_xcd"])
+    moved = 0.0
+    for v, e, c in zip(ws.tolist(), starts.tolist(), cols.tolist()):
+        x = (v // nw) % topo["n_xcd"]
+        per_xcd[x] += rc(c)
+        if home[slice_of[e]] != x:
+            moved += rc(c)
+    return per_xcd, moved
+
+
+@pytest.mark.parametrize("pattern", ["all_on_one", "first_portion", "skewed", "virtual"])
+def test_xcd_load_balancer(pattern):
+    """Section 4.2: whatever the homes, after load balancing every XCD carries its share
+    within about a row, and the moved load is the least any balancer must move (plus row
+    rounding). 'first_portion' is the pathology where every slice is homed on the bank of its
+    first byte, which puts everything on one bank."""
+    w = workloads.generate("c5", batch=120)
+    topo = dict(n_cu=32, n_xcd=8, wg_per_cu=1, wg_threads=128)
+    rng = np.random.default_rng(3)
+    home = {
+        "all_on_one": np.zeros(w.batch, np.int8),
+        "first_portion": np.full(w.batch, 5, np.int8),
+        "skewed": rng.choice([0, 1, 2], size=w.batch).astype(np.int8),
+        "virtual": None,
+    }[pattern]
+    d, ptr, items, home_out, _ = _plan(w, "xcd", topo, home=home)
+    assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == []
+    per_xcd, moved = _xcd_loads(w, d, ptr, items, topo, home_out)
+    share = per_xcd.sum() / topo["n_xcd"]
+    biggest_row = ROW_COST + 2 * 4 * int(w.cols.max())
+    assert per_xcd.max() <= share + 2 * biggest_row
+    assert abs(moved - d["moved_cost"]) < 1e-6 * max(1.0, moved)
+    # the balancer cuts at whole rows (midpoint rule): within half a row per XCD of the least
+    # possible move, on either side
+    assert abs(d["moved_cost"] - d["min_moved_cost"]) <= topo["n_xcd"] * biggest_row / 2
+    loads_before = np.zeros(topo["n_xcd"])
+    rc = _row_cost(4)
+    for s in range(w.batch):
+        loads_before[home_out[s]] += int(w.rows[s]) * rc(int(w.cols[s]))
+    assert d["min_moved_cost"] == pytest.approx(
+        pc.min_moved(loads_before, [loads_before.sum() / topo["n_xcd"]] * topo["n_xcd"]), abs=8)
+
+
+def test_one_bank_needs_no_moves_and_matches_balanced():
+    """Section 3: with the whole tensor on one bank and one XCD, the XCD schedule has nothing
+    to move and balances exactly like BALANCED."""
+    w = workloads.generate("c5", batch=50)
+    topo = dict(n_cu=16, n_xcd=1, wg_per_cu=2, wg_threads=128)
+    d_x, p_x, i_x, _, _ = _plan(w, "xcd", topo)
+    d_b, p_b, i_b, _, _ = _plan(w, "balanced", topo)
+    assert d_x["moved_bytes"] == 0
+    assert np.array_equal(p_x, p_b) and np.array_equal(i_x, i_b)
+
+
+@pytest.mark.parametrize("schedule", ["rr", "balanced", "xcd"])
+def test_plans_are_deterministic(schedule):
+    w = WL["c5"]
+    a = _plan(w, schedule, MI355X)
+    b = _plan(w, schedule, MI355X)
+    for x, y in zip(a[1:], b[1:]):
+        assert np.array_equal(x, y)
+
+
+def test_uniform_and_explicit_offsets_give_the_same_table():
+    w = WL["c2"]
+    p = bsm.bsm_plan_create(512, 512, None, batch=w.batch, dtype="f32", schedule="balanced",
+                            topology=MI355X, device=-1)
+    a = bsm.bsm_plan_export(p)
+    p.destroy()
+    b = _plan(w, "balanced", MI355X)[1:]
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_strided_items_fold_regular_pieces():
+    """On a uniform batch every wave's pieces are equally spaced: one strided item each."""
+    d, ptr, items, _, _ = _plan(WL["c2"], "balanced", MI355X)
+    assert d["n_items"] == d["n_workers"]
+    assert np.all(items["reps"] == d["n_rounds"])
+
+
+def test_item_metadata_names_the_first_row():
+    w = WL["ragged_gaps"]
+    d, ptr, items, _, _ = _plan(w, "balanced", dict(n_cu=3, n_xcd=1, wg_per_cu=1, wg_threads=64))
+    for it in items:
+        s, r = int(it["slice"]), int(it["row_begin"])
+        assert int(w.offsets[s]) + r * int(w.cols[s]) == int(it["elem_offset"])
+        assert int(w.cols[s]) == int(it["cols"])

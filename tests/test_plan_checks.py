@@ -73,41 +73,51 @@ def test_bank_bounds_cover_span_exactly():
     assert all(b[i] <= b[i + 1] for i in range(8))
 
 
-def _table(pairs_per_wg):
-    wg_ptr = [0]
+# geometry for the coverage pins: slice 0 is 5 x 4 at element 0, slice 1 is 1 x 6 at 30
+OFF, ROWS, COLS = [0, 30], [5, 1], [4, 6]
+
+
+def _table(per_worker):
+    """per_worker: lists of (elem_offset, cols, nrows, reps, rep_stride)."""
+    ptr = [0]
     items = []
-    for pairs in pairs_per_wg:
-        for (s, r0, n) in pairs:
-            items.append(dict(slice=s, row_begin=r0, nrows=n))
-        wg_ptr.append(len(items))
-    return wg_ptr, items
+    for its in per_worker:
+        for (e, c, n, k, st) in its:
+            items.append(dict(elem_offset=e, cols=c, nrows=n, reps=k, rep_stride=st))
+        ptr.append(len(items))
+    return ptr, items
 
 
-def test_exactly_once_accepts_a_valid_table():
-    wg_ptr, items = _table([[(0, 0, 3)], [(0, 3, 2), (1, 0, 1)], []])
-    assert pc.check_exactly_once(wg_ptr, items, [5, 1]) == []
+def test_exactly_once_accepts_valid_tables():
+    ptr, items = _table([[(0, 4, 3, 1, 0)], [(12, 4, 2, 1, 0), (30, 6, 1, 1, 0)], []])
+    assert pc.check_exactly_once(ptr, items, OFF, ROWS, COLS) == []
+    # strided: rows 0, 2, 4 and rows 1, 3 of slice 0
+    ptr, items = _table([[(0, 4, 1, 3, 2)], [(4, 4, 1, 2, 2), (30, 6, 1, 1, 0)]])
+    assert pc.check_exactly_once(ptr, items, OFF, ROWS, COLS) == []
 
 
 @pytest.mark.parametrize("tables", [
-    [[(0, 0, 3)], [(0, 2, 3), (1, 0, 1)]],   # row (0,2) twice
-    [[(0, 0, 3)], [(0, 4, 1), (1, 0, 1)]],   # row (0,3) missing
-    [[(0, 0, 5)], [(1, 0, 2)]],              # row (1,1) does not exist
-    [[(0, 0, 5)], [(2, 0, 1)]],              # slice 2 does not exist
+    [[(0, 4, 3, 1, 0)], [(8, 4, 3, 1, 0), (30, 6, 1, 1, 0)]],    # row 2 of slice 0 twice
+    [[(0, 4, 3, 1, 0)], [(16, 4, 1, 1, 0), (30, 6, 1, 1, 0)]],   # row 3 of slice 0 missing
+    [[(0, 4, 5, 1, 0)], [(30, 6, 2, 1, 0)]],                     # a row past slice 1
+    [[(0, 4, 5, 1, 0)], [(30, 4, 1, 1, 0)]],                     # wrong row length
+    [[(0, 4, 1, 3, 2)], [(4, 4, 1, 2, 1), (30, 6, 1, 1, 0)]],    # strided overlap
+    [[(0, 4, 5, 1, 0)], [(30, 6, 1, 0, 0)]],                     # zero repetitions
 ])
 def test_exactly_once_catches_planted_mistakes(tables):
-    wg_ptr, items = _table(tables)
-    assert pc.check_exactly_once(wg_ptr, items, [5, 1]) != []
+    ptr, items = _table(tables)
+    assert pc.check_exactly_once(ptr, items, OFF, ROWS, COLS) != []
 
 
 def test_exactly_once_catches_bad_csr():
-    wg_ptr, items = _table([[(0, 0, 5)], [(1, 0, 1)]])
-    assert pc.check_exactly_once([0, 2, 1], items, [5, 1]) != []
-    assert pc.check_exactly_once([0, 1, 3], items, [5, 1]) != []
+    ptr, items = _table([[(0, 4, 5, 1, 0)], [(30, 6, 1, 1, 0)]])
+    assert pc.check_exactly_once([0, 2, 1], items, OFF, ROWS, COLS) != []
+    assert pc.check_exactly_once([0, 1, 3], items, OFF, ROWS, COLS) != []
 
 
-def test_wg_loads_and_min_moved():
-    wg_ptr, items = _table([[(0, 0, 3)], [(0, 3, 2), (1, 0, 1)]])
-    loads = pc.wg_loads(wg_ptr, items, row_cost=lambda s: [10, 100][s], item_cost=1)
-    assert loads.tolist() == [31, 122]
+def test_worker_loads_and_min_moved():
+    ptr, items = _table([[(0, 4, 3, 1, 0)], [(12, 4, 2, 1, 0), (30, 6, 1, 1, 0)]])
+    loads = pc.worker_loads(ptr, items, row_cost=lambda c: 10 * c, item_cost=1)
+    assert loads.tolist() == [121, 142]
     assert pc.min_moved([10, 2, 6], [6, 6, 6]) == 4
     assert pc.min_moved([6, 6], [6, 6]) == 0
