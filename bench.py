@@ -17,6 +17,7 @@ fp64 oracle timed on this host's cores on the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -31,6 +32,28 @@ if ROOT not in sys.path:
 METRIC = "batched-softmax HBM GB/s (% of MI355X peak) at 384×512×512 fp32"
 PEAK_HBM_GBS = 8000.0   # MI355X published HBM3E bandwidth
 MALL_BYTES = 256 << 20  # last-level Infinity Cache; rotation keeps reuse distance above it
+
+
+KERNEL_SOURCES = ("paper_2002_07062_amd/csrc/bsm_kernels.hip", "paper_2002_07062_amd/csrc/bsm_tile.hpp")
+
+
+def _kernel_sha() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _profiled(workload: str, schedule: str):
+    """Figures of the committed rocprofv3 summary for this workload and schedule, and whether
+    they were taken on the kernel as it is now (same source hash)."""
+    path = os.path.join(ROOT, "profiles", f"bsm_softmax_kernel.{workload}.{schedule}.json")
+    if not os.path.exists(path):
+        return None, False
+    with open(path) as fh:
+        fig = json.load(fh)
+    return fig, fig.get("kernel_sources_sha256") == _kernel_sha()
 
 
 def _to_device(w):
@@ -154,7 +177,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c2")
-    ap.add_argument("--schedule", default="xcd", choices=["rr", "balanced", "xcd"])
+    ap.add_argument("--schedule", default="balanced", choices=["rr", "balanced", "xcd"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="headline line only")
     args = ap.parse_args()
@@ -198,14 +221,17 @@ def main() -> int:
                 continue
             r, _ = run_workload(args.workload, sch, args.steps, args.warmup, w=w)
             extra[f"{args.workload}_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_worker_cost")}
-        w5 = None
-        for sch in ("rr", "balanced", "xcd"):
-            r, w5 = run_workload("c5", sch, args.steps, args.warmup, w=w5)
-            extra[f"c5_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_worker_cost", "moved_bytes")}
-        del w5
+        for cfg in ("c3", "c4", "c5"):
+            wk = None
+            for sch in ("rr", "balanced", "xcd"):
+                r, wk = run_workload(cfg, sch, args.steps, args.warmup, w=wk)
+                extra[f"{cfg}_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "max_over_mean_worker_cost",
+                                                        "moved_bytes", "n_items")}
+            del wk
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
     achieved = head["launch_gbs"]
+    prof, current = _profiled(head["workload"], args.schedule)
     line = {
         "metric": METRIC,
         "value": round(head["gbs"], 2),
@@ -228,7 +254,10 @@ def main() -> int:
         "pct_of_peak": round(100.0 * head["gbs"] / PEAK_HBM_GBS, 2),
         "slices_per_s": round(head["slices_per_s"], 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": prof["traffic_bytes_per_launch"] if (prof and current) else None,
+                     "traffic_over_algorithmic": round(prof["traffic_over_algorithmic"], 5) if (prof and current) else None,
+                     "rocprof_avg_us": round(prof["avg_ns"] / 1e3, 2) if (prof and current) else None,
                      "kernel": "bsm_softmax_kernel",
                      "launch_us_avg": round(head["launch_ms_avg"] * 1e3, 2),
                      "launch_us_median_single": round(head["launch_ms_median"] * 1e3, 2),

@@ -209,7 +209,7 @@ def _check_sizes(extent: int, *tensors) -> None:
                              f"extent ({extent} elements)")
 
 
-def bsm_softmax(x, out, rows, cols, slice_offsets=None, batch=None, schedule="xcd",
+def bsm_softmax(x, out, rows, cols, slice_offsets=None, batch=None, schedule="balanced",
                 stream=None):
     """out = row softmax of x over every slice (see bsm.h). x, out: contiguous GPU tensors of
     float32 or bfloat16 (out may be x). Returns out."""
@@ -253,7 +253,7 @@ class Plan:
             pass
 
 
-def bsm_plan_create(rows, cols, slice_offsets=None, batch=None, dtype="f32", schedule="xcd",
+def bsm_plan_create(rows, cols, slice_offsets=None, batch=None, dtype="f32", schedule="balanced",
                     home_xcd=None, topology=None, device=0) -> Plan:
     """Build a plan. `topology`: None, a bsm_topology or a dict of its fields. device=-1 makes
     a host-only plan (needs a topology) that can be described and exported but not run."""

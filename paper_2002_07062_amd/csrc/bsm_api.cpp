@@ -70,7 +70,10 @@ struct DeviceGuard {
     }
 };
 
-constexpr int kDefaultWgPerCu = 2;
+// Waves per CU that measured fastest on MI355X: 8 for fp32 rows (more waves only add DRAM
+// page conflicts), 16 for bf16 rows, which carry twice the ALU work per byte and need the
+// extra waves to overlap it with memory.
+int default_waves_per_cu(bsm_dtype d) { return d == BSM_BF16 ? 16 : 8; }
 constexpr int kDefaultPieceBytes = 8192;
 constexpr float kDefaultItemCost = 1024.0f;
 constexpr float kDefaultRowCost = 64.0f;
@@ -81,10 +84,9 @@ bool valid_dtype(int d) { return d == BSM_F32 || d == BSM_BF16; }
 bool valid_schedule(int s) { return s == BSM_SCHED_RR || s == BSM_SCHED_BALANCED || s == BSM_SCHED_XCD; }
 
 // Defaults for a device: all CUs, the runtime's XCD count, 256-thread workgroups.  wg_per_cu
-// is left 0: a plan uses kDefaultWgPerCu, capped by the occupancy of the kernel instance it
-// launches, so the persistent grid is always fully resident and the static table is what
-// actually runs.  Two 4-wave workgroups per CU (8 waves) measured fastest for streaming rows
-// on MI355X: more waves only add DRAM page conflicts.
+// is left 0: a plan picks it from the element type (default_waves_per_cu), capped by the
+// occupancy of the kernel instance it launches, so the persistent grid is always fully
+// resident and the static table is what actually runs.
 bsm_status default_topology(int device, bsm_topology* t) {
     hipDeviceProp_t prop;
     hipError_t e = hipGetDeviceProperties(&prop, device);
@@ -132,15 +134,16 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         if (user->item_cost > 0.0f) t.item_cost = user->item_cost;
         if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
     }
-    if (t.wg_per_cu <= 0) {
-        t.wg_per_cu = kDefaultWgPerCu;
-        if (device >= 0 && t.wg_threads >= 64 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
+    if (t.wg_per_cu <= 0 && t.wg_threads >= 64) {
+        const int want = std::max(1, default_waves_per_cu(dtype) / (t.wg_threads / 64));
+        t.wg_per_cu = want;
+        if (device >= 0 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
             int n = 0;
             DeviceGuard g;
             hipError_t e = g.enter(device);
             if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, &n);
             if (e != hipSuccess) return hip_fail(e, "occupancy query");
-            t.wg_per_cu = std::max(1, std::min(kDefaultWgPerCu, n));
+            t.wg_per_cu = std::max(1, std::min(want, n));
         }
     }
     out->n_cu = t.n_cu;

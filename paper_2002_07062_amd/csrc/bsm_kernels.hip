@@ -202,10 +202,9 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
                                              int64_t base, int cols, int nrows, int reps,
                                              int64_t stride, int wave, int nwaves, int lane64) {
     constexpr int RPW = 64 / G;
-    // Rows in flight per group: about kValuesInFlight values per lane for aligned rows; one
-    // row for the element-wise path, whose per-element addresses cost registers.
-    constexpr int K = V * E::kEPV;
-    constexpr int U = (!VEC || K >= bsm::kValuesInFlight) ? 1 : bsm::kValuesInFlight / K;
+    // Rows in flight per group: kVecsInFlight 16-byte loads per lane for aligned rows; one row
+    // for the element-wise path, whose per-element addresses cost registers.
+    constexpr int U = bsm::rows_per_group_in_flight(V, VEC);
     const int sub = lane64 / G;
     const int lane = lane64 % G;
     const int step = nwaves * RPW;

@@ -7,8 +7,8 @@
 namespace bsm {
 
 constexpr int kWave = 64;
-constexpr int kVecBytes = 16;          // one 128-bit access
-constexpr int kValuesInFlight = 16;    // fp32 values per lane a wave keeps in flight
+constexpr int kVecBytes = 16;   // one 128-bit access
+constexpr int kVecsInFlight = 4;  // 16-byte loads per lane a wave keeps in flight (any dtype)
 
 // Lanes per row G and 16-byte vectors per lane V for a row of `nvec` vectors.  Rows beyond
 // 64 * max_v vectors take the two-pass path (G = 64, V = 0).
@@ -27,11 +27,15 @@ constexpr Tile tile_for(int64_t nvec, int max_v) {
     return Tile{64, 0};
 }
 
-// Rows a wave keeps in flight per step: U rows per group of G lanes, 64/G groups per wave.
-constexpr int rows_in_flight(int G, int V, int elems_per_vec, bool vec_path) {
-    const int k = V * elems_per_vec;
-    const int u = (!vec_path || V == 0 || k >= kValuesInFlight) ? 1 : kValuesInFlight / k;
-    return (kWave / G) * u;
+// Rows per group a wave keeps in flight: enough rows that each lane has kVecsInFlight 16-byte
+// loads outstanding (one row for the element-wise and two-pass paths).
+constexpr int rows_per_group_in_flight(int V, bool vec_path) {
+    return (!vec_path || V == 0 || V >= kVecsInFlight) ? 1 : kVecsInFlight / V;
+}
+
+// Rows a wave keeps in flight per step: that many rows per group of G lanes, 64/G groups.
+constexpr int rows_in_flight(int G, int V, bool vec_path) {
+    return (kWave / G) * rows_per_group_in_flight(V, vec_path);
 }
 
 // Largest register tile (vectors per lane) a kernel class carries.
@@ -43,7 +47,7 @@ constexpr int max_v_of_class(int kernel_class) {
 constexpr int wave_step_rows(int64_t cols, int elem_bytes, int kernel_class) {
     const int64_t nvec = (cols * elem_bytes + kVecBytes - 1) / kVecBytes;
     const Tile t = tile_for(nvec, max_v_of_class(kernel_class));
-    return rows_in_flight(t.G, t.V, kVecBytes / elem_bytes, true);
+    return rows_in_flight(t.G, t.V, true);
 }
 
 }  // namespace bsm
