@@ -158,6 +158,41 @@ def run_workload(name, schedule, steps, warmup, rotate=None, w=None):
     return res, w
 
 
+def trace_stats(w, schedule):
+    """One traced launch (outside any timed region): per-wave busy intervals from the kernel's
+    constant-rate clock give the makespan, the mean wave busy time, the fraction of wave-time
+    idle before the last wave ends, and the busiest XCD's time."""
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    hz = bsm.bsm_device_info(0)["wall_clock_hz"] or 100_000_000
+    x = _to_device(w)
+    out = torch.empty_like(x)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule=schedule, device=0)
+    st = bsm.bsm_plan_describe(plan)
+    trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device=x.device)
+    bsm.bsm_plan_execute(plan, x, out)  # warm
+    bsm.bsm_plan_execute(plan, x, out, trace=trace)
+    torch.cuda.synchronize()
+    plan.destroy()
+    rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+    busy = (rec["t_end"] - rec["t_start"]).astype(np.float64) / hz * 1e6
+    t0, t1 = int(rec["t_start"].min()), int(rec["t_end"].max())
+    span = (t1 - t0) / hz * 1e6
+    per_xcd = {}
+    for x_id in np.unique(rec["xcc_id"]):
+        m = rec["xcc_id"] == x_id
+        per_xcd[int(x_id)] = round(float((rec["t_end"][m].max() - t0) / hz * 1e6), 2)
+    working = rec["rows"] > 0
+    return {"makespan_us": round(span, 2), "mean_wave_busy_us": round(float(busy.mean()), 2),
+            "idle_frac": round(1.0 - float(busy.sum()) / (len(busy) * span), 4) if span > 0 else 0.0,
+            "waves_with_work": int(working.sum()), "waves": int(len(rec)),
+            "xcd_finish_us": per_xcd}
+
+
 def cpu_baseline(w):
     import oracle
 
@@ -221,14 +256,20 @@ def main() -> int:
                 continue
             r, _ = run_workload(args.workload, sch, args.steps, args.warmup, w=w)
             extra[f"{args.workload}_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_worker_cost")}
+        for sch in ("rr", "balanced", "xcd"):
+            if sch != args.schedule:
+                extra[f"{args.workload}_{sch}"]["trace"] = trace_stats(w, sch)
         for cfg in ("c3", "c4", "c5"):
             wk = None
             for sch in ("rr", "balanced", "xcd"):
                 r, wk = run_workload(cfg, sch, args.steps, args.warmup, w=wk)
                 extra[f"{cfg}_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "max_over_mean_worker_cost",
                                                         "moved_bytes", "n_items")}
+                if cfg == "c5":
+                    extra[f"{cfg}_{sch}"]["trace"] = trace_stats(wk, sch)
             del wk
 
+    head_trace = None if args.no_extra else trace_stats(w, args.schedule)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
     achieved = head["launch_gbs"]
     prof, current = _profiled(head["workload"], args.schedule)
@@ -264,6 +305,7 @@ def main() -> int:
                      "launch_us_p10_single": round(head["launch_ms_p10"] * 1e3, 2),
                      "launch_us_p90_single": round(head["launch_ms_p90"] * 1e3, 2),
                      "bytes_per_launch": head["algorithmic_bytes"]},
+        "trace": head_trace,
         "copy_ceiling": {"gbs": round(copy_gbs, 2), "us": round(copy_ms * 1e3, 2),
                          "softmax_pct_of_copy": round(100.0 * head["gbs"] / copy_gbs, 2)},
         "cpu_baseline": cpu,
