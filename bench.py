@@ -120,7 +120,7 @@ def time_copy(xs, outs, nbytes, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def run_workload(name, schedule, steps, warmup, rotate=None, w=None):
+def run_workload(name, schedule, steps, warmup, rotate=None, w=None, topology=None):
     """Bench one (workload, schedule). Returns a dict of measurements."""
     import torch
 
@@ -135,7 +135,7 @@ def run_workload(name, schedule, steps, warmup, rotate=None, w=None):
     outs = [torch.empty_like(x0) for _ in range(n_pairs)]
     t_plan = time.perf_counter()
     plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
-                               schedule=schedule, device=0)
+                               schedule=schedule, topology=topology, device=0)
     plan_ms = (time.perf_counter() - t_plan) * 1e3
     st = bsm.bsm_plan_describe(plan)
     region_ms, launch_ms = time_plan(plan, xs, outs, steps, warmup)
@@ -152,7 +152,8 @@ def run_workload(name, schedule, steps, warmup, rotate=None, w=None):
         n_wg=st["n_wg"], wg_threads=st["wg_threads"], n_items=st["n_items"],
         kernel_class=st["kernel_class"], n_workers=st["n_workers"], n_rounds=st["n_rounds"],
         max_over_mean_worker_cost=st["max_worker_cost"] / max(st["mean_worker_cost"], 1e-9),
-        moved_bytes=st["moved_bytes"], buffers_rotated=n_pairs)
+        moved_bytes=st["moved_bytes"], buffers_rotated=n_pairs,
+        lds_bytes_per_wave=st["lds_bytes_per_wave"])
     del xs, outs, x0
     torch.cuda.empty_cache()
     return res, w
@@ -268,6 +269,11 @@ def main() -> int:
                 if cfg == "c5":
                     extra[f"{cfg}_{sch}"]["trace"] = trace_stats(wk, sch)
             del wk
+        # rows longer than the register tile: 4096-element rows fit a wave's LDS region and
+        # are read once; 8192-element rows take the two-pass path (1.25x the traffic)
+        for name in ("long4k", "long"):
+            r, _ = run_workload(name, "balanced", args.steps, args.warmup)
+            extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "lds_bytes_per_wave")}
 
     head_trace = None if args.no_extra else trace_stats(w, args.schedule)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)

@@ -117,6 +117,8 @@ typedef struct bsm_plan_stats {
     int32_t n_overlap;         /* XCD: slices straddling two or more virtual banks */
     int32_t max_cols;          /* longest row */
     int32_t kernel_class;      /* which kernel instance the plan launches (internal) */
+    int32_t lds_bytes_per_wave; /* LDS each wave stages long rows in (0: two-pass path only) */
+    int32_t reserved0;
     double max_worker_cost;    /* planner cost of the most loaded worker */
     double mean_worker_cost;   /* total planner cost / n_workers */
     double max_row_cost;       /* planner cost of the most expensive single row */
@@ -145,6 +147,7 @@ typedef struct bsm_device_props {
     int32_t wave_size;
     int32_t max_threads_per_cu;
     int64_t lds_bytes_per_cu;
+    int64_t lds_bytes_per_wg;  /* largest LDS allocation of one workgroup */
     int64_t l2_bytes;          /* as reported by the runtime */
     int64_t hbm_bytes;
     int64_t wall_clock_hz;     /* rate of the counter in bsm_trace_rec */

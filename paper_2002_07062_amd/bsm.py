@@ -69,6 +69,7 @@ class bsm_plan_stats(ctypes.Structure):
                 ("wg_threads", ctypes.c_int32), ("schedule", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("n_overlap", ctypes.c_int32),
                 ("max_cols", ctypes.c_int32), ("kernel_class", ctypes.c_int32),
+                ("lds_bytes_per_wave", ctypes.c_int32), ("reserved0", ctypes.c_int32),
                 ("max_worker_cost", ctypes.c_double), ("mean_worker_cost", ctypes.c_double),
                 ("max_row_cost", ctypes.c_double), ("moved_cost", ctypes.c_double),
                 ("min_moved_cost", ctypes.c_double), ("build_us", ctypes.c_double),
@@ -80,7 +81,8 @@ class bsm_plan_stats(ctypes.Structure):
 class bsm_device_props(ctypes.Structure):
     _fields_ = [("n_cu", ctypes.c_int32), ("n_xcd", ctypes.c_int32),
                 ("wave_size", ctypes.c_int32), ("max_threads_per_cu", ctypes.c_int32),
-                ("lds_bytes_per_cu", ctypes.c_int64), ("l2_bytes", ctypes.c_int64),
+                ("lds_bytes_per_cu", ctypes.c_int64), ("lds_bytes_per_wg", ctypes.c_int64),
+                ("l2_bytes", ctypes.c_int64),
                 ("hbm_bytes", ctypes.c_int64), ("wall_clock_hz", ctypes.c_int64),
                 ("peak_hbm_gbs", ctypes.c_double), ("clock_khz", ctypes.c_int32),
                 ("arch", ctypes.c_char * 64)]

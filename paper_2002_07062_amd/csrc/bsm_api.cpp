@@ -26,6 +26,7 @@ struct bsm_plan_s {
     bsm::Geometry geo;
     bsm::Table table;
     int kernel_class = 0;
+    int lds_floats_per_wave = 0;  // long-row staging (kernel class 4 on a device)
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
     const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
@@ -72,8 +73,29 @@ struct DeviceGuard {
 
 // Waves per CU that measured fastest on MI355X: 8 for fp32 rows (more waves only add DRAM
 // page conflicts), 16 for bf16 rows, which carry twice the ALU work per byte and need the
-// extra waves to overlap it with memory.
-int default_waves_per_cu(bsm_dtype d) { return d == BSM_BF16 ? 16 : 8; }
+// extra waves to overlap it with memory.  Plans with rows beyond the register tile also run 8
+// waves per CU, each staging rows of up to an eighth of the CU's LDS (20 KiB: 5120 fp32): with
+// fewer waves the staged rows' LDS passes leave HBM idle and the two-pass path wins (measured:
+// 4096-element rows 4.29 TB/s staged at 8 waves vs 3.77 two-pass; staging 8192-element rows at
+// 4 waves/CU, 3.0 TB/s, loses to two-pass at 8 waves, 3.8).
+constexpr int kLongRowClass = 4;
+int default_waves_per_cu(bsm_dtype d, int kclass) {
+    if (kclass >= kLongRowClass) return 8;
+    return d == BSM_BF16 ? 16 : 8;
+}
+
+// Smallest LDS region worth staging a row in (shorter rows never reach the long-row path).
+constexpr int64_t kMinStageBytes = 8192;
+
+// LDS per wave for long-row staging: the CU's LDS split over its resident waves, capped by the
+// per-workgroup limit, rounded down to 64 bytes.
+int64_t lds_bytes_per_wave(const hipDeviceProp_t& prop, const bsm::Topology& t) {
+    const int64_t per_cu = static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor);
+    const int64_t per_wg = std::min<int64_t>(per_cu / std::max(1, t.wg_per_cu),
+                                             static_cast<int64_t>(prop.sharedMemPerBlock));
+    const int64_t per_wave = (per_wg / t.waves_per_wg()) & ~static_cast<int64_t>(63);
+    return per_wave >= kMinStageBytes ? per_wave : 0;
+}
 constexpr int kDefaultPieceBytes = 8192;
 constexpr float kDefaultItemCost = 1024.0f;
 constexpr float kDefaultRowCost = 64.0f;
@@ -135,13 +157,22 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
     }
     if (t.wg_per_cu <= 0 && t.wg_threads >= 64) {
-        const int want = std::max(1, default_waves_per_cu(dtype) / (t.wg_threads / 64));
+        const int want = std::max(1, default_waves_per_cu(dtype, kclass) / (t.wg_threads / 64));
         t.wg_per_cu = want;
         if (device >= 0 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
             int n = 0;
             DeviceGuard g;
             hipError_t e = g.enter(device);
-            if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, &n);
+            hipDeviceProp_t prop;
+            if (e == hipSuccess) e = hipGetDeviceProperties(&prop, device);
+            size_t lds = 0;
+            if (e == hipSuccess && kclass >= kLongRowClass) {
+                bsm::Topology probe;
+                probe.wg_per_cu = want;
+                probe.wg_threads = t.wg_threads;
+                lds = static_cast<size_t>(lds_bytes_per_wave(prop, probe)) * (t.wg_threads / 64);
+            }
+            if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, lds, &n);
             if (e != hipSuccess) return hip_fail(e, "occupancy query");
             t.wg_per_cu = std::max(1, std::min(want, n));
         }
@@ -211,6 +242,14 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         DeviceGuard g;
         hipError_t e = g.enter(device);
         if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+        if (p->kernel_class >= kLongRowClass) {
+            hipDeviceProp_t prop;
+            e = hipGetDeviceProperties(&prop, device);
+            if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+            const int64_t b = lds_bytes_per_wave(prop, p->topo);
+            p->lds_floats_per_wave = static_cast<int>(b / static_cast<int64_t>(sizeof(float)));
+            p->table.stats.lds_bytes_per_wave = static_cast<int32_t>(b);
+        }
         const size_t ptr_bytes = p->table.worker_ptr.size() * sizeof(int32_t);
         const size_t items_at = (ptr_bytes + 255) & ~static_cast<size_t>(255);
         const size_t bytes = items_at + std::max<size_t>(p->table.items.size(), 1) * sizeof(bsm_item);
@@ -256,7 +295,8 @@ bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, voi
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
     e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_worker_ptr, p->d_items,
-                            p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0, trace, s);
+                            p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0,
+                            p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     e = hipEventRecord(p->last_use, s);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -410,6 +450,7 @@ bsm_status bsm_device_info(int device, bsm_device_props* info) {
     info->wave_size = prop.warpSize;
     info->max_threads_per_cu = prop.maxThreadsPerMultiProcessor;
     info->lds_bytes_per_cu = static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor);
+    info->lds_bytes_per_wg = static_cast<int64_t>(prop.sharedMemPerBlock);
     info->l2_bytes = prop.l2CacheSize;
     info->hbm_bytes = static_cast<int64_t>(prop.totalGlobalMem);
     info->wall_clock_hz = static_cast<int64_t>(wall) * 1000;  // attribute is in kHz

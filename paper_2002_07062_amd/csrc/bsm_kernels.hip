@@ -223,38 +223,179 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
     return done;
 }
 
-// Rows longer than the register tile: one wave per row, two passes.  Pass 1 keeps a per-lane
-// running max and a sum rescaled whenever the max grows; the lanes' pairs are then merged.
-// Pass 2 re-reads the row and writes e * (1/S).
+// Rows longer than the register tile, one wave per row, in chunks of CH 16-byte vectors per
+// lane (32 values) so each lane keeps CH loads in flight; the rare element-wise path (rows not
+// 16-byte aligned) uses chunks of 8 elements, whose per-element addresses cost registers.
+//
+// When the row fits the wave's LDS region (`cap` floats, given to plans with long rows), it is
+// read from HBM once: pass 1 keeps a per-lane max while staging the values in LDS, pass 2
+// turns the staged values into e = 2^((x - M) log2 e) in place and sums them, pass 3 writes
+// e * (1/S).  Every lane re-reads only what it wrote itself, so no barrier is needed.
+//
+// Otherwise two passes over HBM: pass 1 keeps a per-lane running max and a sum rescaled
+// whenever a chunk raises the max, the lanes' pairs are merged, pass 2 re-reads the row and
+// writes e * (1/S) (1.5x the bytes of the staged path).
 template <class E, bool VEC>
-__device__ __forceinline__ void long_row(const typename E::T* src, typename E::T* dst, int cols,
-                                      int lane) {
-    constexpr int EPV = E::kEPV;
-    float m = kNegInf, s = 0.0f;
-    if constexpr (VEC) {
-        const int nvec = cols / EPV;
-        for (int vi = lane; vi < nvec; vi += 64) {
-            float x[EPV];
-            E::load_vec(src + vi * EPV, x);
-            const float cm = lane_reduce<EPV, OpMax>(x);
-            if (cm > m) {
-                s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
-                m = cm;
-            }
-            if (m != kNegInf) {
+struct LongRow {
+    using T = typename E::T;
+    static constexpr int EPV = E::kEPV;
+    static constexpr int CH = 32 / EPV;        // vectors per lane per chunk (aligned rows)
+    static constexpr int K = VEC ? CH * EPV : 8;  // values per lane per chunk
+
+    // Loads chunk c0 (vector index of the lane's first vector, stride 64) into x; vectors past
+    // the row are -inf.  Element-wise variant: elements j0 + 64 k.
+    __device__ __forceinline__ static void load(const T* src, int cols, int first, float* x) {
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
 #pragma unroll
-                for (int i = 0; i < EPV; ++i) x[i] = __builtin_amdgcn_exp2f((x[i] - m) * kLog2e);
-                s += lane_reduce<EPV, OpAdd>(x);
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+                if (vi < nvec) {
+                    E::load_vec(src + vi * EPV, x + c * EPV);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < EPV; ++i) x[c * EPV + i] = kNegInf;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = first + k * 64;
+                x[k] = j < cols ? E::load1(src + j) : kNegInf;
             }
         }
-    } else {
-        for (int j = lane; j < cols; j += 64) {
-            const float x = E::load1(src + j);
-            if (x > m) {
-                s *= __builtin_amdgcn_exp2f((m - x) * kLog2e);
-                m = x;
+    }
+    __device__ __forceinline__ static void store(T* dst, int cols, int first, const float* y) {
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+                if (vi < nvec) E::store_vec(dst + vi * EPV, y + c * EPV);
             }
-            if (m != kNegInf) s += __builtin_amdgcn_exp2f((x - m) * kLog2e);
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = first + k * 64;
+                if (j < cols) E::store1(dst + j, y[k]);
+            }
+        }
+    }
+    static constexpr int kStep = VEC ? CH * 64 : K * 64;
+    __device__ __forceinline__ static int extent(int cols) { return VEC ? cols / EPV : cols; }
+};
+
+template <class E, bool VEC, bool STAGE>
+__device__ __forceinline__ void long_row(const typename E::T* src, typename E::T* dst, int cols,
+                                         int lane, float* lds, int cap) {
+    using L = LongRow<E, VEC>;
+    constexpr int K = L::K;
+    const int n = L::extent(cols);
+    const int step = L::kStep;
+    if (STAGE && cols <= cap) {
+        // LDS holds the row as floats at their element index; aligned rows move whole 16-byte
+        // vectors (consecutive lanes on consecutive 16 bytes: no bank conflicts).
+        constexpr int EPV = E::kEPV;
+        float m = kNegInf;
+        for (int first = lane; first < n; first += step) {
+            float x[K];
+            L::load(src, cols, first, x);
+            m = __builtin_fmaxf(m, lane_reduce<K, OpMax>(x));
+            if constexpr (VEC) {
+#pragma unroll
+                for (int c = 0; c < L::CH; ++c) {
+                    const int vi = first + c * 64;
+                    if (vi < n) {
+#pragma unroll
+                        for (int i = 0; i < EPV; i += 4)
+                            *reinterpret_cast<f32x4*>(lds + vi * EPV + i) =
+                                f32x4{x[c * EPV + i], x[c * EPV + i + 1], x[c * EPV + i + 2], x[c * EPV + i + 3]};
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const int j = first + k * 64;
+                    if (j < cols) lds[j] = x[k];
+                }
+            }
+        }
+        const float M = group_reduce<64, OpMax>(m);
+        const float Ms = (M == kNegInf) ? 0.0f : M;
+        float s = 0.0f;
+        for (int first = lane; first < n; first += step) {
+            float e[K];
+            if constexpr (VEC) {
+#pragma unroll
+                for (int c = 0; c < L::CH; ++c) {
+                    const int vi = first + c * 64;
+#pragma unroll
+                    for (int i = 0; i < EPV; i += 4) {
+                        f32x4 v = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
+                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
+                        v.x = __builtin_amdgcn_exp2f((v.x - Ms) * kLog2e);
+                        v.y = __builtin_amdgcn_exp2f((v.y - Ms) * kLog2e);
+                        v.z = __builtin_amdgcn_exp2f((v.z - Ms) * kLog2e);
+                        v.w = __builtin_amdgcn_exp2f((v.w - Ms) * kLog2e);
+                        e[c * EPV + i] = v.x;
+                        e[c * EPV + i + 1] = v.y;
+                        e[c * EPV + i + 2] = v.z;
+                        e[c * EPV + i + 3] = v.w;
+                        if (vi < n) *reinterpret_cast<f32x4*>(lds + vi * EPV + i) = v;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const int j = first + k * 64;
+                    e[k] = j < cols ? __builtin_amdgcn_exp2f((lds[j] - Ms) * kLog2e) : 0.0f;
+                    if (j < cols) lds[j] = e[k];
+                }
+            }
+            s += lane_reduce<K, OpAdd>(e);
+        }
+        const float S = group_reduce<64, OpAdd>(s);
+        const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
+        for (int first = lane; first < n; first += step) {
+            float y[K];
+            if constexpr (VEC) {
+#pragma unroll
+                for (int c = 0; c < L::CH; ++c) {
+                    const int vi = first + c * 64;
+#pragma unroll
+                    for (int i = 0; i < EPV; i += 4) {
+                        f32x4 v = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
+                        y[c * EPV + i] = v.x * inv;
+                        y[c * EPV + i + 1] = v.y * inv;
+                        y[c * EPV + i + 2] = v.z * inv;
+                        y[c * EPV + i + 3] = v.w * inv;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const int j = first + k * 64;
+                    y[k] = j < cols ? lds[j] * inv : 0.0f;
+                }
+            }
+            L::store(dst, cols, first, y);
+        }
+        return;
+    }
+    float m = kNegInf, s = 0.0f;
+    for (int first = lane; first < n; first += step) {
+        float x[K];
+        L::load(src, cols, first, x);
+        const float cm = lane_reduce<K, OpMax>(x);
+        if (cm > m) {
+            s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
+            m = cm;
+        }
+        if (m != kNegInf) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - m) * kLog2e);
+            s += lane_reduce<K, OpAdd>(x);
         }
     }
     const float M = group_reduce<64, OpMax>(m);
@@ -262,18 +403,12 @@ __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T
     const float scale = (m == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f((m - Ms) * kLog2e);
     const float S = group_reduce<64, OpAdd>(s * scale);
     const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
-    if constexpr (VEC) {
-        const int nvec = cols / EPV;
-        for (int vi = lane; vi < nvec; vi += 64) {
-            float x[EPV];
-            E::load_vec(src + vi * EPV, x);
+    for (int first = lane; first < n; first += step) {
+        float x[K];
+        L::load(src, cols, first, x);
 #pragma unroll
-            for (int i = 0; i < EPV; ++i) x[i] = __builtin_amdgcn_exp2f((x[i] - Ms) * kLog2e) * inv;
-            E::store_vec(dst + vi * EPV, x);
-        }
-    } else {
-        for (int j = lane; j < cols; j += 64)
-            E::store1(dst + j, __builtin_amdgcn_exp2f((E::load1(src + j) - Ms) * kLog2e) * inv);
+        for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - Ms) * kLog2e) * inv;
+        L::store(dst, cols, first, x);
     }
 }
 
@@ -282,7 +417,7 @@ template <class E, int KCLASS, bool VEC>
 __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
                                                   int64_t base, int cols, int nrows, int reps,
                                                   int64_t stride, int wave, int nwaves,
-                                                  int lane64) {
+                                                  int lane64, float* lds, int cap) {
     const int nvec = (cols + E::kEPV - 1) / E::kEPV;
 #define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     if (nvec <= 16) return BSM_RUN(16, 1);
@@ -304,7 +439,8 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
         for (int k = 0; k < reps; ++k) {
             for (int r = wave; r < nrows; r += nwaves) {
                 const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
-                long_row<E, VEC>(in + o, out + o, cols, lane64);
+                // only the long-row class is launched with LDS to stage rows in
+                long_row<E, VEC, (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
                 ++done;
             }
         }
@@ -319,7 +455,8 @@ template <class E, int KCLASS>
 __global__ void __launch_bounds__(1024)
 bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
                    const bsm_item* __restrict__ items, int base_aligned, int per_wave,
-                   bsm_trace_rec* __restrict__ trace) {
+                   int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
+    extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int nwaves = static_cast<int>(blockDim.x) >> 6;
@@ -328,6 +465,7 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
     const int worker = per_wave ? w * nwaves + wave : w;
     const int my_wave = per_wave ? 0 : wave;
     const int my_nwaves = per_wave ? 1 : nwaves;
+    float* const lds = bsm_lds + wave * lds_floats_per_wave;
     uint32_t rows = 0;
     const int i0 = worker_ptr[worker];
     const int i1 = worker_ptr[worker + 1];
@@ -341,10 +479,12 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
                          ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
         if (vec)
             rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, reps, stride,
-                                                   my_wave, my_nwaves, lane64);
+                                                   my_wave, my_nwaves, lane64, lds,
+                                                   lds_floats_per_wave);
         else
             rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, reps, stride,
-                                                    my_wave, my_nwaves, lane64);
+                                                    my_wave, my_nwaves, lane64, lds,
+                                                    lds_floats_per_wave);
     }
     if (trace && lane64 == 0) {
         bsm_trace_rec rec;
@@ -379,19 +519,21 @@ __global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char
 
 template <class E, int KCLASS>
 hipError_t launch_t(const void* in, void* out, const int32_t* worker_ptr, const bsm_item* items,
-                    int n_wg, int wg_threads, int aligned, int per_wave, void* trace,
-                    hipStream_t stream) {
-    hipLaunchKernelGGL((bsm_softmax_kernel<E, KCLASS>), dim3(n_wg), dim3(wg_threads), 0, stream,
-                       static_cast<const typename E::T*>(in), static_cast<typename E::T*>(out),
-                       worker_ptr, items, aligned, per_wave, static_cast<bsm_trace_rec*>(trace));
+                    int n_wg, int wg_threads, int aligned, int per_wave, int lds_floats,
+                    void* trace, hipStream_t stream) {
+    const size_t lds_bytes = static_cast<size_t>(lds_floats) * sizeof(float) * (wg_threads / 64);
+    hipLaunchKernelGGL((bsm_softmax_kernel<E, KCLASS>), dim3(n_wg), dim3(wg_threads), lds_bytes,
+                       stream, static_cast<const typename E::T*>(in),
+                       static_cast<typename E::T*>(out), worker_ptr, items, aligned, per_wave,
+                       lds_floats, static_cast<bsm_trace_rec*>(trace));
     return hipGetLastError();
 }
 
 template <class E>
 hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* worker_ptr,
                         const bsm_item* items, int n_wg, int wg_threads, int aligned, int per_wave,
-                        void* trace, hipStream_t stream) {
-#define BSM_LAUNCH(K) launch_t<E, K>(in, out, worker_ptr, items, n_wg, wg_threads, aligned, per_wave, trace, stream)
+                        int lds_floats, void* trace, hipStream_t stream) {
+#define BSM_LAUNCH(K) launch_t<E, K>(in, out, worker_ptr, items, n_wg, wg_threads, aligned, per_wave, lds_floats, trace, stream)
     switch (kclass) {
         case 0: return BSM_LAUNCH(0);
         case 1: return BSM_LAUNCH(1);
@@ -417,17 +559,19 @@ int kernel_class_for(int32_t max_cols, int elem_bytes) {
 
 hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
                           const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg,
-                          int wg_threads, int per_wave, void* trace, hipStream_t stream) {
+                          int wg_threads, int per_wave, int lds_floats_per_wave, void* trace,
+                          hipStream_t stream) {
     const int aligned = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
     (void)hipGetLastError();  // start from a clean error state
     if (dtype == BSM_BF16)
         return launch_dtype<BF16>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
-                                  aligned, per_wave, trace, stream);
+                                  aligned, per_wave, lds_floats_per_wave, trace, stream);
     return launch_dtype<F32>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
-                             aligned, per_wave, trace, stream);
+                             aligned, per_wave, lds_floats_per_wave, trace, stream);
 }
 
-hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads, int* n) {
+hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
+                               size_t dyn_lds_bytes, int* n) {
     const void* fn = nullptr;
     if (dtype == BSM_BF16) {
         switch (kernel_class) {
@@ -446,7 +590,7 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads
             default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 4>); break;
         }
     }
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(n, fn, wg_threads, 0);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(n, fn, wg_threads, dyn_lds_bytes);
 }
 
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipStream_t stream) {

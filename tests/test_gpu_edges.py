@@ -44,14 +44,21 @@ def test_ragged_odd_cols_with_gaps(dtype, schedule):
     _check_ragged(w, schedule)
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_long_rows_two_pass_path(dtype):
+def test_long_rows_lds_staged_and_two_pass(dtype, schedule):
+    """Rows beyond the register tile: those that fit a wave's LDS region are staged there (read
+    once), longer ones take the two-pass path; both against the oracle."""
     cols = [2049, 4095, 4096, 4100, 8192, 10000, 40000, 100003]
     rows = [3, 2, 2, 3, 2, 2, 1, 1]
     w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=9, gap=8)
-    print(f"[long {dtype}]", flush=True)
-    bits, st = _check_ragged(w, "balanced")
+    print(f"[long {dtype} {schedule}]", flush=True)
+    bits, st = _check_ragged(w, schedule)
     assert st["kernel_class"] == 4
+    cap = st["lds_bytes_per_wave"] // 4
+    print(f"  LDS per wave {st['lds_bytes_per_wave']} B = rows up to {cap} staged", flush=True)
+    assert cap >= 2048
+    assert any(c <= cap for c in cols) and any(c > cap for c in cols)
 
 
 @pytest.mark.parametrize("shift", [1, 2, 3])
@@ -190,3 +197,94 @@ def test_device_info():
     print(d, flush=True)
     assert d["n_cu"] > 0 and d["wave_size"] == 64
     assert "gfx950" in d["arch"]
+
+
+def test_plan_cache_eviction_and_reuse():
+    """More distinct geometries than the one-shot cache holds: every call stays correct."""
+    bsm.bsm_cache_clear()
+    rng = np.random.default_rng(21)
+    cases = []
+    for i in range(40):
+        C = int(rng.integers(8, 700))
+        R = int(rng.integers(1, 9))
+        B = int(rng.integers(1, 6))
+        cases.append((B, R, C))
+    for rep in range(2):
+        for (B, R, C) in cases:
+            w = workloads.custom([R] * B, [C] * B, sigma=2.0, seed=B * 1000 + C)
+            x = to_device(w.x, "f32")
+            out = sentinel_like(x.numel(), "f32")
+            bsm.bsm_softmax(x, out, R, C, batch=B, schedule=SCHEDULES[(B + rep) % 3])
+            torch.cuda.synchronize()
+            ref = oracle.softmax(w.x, "f32", w.offsets[:-1], w.rows, w.cols)
+            compare(to_host_bits(out), ref, "f32")
+    bsm.bsm_cache_clear()
+
+
+def test_two_threads_two_streams():
+    """Plans built and run concurrently from two host threads on two streams."""
+    import threading
+
+    w = workloads.generate("c5", batch=48)
+    x = to_device(w.x, w.dtype)
+    ref, _ = run_plan(w, "balanced", x=x)
+    results, errors = {}, []
+
+    def work(k):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                out = torch.empty_like(x)
+                for _ in range(5):
+                    bsm.bsm_softmax(x, out, w.rows, w.cols, slice_offsets=w.offsets[:-1],
+                                    schedule="balanced")
+            s.synchronize()
+            results[k] = out
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    ts = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not errors, errors
+    for k in range(2):
+        assert torch.equal(results[k].view(torch.int32), ref.view(torch.int32))
+    bsm.bsm_cache_clear()
+
+
+def test_bf16_one_shot_ragged_all_schedules():
+    w = workloads.custom([5, 17, 3, 40], [520, 64, 1000, 8], dtype="bf16", sigma=3.0, seed=12,
+                         gap=8)
+    x = to_device(w.x, "bf16")
+    ref = oracle.softmax(w.x, "bf16", w.offsets[:-1], w.rows, w.cols)
+    mask = covered_mask(w.offsets[:-1], w.rows, w.cols, x.numel())
+    prev = None
+    for sch in SCHEDULES:
+        out = sentinel_like(x.numel(), "bf16")
+        bsm.bsm_softmax(x, out, w.rows, w.cols, slice_offsets=w.offsets[:-1], schedule=sch)
+        torch.cuda.synchronize()
+        bits = to_host_bits(out)
+        compare(bits, ref, "bf16", mask)
+        assert np.all(bits[~mask] == SENTINEL_BF16)
+        if prev is not None:
+            assert np.array_equal(prev, bits)
+        prev = bits
+    bsm.bsm_cache_clear()
+
+
+def test_explicit_stream_and_plan_reuse():
+    w = workloads.generate("c4", batch=64)
+    x = to_device(w.x, w.dtype)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[:-1], dtype="f32", schedule="xcd")
+    s = torch.cuda.Stream()
+    outs = [torch.empty_like(x) for _ in range(3)]
+    with torch.cuda.stream(s):
+        for o in outs:
+            bsm.bsm_plan_execute(plan, x, o)
+    s.synchronize()
+    plan.destroy()  # waits on the plan's last use
+    ref = oracle.softmax(w.x, "f32", w.offsets[:-1], w.rows, w.cols)
+    for o in outs:
+        compare(to_host_bits(o), ref, "f32")

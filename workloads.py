@@ -56,12 +56,20 @@ SPECS = {
         "c5_384_ragged_f32", 384, 0, 0, F32, 3.0, 5, ragged=(64, 1024, 8),
         doc="384 ragged fp32 slices, R_s and C_s independently uniform over multiples of 8 "
             "in [64, 1024], packed contiguously with int64 offsets, N(0,9)"),
+    # long rows (beyond the register tile): long-context attention scores
+    "long_128x64x4096_f32": Spec(
+        "long_128x64x4096_f32", 128, 64, 4096, F32, 3.0, 7,
+        doc="128 slices x 64x4096 fp32, N(0,9): rows that fit a wave's LDS region"),
+    "long_64x64x8192_f32": Spec(
+        "long_64x64x8192_f32", 64, 64, 8192, F32, 3.0, 6,
+        doc="64 slices x 64x8192 fp32, N(0,9): rows longer than one wave's register tile"),
 }
 
 # Short aliases used by the bench and the tests.
 ALIASES = {"c1": "c1_8x64x64_f32", "c2": "c2_384x512x512_f32",
            "c3": "c3_384x512x512_bf16_mask", "c4": "c4_16384x128x128_f32",
-           "c5": "c5_384_ragged_f32"}
+           "c5": "c5_384_ragged_f32", "long": "long_64x64x8192_f32",
+           "long4k": "long_128x64x4096_f32"}
 
 
 @dataclasses.dataclass
