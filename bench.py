@@ -34,7 +34,9 @@ PEAK_HBM_GBS = 8000.0   # MI355X published HBM3E bandwidth
 MALL_BYTES = 256 << 20  # last-level Infinity Cache; rotation keeps reuse distance above it
 
 
-KERNEL_SOURCES = ("paper_2002_07062_amd/csrc/bsm_kernels.hip", "paper_2002_07062_amd/csrc/bsm_tile.hpp")
+# device code of the kernel (launch wrappers excluded): a profile's counters stay valid while
+# these files are unchanged
+KERNEL_SOURCES = ("paper_2002_07062_amd/csrc/bsm_device.hpp", "paper_2002_07062_amd/csrc/bsm_tile.hpp")
 
 
 def _kernel_sha() -> str:

@@ -30,8 +30,11 @@ struct bsm_plan_s {
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
     const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
-    hipEvent_t last_use = nullptr;
+    hipEvent_t last_use = nullptr;  // recorded after every execution
     bool used = false;
+    hipStream_t last_stream = nullptr;
+    bool many_streams = false;      // executed on more than one stream since creation
+    std::mutex mu;                  // guards the launch + event bookkeeping above
 };
 
 namespace {
@@ -194,7 +197,10 @@ void free_device(bsm_plan p) {
     DeviceGuard g;
     if (g.enter(p->device) != hipSuccess) return;
     if (p->last_use) {
-        if (p->used) (void)hipEventSynchronize(p->last_use);
+        // The event marks the last execution on the last stream; executions on other streams
+        // may still be reading the table, so then wait for the whole device.
+        if (p->many_streams) (void)hipDeviceSynchronize();
+        else if (p->used) (void)hipEventSynchronize(p->last_use);
         (void)hipEventDestroy(p->last_use);
         p->last_use = nullptr;
     }
@@ -294,12 +300,15 @@ bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, voi
     hipError_t e = g.enter(p->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    std::lock_guard<std::mutex> lock(p->mu);
     e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_worker_ptr, p->d_items,
                             p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0,
                             p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     e = hipEventRecord(p->last_use, s);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (p->used && s != p->last_stream) p->many_streams = true;
+    p->last_stream = s;
     p->used = true;
     return BSM_OK;
 }

@@ -1,532 +1,29 @@
-// Persistent batched row-softmax kernels for gfx950 (CDNA4, wave64).
-//
-// One launch runs a grid of n_wg persistent workgroups.  Workgroup w walks the items
-// [wg_ptr[w], wg_ptr[w+1]) of the host-built work table (the paper's Patch<->Cluster mapping
-// table, Section 5: geometry is read per item, the instructions are the same for every patch).
-// Inside an item, rows are spread over the workgroup's waves; no barrier is ever needed
-// because every row is owned by one group of lanes of one wave.
-//
-// Per row (softmax over the row, the operation of the problem statement, Section 2):
-//   128-bit loads (fp32 or bf16 -> fp32 registers)  -> lane max -> group max (DPP, permlane)
-//   -> e = 2^((x - m) * log2 e) (v_exp_f32)          -> lane sum (pairwise) -> group sum
-//   -> y = e * (1/S)                                 -> RNE to bf16 if needed -> 128-bit stores
-// Reductions combine each lane with a partner that combines the same two values in the other
-// order; IEEE max and add are commutative, so every lane of a group ends with the same bits,
-// and a row's result depends only on its values and length, never on the schedule.
-//
-// A group of G lanes (16, 32 or 64) owns one row and holds V 16-byte vectors per lane, so a
-// wave covers 64/G rows at a time.  Rows longer than the register tile of the kernel class
-// use a two-pass online max/sum (reads the row twice).  Rows whose start or length is not
-// 16-byte aligned use element loads with the same lane layout while they fit one vector's
-// worth of elements per lane, and the two-pass path beyond that.  This is bandwidth-bound
-// work: no MFMA, no LDS.
+// Host launch wrappers of the persistent softmax and copy kernels (device code in
+// bsm_device.hpp).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 #include "bsm.h"
+#include "bsm_device.hpp"
 #include "bsm_launch.hpp"
-#include "bsm_tile.hpp"
 
 namespace {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-constexpr float kLog2e = 1.44269504088896340736f;
-constexpr float kNegInf = -__builtin_huge_valf();
-
-__device__ __forceinline__ float bits_f(unsigned v) { return __builtin_bit_cast(float, v); }
-__device__ __forceinline__ unsigned f_bits(float v) { return __builtin_bit_cast(unsigned, v); }
-
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __builtin_bit_cast(
-        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-
-struct OpMax {
-    __device__ __forceinline__ static float f(float a, float b) { return __builtin_fmaxf(a, b); }
-};
-struct OpAdd {
-    __device__ __forceinline__ static float f(float a, float b) { return a + b; }
-};
-
-// Reduction over aligned groups of G lanes; all lanes of a group end with identical bits.
-template <int G, class Op>
-__device__ __forceinline__ float group_reduce(float v) {
-    static_assert(G == 16 || G == 32 || G == 64, "group size");
-    v = Op::f(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]: partner lane ^ 1
-    v = Op::f(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]: partner lane ^ 2
-    v = Op::f(v, dpp<0x141>(v));  // row_half_mirror: partner in the other quad of 8
-    v = Op::f(v, dpp<0x140>(v));  // row_mirror: partner in the other half of the 16-lane row
-    if constexpr (G >= 32) {      // rows 2k and 2k+1 meet
-        auto p = __builtin_amdgcn_permlane16_swap(f_bits(v), f_bits(v), false, false);
-        v = Op::f(bits_f(p[0]), bits_f(p[1]));
-    }
-    if constexpr (G == 64) {      // the two 32-lane halves meet
-        auto p = __builtin_amdgcn_permlane32_swap(f_bits(v), f_bits(v), false, false);
-        v = Op::f(bits_f(p[0]), bits_f(p[1]));
-    }
-    return v;
-}
-
-// In-lane pairwise reduction of K values (K a power of two).
-template <int K, class Op>
-__device__ __forceinline__ float lane_reduce(const float* x) {
-    if constexpr (K == 1) {
-        return x[0];
-    } else {
-        float t[K / 2];
-#pragma unroll
-        for (int i = 0; i < K / 2; ++i) t[i] = Op::f(x[2 * i], x[2 * i + 1]);
-        return lane_reduce<K / 2, Op>(t);
-    }
-}
-
-struct F32 {
-    using T = float;
-    static constexpr int kBytes = 4;
-    static constexpr int kEPV = 4;  // elements per 16-byte vector
-    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
-        x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
-    }
-    __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        __builtin_nontemporal_store(f32x4{y[0], y[1], y[2], y[3]}, reinterpret_cast<f32x4*>(p));
-    }
-    __device__ __forceinline__ static float load1(const T* p) { return *p; }
-    __device__ __forceinline__ static void store1(T* p, float y) { *p = y; }
-};
-
-struct BF16 {
-    using T = uint16_t;  // raw bf16 bit pattern
-    static constexpr int kBytes = 2;
-    static constexpr int kEPV = 8;
-    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            x[2 * i] = bits_f(v[i] << 16);
-            x[2 * i + 1] = bits_f(v[i] & 0xFFFF0000u);
-        }
-    }
-    __device__ __forceinline__ static unsigned pack(float a, float b) {
-        // round to nearest even, NaN stays NaN (v_cvt_pk_bf16_f32)
-        return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
-    }
-    __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        __builtin_nontemporal_store(
-            u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])},
-            reinterpret_cast<u32x4*>(p));
-    }
-    __device__ __forceinline__ static float load1(const T* p) {
-        return bits_f(static_cast<unsigned>(*p) << 16);
-    }
-    __device__ __forceinline__ static void store1(T* p, float y) {
-        *p = __builtin_bit_cast(uint16_t, static_cast<__bf16>(y));
-    }
-};
-
-// Softmax of U rows per group, all loads first (U rows x V vectors in flight per lane).
-//   row r of the item starts at element base + r * cols; rows r0, r0 + step, ...
-template <class E, int G, int V, int U, bool VEC>
-__device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* out, int64_t base,
-                                       int cols, int nrows, int r0, int step, int lane) {
-    constexpr int EPV = E::kEPV;
-    constexpr int K = V * EPV;
-    float x[U][K];
-    bool act[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int r = r0 + u * step;
-        act[u] = r < nrows;
-        const typename E::T* src = in + base + static_cast<int64_t>(r) * cols;
-        if constexpr (VEC) {
-            const int nvec = cols / EPV;
-#pragma unroll
-            for (int v = 0; v < V; ++v) {
-                const int vi = lane + v * G;
-                if (act[u] && vi < nvec) {
-                    E::load_vec(src + vi * EPV, &x[u][v * EPV]);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < EPV; ++i) x[u][v * EPV + i] = kNegInf;
-                }
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const int j = lane + k * G;
-                x[u][k] = (act[u] && j < cols) ? E::load1(src + j) : kNegInf;
-            }
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        float m = group_reduce<G, OpMax>(lane_reduce<K, OpMax>(x[u]));
-        const float ms = (m == kNegInf) ? 0.0f : m;  // fully masked row: every e is 0
-#pragma unroll
-        for (int k = 0; k < K; ++k) x[u][k] = __builtin_amdgcn_exp2f((x[u][k] - ms) * kLog2e);
-        const float s = group_reduce<G, OpAdd>(lane_reduce<K, OpAdd>(x[u]));
-        const float inv = (s == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(s);
-#pragma unroll
-        for (int k = 0; k < K; ++k) x[u][k] *= inv;
-        const int r = r0 + u * step;
-        typename E::T* dst = out + base + static_cast<int64_t>(r) * cols;
-        if constexpr (VEC) {
-            const int nvec = cols / EPV;
-#pragma unroll
-            for (int v = 0; v < V; ++v) {
-                const int vi = lane + v * G;
-                if (act[u] && vi < nvec) E::store_vec(dst + vi * EPV, &x[u][v * EPV]);
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const int j = lane + k * G;
-                if (act[u] && j < cols) E::store1(dst + j, x[u][k]);
-            }
-        }
-    }
-}
-
-// One item with G lanes per row: `reps` ranges of `nrows` rows, range k starting at element
-// base + k * stride.  Within a range the worker's rows are wave*RPW + sub + j*step, j = 0, 1,
-// ... (RPW = 64/G rows per wave, step = rows covered by all the worker's waves at once); loop
-// trip counts depend on the wave only, so lanes never diverge across iterations.
-template <class E, int G, int V, bool VEC>
-__device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E::T* out,
-                                             int64_t base, int cols, int nrows, int reps,
-                                             int64_t stride, int wave, int nwaves, int lane64) {
-    constexpr int RPW = 64 / G;
-    // Rows in flight per group: kVecsInFlight 16-byte loads per lane for aligned rows; one row
-    // for the element-wise path, whose per-element addresses cost registers.
-    constexpr int U = bsm::rows_per_group_in_flight(V, VEC);
-    const int sub = lane64 / G;
-    const int lane = lane64 % G;
-    const int step = nwaves * RPW;
-    uint32_t done = 0;
-    for (int k = 0; k < reps; ++k) {
-        const int64_t b = base + k * stride;
-        for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
-            rows_u<E, G, V, U, VEC>(in, out, b, cols, nrows, r0 + sub, step, lane);
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int left = nrows - (r0 + u * step);
-                done += left <= 0 ? 0 : (left < RPW ? left : RPW);
-            }
-        }
-    }
-    return done;
-}
-
-// Rows longer than the register tile, one wave per row, in chunks of CH 16-byte vectors per
-// lane (32 values) so each lane keeps CH loads in flight; the rare element-wise path (rows not
-// 16-byte aligned) uses chunks of 8 elements, whose per-element addresses cost registers.
-//
-// When the row fits the wave's LDS region (`cap` floats, given to plans with long rows), it is
-// read from HBM once: pass 1 keeps a per-lane max while staging the values in LDS, pass 2
-// turns the staged values into e = 2^((x - M) log2 e) in place and sums them, pass 3 writes
-// e * (1/S).  Every lane re-reads only what it wrote itself, so no barrier is needed.
-//
-// Otherwise two passes over HBM: pass 1 keeps a per-lane running max and a sum rescaled
-// whenever a chunk raises the max, the lanes' pairs are merged, pass 2 re-reads the row and
-// writes e * (1/S) (1.5x the bytes of the staged path).
-template <class E, bool VEC>
-struct LongRow {
-    using T = typename E::T;
-    static constexpr int EPV = E::kEPV;
-    static constexpr int CH = 32 / EPV;        // vectors per lane per chunk (aligned rows)
-    static constexpr int K = VEC ? CH * EPV : 8;  // values per lane per chunk
-
-    // Loads chunk c0 (vector index of the lane's first vector, stride 64) into x; vectors past
-    // the row are -inf.  Element-wise variant: elements j0 + 64 k.
-    __device__ __forceinline__ static void load(const T* src, int cols, int first, float* x) {
-        if constexpr (VEC) {
-            const int nvec = cols / EPV;
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int vi = first + c * 64;
-                if (vi < nvec) {
-                    E::load_vec(src + vi * EPV, x + c * EPV);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < EPV; ++i) x[c * EPV + i] = kNegInf;
-                }
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const int j = first + k * 64;
-                x[k] = j < cols ? E::load1(src + j) : kNegInf;
-            }
-        }
-    }
-    __device__ __forceinline__ static void store(T* dst, int cols, int first, const float* y) {
-        if constexpr (VEC) {
-            const int nvec = cols / EPV;
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int vi = first + c * 64;
-                if (vi < nvec) E::store_vec(dst + vi * EPV, y + c * EPV);
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const int j = first + k * 64;
-                if (j < cols) E::store1(dst + j, y[k]);
-            }
-        }
-    }
-    static constexpr int kStep = VEC ? CH * 64 : K * 64;
-    __device__ __forceinline__ static int extent(int cols) { return VEC ? cols / EPV : cols; }
-};
-
-template <class E, bool VEC, bool STAGE>
-__device__ __forceinline__ void long_row(const typename E::T* src, typename E::T* dst, int cols,
-                                         int lane, float* lds, int cap) {
-    using L = LongRow<E, VEC>;
-    constexpr int K = L::K;
-    const int n = L::extent(cols);
-    const int step = L::kStep;
-    if (STAGE && cols <= cap) {
-        // LDS holds the row as floats at their element index; aligned rows move whole 16-byte
-        // vectors (consecutive lanes on consecutive 16 bytes: no bank conflicts).
-        constexpr int EPV = E::kEPV;
-        float m = kNegInf;
-        for (int first = lane; first < n; first += step) {
-            float x[K];
-            L::load(src, cols, first, x);
-            m = __builtin_fmaxf(m, lane_reduce<K, OpMax>(x));
-            if constexpr (VEC) {
-#pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-                    if (vi < n) {
-#pragma unroll
-                        for (int i = 0; i < EPV; i += 4)
-                            *reinterpret_cast<f32x4*>(lds + vi * EPV + i) =
-                                f32x4{x[c * EPV + i], x[c * EPV + i + 1], x[c * EPV + i + 2], x[c * EPV + i + 3]};
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    if (j < cols) lds[j] = x[k];
-                }
-            }
-        }
-        const float M = group_reduce<64, OpMax>(m);
-        const float Ms = (M == kNegInf) ? 0.0f : M;
-        float s = 0.0f;
-        for (int first = lane; first < n; first += step) {
-            float e[K];
-            if constexpr (VEC) {
-#pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-#pragma unroll
-                    for (int i = 0; i < EPV; i += 4) {
-                        f32x4 v = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
-                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
-                        v.x = __builtin_amdgcn_exp2f((v.x - Ms) * kLog2e);
-                        v.y = __builtin_amdgcn_exp2f((v.y - Ms) * kLog2e);
-                        v.z = __builtin_amdgcn_exp2f((v.z - Ms) * kLog2e);
-                        v.w = __builtin_amdgcn_exp2f((v.w - Ms) * kLog2e);
-                        e[c * EPV + i] = v.x;
-                        e[c * EPV + i + 1] = v.y;
-                        e[c * EPV + i + 2] = v.z;
-                        e[c * EPV + i + 3] = v.w;
-                        if (vi < n) *reinterpret_cast<f32x4*>(lds + vi * EPV + i) = v;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    e[k] = j < cols ? __builtin_amdgcn_exp2f((lds[j] - Ms) * kLog2e) : 0.0f;
-                    if (j < cols) lds[j] = e[k];
-                }
-            }
-            s += lane_reduce<K, OpAdd>(e);
-        }
-        const float S = group_reduce<64, OpAdd>(s);
-        const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
-        for (int first = lane; first < n; first += step) {
-            float y[K];
-            if constexpr (VEC) {
-#pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-#pragma unroll
-                    for (int i = 0; i < EPV; i += 4) {
-                        f32x4 v = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
-                        y[c * EPV + i] = v.x * inv;
-                        y[c * EPV + i + 1] = v.y * inv;
-                        y[c * EPV + i + 2] = v.z * inv;
-                        y[c * EPV + i + 3] = v.w * inv;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    y[k] = j < cols ? lds[j] * inv : 0.0f;
-                }
-            }
-            L::store(dst, cols, first, y);
-        }
-        return;
-    }
-    float m = kNegInf, s = 0.0f;
-    for (int first = lane; first < n; first += step) {
-        float x[K];
-        L::load(src, cols, first, x);
-        const float cm = lane_reduce<K, OpMax>(x);
-        if (cm > m) {
-            s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
-            m = cm;
-        }
-        if (m != kNegInf) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - m) * kLog2e);
-            s += lane_reduce<K, OpAdd>(x);
-        }
-    }
-    const float M = group_reduce<64, OpMax>(m);
-    const float Ms = (M == kNegInf) ? 0.0f : M;
-    const float scale = (m == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f((m - Ms) * kLog2e);
-    const float S = group_reduce<64, OpAdd>(s * scale);
-    const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
-    for (int first = lane; first < n; first += step) {
-        float x[K];
-        L::load(src, cols, first, x);
-#pragma unroll
-        for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - Ms) * kLog2e) * inv;
-        L::store(dst, cols, first, x);
-    }
-}
-
-// Register-tile choice per item (wave-uniform branch); the thresholds are bsm::tile_for's.
-template <class E, int KCLASS, bool VEC>
-__device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
-                                                  int64_t base, int cols, int nrows, int reps,
-                                                  int64_t stride, int wave, int nwaves,
-                                                  int lane64, float* lds, int cap) {
-    const int nvec = (cols + E::kEPV - 1) / E::kEPV;
-#define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
-    if (nvec <= 16) return BSM_RUN(16, 1);
-    if (nvec <= 32) return BSM_RUN(32, 1);
-    if (nvec <= 64) return BSM_RUN(64, 1);
-    // Larger register tiles only for aligned rows; unaligned longer rows take the two-pass path.
-    if constexpr (VEC && KCLASS >= 1) {
-        if (nvec <= 128) return BSM_RUN(64, 2);
-    }
-    if constexpr (VEC && KCLASS >= 2) {
-        if (nvec <= 256) return BSM_RUN(64, 4);
-    }
-    if constexpr (VEC && KCLASS >= 3) {
-        if (nvec <= 512) return BSM_RUN(64, 8);
-    }
-#undef BSM_RUN
-    if constexpr (!VEC || KCLASS >= 4) {
-        uint32_t done = 0;
-        for (int k = 0; k < reps; ++k) {
-            for (int r = wave; r < nrows; r += nwaves) {
-                const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
-                // only the long-row class is launched with LDS to stage rows in
-                long_row<E, VEC, (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
-                ++done;
-            }
-        }
-        return done;
-    }
-    return 0;  // unreachable: the host picks a class that covers the plan's longest row
-}
-
-// Worker w of the table is workgroup w (all its waves share each item) or, when per_wave is
-// set, wave (w * waves_per_workgroup + wave), which then runs its own items alone.
-template <class E, int KCLASS>
-__global__ void __launch_bounds__(1024)
-bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
-                   const bsm_item* __restrict__ items, int base_aligned, int per_wave,
-                   int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
-    extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
-    const int w = blockIdx.x;
-    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
-    const int nwaves = static_cast<int>(blockDim.x) >> 6;
-    const int lane64 = static_cast<int>(threadIdx.x) & 63;
-    const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
-    const int worker = per_wave ? w * nwaves + wave : w;
-    const int my_wave = per_wave ? 0 : wave;
-    const int my_nwaves = per_wave ? 1 : nwaves;
-    float* const lds = bsm_lds + wave * lds_floats_per_wave;
-    uint32_t rows = 0;
-    const int i0 = worker_ptr[worker];
-    const int i1 = worker_ptr[worker + 1];
-    for (int i = i0; i < i1; ++i) {
-        const int64_t base = items[i].elem_offset;
-        const int cols = items[i].cols;
-        const int nrows = items[i].nrows;
-        const int reps = items[i].reps;
-        const int64_t stride = static_cast<int64_t>(items[i].rep_stride) * cols;
-        const bool vec = base_aligned && ((base * E::kBytes) & 15) == 0 &&
-                         ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
-        if (vec)
-            rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, reps, stride,
-                                                   my_wave, my_nwaves, lane64, lds,
-                                                   lds_floats_per_wave);
-        else
-            rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, reps, stride,
-                                                    my_wave, my_nwaves, lane64, lds,
-                                                    lds_floats_per_wave);
-    }
-    if (trace && lane64 == 0) {
-        bsm_trace_rec rec;
-        rec.wg = static_cast<uint32_t>(w);
-        // XCC_ID register (id 20), bits [3:0]; HW_ID register (id 4), all 32 bits
-        rec.xcc_id = __builtin_amdgcn_s_getreg(20 | (0 << 6) | ((4 - 1) << 11)) & 0xF;
-        rec.hw_id = __builtin_amdgcn_s_getreg(4 | (0 << 6) | ((32 - 1) << 11));
-        rec.rows = rows;
-        rec.t_start = t0;
-        rec.t_end = __builtin_amdgcn_s_memrealtime();
-        trace[static_cast<int64_t>(w) * nwaves + wave] = rec;
-    }
-}
-
-// Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the
-// whole grid sweeps one compact window (the fastest copy layout measured on MI355X); a byte
-// loop handles an unaligned remainder.
-__global__ void __launch_bounds__(256) bsm_copy_kernel(const u32x4* __restrict__ src,
-                                                       u32x4* __restrict__ dst, int64_t n_vec) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n_vec; i += stride)
-        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
-}
-
-__global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char* __restrict__ src,
-                                                             unsigned char* __restrict__ dst,
-                                                             int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += stride)
-        dst[i] = src[i];
-}
+using namespace bsm_dev;
 
 template <class E, int KCLASS>
 hipError_t launch_t(const void* in, void* out, const int32_t* worker_ptr, const bsm_item* items,
                     int n_wg, int wg_threads, int aligned, int per_wave, int lds_floats,
                     void* trace, hipStream_t stream) {
     const size_t lds_bytes = static_cast<size_t>(lds_floats) * sizeof(float) * (wg_threads / 64);
-    hipLaunchKernelGGL((bsm_softmax_kernel<E, KCLASS>), dim3(n_wg), dim3(wg_threads), lds_bytes,
-                       stream, static_cast<const typename E::T*>(in),
-                       static_cast<typename E::T*>(out), worker_ptr, items, aligned, per_wave,
-                       lds_floats, static_cast<bsm_trace_rec*>(trace));
-    return hipGetLastError();
+    const typename E::T* a_in = static_cast<const typename E::T*>(in);
+    typename E::T* a_out = static_cast<typename E::T*>(out);
+    bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
+    void* args[] = {&a_in, &a_out, &worker_ptr, &items, &aligned, &per_wave, &lds_floats, &a_trace};
+    // hipLaunchKernel reports a failed launch itself, without touching the thread's last error
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_softmax_kernel<E, KCLASS>),
+                           dim3(n_wg), dim3(wg_threads), args, lds_bytes, stream);
 }
 
 template <class E>
@@ -562,7 +59,6 @@ hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, voi
                           int wg_threads, int per_wave, int lds_floats_per_wave, void* trace,
                           hipStream_t stream) {
     const int aligned = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
-    (void)hipGetLastError();  // start from a clean error state
     if (dtype == BSM_BF16)
         return launch_dtype<BF16>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
                                   aligned, per_wave, lds_floats_per_wave, trace, stream);
@@ -594,25 +90,33 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads
 }
 
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipStream_t stream) {
-    (void)hipGetLastError();
     const bool aligned = ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
     const int64_t n_vec = aligned ? bytes / 16 : 0;
     const int64_t max_grid = static_cast<int64_t>(n_cu > 0 ? n_cu : 256) * 4;
     if (n_vec > 0) {
         int64_t grid = (n_vec + 255) / 256;
         if (grid > max_grid) grid = max_grid;
-        hipLaunchKernelGGL(bsm_copy_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, stream,
-                           static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), n_vec);
+        const u32x4* a_src = static_cast<const u32x4*>(src);
+        u32x4* a_dst = static_cast<u32x4*>(dst);
+        int64_t a_n = n_vec;
+        void* args[] = {&a_src, &a_dst, &a_n};
+        const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&bsm_copy_kernel),
+                                             dim3(static_cast<unsigned>(grid)), dim3(256), args, 0,
+                                             stream);
+        if (e != hipSuccess) return e;
     }
     const int64_t rest = bytes - n_vec * 16;
     if (rest > 0) {
         int64_t grid = (rest + 255) / 256;
         if (grid > max_grid) grid = max_grid;
-        hipLaunchKernelGGL(bsm_copy_bytes_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
-                           stream, static_cast<const unsigned char*>(src) + n_vec * 16,
-                           static_cast<unsigned char*>(dst) + n_vec * 16, rest);
+        const unsigned char* a_src = static_cast<const unsigned char*>(src) + n_vec * 16;
+        unsigned char* a_dst = static_cast<unsigned char*>(dst) + n_vec * 16;
+        int64_t a_n = rest;
+        void* args[] = {&a_src, &a_dst, &a_n};
+        return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_copy_bytes_kernel),
+                               dim3(static_cast<unsigned>(grid)), dim3(256), args, 0, stream);
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace bsm
