@@ -196,6 +196,84 @@ def trace_stats(w, schedule):
             "xcd_finish_us": per_xcd}
 
 
+def producer_consumer(iters=20):
+    """Softmax right after a producer wrote its input (a device copy, standing in for the GEMM
+    that computes attention scores), with the default streaming (nontemporal) accesses vs
+    BSM_FLAG_TEMPORAL, at three batch sizes against the 256 MB Infinity Cache. Times the
+    softmax launch only."""
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    cases = (("16MB", workloads.custom([512] * 16, [512] * 16, sigma=3.0, seed=4)),
+             ("64MB", workloads.custom([512] * 64, [512] * 64, sigma=3.0, seed=4)),
+             ("c3_201MB_bf16", workloads.generate("c3")))
+    res = {}
+    for name, w in cases:
+        src = _to_device(w)
+        x = torch.empty_like(src)
+        out = torch.empty_like(src)
+        row = {}
+        for label, flags in (("streaming", 0), ("temporal", bsm.BSM_FLAG_TEMPORAL)):
+            plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                                       schedule="balanced", topology={"flags": flags}, device=0)
+            ts = []
+            for _ in range(iters):
+                x.copy_(src)  # the producer
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                bsm.bsm_plan_execute(plan, x, out)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            plan.destroy()
+            row[label + "_us"] = round(statistics.median(ts) * 1e3, 2)
+        res[name] = row
+        del src, x, out
+    return res
+
+
+def l2_locality(nslices=16, iters=30):
+    """Producer on each slice's home XCD, then the consumer on the same XCD or on the next one
+    (XCD schedule with explicit homes), 16 MB working set: does the consumer find the
+    producer's data in its XCD's L2 across the kernel boundary? Both policies."""
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    w = workloads.custom([512] * nslices, [512] * nslices, sigma=3.0, seed=3)
+    x = _to_device(w)
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=x.device)
+    home = (np.arange(nslices) % 8).astype(np.int8)
+    res = {}
+    for label, flags in (("streaming", 0), ("temporal", bsm.BSM_FLAG_TEMPORAL)):
+        topo = {"flags": flags}
+        mk = lambda h: bsm.bsm_plan_create(w.rows, w.cols, w.offsets[:-1], schedule="xcd",
+                                           home_xcd=h, topology=topo, device=0)
+        prod, same, skew = mk(home), mk(home), mk(((home + 1) % 8).astype(np.int8))
+        ts = {"same_xcd": [], "next_xcd": [], "no_producer": []}
+        for _ in range(iters):
+            for k, plan in (("same_xcd", same), ("next_xcd", skew), ("no_producer", same)):
+                flush.zero_()  # evict what the previous round left in the caches
+                if k != "no_producer":
+                    bsm.bsm_plan_execute(prod, x, y)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                bsm.bsm_plan_execute(plan, y, z)
+                e1.record()
+                torch.cuda.synchronize()
+                ts[k].append(e0.elapsed_time(e1) * 1e3)
+        for p in (prod, same, skew):
+            p.destroy()
+        res[label] = {k: round(statistics.median(v), 2) for k, v in ts.items()}
+    res["working_set_bytes"] = int(w.algorithmic_bytes // 2)
+    return res
+
+
 def cpu_baseline(w):
     import oracle
 
@@ -271,6 +349,8 @@ def main() -> int:
                 if cfg == "c5":
                     extra[f"{cfg}_{sch}"]["trace"] = trace_stats(wk, sch)
             del wk
+        extra["producer_consumer"] = producer_consumer()
+        extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region and
         # are read once; 8192-element rows take the two-pass path (1.25x the traffic)
         for name in ("long4k", "long"):

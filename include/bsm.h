@@ -81,8 +81,15 @@ typedef struct bsm_topology {
     int32_t piece_bytes; /* BALANCED / XCD: traffic of one worker's piece of a round */
     float item_cost;     /* planner cost of one work item, in byte equivalents (<= 0: default) */
     float row_cost;      /* planner cost of one row on top of its bytes (<= 0: default) */
-    int32_t reserved;    /* must be 0 */
+    int32_t flags;       /* BSM_FLAG_* bits; 0 = defaults */
 } bsm_topology;
+
+/* Cache policy.  By default rows are loaded and stored with nontemporal hints (streaming: best
+ * for data that is not in any cache).  BSM_FLAG_TEMPORAL uses ordinary accesses instead, so
+ * input that a producer kernel just wrote is served from the memory-side Infinity Cache
+ * (256 MB on MI355X) and the output stays there for the consumer; use it when the batch fits.
+ * The output bits are the same under both policies. */
+#define BSM_FLAG_TEMPORAL 1
 
 /* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): `reps`
  * ranges of `nrows` rows each; range k starts at element elem_offset + k*rep_stride*cols.
@@ -118,7 +125,7 @@ typedef struct bsm_plan_stats {
     int32_t max_cols;          /* longest row */
     int32_t kernel_class;      /* which kernel instance the plan launches (internal) */
     int32_t lds_bytes_per_wave; /* LDS each wave stages long rows in (0: two-pass path only) */
-    int32_t reserved0;
+    int32_t flags;             /* the BSM_FLAG_* bits the plan runs with */
     double max_worker_cost;    /* planner cost of the most loaded worker */
     double mean_worker_cost;   /* total planner cost / n_workers */
     double max_row_cost;       /* planner cost of the most expensive single row */

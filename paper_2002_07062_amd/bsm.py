@@ -22,6 +22,7 @@ BSM_OK, BSM_ERR_INVALID_ARG, BSM_ERR_UNSUPPORTED, BSM_ERR_ALIAS, BSM_ERR_OOM, BS
 BSM_F32, BSM_BF16 = 0, 1
 BSM_SCHED_RR, BSM_SCHED_BALANCED, BSM_SCHED_XCD = 0, 1, 2
 BSM_MAX_XCD = 16
+BSM_FLAG_TEMPORAL = 1
 
 SCHEDULES = {"rr": BSM_SCHED_RR, "balanced": BSM_SCHED_BALANCED, "xcd": BSM_SCHED_XCD}
 DTYPES = {"f32": BSM_F32, "bf16": BSM_BF16}
@@ -42,7 +43,7 @@ class bsm_topology(ctypes.Structure):
     _fields_ = [("n_cu", ctypes.c_int32), ("n_xcd", ctypes.c_int32),
                 ("wg_per_cu", ctypes.c_int32), ("wg_threads", ctypes.c_int32),
                 ("piece_bytes", ctypes.c_int32), ("item_cost", ctypes.c_float),
-                ("row_cost", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("row_cost", ctypes.c_float), ("flags", ctypes.c_int32)]
 
 
 class bsm_item(ctypes.Structure):
@@ -69,7 +70,7 @@ class bsm_plan_stats(ctypes.Structure):
                 ("wg_threads", ctypes.c_int32), ("schedule", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("n_overlap", ctypes.c_int32),
                 ("max_cols", ctypes.c_int32), ("kernel_class", ctypes.c_int32),
-                ("lds_bytes_per_wave", ctypes.c_int32), ("reserved0", ctypes.c_int32),
+                ("lds_bytes_per_wave", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("max_worker_cost", ctypes.c_double), ("mean_worker_cost", ctypes.c_double),
                 ("max_row_cost", ctypes.c_double), ("moved_cost", ctypes.c_double),
                 ("min_moved_cost", ctypes.c_double), ("build_us", ctypes.c_double),

@@ -27,6 +27,7 @@ struct bsm_plan_s {
     bsm::Table table;
     int kernel_class = 0;
     int lds_floats_per_wave = 0;  // long-row staging (kernel class 4 on a device)
+    int32_t flags = 0;            // BSM_FLAG_* bits
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
     const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
@@ -147,7 +148,8 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         t.row_cost = kDefaultRowCost;
     }
     if (user) {
-        if (user->reserved != 0) return fail(BSM_ERR_INVALID_ARG, "topology.reserved must be 0");
+        if ((user->flags & ~BSM_FLAG_TEMPORAL) != 0)
+            return fail(BSM_ERR_INVALID_ARG, "topology.flags has unknown bits 0x%x", user->flags);
         if (user->n_cu < 0 || user->n_xcd < 0 || user->wg_per_cu < 0 || user->wg_threads < 0 ||
             user->piece_bytes < 0)
             return fail(BSM_ERR_INVALID_ARG, "topology fields must be >= 0 (0 = default)");
@@ -241,6 +243,8 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
     p->device = device;
     p->dtype = dtype;
     p->schedule = schedule;
+    p->flags = topology ? topology->flags : 0;
+    p->table.stats.flags = p->flags;
     p->table.stats.dtype = dtype;
     p->table.stats.kernel_class = p->kernel_class;
 
@@ -301,7 +305,8 @@ bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, voi
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::lock_guard<std::mutex> lock(p->mu);
-    e = bsm::launch_softmax(p->dtype, p->kernel_class, in, out, p->d_worker_ptr, p->d_items,
+    e = bsm::launch_softmax(p->dtype, p->kernel_class, (p->flags & BSM_FLAG_TEMPORAL) != 0, in,
+                            out, p->d_worker_ptr, p->d_items,
                             p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0,
                             p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");

@@ -7,9 +7,10 @@
 // row is owned by one group of lanes of one wave.
 //
 // Per row (softmax over the row, the operation of the problem statement, Section 2):
-//   128-bit nontemporal loads (fp32, or bf16 widened to fp32) -> lane max -> group max (DPP,
+//   128-bit loads (fp32, or bf16 widened to fp32; nontemporal unless the plan asks for cache-
+//   resident accesses) -> lane max -> group max (DPP,
 //   permlane) -> e = 2^((x - m) * log2 e) (v_exp_f32) -> lane sum (pairwise) -> group sum
-//   -> y = e * (1/S) -> round-to-nearest-even to bf16 if needed -> 128-bit nontemporal stores.
+//   -> y = e * (1/S) -> round-to-nearest-even to bf16 if needed -> 128-bit stores.
 // Reductions combine each lane with a partner that combines the same two values in the other
 // order; IEEE max and add are commutative, so every lane of a group ends with the same bits,
 // and a row's result depends only on its values and length, never on the schedule.
@@ -87,27 +88,41 @@ __device__ __forceinline__ float lane_reduce(const float* x) {
     }
 }
 
+// 16-byte accesses, nontemporal (streaming) or ordinary (cache-resident) by NT.
+template <bool NT, class V>
+__device__ __forceinline__ V load16(const V* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    return *p;
+}
+template <bool NT, class V>
+__device__ __forceinline__ void store16(V* p, V v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+template <bool NT>
 struct F32 {
     using T = float;
     static constexpr int kBytes = 4;
     static constexpr int kEPV = 4;  // elements per 16-byte vector
     __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+        const f32x4 v = load16<NT>(reinterpret_cast<const f32x4*>(p));
         x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
     }
     __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        __builtin_nontemporal_store(f32x4{y[0], y[1], y[2], y[3]}, reinterpret_cast<f32x4*>(p));
+        store16<NT>(reinterpret_cast<f32x4*>(p), f32x4{y[0], y[1], y[2], y[3]});
     }
     __device__ __forceinline__ static float load1(const T* p) { return *p; }
     __device__ __forceinline__ static void store1(T* p, float y) { *p = y; }
 };
 
+template <bool NT>
 struct BF16 {
     using T = uint16_t;  // raw bf16 bit pattern
     static constexpr int kBytes = 2;
     static constexpr int kEPV = 8;
     __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        const u32x4 v = load16<NT>(reinterpret_cast<const u32x4*>(p));
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             x[2 * i] = bits_f(v[i] << 16);
@@ -119,9 +134,8 @@ struct BF16 {
         return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
     }
     __device__ __forceinline__ static void store_vec(T* p, const float* y) {
-        __builtin_nontemporal_store(
-            u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])},
-            reinterpret_cast<u32x4*>(p));
+        store16<NT>(reinterpret_cast<u32x4*>(p),
+                    u32x4{pack(y[0], y[1]), pack(y[2], y[3]), pack(y[4], y[5]), pack(y[6], y[7])});
     }
     __device__ __forceinline__ static float load1(const T* p) {
         return bits_f(static_cast<unsigned>(*p) << 16);

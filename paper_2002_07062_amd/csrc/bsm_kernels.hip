@@ -27,7 +27,7 @@ hipError_t launch_t(const void* in, void* out, const int32_t* worker_ptr, const 
 }
 
 template <class E>
-hipError_t launch_dtype(int kclass, const void* in, void* out, const int32_t* worker_ptr,
+hipError_t launch_class(int kclass, const void* in, void* out, const int32_t* worker_ptr,
                         const bsm_item* items, int n_wg, int wg_threads, int aligned, int per_wave,
                         int lds_floats, void* trace, hipStream_t stream) {
 #define BSM_LAUNCH(K) launch_t<E, K>(in, out, worker_ptr, items, n_wg, wg_threads, aligned, per_wave, lds_floats, trace, stream)
@@ -54,16 +54,16 @@ int kernel_class_for(int32_t max_cols, int elem_bytes) {
     return 4;
 }
 
-hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
-                          const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg,
-                          int wg_threads, int per_wave, int lds_floats_per_wave, void* trace,
-                          hipStream_t stream) {
+hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool temporal, const void* in,
+                          void* out, const int32_t* d_worker_ptr, const bsm_item* d_items,
+                          int n_wg, int wg_threads, int per_wave, int lds_floats_per_wave,
+                          void* trace, hipStream_t stream) {
     const int aligned = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+#define BSM_ARGS kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads, aligned, per_wave, lds_floats_per_wave, trace, stream
     if (dtype == BSM_BF16)
-        return launch_dtype<BF16>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
-                                  aligned, per_wave, lds_floats_per_wave, trace, stream);
-    return launch_dtype<F32>(kernel_class, in, out, d_worker_ptr, d_items, n_wg, wg_threads,
-                             aligned, per_wave, lds_floats_per_wave, trace, stream);
+        return temporal ? launch_class<BF16<false>>(BSM_ARGS) : launch_class<BF16<true>>(BSM_ARGS);
+    return temporal ? launch_class<F32<false>>(BSM_ARGS) : launch_class<F32<true>>(BSM_ARGS);
+#undef BSM_ARGS
 }
 
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
@@ -71,19 +71,19 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads
     const void* fn = nullptr;
     if (dtype == BSM_BF16) {
         switch (kernel_class) {
-            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 0>); break;
-            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 1>); break;
-            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 2>); break;
-            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 3>); break;
-            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16, 4>); break;
+            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 0>); break;
+            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 1>); break;
+            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 2>); break;
+            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 3>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 4>); break;
         }
     } else {
         switch (kernel_class) {
-            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 0>); break;
-            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 1>); break;
-            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 2>); break;
-            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 3>); break;
-            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32, 4>); break;
+            case 0: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 0>); break;
+            case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 1>); break;
+            case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 2>); break;
+            case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 3>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 4>); break;
         }
     }
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(n, fn, wg_threads, dyn_lds_bytes);

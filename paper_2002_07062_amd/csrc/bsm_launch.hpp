@@ -20,11 +20,12 @@ int kernel_class_for(int32_t max_cols, int elem_bytes);
 
 // Launches the persistent kernel: n_wg workgroups of wg_threads threads.  Worker v owns items
 // [d_worker_ptr[v], d_worker_ptr[v+1]); workers are workgroups, or waves when per_wave is 1.
-// Each wave gets lds_floats_per_wave floats of LDS to stage long rows (0: none).
-hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, const void* in, void* out,
-                          const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg,
-                          int wg_threads, int per_wave, int lds_floats_per_wave, void* trace,
-                          hipStream_t stream);
+// Each wave gets lds_floats_per_wave floats of LDS to stage long rows (0: none).  temporal
+// selects ordinary (cache-resident) instead of nontemporal row accesses.
+hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool temporal, const void* in,
+                          void* out, const int32_t* d_worker_ptr, const bsm_item* d_items,
+                          int n_wg, int wg_threads, int per_wave, int lds_floats_per_wave,
+                          void* trace, hipStream_t stream);
 
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,

@@ -30,6 +30,7 @@ using i128 = __int128;
 
 constexpr int64_t kMaxElems = int64_t(1) << 60;
 constexpr int64_t kMaxBins = int64_t(1) << 26;
+constexpr int kLongRowKernelClass = 4;  // the kernel class that runs rows beyond the register tile
 
 // Rows [0, nrows) of row length `cols`; row r starts at element off + r * cols.
 struct Span {
@@ -486,8 +487,19 @@ std::string build_table(const Geometry& g, bsm_schedule schedule, const Topology
             std::vector<Span> stream;
             for (int64_t s = 0; s < g.batch; ++s)
                 if (g.R[s] > 0 && g.C[s] > 0) push_span(&stream, Span{g.off[s], g.C[s], g.R[s]});
-            std::vector<int32_t> workers(static_cast<size_t>(P) * nw);
-            std::iota(workers.begin(), workers.end(), 0);
+            // Order of the workers within a round, chosen by measurement on MI355X: for rows
+            // in a register tile, XCD-major (each XCD takes one contiguous part of every round:
+            // +7% on 16384 x 128 x 128, equal elsewhere); for long rows, workgroup order
+            // (consecutive pieces on consecutive workgroups, hence alternating XCDs: +8%).
+            std::vector<int32_t> workers;
+            workers.reserve(static_cast<size_t>(P) * nw);
+            if (kernel_class >= kLongRowKernelClass) {
+                for (int v = 0; v < P * nw; ++v) workers.push_back(v);
+            } else {
+                for (int x = 0; x < t.n_xcd; ++x)
+                    for (int w = x; w < P; w += t.n_xcd)
+                        for (int k = 0; k < nw; ++k) workers.push_back(w * nw + k);
+            }
             rounds = assign_rounds(stream, workers, t, es, kernel_class, &per_worker);
             tab->home.assign(static_cast<size_t>(g.batch), -1);
             tab->overlap.assign(static_cast<size_t>(g.batch), 0);

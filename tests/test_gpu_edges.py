@@ -288,3 +288,15 @@ def test_explicit_stream_and_plan_reuse():
     ref = oracle.softmax(w.x, "f32", w.offsets[:-1], w.rows, w.cols)
     for o in outs:
         compare(to_host_bits(o), ref, "f32")
+
+
+@pytest.mark.parametrize("cfg", ["c3", "c5"])
+def test_temporal_cache_policy_gives_the_same_bits(cfg):
+    """BSM_FLAG_TEMPORAL only changes the cache hints of the row accesses."""
+    w = workloads.generate(cfg, batch=32)
+    x = to_device(w.x, w.dtype)
+    a, _ = run_plan(w, "balanced", x=x)
+    b, st = run_plan(w, "balanced", x=x, topology={"flags": bsm.BSM_FLAG_TEMPORAL})
+    assert st["flags"] == bsm.BSM_FLAG_TEMPORAL
+    view = torch.int16 if w.dtype == "bf16" else torch.int32
+    assert torch.equal(a.view(view), b.view(view))
