@@ -61,6 +61,57 @@ def test_long_rows_lds_staged_and_two_pass(dtype, schedule):
     assert any(c <= cap for c in cols) and any(c > cap for c in cols)
 
 
+# Aligned rows whose 16-byte vector count n = cols * elem_bytes / 16 is not a power of two
+# leave part of their register tile empty (masked lanes hold -inf and store nothing).
+PARTIAL_TILE_COLS = {
+    "f32": [12, 20, 48, 68, 96, 132, 200, 252, 260, 400, 516, 800, 1020],  # n = 3 ... 255
+    "bf16": [24, 40, 136, 200, 504, 520, 1016],                            # n = 3 ... 127
+}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_partial_tile_widths_all_schedules(dtype):
+    """Widths with a partly empty register tile, row counts that leave partial wave steps,
+    16-byte aligned slices: every schedule matches the oracle and all three give the same
+    bits."""
+    cols = PARTIAL_TILE_COLS[dtype]
+    rng = np.random.default_rng(21)
+    rows = [int(r) for r in rng.integers(1, 90, size=len(cols))]
+    gap = 4 if dtype == "f32" else 8
+    w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=22, gap=gap)
+    assert all(int(o) * (4 if dtype == "f32" else 2) % 16 == 0 for o in w.offsets)
+    results = []
+    for schedule in SCHEDULES:
+        print(f"[partial tile {dtype} {schedule}] cols {cols}", flush=True)
+        bits, _ = _check_ragged(w, schedule)
+        results.append(bits)
+    assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_partial_tile_special_values_stay_in_their_row(dtype):
+    """Rows handled side by side in one wave step: a NaN, +inf or fully masked row changes only
+    itself."""
+    C = 132 if dtype == "f32" else 200  # n = 33 / 25
+    R = 9
+    rows = np.random.default_rng(23).standard_normal((R, C)).astype(np.float32) * 4
+    rows[1, :] = -np.inf
+    rows[2, 7] = np.nan
+    rows[4, C - 1] = np.inf
+    rows[5, 3:] = -np.inf
+    rows[7, :] = 0.0
+    x = rows.reshape(-1)
+    if dtype == "bf16":
+        x = workloads._to_bf16_bits(x)
+    w = workloads.Workload("partial_tile_special", dtype, x, np.array([0, R * C], np.int64),
+                           np.array([R], np.int32), np.array([C], np.int32), True)
+    for schedule in SCHEDULES:
+        out, _ = run_plan(w, schedule)
+        bits = to_host_bits(out)
+        compare(bits, oracle.softmax(w.x, dtype, [0], [R], [C]), dtype)
+        assert np.all(bits[C:2 * C] == 0)
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 def test_unaligned_base_pointer(shift):
     """Input and output start a few elements past a 16-byte boundary: the element-wise path."""
