@@ -308,6 +308,7 @@ def main() -> int:
     import torch
 
     import paper_2002_07062_amd as bsm
+    import workloads
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -349,6 +350,13 @@ def main() -> int:
                 if cfg == "c5":
                     extra[f"{cfg}_{sch}"]["trace"] = trace_stats(wk, sch)
             del wk
+        # one GPU's share of C2 under 8-way head sharding: 48 slices, where a slice per
+        # workgroup can occupy at most 48 of the 512 workgroups
+        wk = workloads.generate("c2", batch=48)
+        for sch in ("rr", "balanced", "xcd"):
+            r, _ = run_workload("c2", sch, args.steps, args.warmup, w=wk)
+            extra[f"shard8_48x512x512_f32_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "n_items")}
+        del wk
         extra["producer_consumer"] = producer_consumer()
         extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region and

@@ -1,4 +1,5 @@
-"""fp64 CPU oracle of the batched row softmax and checks of its slice schedules.
+"""fp64 CPU oracle of the batched row softmax (forward and backward) and checks of its slice
+schedules.
 
 TEST INFRASTRUCTURE ONLY. Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline
 leg may import this package. It shares no code with the HIP library
@@ -10,6 +11,8 @@ tests/test_oracle.py and tests/test_plan_checks.py; every function here has at l
 """
 
 from . import plan_checks
-from .softmax import DTYPE_CODE, build, softmax, softmax_rows
+from .softmax import (DTYPE_CODE, build, softmax, softmax_backward, softmax_backward_rows,
+                      softmax_rows)
 
-__all__ = ["DTYPE_CODE", "build", "plan_checks", "softmax", "softmax_rows"]
+__all__ = ["DTYPE_CODE", "build", "plan_checks", "softmax", "softmax_backward",
+           "softmax_backward_rows", "softmax_rows"]

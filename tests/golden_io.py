@@ -56,3 +56,24 @@ def paper_bank_table():
                                  flags=[int(t) for t in tok[5:5 + banks]],
                                  overlap=int(tok[5 + banks])))
     return banks, rows
+
+
+def backward_hand_values():
+    """Cases of tests/golden/softmax_backward_hand_values.txt: dicts with name, R, C, dyadic,
+    y, dy, dx (floats; dx exact fractions converted once)."""
+    cases = []
+    cur = None
+    with open(os.path.join(HERE, "softmax_backward_hand_values.txt")) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            tok = line.split()
+            if tok[0] == "case":
+                cur = dict(name=tok[1], R=int(tok[2]), C=int(tok[3]), dyadic="dyadic" in tok[4:])
+                cases.append(cur)
+            elif tok[0] in ("y", "dy", "dx"):
+                cur[tok[0]] = [_out_token(t) for t in tok[1:]]
+    for c in cases:
+        assert len(c["y"]) == len(c["dy"]) == len(c["dx"]) == c["R"] * c["C"], c["name"]
+    return cases
