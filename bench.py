@@ -161,6 +161,46 @@ def run_workload(name, schedule, steps, warmup, rotate=None, w=None, topology=No
     return res, w
 
 
+def run_backward(name, schedule, steps, warmup, w=None):
+    """Bench the backward op (dx from y and dy) on one workload: algorithmic bytes = every
+    element of y and dy read once and dx written once. Inputs are the forward input itself
+    and a seeded gradient: the kernel's work does not depend on the values."""
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    w = w or workloads.generate(name)
+    nbytes = w.algorithmic_bytes * 3 // 2
+    n_sets = _rotation(nbytes)
+    y0 = _to_device(w)
+    g = workloads.gradient(w)
+    dy0 = (torch.from_numpy(g).cuda() if w.dtype == "f32"
+           else torch.from_numpy(g.view("int16")).view(torch.bfloat16).cuda())
+    ys = [y0] + [y0.clone() for _ in range(n_sets - 1)]
+    dys = [dy0] + [dy0.clone() for _ in range(n_sets - 1)]
+    dxs = [torch.empty_like(y0) for _ in range(n_sets)]
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule=schedule, device=0)
+    for i in range(warmup):
+        bsm.bsm_plan_execute_backward(plan, ys[i % n_sets], dys[i % n_sets], dxs[i % n_sets])
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(steps):
+        bsm.bsm_plan_execute_backward(plan, ys[i % n_sets], dys[i % n_sets], dxs[i % n_sets])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    plan.destroy()
+    ms = t0.elapsed_time(t1) / steps
+    del ys, dys, dxs, y0, dy0
+    torch.cuda.empty_cache()
+    return dict(workload=w.name, schedule=schedule, algorithmic_bytes=nbytes, ms_per_step=ms,
+                gbs=nbytes / (ms * 1e-3) / 1e9, buffers_rotated=n_sets)
+
+
 def trace_stats(w, schedule):
     """One traced launch (outside any timed region): per-wave busy intervals from the kernel's
     constant-rate clock give the makespan, the mean wave busy time, the fraction of wave-time
@@ -357,6 +397,11 @@ def main() -> int:
             r, _ = run_workload("c2", sch, args.steps, args.warmup, w=wk)
             extra[f"shard8_48x512x512_f32_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "n_items")}
         del wk
+        # the backward op (dx = y * (dy - sum(dy * y))): three streams, same tables
+        for cfg, sch in (("c2", "balanced"), ("c2", "xcd"), ("c2", "rr"), ("c3", "balanced"),
+                         ("c5", "balanced"), ("c5", "rr")):
+            r = run_backward(cfg, sch, args.steps, args.warmup)
+            extra[f"{cfg}_backward_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "algorithmic_bytes")}
         extra["producer_consumer"] = producer_consumer()
         extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region and

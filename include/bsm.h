@@ -200,6 +200,25 @@ bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets,
  * stats.trace_bytes bytes that receives one bsm_trace_rec per wave. */
 bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace);
 
+/* Softmax backward under a plan (the gradient pass that Section 1 says these batch
+ * algorithms also run): for every row, with y the forward output and dy the gradient with
+ * respect to y,
+ *     d = sum_j dy_j * y_j,   dx_j = y_j * (dy_j - d)
+ * (the softmax Jacobian diag(y) - y y^T applied to dy).  y, dy and dx are device buffers of the
+ * plan's dtype and geometry; the arithmetic is fp32 (bf16 in and out rounds to nearest even).
+ * dx may be y or dy exactly (in place); any other overlap of dx with an input is
+ * BSM_ERR_ALIAS; y and dy may overlap freely.  Same table, stream and trace semantics as
+ * bsm_plan_execute. */
+bsm_status bsm_plan_execute_backward(bsm_plan plan, const void* y, const void* dy, void* dx,
+                                     void* stream, void* trace);
+
+/* One-shot softmax backward: the arguments of bsm_softmax, with y and dy in place of in and dx
+ * in place of out; plans come from the same per-device cache. */
+bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
+                                const int64_t* slice_offsets, const int32_t* rows,
+                                const int32_t* cols, int64_t batch, bsm_dtype dtype,
+                                bsm_schedule schedule, void* stream);
+
 bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats);
 
 /* Copy the host work table out: worker_ptr [n_workers + 1] (CSR row pointer: worker v owns

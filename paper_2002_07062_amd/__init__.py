@@ -9,5 +9,6 @@ from .bsm import (  # noqa: F401
     BSM_F32, BSM_FLAG_TEMPORAL, BSM_OK, BSM_SCHED_BALANCED, BSM_SCHED_RR, BSM_SCHED_XCD, DTYPES, ITEM_DTYPE,
     LIB_PATH, SCHEDULES, TRACE_DTYPE, BsmError, Plan, bsm_abi_version, bsm_cache_clear, bsm_copy,
     bsm_default_topology, bsm_device_info, bsm_last_error, bsm_plan_create, bsm_plan_describe,
-    bsm_plan_destroy, bsm_plan_execute, bsm_plan_export, bsm_softmax, bsm_status_string,
+    bsm_plan_destroy, bsm_plan_execute, bsm_plan_execute_backward, bsm_plan_export, bsm_softmax,
+    bsm_softmax_backward, bsm_status_string,
     bsm_topology, load)

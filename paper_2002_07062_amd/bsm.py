@@ -109,6 +109,9 @@ def load() -> ctypes.CDLL:
         "bsm_plan_create": ([P(vp), P(i64), P(i32), P(i32), i64, ctypes.c_int, ctypes.c_int,
                              P(ctypes.c_int8), P(bsm_topology), ctypes.c_int], ctypes.c_int),
         "bsm_plan_execute": ([vp, vp, vp, vp, vp], ctypes.c_int),
+        "bsm_plan_execute_backward": ([vp, vp, vp, vp, vp, vp], ctypes.c_int),
+        "bsm_softmax_backward": ([vp, vp, vp, P(i64), P(i32), P(i32), i64, ctypes.c_int,
+                                  ctypes.c_int, vp], ctypes.c_int),
         "bsm_plan_describe": ([vp, P(bsm_plan_stats)], ctypes.c_int),
         "bsm_plan_export": ([vp, P(i32), vp, P(ctypes.c_int8), P(ctypes.c_uint8)], ctypes.c_int),
         "bsm_plan_destroy": ([vp], ctypes.c_int),
@@ -228,15 +231,43 @@ def bsm_softmax(x, out, rows, cols, slice_offsets=None, batch=None, schedule="ba
     return out
 
 
+def bsm_softmax_backward(y, dy, dx, rows, cols, slice_offsets=None, batch=None,
+                         schedule="balanced", stream=None):
+    """dx = softmax backward of (y, dy) over every slice: per row d = sum(dy * y),
+    dx = y * (dy - d) (see bsm.h). y, dy, dx: contiguous GPU tensors of one dtype (dx may be y
+    or dy). Returns dx."""
+    lib = load()
+    if not (y.dtype == dy.dtype == dx.dtype):
+        raise TypeError("y, dy and dx must share a dtype")
+    keep = _geometry(rows, cols, slice_offsets, batch)
+    o, op, r, rp, c, cp, n = keep
+    _check_sizes(_extent(o, r, c, n), y, dy, dx)
+    with torch.cuda.device(y.device):
+        _check(lib.bsm_softmax_backward(_ptr(y), _ptr(dy), _ptr(dx), op, rp, cp, n,
+                                        _dtype_code(y.dtype), _schedule_code(schedule),
+                                        _stream_of(y, stream)))
+    return dx
+
+
 class Plan:
     """A built work table (bsm_plan). Use bsm_plan_create to make one."""
 
-    def __init__(self, handle: int, batch: int, device: int, extent: int, trace_bytes: int):
+    def __init__(self, handle: int, batch: int, device: int, extent: int, trace_bytes: int,
+                 dtype: int = BSM_F32):
         self.handle = handle
         self.batch = batch
         self.device = device
         self.extent = extent
         self.trace_bytes = trace_bytes
+        self.dtype = dtype
+
+    def check_tensors(self, *tensors) -> None:
+        """Every tensor covers the plan's extent and has the plan's element type."""
+        _check_sizes(self.extent, *tensors)
+        want = torch.float32 if self.dtype == BSM_F32 else torch.bfloat16
+        for t in tensors:
+            if isinstance(t, torch.Tensor) and t.dtype != want:
+                raise TypeError(f"plan is for {want}, got a {t.dtype} tensor")
 
     def __enter__(self):
         return self
@@ -273,20 +304,34 @@ def bsm_plan_create(rows, cols, slice_offsets=None, batch=None, dtype="f32", sch
     del keep, h
     st = bsm_plan_stats()
     _check(lib.bsm_plan_describe(handle.value, ctypes.byref(st)))
-    return Plan(handle.value, n, int(device), int(st.extent_elems), int(st.trace_bytes))
+    return Plan(handle.value, n, int(device), int(st.extent_elems), int(st.trace_bytes),
+                int(st.dtype))
 
 
 def bsm_plan_execute(plan: Plan, x, out, stream=None, trace=None):
     """out = row softmax of x under the plan. `trace`: None or a GPU tensor of at least
     stats['trace_bytes'] bytes (one TRACE_DTYPE record per wave)."""
     lib = load()
-    _check_sizes(plan.extent, x, out)
+    plan.check_tensors(x, out)
     if trace is not None and trace.numel() * trace.element_size() < plan.trace_bytes:
         raise ValueError(f"trace buffer needs {plan.trace_bytes} bytes")
     with torch.cuda.device(plan.device):
         _check(lib.bsm_plan_execute(plan.handle, _ptr(x), _ptr(out), _stream_of(x, stream),
                                     _ptr(trace)))
     return out
+
+
+def bsm_plan_execute_backward(plan: Plan, y, dy, dx, stream=None, trace=None):
+    """dx = softmax backward of (y, dy) under the plan (same geometry and dtype as its
+    forward). `trace` as for bsm_plan_execute."""
+    lib = load()
+    plan.check_tensors(y, dy, dx)
+    if trace is not None and trace.numel() * trace.element_size() < plan.trace_bytes:
+        raise ValueError(f"trace buffer needs {plan.trace_bytes} bytes")
+    with torch.cuda.device(plan.device):
+        _check(lib.bsm_plan_execute_backward(plan.handle, _ptr(y), _ptr(dy), _ptr(dx),
+                                             _stream_of(y, stream), _ptr(trace)))
+    return dx
 
 
 def bsm_plan_describe(plan: Plan) -> dict:

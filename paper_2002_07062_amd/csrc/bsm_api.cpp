@@ -288,27 +288,44 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
     return BSM_OK;
 }
 
-bsm_status execute_plan(bsm_plan p, const void* in, void* out, void* stream, void* trace) {
+// An output may be one of the inputs exactly (in place) or lie apart from it; any other
+// overlap of `extent_bytes`-long buffers is refused.
+bool partial_overlap(const void* x, const void* y, int64_t extent_bytes) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(x), b = reinterpret_cast<uintptr_t>(y);
+    return a != b && a < b + static_cast<uintptr_t>(extent_bytes) &&
+           b < a + static_cast<uintptr_t>(extent_bytes);
+}
+
+// Forward (b == nullptr: out = softmax(a)) or backward (out = dx of y = a, dy = b).
+bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b, void* out,
+                        void* stream, void* trace) {
     if (!p) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
     if (p->device < 0) return fail(BSM_ERR_UNSUPPORTED, "host-only plan (device -1) cannot execute");
     const int64_t extent_bytes = p->geo.extent * elem_bytes_of(p->dtype);
     if (p->geo.total_elems == 0) return BSM_OK;
-    if (!in || !out) return fail(BSM_ERR_INVALID_ARG, "in or out is NULL");
-    const uintptr_t a = reinterpret_cast<uintptr_t>(in), b = reinterpret_cast<uintptr_t>(out);
-    if (a != b && a < b + static_cast<uintptr_t>(extent_bytes) && b < a + static_cast<uintptr_t>(extent_bytes))
-        return fail(BSM_ERR_ALIAS, "in and out overlap without being equal (extent %lld bytes)",
+    if (!a || !out || (backward && !b)) return fail(BSM_ERR_INVALID_ARG, "an input or the output is NULL");
+    if (partial_overlap(a, out, extent_bytes) || (backward && partial_overlap(b, out, extent_bytes)))
+        return fail(BSM_ERR_ALIAS, "an input and the output overlap without being equal (extent %lld bytes)",
                     static_cast<long long>(extent_bytes));
-    if ((a % elem_bytes_of(p->dtype)) != 0 || (b % elem_bytes_of(p->dtype)) != 0)
-        return fail(BSM_ERR_INVALID_ARG, "in/out not aligned to the element size");
+    const int es = elem_bytes_of(p->dtype);
+    if (reinterpret_cast<uintptr_t>(a) % es != 0 || reinterpret_cast<uintptr_t>(out) % es != 0 ||
+        (backward && reinterpret_cast<uintptr_t>(b) % es != 0))
+        return fail(BSM_ERR_INVALID_ARG, "a buffer is not aligned to the element size");
     DeviceGuard g;
     hipError_t e = g.enter(p->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::lock_guard<std::mutex> lock(p->mu);
-    e = bsm::launch_softmax(p->dtype, p->kernel_class, (p->flags & BSM_FLAG_TEMPORAL) != 0, in,
-                            out, p->d_worker_ptr, p->d_items,
-                            p->topo.n_wg(), p->topo.wg_threads, p->table.per_wave ? 1 : 0,
-                            p->lds_floats_per_wave, trace, s);
+    const bool temporal = (p->flags & BSM_FLAG_TEMPORAL) != 0;
+    if (backward)
+        e = bsm::launch_softmax_backward(p->dtype, p->kernel_class, temporal, a, b, out,
+                                         p->d_worker_ptr, p->d_items, p->topo.n_wg(),
+                                         p->topo.wg_threads, p->table.per_wave ? 1 : 0,
+                                         p->lds_floats_per_wave, trace, s);
+    else
+        e = bsm::launch_softmax(p->dtype, p->kernel_class, temporal, a, out, p->d_worker_ptr,
+                                p->d_items, p->topo.n_wg(), p->topo.wg_threads,
+                                p->table.per_wave ? 1 : 0, p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     e = hipEventRecord(p->last_use, s);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -348,51 +365,13 @@ void destroy_plan(bsm_plan p) {
     delete p;
 }
 
-}  // namespace
-
-extern "C" {
-
-bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets, const int32_t* rows,
-                           const int32_t* cols, int64_t batch, bsm_dtype dtype,
-                           bsm_schedule schedule, const int8_t* home_xcd,
-                           const bsm_topology* topology, int device) {
-    return create_plan(out_plan, slice_offsets, rows, cols, batch, dtype, schedule, home_xcd,
-                       topology, device);
-}
-
-bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace) {
-    return execute_plan(plan, in, out, stream, trace);
-}
-
-bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats) {
-    if (!plan || !stats) return fail(BSM_ERR_INVALID_ARG, "plan or stats is NULL");
-    *stats = plan->table.stats;
-    return BSM_OK;
-}
-
-bsm_status bsm_plan_export(bsm_plan plan, int32_t* worker_ptr, bsm_item* items, int8_t* home,
-                           uint8_t* overlap) {
-    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
-    const bsm::Table& t = plan->table;
-    if (worker_ptr) std::memcpy(worker_ptr, t.worker_ptr.data(), t.worker_ptr.size() * sizeof(int32_t));
-    if (items && !t.items.empty()) std::memcpy(items, t.items.data(), t.items.size() * sizeof(bsm_item));
-    if (home && !t.home.empty()) std::memcpy(home, t.home.data(), t.home.size());
-    if (overlap && !t.overlap.empty()) std::memcpy(overlap, t.overlap.data(), t.overlap.size());
-    return BSM_OK;
-}
-
-bsm_status bsm_plan_destroy(bsm_plan plan) {
-    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
-    destroy_plan(plan);
-    return BSM_OK;
-}
-
-bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, const int32_t* rows,
-                       const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
-                       void* stream) {
+// One-shot call: validates the geometry (no HIP call for bad arguments or no-ops), then runs a
+// plan from the per-device cache (built on a miss; plans do not depend on the op).
+bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
+                    const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
+                    int64_t batch, bsm_dtype dtype, bsm_schedule schedule, void* stream) {
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
     if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
-    // Validate the geometry before any HIP call (also decides the no-op cases).
     bsm::Geometry geo;
     std::string err;
     try {
@@ -402,11 +381,10 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, 
     }
     if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
     if (geo.total_elems == 0) return BSM_OK;
-    if (!in || !out) return fail(BSM_ERR_INVALID_ARG, "in or out is NULL");
+    if (!a || !out || (backward && !b)) return fail(BSM_ERR_INVALID_ARG, "an input or the output is NULL");
     const int64_t extent_bytes = geo.extent * elem_bytes_of(dtype);
-    const uintptr_t a = reinterpret_cast<uintptr_t>(in), b = reinterpret_cast<uintptr_t>(out);
-    if (a != b && a < b + static_cast<uintptr_t>(extent_bytes) && b < a + static_cast<uintptr_t>(extent_bytes))
-        return fail(BSM_ERR_ALIAS, "in and out overlap without being equal");
+    if (partial_overlap(a, out, extent_bytes) || (backward && partial_overlap(b, out, extent_bytes)))
+        return fail(BSM_ERR_ALIAS, "an input and the output overlap without being equal");
 
     int device = 0;
     hipError_t e = hipGetDevice(&device);
@@ -439,7 +417,65 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, 
             g_cache.pop_back();
         }
     }
-    return execute_plan(plan, in, out, stream, nullptr);
+    return execute_plan(plan, backward, a, b, out, stream, nullptr);
+}
+
+}  // namespace
+
+extern "C" {
+
+bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets, const int32_t* rows,
+                           const int32_t* cols, int64_t batch, bsm_dtype dtype,
+                           bsm_schedule schedule, const int8_t* home_xcd,
+                           const bsm_topology* topology, int device) {
+    return create_plan(out_plan, slice_offsets, rows, cols, batch, dtype, schedule, home_xcd,
+                       topology, device);
+}
+
+bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace) {
+    return execute_plan(plan, false, in, nullptr, out, stream, trace);
+}
+
+bsm_status bsm_plan_execute_backward(bsm_plan plan, const void* y, const void* dy, void* dx,
+                                     void* stream, void* trace) {
+    return execute_plan(plan, true, y, dy, dx, stream, trace);
+}
+
+bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats) {
+    if (!plan || !stats) return fail(BSM_ERR_INVALID_ARG, "plan or stats is NULL");
+    *stats = plan->table.stats;
+    return BSM_OK;
+}
+
+bsm_status bsm_plan_export(bsm_plan plan, int32_t* worker_ptr, bsm_item* items, int8_t* home,
+                           uint8_t* overlap) {
+    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    const bsm::Table& t = plan->table;
+    if (worker_ptr) std::memcpy(worker_ptr, t.worker_ptr.data(), t.worker_ptr.size() * sizeof(int32_t));
+    if (items && !t.items.empty()) std::memcpy(items, t.items.data(), t.items.size() * sizeof(bsm_item));
+    if (home && !t.home.empty()) std::memcpy(home, t.home.data(), t.home.size());
+    if (overlap && !t.overlap.empty()) std::memcpy(overlap, t.overlap.data(), t.overlap.size());
+    return BSM_OK;
+}
+
+bsm_status bsm_plan_destroy(bsm_plan plan) {
+    if (!plan) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    destroy_plan(plan);
+    return BSM_OK;
+}
+
+bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, const int32_t* rows,
+                       const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
+                       void* stream) {
+    return one_shot(false, in, nullptr, out, slice_offsets, rows, cols, batch, dtype, schedule,
+                    stream);
+}
+
+bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
+                                const int64_t* slice_offsets, const int32_t* rows,
+                                const int32_t* cols, int64_t batch, bsm_dtype dtype,
+                                bsm_schedule schedule, void* stream) {
+    return one_shot(true, y, dy, dx, slice_offsets, rows, cols, batch, dtype, schedule, stream);
 }
 
 bsm_status bsm_cache_clear(void) {

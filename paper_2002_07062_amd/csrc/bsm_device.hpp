@@ -239,7 +239,7 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
 }
 
 // Rows longer than the register tile, one wave per row, in chunks of CH 16-byte vectors per
-// lane (32 values) so each lane keeps CH loads in flight; the rare element-wise path (rows not
+// lane (VALS values: 32 for one input stream, 16 for two) so each lane keeps CH loads in flight; the rare element-wise path (rows not
 // 16-byte aligned) uses chunks of 8 elements, whose per-element addresses cost registers.
 //
 // When the row fits the wave's LDS region (`cap` floats, given to plans with long rows), it is
@@ -250,16 +250,17 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
 // Otherwise two passes over HBM: pass 1 keeps a per-lane running max and a sum rescaled
 // whenever a chunk raises the max, the lanes' pairs are merged, pass 2 re-reads the row and
 // writes e * (1/S) (1.5x the bytes of the staged path).
-template <class E, bool VEC>
+template <class E, bool VEC, int VALS = 32>
 struct LongRow {
     using T = typename E::T;
     static constexpr int EPV = E::kEPV;
-    static constexpr int CH = 32 / EPV;        // vectors per lane per chunk (aligned rows)
+    static constexpr int CH = VALS / EPV;      // vectors per lane per chunk (aligned rows)
     static constexpr int K = VEC ? CH * EPV : 8;  // values per lane per chunk
 
     // Loads chunk c0 (vector index of the lane's first vector, stride 64) into x; vectors past
     // the row are -inf.  Element-wise variant: elements j0 + 64 k.
-    __device__ __forceinline__ static void load(const T* src, int cols, int first, float* x) {
+    __device__ __forceinline__ static void load(const T* src, int cols, int first, float* x,
+                                                float pad = kNegInf) {
         if constexpr (VEC) {
             const int nvec = cols / EPV;
 #pragma unroll
@@ -269,14 +270,62 @@ struct LongRow {
                     E::load_vec(src + vi * EPV, x + c * EPV);
                 } else {
 #pragma unroll
-                    for (int i = 0; i < EPV; ++i) x[c * EPV + i] = kNegInf;
+                    for (int i = 0; i < EPV; ++i) x[c * EPV + i] = pad;
                 }
             }
         } else {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const int j = first + k * 64;
-                x[k] = j < cols ? E::load1(src + j) : kNegInf;
+                x[k] = j < cols ? E::load1(src + j) : pad;
+            }
+        }
+    }
+    // The lane's values of a chunk to / from LDS at their element index (each lane touches
+    // only what it wrote itself).
+    __device__ __forceinline__ static void to_lds(float* lds, int cols, int first, const float* x) {
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+                if (vi < nvec) {
+#pragma unroll
+                    for (int i = 0; i < EPV; i += 4)
+                        *reinterpret_cast<f32x4*>(lds + vi * EPV + i) =
+                            f32x4{x[c * EPV + i], x[c * EPV + i + 1], x[c * EPV + i + 2], x[c * EPV + i + 3]};
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = first + k * 64;
+                if (j < cols) lds[j] = x[k];
+            }
+        }
+    }
+    __device__ __forceinline__ static void from_lds(const float* lds, int cols, int first, float* x,
+                                                    float pad) {
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+#pragma unroll
+                for (int i = 0; i < EPV; i += 4) {
+                    f32x4 v = f32x4{pad, pad, pad, pad};
+                    if (vi < nvec) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
+                    x[c * EPV + i] = v.x;
+                    x[c * EPV + i + 1] = v.y;
+                    x[c * EPV + i + 2] = v.z;
+                    x[c * EPV + i + 3] = v.w;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = first + k * 64;
+                x[k] = j < cols ? lds[j] : pad;
             }
         }
     }
@@ -464,14 +513,186 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
     return 0;  // unreachable: the host picks a class that covers the plan's longest row
 }
 
+// ------------------------------------------------------------------------------- backward
+// Gradient of the row softmax (the backward pass of Section 1's batch algorithms): with y the
+// forward output and dy the gradient with respect to y, dx = y * (dy - d), d = sum_j dy_j y_j.
+// Same register tiles as the forward pass: d is an in-lane pairwise tree of the products, then
+// the group's fixed butterfly, so the bits depend on the row's values and length only.  Two
+// input streams: half as many rows per group in flight, and tiles up to 4 vectors per lane
+// (longer rows take the long-row path).
+
+template <class E, int G, int V, int U, bool VEC>
+__device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typename E::T* dy,
+                                           typename E::T* dx, int64_t base, int cols, int nrows,
+                                           int r0, int step, int lane) {
+    constexpr int EPV = E::kEPV;
+    constexpr int K = V * EPV;
+    float a[U][K], g[U][K];
+    bool act[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = r0 + u * step;
+        act[u] = r < nrows;
+        const int64_t o = base + static_cast<int64_t>(r) * cols;
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const int vi = lane + v * G;
+                if (act[u] && vi < nvec) {
+                    E::load_vec(y + o + vi * EPV, &a[u][v * EPV]);
+                    E::load_vec(dy + o + vi * EPV, &g[u][v * EPV]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < EPV; ++i) a[u][v * EPV + i] = g[u][v * EPV + i] = 0.0f;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = lane + k * G;
+                const bool in = act[u] && j < cols;
+                a[u][k] = in ? E::load1(y + o + j) : 0.0f;
+                g[u][k] = in ? E::load1(dy + o + j) : 0.0f;
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float p[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) p[k] = a[u][k] * g[u][k];
+        const float d = group_reduce<G, OpAdd>(lane_reduce<K, OpAdd>(p));
+#pragma unroll
+        for (int k = 0; k < K; ++k) a[u][k] = a[u][k] * (g[u][k] - d);
+        const int r = r0 + u * step;
+        typename E::T* dst = dx + base + static_cast<int64_t>(r) * cols;
+        if constexpr (VEC) {
+            const int nvec = cols / EPV;
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                const int vi = lane + v * G;
+                if (act[u] && vi < nvec) E::store_vec(dst + vi * EPV, &a[u][v * EPV]);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const int j = lane + k * G;
+                if (act[u] && j < cols) E::store1(dst + j, a[u][k]);
+            }
+        }
+    }
+}
+
+template <class E, int G, int V, bool VEC>
+__device__ __forceinline__ uint32_t run_item_bwd(const typename E::T* y, const typename E::T* dy,
+                                                 typename E::T* dx, int64_t base, int cols,
+                                                 int nrows, int reps, int64_t stride, int wave,
+                                                 int nwaves, int lane64) {
+    constexpr int RPW = 64 / G;
+    constexpr int UF = bsm::rows_per_group_in_flight(V, VEC);
+    constexpr int U = UF >= 2 ? UF / 2 : 1;
+    const int sub = lane64 / G;
+    const int lane = lane64 % G;
+    const int step = nwaves * RPW;
+    uint32_t done = 0;
+    for (int k = 0; k < reps; ++k) {
+        const int64_t b = base + k * stride;
+        for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
+            rows_u_bwd<E, G, V, U, VEC>(y, dy, dx, b, cols, nrows, r0 + sub, step, lane);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int left = nrows - (r0 + u * step);
+                done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+            }
+        }
+    }
+    return done;
+}
+
+// One row beyond the tile, one wave: pass 1 streams y and dy once, keeping the lane's partial
+// sum of products (each chunk's products by the in-lane tree, chunks in order) and, when both
+// fit the wave's LDS region (2 cols <= cap), staging them there; pass 2 forms dx from LDS or,
+// otherwise, from a second read of y and dy.  Both variants add in the same order.
+template <class E, bool VEC, bool STAGE>
+__device__ __forceinline__ void long_row_bwd(const typename E::T* y, const typename E::T* dy,
+                                             typename E::T* dx, int cols, int lane, float* lds,
+                                             int cap) {
+    using L = LongRow<E, VEC, 16>;  // two streams: half the values per lane per chunk
+    constexpr int K = L::K;
+    const int n = L::extent(cols);
+    const int step = L::kStep;
+    const bool stage = STAGE && 2 * cols <= cap;
+    float s = 0.0f;
+    for (int first = lane; first < n; first += step) {
+        float a[K], g[K];
+        L::load(y, cols, first, a, 0.0f);
+        L::load(dy, cols, first, g, 0.0f);
+        if (stage) {
+            L::to_lds(lds, cols, first, a);
+            L::to_lds(lds + cols, cols, first, g);
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) g[k] *= a[k];
+        s += lane_reduce<K, OpAdd>(g);
+    }
+    const float d = group_reduce<64, OpAdd>(s);
+    for (int first = lane; first < n; first += step) {
+        float a[K], g[K];
+        if (stage) {
+            L::from_lds(lds, cols, first, a, 0.0f);
+            L::from_lds(lds + cols, cols, first, g, 0.0f);
+        } else {
+            L::load(y, cols, first, a, 0.0f);
+            L::load(dy, cols, first, g, 0.0f);
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) a[k] = a[k] * (g[k] - d);
+        L::store(dx, cols, first, a);
+    }
+}
+
+template <class E, int KCLASS, bool VEC>
+__device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
+                                                      const typename E::T* dy, typename E::T* dx,
+                                                      int64_t base, int cols, int nrows, int reps,
+                                                      int64_t stride, int wave, int nwaves,
+                                                      int lane64, float* lds, int cap) {
+    const int nvec = (cols + E::kEPV - 1) / E::kEPV;
+#define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    if (nvec <= 16) return BSM_RUN_BWD(16, 1);
+    if (nvec <= 32) return BSM_RUN_BWD(32, 1);
+    if (nvec <= 64) return BSM_RUN_BWD(64, 1);
+    if constexpr (VEC && KCLASS >= 1) {
+        if (nvec <= 128) return BSM_RUN_BWD(64, 2);
+    }
+    if constexpr (VEC && KCLASS >= 2) {
+        if (nvec <= 256) return BSM_RUN_BWD(64, 4);
+    }
+#undef BSM_RUN_BWD
+    if constexpr (!VEC || KCLASS >= 3) {
+        uint32_t done = 0;
+        for (int k = 0; k < reps; ++k) {
+            for (int r = wave; r < nrows; r += nwaves) {
+                const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
+                long_row_bwd<E, VEC, (KCLASS >= 4)>(y + o, dy + o, dx + o, cols, lane64, lds, cap);
+                ++done;
+            }
+        }
+        return done;
+    }
+    return 0;  // unreachable: the host picks a class that covers the plan's longest row
+}
+
 // Worker w of the table is workgroup w (all its waves share each item) or, when per_wave is
-// set, wave (w * waves_per_workgroup + wave), which then runs its own items alone.
-template <class E, int KCLASS>
-__global__ void __launch_bounds__(1024)
-bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
-                   const bsm_item* __restrict__ items, int base_aligned, int per_wave,
-                   int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
-    extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
+// set, wave (w * waves_per_workgroup + wave), which then runs its own items alone.  BWD selects
+// the backward op (a = y, b = dy, out = dx); the forward op reads a only.
+template <class E, int KCLASS, bool BWD>
+__device__ __forceinline__ void worker_loop(const typename E::T* a, const typename E::T* b,
+                                            typename E::T* out, const int32_t* __restrict__ worker_ptr,
+                                            const bsm_item* __restrict__ items, int base_aligned,
+                                            int per_wave, int lds_floats_per_wave,
+                                            bsm_trace_rec* __restrict__ trace, float* lds_base) {
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int nwaves = static_cast<int>(blockDim.x) >> 6;
@@ -480,7 +701,7 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
     const int worker = per_wave ? w * nwaves + wave : w;
     const int my_wave = per_wave ? 0 : wave;
     const int my_nwaves = per_wave ? 1 : nwaves;
-    float* const lds = bsm_lds + wave * lds_floats_per_wave;
+    float* const lds = lds_base + wave * lds_floats_per_wave;
     uint32_t rows = 0;
     const int i0 = worker_ptr[worker];
     const int i1 = worker_ptr[worker + 1];
@@ -492,14 +713,25 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
         const int64_t stride = static_cast<int64_t>(items[i].rep_stride) * cols;
         const bool vec = base_aligned && ((base * E::kBytes) & 15) == 0 &&
                          ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
-        if (vec)
-            rows += dispatch_item<E, KCLASS, true>(in, out, base, cols, nrows, reps, stride,
-                                                   my_wave, my_nwaves, lane64, lds,
-                                                   lds_floats_per_wave);
-        else
-            rows += dispatch_item<E, KCLASS, false>(in, out, base, cols, nrows, reps, stride,
-                                                    my_wave, my_nwaves, lane64, lds,
-                                                    lds_floats_per_wave);
+        if constexpr (BWD) {
+            if (vec)
+                rows += dispatch_item_bwd<E, KCLASS, true>(a, b, out, base, cols, nrows, reps, stride,
+                                                           my_wave, my_nwaves, lane64, lds,
+                                                           lds_floats_per_wave);
+            else
+                rows += dispatch_item_bwd<E, KCLASS, false>(a, b, out, base, cols, nrows, reps, stride,
+                                                            my_wave, my_nwaves, lane64, lds,
+                                                            lds_floats_per_wave);
+        } else {
+            if (vec)
+                rows += dispatch_item<E, KCLASS, true>(a, out, base, cols, nrows, reps, stride,
+                                                       my_wave, my_nwaves, lane64, lds,
+                                                       lds_floats_per_wave);
+            else
+                rows += dispatch_item<E, KCLASS, false>(a, out, base, cols, nrows, reps, stride,
+                                                        my_wave, my_nwaves, lane64, lds,
+                                                        lds_floats_per_wave);
+        }
     }
     if (trace && lane64 == 0) {
         bsm_trace_rec rec;
@@ -512,6 +744,28 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
         rec.t_end = __builtin_amdgcn_s_memrealtime();
         trace[static_cast<int64_t>(w) * nwaves + wave] = rec;
     }
+}
+
+extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
+
+template <class E, int KCLASS>
+__global__ void __launch_bounds__(1024)
+bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
+                   const bsm_item* __restrict__ items, int base_aligned, int per_wave,
+                   int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
+    worker_loop<E, KCLASS, false>(in, nullptr, out, worker_ptr, items, base_aligned, per_wave,
+                                  lds_floats_per_wave, trace, bsm_lds);
+}
+
+// dx = softmax backward of (y, dy) under the same work table.
+template <class E, int KCLASS>
+__global__ void __launch_bounds__(1024)
+bsm_softmax_bwd_kernel(const typename E::T* y, const typename E::T* dy, typename E::T* dx,
+                       const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
+                       int base_aligned, int per_wave, int lds_floats_per_wave,
+                       bsm_trace_rec* __restrict__ trace) {
+    worker_loop<E, KCLASS, true>(y, dy, dx, worker_ptr, items, base_aligned, per_wave,
+                                 lds_floats_per_wave, trace, bsm_lds);
 }
 
 // Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the

@@ -41,6 +41,36 @@ hipError_t launch_class(int kclass, const void* in, void* out, const int32_t* wo
 #undef BSM_LAUNCH
 }
 
+template <class E, int KCLASS>
+hipError_t launch_bwd_t(const void* y, const void* dy, void* dx, const int32_t* worker_ptr,
+                        const bsm_item* items, int n_wg, int wg_threads, int aligned, int per_wave,
+                        int lds_floats, void* trace, hipStream_t stream) {
+    const size_t lds_bytes = static_cast<size_t>(lds_floats) * sizeof(float) * (wg_threads / 64);
+    const typename E::T* a_y = static_cast<const typename E::T*>(y);
+    const typename E::T* a_dy = static_cast<const typename E::T*>(dy);
+    typename E::T* a_dx = static_cast<typename E::T*>(dx);
+    bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
+    void* args[] = {&a_y, &a_dy, &a_dx, &worker_ptr, &items, &aligned, &per_wave, &lds_floats, &a_trace};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_softmax_bwd_kernel<E, KCLASS>),
+                           dim3(n_wg), dim3(wg_threads), args, lds_bytes, stream);
+}
+
+template <class E>
+hipError_t launch_class_bwd(int kclass, const void* y, const void* dy, void* dx,
+                            const int32_t* worker_ptr, const bsm_item* items, int n_wg,
+                            int wg_threads, int aligned, int per_wave, int lds_floats, void* trace,
+                            hipStream_t stream) {
+#define BSM_LAUNCH(K) launch_bwd_t<E, K>(y, dy, dx, worker_ptr, items, n_wg, wg_threads, aligned, per_wave, lds_floats, trace, stream)
+    switch (kclass) {
+        case 0: return BSM_LAUNCH(0);
+        case 1: return BSM_LAUNCH(1);
+        case 2: return BSM_LAUNCH(2);
+        case 3: return BSM_LAUNCH(3);
+        default: return BSM_LAUNCH(4);
+    }
+#undef BSM_LAUNCH
+}
+
 }  // namespace
 
 namespace bsm {
@@ -63,6 +93,19 @@ hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool temporal, cons
     if (dtype == BSM_BF16)
         return temporal ? launch_class<BF16<false>>(BSM_ARGS) : launch_class<BF16<true>>(BSM_ARGS);
     return temporal ? launch_class<F32<false>>(BSM_ARGS) : launch_class<F32<true>>(BSM_ARGS);
+#undef BSM_ARGS
+}
+
+hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool temporal, const void* y,
+                                   const void* dy, void* dx, const int32_t* d_worker_ptr,
+                                   const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
+                                   int lds_floats_per_wave, void* trace, hipStream_t stream) {
+    const int aligned = ((reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(dy) |
+                          reinterpret_cast<uintptr_t>(dx)) & 15) == 0;
+#define BSM_ARGS kernel_class, y, dy, dx, d_worker_ptr, d_items, n_wg, wg_threads, aligned, per_wave, lds_floats_per_wave, trace, stream
+    if (dtype == BSM_BF16)
+        return temporal ? launch_class_bwd<BF16<false>>(BSM_ARGS) : launch_class_bwd<BF16<true>>(BSM_ARGS);
+    return temporal ? launch_class_bwd<F32<false>>(BSM_ARGS) : launch_class_bwd<F32<true>>(BSM_ARGS);
 #undef BSM_ARGS
 }
 

@@ -27,6 +27,12 @@ hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool temporal, cons
                           int n_wg, int wg_threads, int per_wave, int lds_floats_per_wave,
                           void* trace, hipStream_t stream);
 
+// The backward op under the same table: dx = y * (dy - sum(dy * y)) per row.
+hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool temporal, const void* y,
+                                   const void* dy, void* dx, const int32_t* d_worker_ptr,
+                                   const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
+                                   int lds_floats_per_wave, void* trace, hipStream_t stream);
+
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
                                size_t dyn_lds_bytes, int* n);

@@ -103,3 +103,80 @@ def run_plan(w, schedule="xcd", x=None, out=None, topology=None, trace=None, hom
 
 def oracle_full(w, nthreads=16):
     return oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=nthreads)
+
+
+# ------------------------------------------------------------------------------- backward
+def backward_inputs(w, seed=1000, nthreads=16):
+    """Seeded inputs of the backward pass for workload w: y = the oracle's softmax of w.x rounded
+    to w's dtype (0 outside the slices), dy = workloads.gradient(w). Returns (y, dy) as host
+    arrays in w's storage dtype (bf16 as bit patterns)."""
+    import workloads
+
+    y64 = oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=nthreads)
+    y32 = np.nan_to_num(y64, nan=0.0).astype(np.float32)
+    y = workloads._to_bf16_bits(y32) if w.dtype == "bf16" else y32
+    return y, workloads.gradient(w, seed)
+
+
+def _as_f64(a, dtype):
+    if dtype == "f32":
+        return a.astype(np.float64)
+    return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def backward_tolerance(y, dy, dtype, offsets, rows, cols):
+    """Per-element bound on |dx - dx_ref| for fp32 arithmetic on the given inputs, derived from
+    the kernel's operations: d is a tree sum of C rounded products, so |d - d_ref| <=
+    (ceil(log2 C) + 1) u sum_k |y_k dy_k|; dx = y (dy - d) adds two roundings,
+    2 u |y| (|dy| + |d|).  u = 2^-24; the bound is doubled for second-order terms."""
+    y64, d64 = _as_f64(y, dtype), _as_f64(dy, dtype)
+    tol = np.zeros(y64.shape[0])
+    u = 2.0 ** -24
+    for o, R, C in zip(offsets, rows, cols):
+        o, R, C = int(o), int(R), int(C)
+        if R == 0 or C == 0:
+            continue
+        ys = y64[o:o + R * C].reshape(R, C)
+        ds = d64[o:o + R * C].reshape(R, C)
+        prod = ys * ds
+        sabs = np.abs(prod).sum(axis=1, keepdims=True)
+        d = prod.sum(axis=1, keepdims=True)
+        k = int(np.ceil(np.log2(C))) + 1 if C > 1 else 1
+        t = np.abs(ys) * (k * u * sabs + 2 * u * (np.abs(ds) + np.abs(d)))
+        tol[o:o + R * C] = 2.0 * t.reshape(-1)
+    return tol
+
+
+def compare_backward(dx_bits, ref, y, dy, dtype, offsets, rows, cols, mask=None):
+    """Checks GPU dx against the fp64 oracle within the derived bound (fp32), or 2^-8 relative
+    plus twice that bound (bf16: one final rounding). NaN positions must agree."""
+    got = bits_to_f64(dx_bits)
+    tol = backward_tolerance(y, dy, dtype, offsets, rows, cols)
+    if dtype == "bf16":
+        tol = 2.0 ** -8 * np.abs(np.nan_to_num(ref)) + 2.0 * tol
+    if mask is not None:
+        got, ref, tol = got[mask], ref[mask], tol[mask]
+    nan_ref = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan_ref), "NaN positions differ"
+    err = np.abs(got[~nan_ref] - ref[~nan_ref])
+    bad = err > tol[~nan_ref]
+    assert not bad.any(), (f"{int(bad.sum())} of {err.size} dx beyond the bound; worst excess "
+                           f"{float((err - tol[~nan_ref]).max()):.3e}")
+    return float(err.max()) if err.size else 0.0
+
+
+def run_plan_backward(w, y, dy, schedule="xcd", dx=None, topology=None, trace=None):
+    """Backward through bsm_plan_create/execute_backward; y, dy device tensors. Returns
+    (dx tensor, plan stats)."""
+    n = int(w.offsets[-1]) if len(w.offsets) else 0
+    if dx is None:
+        dx = sentinel_like(max(n, 1), w.dtype)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule=schedule, topology=topology, device=0)
+    try:
+        bsm.bsm_plan_execute_backward(plan, y, dy, dx, trace=trace)
+        torch.cuda.synchronize()
+        stats = bsm.bsm_plan_describe(plan)
+    finally:
+        plan.destroy()
+    return dx, stats

@@ -136,3 +136,24 @@ def test_describe_reports_the_plan():
     assert d["max_cols"] == 1000 and d["dtype"] == bsm.BSM_BF16
     assert d["kernel_class"] == 1  # 1000 bf16 = 125 vectors
     assert d["schedule"] == bsm.BSM_SCHED_XCD
+
+
+def test_backward_validation_happens_before_any_gpu_call():
+    lib = bsm.load()
+    r, c, o, rp, cp, op = _c_arrays([4, 4], [64, 64], [0, 256])
+    V = ctypes.c_void_p
+    # no work: OK without touching a GPU
+    assert lib.bsm_softmax_backward(None, None, None, None, rp, cp, 0, 0, 0, None) == bsm.BSM_OK
+    # work but a NULL input
+    assert lib.bsm_softmax_backward(V(16), None, V(4096), op, rp, cp, 2, 0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    # dx partly overlapping dy (fake addresses, never dereferenced)
+    assert lib.bsm_softmax_backward(V(1 << 24), V(1 << 20), V((1 << 20) + 64), op, rp, cp, 2,
+                                    0, 0, None) == bsm.BSM_ERR_ALIAS
+    # dx partly overlapping y
+    assert lib.bsm_softmax_backward(V(1 << 20), V(1 << 24), V((1 << 20) + 64), op, rp, cp, 2,
+                                    0, 0, None) == bsm.BSM_ERR_ALIAS
+    assert lib.bsm_softmax_backward(V(16), V(16), V(16), op, rp, cp, 2, 7, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    p = bsm.bsm_plan_create([4], [4], [0], dtype="f32", topology=TOPO, device=-1)
+    assert lib.bsm_plan_execute_backward(p.handle, V(16), V(4096), V(8192), None, None) == bsm.BSM_ERR_UNSUPPORTED
+    p.destroy()
+    assert lib.bsm_plan_execute_backward(None, V(16), V(16), V(16), None, None) == bsm.BSM_ERR_INVALID_ARG
