@@ -336,6 +336,9 @@ def main() -> int:
     ap.add_argument("--schedule", default="balanced", choices=["rr", "balanced", "xcd"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="headline line only")
+    ap.add_argument("--op", default="forward", choices=["forward", "backward"],
+                    help="backward: time the gradient kernel alone on --workload and print its "
+                         "line (not the headline metric)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -355,6 +358,27 @@ def main() -> int:
         return 2
     bsm.load()
     info = bsm.bsm_device_info(0)
+
+    if args.op == "backward":
+        # the backward op alone, with the copy reference for the counters' scale factors
+        r = run_backward(args.workload, args.schedule, args.steps, args.warmup)
+        wb = workloads.generate(args.workload)
+        x0 = _to_device(wb)
+        n_pairs = _rotation(wb.algorithmic_bytes)
+        xs = [x0] + [x0.clone() for _ in range(n_pairs - 1)]
+        outs = [torch.empty_like(x0) for _ in range(n_pairs)]
+        copy_ms = time_copy(xs, outs, wb.algorithmic_bytes // 2, args.steps, args.warmup)
+        print(json.dumps({
+            "metric": "batched-softmax backward HBM GB/s (read y and dy, write dx)",
+            "value": round(r["gbs"], 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(r["ms_per_step"], 5),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": wb.dtype, "data": "synthetic",
+            "config": {"workload": wb.name, "schedule": args.schedule, "op": "backward"},
+            "pct_of_peak": round(100 * r["gbs"] / PEAK_HBM_GBS, 2),
+            "algorithmic_bytes": r["algorithmic_bytes"],
+            "copy_reference_gbs": round(wb.algorithmic_bytes / (copy_ms * 1e-3) / 1e9, 1)}))
+        return 0
 
     head, w = run_workload(args.workload, args.schedule, args.steps, args.warmup)
 
