@@ -112,6 +112,45 @@ def test_partial_tile_special_values_stay_in_their_row(dtype):
         assert np.all(bits[C:2 * C] == 0)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_offsets_beyond_2_32_elements(dtype):
+    """Slices placed past 2^31 and 2^32 elements and straddling both, in buffers of more than
+    2^32 elements (17 GB per fp32 buffer): 64-bit indexing end to end. Only the slices and a
+    guard band around each are uploaded and read back."""
+    rows = [7, 5, 3, 9, 4]
+    cols = [300, 1000, 4096, 64, 513]
+    offs = [(1 << 31) - 700, (1 << 31) + 12344, (1 << 32) - 6144, (1 << 32) + (1 << 20),
+            (1 << 32) + (1 << 21) + 3]
+    n = max(o + r * c for o, r, c in zip(offs, rows, cols)) + 4096
+    guard = 256
+    # compact host copy: the same slices packed back to back, guards in between
+    cw = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=51, gap=2 * guard, base=guard)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    x = torch.zeros(n, dtype=tdt, device="cuda")
+    out = sentinel_like(1, dtype).expand(n).contiguous()
+    xc = to_device(cw.x, dtype)
+    for o, co, R, C in zip(offs, cw.offsets[:-1], rows, cols):
+        x[o:o + R * C] = xc[int(co):int(co) + R * C]
+    ref = oracle.softmax(cw.x, dtype, cw.offsets[:-1], cw.rows, cw.cols)
+    sentinel = SENTINEL_F32 if dtype == "f32" else SENTINEL_BF16
+    for schedule in SCHEDULES:
+        print(f"[big offsets {dtype} {schedule}] n = {n}", flush=True)
+        plan = bsm.bsm_plan_create(rows, cols, offs, dtype=dtype, schedule=schedule, device=0)
+        bsm.bsm_plan_execute(plan, x, out)
+        torch.cuda.synchronize()
+        plan.destroy()
+        for o, co, R, C in zip(offs, cw.offsets[:-1], rows, cols):
+            co = int(co)
+            got = to_host_bits(out[o:o + R * C])
+            compare(got, ref[co:co + R * C], dtype)
+            assert np.all(to_host_bits(out[o - guard:o]) == sentinel)
+            assert np.all(to_host_bits(out[o + R * C:o + R * C + guard]) == sentinel)
+        out.view(torch.int32 if dtype == "f32" else torch.int16).fill_(
+            int(sentinel.view(np.int32 if dtype == "f32" else np.int16)))
+    del x, out
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 def test_unaligned_base_pointer(shift):
     """Input and output start a few elements past a 16-byte boundary: the element-wise path."""

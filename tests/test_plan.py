@@ -262,3 +262,24 @@ def test_item_metadata_names_the_first_row():
         s, r = int(it["slice"]), int(it["row_begin"])
         assert int(w.offsets[s]) + r * int(w.cols[s]) == int(it["elem_offset"])
         assert int(w.cols[s]) == int(it["cols"])
+
+
+# Slices placed past 2^31 and 2^32 elements (and straddling both): the table carries 64-bit
+# element offsets, and every row is still scheduled exactly once.
+BIG_ROWS = [7, 5, 3, 9, 4]
+BIG_COLS = [300, 1000, 4096, 64, 513]
+BIG_OFFS = [(1 << 31) - 700, (1 << 31) + 12344, (1 << 32) - 3 * 4096 // 2, (1 << 32) + (1 << 20),
+            (1 << 32) + (1 << 21) + 3]
+
+
+@pytest.mark.parametrize("schedule", ["rr", "balanced", "xcd"])
+@pytest.mark.parametrize("topo", ["mi355x", "odd"])
+def test_offsets_beyond_2_32_elements(schedule, topo):
+    p = bsm.bsm_plan_create(BIG_ROWS, BIG_COLS, BIG_OFFS, dtype="f32", schedule=schedule,
+                            topology=TOPOLOGIES[topo], device=-1)
+    d = bsm.bsm_plan_describe(p)
+    ptr, items, _, _ = bsm.bsm_plan_export(p)
+    p.destroy()
+    assert pc.check_exactly_once(ptr, items, BIG_OFFS, BIG_ROWS, BIG_COLS) == []
+    assert d["extent_elems"] == max(o + r * c for o, r, c in zip(BIG_OFFS, BIG_ROWS, BIG_COLS))
+    assert int(items["elem_offset"].max()) > (1 << 32)
