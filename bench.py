@@ -122,7 +122,8 @@ def time_copy(xs, outs, nbytes, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def run_workload(name, schedule, steps, warmup, rotate=None, w=None, topology=None):
+def run_workload(name, schedule, steps, warmup, rotate=None, w=None, topology=None,
+                 xcd_weight=None):
     """Bench one (workload, schedule). Returns a dict of measurements."""
     import torch
 
@@ -137,7 +138,8 @@ def run_workload(name, schedule, steps, warmup, rotate=None, w=None, topology=No
     outs = [torch.empty_like(x0) for _ in range(n_pairs)]
     t_plan = time.perf_counter()
     plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
-                               schedule=schedule, topology=topology, device=0)
+                               schedule=schedule, topology=topology, device=0,
+                               xcd_weight=xcd_weight)
     plan_ms = (time.perf_counter() - t_plan) * 1e3
     st = bsm.bsm_plan_describe(plan)
     region_ms, launch_ms = time_plan(plan, xs, outs, steps, warmup)
@@ -199,6 +201,44 @@ def run_backward(name, schedule, steps, warmup, w=None):
     torch.cuda.empty_cache()
     return dict(workload=w.name, schedule=schedule, algorithmic_bytes=nbytes, ms_per_step=ms,
                 gbs=nbytes / (ms * 1e-3) / 1e9, buffers_rotated=n_sets)
+
+
+def xcd_weight_calibration(name, steps, warmup):
+    """Weighted load balancing (Section 4.2) with weights measured on this GPU: one traced
+    launch of the unweighted XCD plan gives each XCD's rate (its bytes over the span of its
+    waves); the weights are those rates (the inverse of each XCD's time per byte). Both plans
+    are then timed."""
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    w = workloads.generate(name)
+    x = _to_device(w)
+    out = torch.empty_like(x)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule="xcd", device=0)
+    st = bsm.bsm_plan_describe(plan)
+    trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device=x.device)
+    rates = np.zeros(st["n_xcd"])
+    for _ in range(3):  # average three traced launches
+        bsm.bsm_plan_execute(plan, x, out)
+        bsm.bsm_plan_execute(plan, x, out, trace=trace)
+        torch.cuda.synchronize()
+        rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+        for xc in range(st["n_xcd"]):
+            r = rec[rec["xcc_id"] == xc]
+            span = float(r["t_end"].max() - r["t_start"].min())
+            rates[xc] += st["xcd_bytes"][xc] / max(span, 1.0)
+    plan.destroy()
+    del x, out, trace
+    torch.cuda.empty_cache()
+    weights = (rates / rates.max()).tolist()
+    r0, _ = run_workload(name, "xcd", steps, warmup, w=w)
+    r1, _ = run_workload(name, "xcd", steps, warmup, w=w, xcd_weight=weights)
+    return {"weights": [round(v, 4) for v in weights], "unweighted_gbs": round(r0["gbs"], 1),
+            "weighted_gbs": round(r1["gbs"], 1)}
 
 
 def trace_stats(w, schedule):
@@ -426,6 +466,7 @@ def main() -> int:
                          ("c5", "balanced"), ("c5", "rr")):
             r = run_backward(cfg, sch, args.steps, args.warmup)
             extra[f"{cfg}_backward_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "algorithmic_bytes")}
+        extra["xcd_weighted_c2"] = xcd_weight_calibration("c2", args.steps, args.warmup)
         extra["producer_consumer"] = producer_consumer()
         extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region and

@@ -196,6 +196,19 @@ bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets,
                            bsm_dtype dtype, bsm_schedule schedule, const int8_t* home_xcd,
                            const bsm_topology* topology, int device);
 
+/* bsm_plan_create with weighted load balancing (Section 4.2): under the XCD schedule, XCD x's
+ * share of the total cost is proportional to (its workgroups) * xcd_weight[x] instead of to its
+ * workgroups alone; the paper derives the weights from latencies, in inverse proportion, and
+ * a caller can pass e.g. each XCD's measured throughput.  xcd_weight: NULL (equal weights, the
+ * same table as bsm_plan_create) or [topology n_xcd] finite values >= 0, not all 0 (any
+ * scale; an XCD of weight 0 receives no rows).  RR and BALANCED ignore the weights.  Other
+ * arguments as bsm_plan_create; BSM_ERR_INVALID_ARG for bad weights. */
+bsm_status bsm_plan_create_weighted(bsm_plan* out_plan, const int64_t* slice_offsets,
+                                    const int32_t* rows, const int32_t* cols, int64_t batch,
+                                    bsm_dtype dtype, bsm_schedule schedule,
+                                    const int8_t* home_xcd, const float* xcd_weight,
+                                    const bsm_topology* topology, int device);
+
 /* Run a plan: out = row softmax of in, on `stream`.  `trace` is NULL or a device buffer of
  * stats.trace_bytes bytes that receives one bsm_trace_rec per wave. */
 bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace);

@@ -186,3 +186,12 @@ def lpt_makespan(costs, n_cores: int):
 def min_moved(loads, targets):
     """Least total load any rebalancing must take off the banks: sum of excess over target."""
     return float(sum(max(0.0, float(l) - float(t)) for l, t in zip(loads, targets)))
+
+
+def weighted_shares(total, workers_per_bank, weights):
+    """Targets of the weighted load balancing of Section 4.2: each bank's share of the total
+    load is proportional to its number of compute units times its weight (the paper takes the
+    weights in inverse proportion to latencies)."""
+    prod = [float(p) * float(w) for p, w in zip(workers_per_bank, weights)]
+    s = sum(prod)
+    return [float(total) * q / s for q in prod]

@@ -108,6 +108,9 @@ def load() -> ctypes.CDLL:
                         ctypes.c_int),
         "bsm_plan_create": ([P(vp), P(i64), P(i32), P(i32), i64, ctypes.c_int, ctypes.c_int,
                              P(ctypes.c_int8), P(bsm_topology), ctypes.c_int], ctypes.c_int),
+        "bsm_plan_create_weighted": ([P(vp), P(i64), P(i32), P(i32), i64, ctypes.c_int,
+                                      ctypes.c_int, P(ctypes.c_int8), P(ctypes.c_float),
+                                      P(bsm_topology), ctypes.c_int], ctypes.c_int),
         "bsm_plan_execute": ([vp, vp, vp, vp, vp], ctypes.c_int),
         "bsm_plan_execute_backward": ([vp, vp, vp, vp, vp, vp], ctypes.c_int),
         "bsm_softmax_backward": ([vp, vp, vp, P(i64), P(i32), P(i32), i64, ctypes.c_int,
@@ -288,20 +291,32 @@ class Plan:
 
 
 def bsm_plan_create(rows, cols, slice_offsets=None, batch=None, dtype="f32", schedule="balanced",
-                    home_xcd=None, topology=None, device=0) -> Plan:
+                    home_xcd=None, topology=None, device=0, xcd_weight=None) -> Plan:
     """Build a plan. `topology`: None, a bsm_topology or a dict of its fields. device=-1 makes
-    a host-only plan (needs a topology) that can be described and exported but not run."""
+    a host-only plan (needs a topology) that can be described and exported but not run.
+    `xcd_weight`: None or one weight per XCD (bsm_plan_create_weighted)."""
     lib = load()
     _, op, _, rp, _, cp, n = keep = _geometry(rows, cols, slice_offsets, batch)
     h, hp = _arr(home_xcd, np.int8)
+    wt, wp = _arr(xcd_weight, np.float32)
     topo = None
     if topology is not None:
         topo = topology if isinstance(topology, bsm_topology) else bsm_topology(**topology)
+    if xcd_weight is not None:
+        n_xcd = topo.n_xcd if topo is not None and topo.n_xcd > 0 else (
+            bsm_default_topology(int(device))["n_xcd"] if int(device) >= 0 else 8)
+        if wt.shape[0] != n_xcd:
+            raise ValueError(f"xcd_weight needs {n_xcd} entries (one per XCD), got {wt.shape[0]}")
     handle = ctypes.c_void_p()
-    _check(lib.bsm_plan_create(ctypes.byref(handle), op, rp, cp, n, _dtype_code(dtype),
-                               _schedule_code(schedule), hp,
-                               ctypes.byref(topo) if topo is not None else None, int(device)))
-    del keep, h
+    tp = ctypes.byref(topo) if topo is not None else None
+    if xcd_weight is None:
+        _check(lib.bsm_plan_create(ctypes.byref(handle), op, rp, cp, n, _dtype_code(dtype),
+                                   _schedule_code(schedule), hp, tp, int(device)))
+    else:
+        _check(lib.bsm_plan_create_weighted(ctypes.byref(handle), op, rp, cp, n,
+                                            _dtype_code(dtype), _schedule_code(schedule), hp, wp,
+                                            tp, int(device)))
+    del keep, h, wt
     st = bsm_plan_stats()
     _check(lib.bsm_plan_describe(handle.value, ctypes.byref(st)))
     return Plan(handle.value, n, int(device), int(st.extent_elems), int(st.trace_bytes),

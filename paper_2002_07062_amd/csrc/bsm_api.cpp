@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -212,9 +213,27 @@ void free_device(bsm_plan p) {
     }
 }
 
+// Caller weights (any positive scale) -> integer weights with the largest at 2^30.
+bsm_status resolve_weights(const float* w, bsm::Topology* t) {
+    t->xcd_weight.clear();
+    if (!w) return BSM_OK;
+    float mx = 0.0f;
+    for (int x = 0; x < t->n_xcd; ++x) {
+        if (!std::isfinite(w[x]) || w[x] < 0.0f)
+            return fail(BSM_ERR_INVALID_ARG, "xcd_weight[%d] = %g: weights must be finite and >= 0", x,
+                        static_cast<double>(w[x]));
+        mx = std::max(mx, w[x]);
+    }
+    if (!(mx > 0.0f)) return fail(BSM_ERR_INVALID_ARG, "xcd_weight: every weight is 0");
+    for (int x = 0; x < t->n_xcd; ++x)
+        t->xcd_weight.push_back(static_cast<int64_t>(std::llround(static_cast<double>(w[x]) / mx * 1073741824.0)));
+    return BSM_OK;
+}
+
 bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* rows,
                        const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
-                       const int8_t* home_xcd, const bsm_topology* topology, int device) {
+                       const int8_t* home_xcd, const float* xcd_weight,
+                       const bsm_topology* topology, int device) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
@@ -235,6 +254,10 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
         bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
         if (st != BSM_OK) return st;
+        st = resolve_weights(xcd_weight, &p->topo);
+        if (st != BSM_OK) return st;
+        err = bsm::check_topology(p->topo);
+        if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "topology: %s", err.c_str());
         err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, p->kernel_class, &p->table);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "plan: %s", err.c_str());
     } catch (const std::bad_alloc&) {
@@ -409,7 +432,7 @@ bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
     }
     if (!plan) {
         bsm_status st = create_plan(&plan, slice_offsets, rows, cols, batch, dtype, schedule,
-                                    nullptr, nullptr, device);
+                                    nullptr, nullptr, nullptr, device);
         if (st != BSM_OK) return st;
         g_cache.push_front(CacheEntry{std::move(key), plan});
         while (g_cache.size() > kCacheMax) {
@@ -429,7 +452,16 @@ bsm_status bsm_plan_create(bsm_plan* out_plan, const int64_t* slice_offsets, con
                            bsm_schedule schedule, const int8_t* home_xcd,
                            const bsm_topology* topology, int device) {
     return create_plan(out_plan, slice_offsets, rows, cols, batch, dtype, schedule, home_xcd,
-                       topology, device);
+                       nullptr, topology, device);
+}
+
+bsm_status bsm_plan_create_weighted(bsm_plan* out_plan, const int64_t* slice_offsets,
+                                    const int32_t* rows, const int32_t* cols, int64_t batch,
+                                    bsm_dtype dtype, bsm_schedule schedule,
+                                    const int8_t* home_xcd, const float* xcd_weight,
+                                    const bsm_topology* topology, int device) {
+    return create_plan(out_plan, slice_offsets, rows, cols, batch, dtype, schedule, home_xcd,
+                       xcd_weight, topology, device);
 }
 
 bsm_status bsm_plan_execute(bsm_plan plan, const void* in, void* out, void* stream, void* trace) {

@@ -263,9 +263,16 @@ std::vector<std::vector<Span>> xcd_streams(const Geometry& g, const Topology& t,
         load[x] += c;
         total += c;
     }
-    // Fair share of XCD x: total * Px / P (XCDs differ only in how many workgroups they run).
+    // Share of XCD x: total * Px Wx / sum(Py Wy), with Px its workgroups and Wx its weight
+    // (Section 4.2's weighted balancing; all weights equal unless the caller gives them).
+    std::vector<i128> Wx(static_cast<size_t>(n));
+    i128 wsum = 0;
+    for (int x = 0; x < n; ++x) {
+        Wx[x] = static_cast<i128>(Px[x]) * (t.xcd_weight.empty() ? 1 : t.xcd_weight[x]);
+        wsum += Wx[x];
+    }
     std::vector<i128> share(static_cast<size_t>(n));
-    for (int x = 0; x < n; ++x) share[x] = total * Px[x] / P;
+    for (int x = 0; x < n; ++x) share[x] = total * Wx[x] / wsum;
     double min_moved = 0.0;
     for (int x = 0; x < n; ++x)
         if (load[x] > share[x]) min_moved += static_cast<double>(load[x] - share[x]);
@@ -308,10 +315,10 @@ std::vector<std::vector<Span>> xcd_streams(const Geometry& g, const Topology& t,
                 any = any || deficit[x] > 0;
             }
         }
-        if (!any) {  // rounding left no deficit: the least loaded XCD (per workgroup) takes it
+        if (!any) {  // rounding left no deficit: the least loaded XCD per weight takes it
             int best = -1;
             for (int x = 0; x < n; ++x)
-                if (Px[x] > 0 && (best < 0 || load[x] * Px[best] < load[best] * Px[x])) best = x;
+                if (Wx[x] > 0 && (best < 0 || load[x] * Wx[best] < load[best] * Wx[x])) best = x;
             deficit[best] = 1;
         }
         std::vector<Span> pool_spans;
@@ -452,6 +459,16 @@ std::string check_topology(const Topology& t) {
     if (!(t.item_cost >= 0.0) || !(t.row_cost >= 0.0) || !std::isfinite(t.item_cost) ||
         !std::isfinite(t.row_cost) || t.row_cost > 1e12 || t.item_cost > 1e12)
         return "cost model values must be finite and >= 0";
+    if (!t.xcd_weight.empty()) {
+        if (static_cast<int>(t.xcd_weight.size()) != t.n_xcd) return "xcd_weight needs n_xcd entries";
+        int64_t with_workers = 0;
+        for (int x = 0; x < t.n_xcd; ++x) {
+            if (t.xcd_weight[x] < 0 || t.xcd_weight[x] > (int64_t(1) << 30))
+                return "xcd_weight out of range";
+            if (x < t.n_wg()) with_workers += t.xcd_weight[x];
+        }
+        if (with_workers == 0) return "xcd_weight gives every XCD with workgroups weight 0";
+    }
     return "";
 }
 

@@ -30,6 +30,9 @@ struct Topology {
     int32_t piece_bytes = 8192;  // traffic per worker piece in one round
     double item_cost = 1024.0;   // byte equivalents
     double row_cost = 64.0;      // byte equivalents on top of the row's bytes
+    // Weighted load balancing (Section 4.2): relative weight of each XCD's share under the XCD
+    // schedule, e.g. in inverse proportion to a measured latency.  Empty = equal weights.
+    std::vector<int64_t> xcd_weight;
     int32_t n_wg() const { return n_cu * wg_per_cu; }
     int32_t waves_per_wg() const { return wg_threads / 64; }
 };

@@ -390,3 +390,25 @@ def test_temporal_cache_policy_gives_the_same_bits(cfg):
     assert st["flags"] == bsm.BSM_FLAG_TEMPORAL
     view = torch.int16 if w.dtype == "bf16" else torch.int32
     assert torch.equal(a.view(view), b.view(view))
+
+
+def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
+    """Weighted load balancing moves rows between XCDs but never changes a result; an XCD of
+    weight 0 runs no rows (per-wave trace)."""
+    w = workloads.generate("c5", batch=96)
+    x = to_device(w.x, "f32")
+    ref, _ = run_plan(w, "xcd", x=x)
+    n = int(w.offsets[-1])
+    out = sentinel_like(n, "f32")
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype="f32", schedule="xcd",
+                               device=0, xcd_weight=[1, 1, 1, 1, 1, 1, 1, 0])
+    st = bsm.bsm_plan_describe(plan)
+    trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
+    bsm.bsm_plan_execute(plan, x, out, trace=trace)
+    torch.cuda.synchronize()
+    plan.destroy()
+    assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
+    rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+    assert rec["rows"][rec["xcc_id"] == 7].sum() == 0
+    assert rec["rows"].sum() == int(w.rows.sum())
+    assert st["xcd_bytes"][7] == 0

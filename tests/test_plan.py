@@ -283,3 +283,63 @@ def test_offsets_beyond_2_32_elements(schedule, topo):
     assert pc.check_exactly_once(ptr, items, BIG_OFFS, BIG_ROWS, BIG_COLS) == []
     assert d["extent_elems"] == max(o + r * c for o, r, c in zip(BIG_OFFS, BIG_ROWS, BIG_COLS))
     assert int(items["elem_offset"].max()) > (1 << 32)
+
+
+def _weighted_plan(w, schedule, topo, weights, home=None):
+    p = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                            schedule=schedule, topology=topo, home_xcd=home, device=-1,
+                            xcd_weight=weights)
+    d = bsm.bsm_plan_describe(p)
+    ptr, items, home_out, ov = bsm.bsm_plan_export(p)
+    p.destroy()
+    return d, ptr, items, home_out, ov
+
+
+@pytest.mark.parametrize("weights", [[1, 2, 3, 4, 1, 2, 3, 4], [5, 1, 1, 1, 1, 1, 1, 1],
+                                     [0.25, 1, 1, 1, 1, 1, 1, 0.5]])
+@pytest.mark.parametrize("pattern", ["skewed", "virtual"])
+def test_weighted_load_balancing(weights, pattern):
+    """Section 4.2's weighted variant: each XCD ends within about a row of its weighted share
+    (workgroups x weight), and the moved load is the least any balancer must move to reach
+    those shares (plus row rounding)."""
+    w = workloads.generate("c5", batch=120)
+    topo = dict(n_cu=32, n_xcd=8, wg_per_cu=1, wg_threads=128)
+    home = None if pattern == "virtual" else \
+        np.random.default_rng(4).choice([0, 1, 2], size=w.batch).astype(np.int8)
+    d, ptr, items, home_out, _ = _weighted_plan(w, "xcd", topo, weights, home)
+    assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == []
+    per_xcd, moved = _xcd_loads(w, d, ptr, items, topo, home_out)
+    px = [topo["n_cu"] * topo["wg_per_cu"] // topo["n_xcd"]] * topo["n_xcd"]
+    share = pc.weighted_shares(per_xcd.sum(), px, weights)
+    biggest_row = ROW_COST + 2 * 4 * int(w.cols.max())
+    assert np.all(np.abs(per_xcd - np.array(share)) <= 2 * biggest_row), (per_xcd, share)
+    loads_before = np.zeros(topo["n_xcd"])
+    rc = _row_cost(4)
+    for s in range(w.batch):
+        loads_before[home_out[s]] += int(w.rows[s]) * rc(int(w.cols[s]))
+    least = pc.min_moved(loads_before, pc.weighted_shares(loads_before.sum(), px, weights))
+    assert abs(d["moved_cost"] - least) <= topo["n_xcd"] * biggest_row / 2 + 8
+
+
+def test_equal_weights_give_the_unweighted_table_and_zero_weight_gets_nothing():
+    w = workloads.generate("c5", batch=100)
+    _, ptr0, items0, _, _ = _plan(w, "xcd", MI355X)
+    _, ptr1, items1, _, _ = _weighted_plan(w, "xcd", MI355X, [3.7] * 8)
+    assert np.array_equal(ptr0, ptr1) and np.array_equal(items0, items1)
+    for sch in ("rr", "balanced"):  # the weights concern the XCD schedule only
+        _, p0, i0, _, _ = _plan(w, sch, MI355X)
+        _, p1, i1, _, _ = _weighted_plan(w, sch, MI355X, [1, 9, 1, 9, 1, 9, 1, 9])
+        assert np.array_equal(p0, p1) and np.array_equal(i0, i1)
+    d, ptr, items, home, _ = _weighted_plan(w, "xcd", MI355X, [1] * 7 + [0])
+    assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == []
+    per_xcd, _ = _xcd_loads(w, d, ptr, items, MI355X, home)
+    assert per_xcd[7] == 0 and np.all(per_xcd[:7] > 0)
+
+
+@pytest.mark.parametrize("weights,err", [([1] * 7 + [-1], bsm.BsmError), ([0] * 8, bsm.BsmError),
+                                         ([1] * 7 + [float("nan")], bsm.BsmError),
+                                         ([1] * 7, ValueError)])
+def test_bad_weights_are_rejected(weights, err):
+    w = workloads.generate("c1")
+    with pytest.raises(err):
+        _weighted_plan(w, "xcd", MI355X, weights)

@@ -121,3 +121,16 @@ def test_worker_loads_and_min_moved():
     assert loads.tolist() == [121, 142]
     assert pc.min_moved([10, 2, 6], [6, 6, 6]) == 4
     assert pc.min_moved([6, 6], [6, 6]) == 0
+
+
+def test_weighted_shares_closed_forms():
+    """Equal weights give shares proportional to compute units; weights scale them; a bank of
+    weight 0 gets nothing; shares always add up to the total."""
+    assert pc.weighted_shares(80, [4, 4, 4, 4], [1, 1, 1, 1]) == [20.0] * 4
+    assert pc.weighted_shares(80, [2, 6, 4, 4], [7, 7, 7, 7]) == [10.0, 30.0, 20.0, 20.0]
+    assert pc.weighted_shares(60, [4, 4, 4], [1, 2, 3]) == [10.0, 20.0, 30.0]
+    assert pc.weighted_shares(30, [4, 4, 4], [1, 0, 2]) == [10.0, 0.0, 20.0]
+    s = pc.weighted_shares(1000, [3, 5, 2, 7], [0.3, 1.7, 2.0, 0.9])
+    assert abs(sum(s) - 1000) < 1e-9
+    # min_moved against weighted targets: only the excess over each target moves
+    assert pc.min_moved([60, 0, 0], pc.weighted_shares(60, [4, 4, 4], [1, 2, 3])) == 50.0
