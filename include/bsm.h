@@ -232,6 +232,37 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
                                 const int32_t* cols, int64_t batch, bsm_dtype dtype,
                                 bsm_schedule schedule, void* stream);
 
+/* ------------------------------------------------------------------ batched matrix products
+ * The two batch matrix multiplications of Section 6 that surround the softmax in BERT
+ * attention -- scores (512 x 64) x (64 x 512) and context (512 x 512) x (512 x 64), batch 384 --
+ * scheduled by the same tables: the outputs C_b are the slices (m rows of n), cut by RR,
+ * BALANCED or XCD exactly as for the softmax (pieces of whole 32-row blocks).
+ *   BSM_GEMM_NT:  C_b = alpha * A_b * B_b^T    A_b m x k,  B_b n x k  (scores Q K^T)
+ *   BSM_GEMM_NN:  C_b = alpha * A_b * B_b      A_b m x k,  B_b k x n  (context P V)
+ * All operands row-major, batch after batch (A_b at b*m*k, B_b at b*n*k, C_b at b*m*n
+ * elements).  A and B are bf16; C is fp32 or bf16 (round to nearest even); accumulation in
+ * fp32 on the matrix cores. */
+typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1 } bsm_gemm_layout;
+
+/* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
+ * bsm_plan_create).  A plan made here runs only with bsm_gemm_execute. */
+bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,
+                                int32_t k, bsm_gemm_layout layout, bsm_dtype out_dtype,
+                                bsm_schedule schedule, const int8_t* home_xcd,
+                                const bsm_topology* topology, int device);
+
+/* C = alpha * product of A and B under the plan, on `stream` (asynchronous).  A, B, C are
+ * device buffers; C must not overlap A or B (BSM_ERR_ALIAS).  k == 0 stores zeros.  `trace`
+ * as for bsm_plan_execute (records count output rows). */
+bsm_status bsm_gemm_execute(bsm_plan plan, const void* a, const void* b, void* c, float alpha,
+                            void* stream, void* trace);
+
+/* One-shot: plan from the per-device cache, then bsm_gemm_execute.  batch, m or n == 0 is a
+ * no-op that touches no GPU. */
+bsm_status bsm_gemm(const void* a, const void* b, void* c, int64_t batch, int32_t m, int32_t n,
+                    int32_t k, bsm_gemm_layout layout, bsm_dtype out_dtype, float alpha,
+                    bsm_schedule schedule, void* stream);
+
 bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats);
 
 /* Copy the host work table out: worker_ptr [n_workers + 1] (CSR row pointer: worker v owns

@@ -25,6 +25,8 @@ BSM_MAX_XCD = 16
 BSM_FLAG_TEMPORAL = 1
 
 SCHEDULES = {"rr": BSM_SCHED_RR, "balanced": BSM_SCHED_BALANCED, "xcd": BSM_SCHED_XCD}
+BSM_GEMM_NT, BSM_GEMM_NN = 0, 1
+GEMM_LAYOUTS = {"nt": BSM_GEMM_NT, "nn": BSM_GEMM_NN}
 DTYPES = {"f32": BSM_F32, "bf16": BSM_BF16}
 
 
@@ -112,6 +114,12 @@ def load() -> ctypes.CDLL:
                                       ctypes.c_int, P(ctypes.c_int8), P(ctypes.c_float),
                                       P(bsm_topology), ctypes.c_int], ctypes.c_int),
         "bsm_plan_execute": ([vp, vp, vp, vp, vp], ctypes.c_int),
+        "bsm_gemm_plan_create": ([P(vp), i64, i32, i32, i32, ctypes.c_int, ctypes.c_int,
+                                  ctypes.c_int, P(ctypes.c_int8), P(bsm_topology), ctypes.c_int],
+                                 ctypes.c_int),
+        "bsm_gemm_execute": ([vp, vp, vp, vp, ctypes.c_float, vp, vp], ctypes.c_int),
+        "bsm_gemm": ([vp, vp, vp, i64, i32, i32, i32, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                      ctypes.c_int, vp], ctypes.c_int),
         "bsm_plan_execute_backward": ([vp, vp, vp, vp, vp, vp], ctypes.c_int),
         "bsm_softmax_backward": ([vp, vp, vp, P(i64), P(i32), P(i32), i64, ctypes.c_int,
                                   ctypes.c_int, vp], ctypes.c_int),
@@ -415,3 +423,66 @@ def bsm_last_error() -> str:
 
 def bsm_abi_version() -> int:
     return int(load().bsm_abi_version())
+
+
+# ------------------------------------------------------------------ batched matrix products
+def _layout_code(layout) -> int:
+    if isinstance(layout, int):
+        return layout
+    return GEMM_LAYOUTS[layout]
+
+
+def _check_gemm_tensors(batch, m, n, k, a, b, c, c_dtype) -> None:
+    for t, need, name in ((a, batch * m * k, "a"), (b, batch * n * k, "b"), (c, batch * m * n, "c")):
+        if t.numel() < need:
+            raise ValueError(f"{name} has {t.numel()} elements, needs {need}")
+    if a.dtype != torch.bfloat16 or b.dtype != torch.bfloat16:
+        raise TypeError("a and b must be bfloat16")
+    if c.dtype != c_dtype:
+        raise TypeError(f"c must be {c_dtype}")
+
+
+def bsm_gemm_plan_create(batch, m, n, k, layout="nt", out_dtype="f32", schedule="balanced",
+                         home_xcd=None, topology=None, device=0) -> Plan:
+    """Plan of the batched product C_b = alpha A_b B_b^T ("nt") or alpha A_b B_b ("nn")."""
+    lib = load()
+    h, hp = _arr(home_xcd, np.int8)
+    topo = None
+    if topology is not None:
+        topo = topology if isinstance(topology, bsm_topology) else bsm_topology(**topology)
+    handle = ctypes.c_void_p()
+    _check(lib.bsm_gemm_plan_create(ctypes.byref(handle), int(batch), int(m), int(n), int(k),
+                                    _layout_code(layout), _dtype_code(out_dtype),
+                                    _schedule_code(schedule), hp,
+                                    ctypes.byref(topo) if topo is not None else None, int(device)))
+    del h
+    st = bsm_plan_stats()
+    _check(lib.bsm_plan_describe(handle.value, ctypes.byref(st)))
+    plan = Plan(handle.value, int(batch), int(device), 0, int(st.trace_bytes), int(st.dtype))
+    plan.gemm = (int(batch), int(m), int(n), int(k))
+    return plan
+
+
+def bsm_gemm_execute(plan: Plan, a, b, c, alpha=1.0, stream=None, trace=None):
+    """c = product of a and b under the plan (see bsm.h). Returns c."""
+    lib = load()
+    batch, m, n, k = plan.gemm
+    _check_gemm_tensors(batch, m, n, k, a, b, c,
+                        torch.float32 if plan.dtype == BSM_F32 else torch.bfloat16)
+    if trace is not None and trace.numel() * trace.element_size() < plan.trace_bytes:
+        raise ValueError(f"trace buffer needs {plan.trace_bytes} bytes")
+    with torch.cuda.device(plan.device):
+        _check(lib.bsm_gemm_execute(plan.handle, _ptr(a), _ptr(b), _ptr(c), float(alpha),
+                                    _stream_of(c, stream), _ptr(trace)))
+    return c
+
+
+def bsm_gemm(a, b, c, batch, m, n, k, layout="nt", alpha=1.0, schedule="balanced", stream=None):
+    """One-shot batched product (plans cached per device). c's dtype picks fp32 or bf16 output."""
+    lib = load()
+    _check_gemm_tensors(batch, m, n, k, a, b, c, c.dtype)
+    with torch.cuda.device(c.device):
+        _check(lib.bsm_gemm(_ptr(a), _ptr(b), _ptr(c), int(batch), int(m), int(n), int(k),
+                            _layout_code(layout), _dtype_code(c.dtype), float(alpha),
+                            _schedule_code(schedule), _stream_of(c, stream)))
+    return c

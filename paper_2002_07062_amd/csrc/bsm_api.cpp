@@ -27,6 +27,11 @@ struct bsm_plan_s {
     bsm::Geometry geo;
     bsm::Table table;
     int kernel_class = 0;
+    // A matrix-product plan (bsm_gemm_plan_create) instead of a softmax plan: the slices are
+    // the outputs C_b (gemm_m x gemm_n), A_b is gemm_m x gemm_k, layout 0 = NT, 1 = NN.
+    bool gemm = false;
+    int gemm_m = 0, gemm_n = 0, gemm_k = 0, gemm_layout = 0;
+    int64_t gemm_batch = 0;
     int lds_floats_per_wave = 0;  // long-row staging (kernel class 4 on a device)
     int32_t flags = 0;            // BSM_FLAG_* bits
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
@@ -233,7 +238,7 @@ bsm_status resolve_weights(const float* w, bsm::Topology* t) {
 bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* rows,
                        const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
                        const int8_t* home_xcd, const float* xcd_weight,
-                       const bsm_topology* topology, int device) {
+                       const bsm_topology* topology, int device, int32_t row_unit = 0) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
@@ -256,6 +261,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         if (st != BSM_OK) return st;
         st = resolve_weights(xcd_weight, &p->topo);
         if (st != BSM_OK) return st;
+        p->topo.row_unit = row_unit;
         err = bsm::check_topology(p->topo);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "topology: %s", err.c_str());
         err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, p->kernel_class, &p->table);
@@ -323,6 +329,7 @@ bool partial_overlap(const void* x, const void* y, int64_t extent_bytes) {
 bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b, void* out,
                         void* stream, void* trace) {
     if (!p) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    if (p->gemm) return fail(BSM_ERR_UNSUPPORTED, "a matrix-product plan runs with bsm_gemm_execute");
     if (p->device < 0) return fail(BSM_ERR_UNSUPPORTED, "host-only plan (device -1) cannot execute");
     const int64_t extent_bytes = p->geo.extent * elem_bytes_of(p->dtype);
     if (p->geo.total_elems == 0) return BSM_OK;
@@ -358,6 +365,75 @@ bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b,
     return BSM_OK;
 }
 
+// --------------------------------------------------------------------- matrix products
+bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n, int32_t k,
+                            int layout, bsm_dtype out_dtype, bsm_schedule schedule,
+                            const int8_t* home_xcd, const bsm_topology* topology, int device) {
+    if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (layout != 0 && layout != 1) return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", layout);
+    if (batch < 0 || m < 0 || n < 0 || k < 0)
+        return fail(BSM_ERR_INVALID_ARG, "negative size (batch %lld, m %d, n %d, k %d)",
+                    static_cast<long long>(batch), m, n, k);
+    if (static_cast<double>(batch) * std::max({m, n, k}) * std::max({m, n, k}) > 1.0e18)
+        return fail(BSM_ERR_INVALID_ARG, "operands too large");
+    const int32_t rows[1] = {m}, cols[1] = {n};
+    bsm_plan p = nullptr;
+    bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
+                                schedule, home_xcd, nullptr, topology, device, /*row_unit=*/32);
+    if (st != BSM_OK) return st;
+    p->gemm = true;
+    p->gemm_m = m;
+    p->gemm_n = n;
+    p->gemm_k = k;
+    p->gemm_layout = layout;
+    p->gemm_batch = batch;
+    p->table.stats.algorithmic_bytes =
+        batch * (2 * (static_cast<int64_t>(m) * k + static_cast<int64_t>(n) * k) +
+                 static_cast<int64_t>(m) * n * elem_bytes_of(out_dtype));
+    *out_plan = p;
+    return BSM_OK;
+}
+
+bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float alpha,
+                        void* stream, void* trace) {
+    if (!p) return fail(BSM_ERR_INVALID_ARG, "plan is NULL");
+    if (!p->gemm) return fail(BSM_ERR_UNSUPPORTED, "a softmax plan runs with bsm_plan_execute");
+    if (p->device < 0) return fail(BSM_ERR_UNSUPPORTED, "host-only plan (device -1) cannot execute");
+    const int64_t nb = p->gemm_batch;
+    const int64_t a_bytes = nb * p->gemm_m * static_cast<int64_t>(p->gemm_k) * 2;
+    const int64_t b_bytes = nb * p->gemm_n * static_cast<int64_t>(p->gemm_k) * 2;
+    const int64_t c_bytes = nb * p->gemm_m * static_cast<int64_t>(p->gemm_n) * elem_bytes_of(p->dtype);
+    if (c_bytes == 0) return BSM_OK;
+    if (!c || !a || !b) return fail(BSM_ERR_INVALID_ARG, "an operand is NULL");
+    if (!std::isfinite(alpha)) return fail(BSM_ERR_INVALID_ARG, "alpha must be finite");
+    auto overlap = [](const void* x, int64_t xn, const void* y, int64_t yn) {
+        const uintptr_t u = reinterpret_cast<uintptr_t>(x), v = reinterpret_cast<uintptr_t>(y);
+        return xn > 0 && yn > 0 && u < v + static_cast<uintptr_t>(yn) && v < u + static_cast<uintptr_t>(xn);
+    };
+    if (overlap(c, c_bytes, a, a_bytes) || overlap(c, c_bytes, b, b_bytes))
+        return fail(BSM_ERR_ALIAS, "C overlaps A or B");
+    if ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b)) % 2 != 0 ||
+        reinterpret_cast<uintptr_t>(c) % elem_bytes_of(p->dtype) != 0)
+        return fail(BSM_ERR_INVALID_ARG, "an operand is not aligned to its element size");
+    DeviceGuard g;
+    hipError_t e = g.enter(p->device);
+    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::lock_guard<std::mutex> lock(p->mu);
+    // k == 0 runs the same kernel: an empty reduction stores zeros
+    e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, a, b, c, p->gemm_m, p->gemm_n,
+                         p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(),
+                         p->topo.wg_threads, p->table.per_wave ? 1 : 0, trace, s);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    e = hipEventRecord(p->last_use, s);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (p->used && s != p->last_stream) p->many_streams = true;
+    p->last_stream = s;
+    p->used = true;
+    return BSM_OK;
+}
+
 // ---------------------------------------------------------------------------- plan cache
 struct CacheKey {
     int device;
@@ -367,11 +443,18 @@ struct CacheKey {
     int64_t batch;
     std::vector<int64_t> off;
     std::vector<int32_t> R, C;
+    int gemm_k = -1;  // >= 0: a matrix-product plan with this reduction depth
+    int gemm_layout = 0;
     bool operator==(const CacheKey& o) const {
         return device == o.device && dtype == o.dtype && schedule == o.schedule &&
-               uniform == o.uniform && batch == o.batch && off == o.off && R == o.R && C == o.C;
+               uniform == o.uniform && batch == o.batch && off == o.off && R == o.R && C == o.C &&
+               gemm_k == o.gemm_k && gemm_layout == o.gemm_layout;
     }
 };
+
+// Looks up (or builds and inserts) the cached plan for `key`; the caller holds g_cache_mu.
+template <class Build>
+bsm_status cached_plan(CacheKey key, Build build, bsm_plan* out);
 
 struct CacheEntry {
     CacheKey key;
@@ -386,6 +469,27 @@ void destroy_plan(bsm_plan p) {
     if (!p) return;
     free_device(p);
     delete p;
+}
+
+template <class Build>
+bsm_status cached_plan(CacheKey key, Build build, bsm_plan* out) {
+    for (auto it = g_cache.begin(); it != g_cache.end(); ++it) {
+        if (it->key == key) {
+            *out = it->plan;
+            g_cache.splice(g_cache.begin(), g_cache, it);
+            return BSM_OK;
+        }
+    }
+    bsm_plan plan = nullptr;
+    bsm_status st = build(&plan);
+    if (st != BSM_OK) return st;
+    g_cache.push_front(CacheEntry{std::move(key), plan});
+    while (g_cache.size() > kCacheMax) {
+        destroy_plan(g_cache.back().plan);
+        g_cache.pop_back();
+    }
+    *out = plan;
+    return BSM_OK;
 }
 
 // One-shot call: validates the geometry (no HIP call for bad arguments or no-ops), then runs a
@@ -423,23 +527,11 @@ bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
     }
     std::lock_guard<std::mutex> lock(g_cache_mu);
     bsm_plan plan = nullptr;
-    for (auto it = g_cache.begin(); it != g_cache.end(); ++it) {
-        if (it->key == key) {
-            plan = it->plan;
-            g_cache.splice(g_cache.begin(), g_cache, it);
-            break;
-        }
-    }
-    if (!plan) {
-        bsm_status st = create_plan(&plan, slice_offsets, rows, cols, batch, dtype, schedule,
-                                    nullptr, nullptr, nullptr, device);
-        if (st != BSM_OK) return st;
-        g_cache.push_front(CacheEntry{std::move(key), plan});
-        while (g_cache.size() > kCacheMax) {
-            destroy_plan(g_cache.back().plan);
-            g_cache.pop_back();
-        }
-    }
+    bsm_status st = cached_plan(std::move(key), [&](bsm_plan* np) {
+        return create_plan(np, slice_offsets, rows, cols, batch, dtype, schedule, nullptr, nullptr,
+                           nullptr, device);
+    }, &plan);
+    if (st != BSM_OK) return st;
     return execute_plan(plan, backward, a, b, out, stream, nullptr);
 }
 
@@ -501,6 +593,43 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, 
                        void* stream) {
     return one_shot(false, in, nullptr, out, slice_offsets, rows, cols, batch, dtype, schedule,
                     stream);
+}
+
+bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,
+                                int32_t k, bsm_gemm_layout layout, bsm_dtype out_dtype,
+                                bsm_schedule schedule, const int8_t* home_xcd,
+                                const bsm_topology* topology, int device) {
+    return create_gemm_plan(out_plan, batch, m, n, k, static_cast<int>(layout), out_dtype, schedule,
+                            home_xcd, topology, device);
+}
+
+bsm_status bsm_gemm_execute(bsm_plan plan, const void* a, const void* b, void* c, float alpha,
+                            void* stream, void* trace) {
+    return execute_gemm(plan, a, b, c, alpha, stream, trace);
+}
+
+bsm_status bsm_gemm(const void* a, const void* b, void* c, int64_t batch, int32_t m, int32_t n,
+                    int32_t k, bsm_gemm_layout layout, bsm_dtype out_dtype, float alpha,
+                    bsm_schedule schedule, void* stream) {
+    if (!valid_dtype(out_dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(out_dtype));
+    if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
+    if (layout != BSM_GEMM_NT && layout != BSM_GEMM_NN)
+        return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", static_cast<int>(layout));
+    if (batch < 0 || m < 0 || n < 0 || k < 0) return fail(BSM_ERR_INVALID_ARG, "negative size");
+    if (batch == 0 || m == 0 || n == 0) return BSM_OK;
+    if (!a || !b || !c) return fail(BSM_ERR_INVALID_ARG, "an operand is NULL");
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    CacheKey key{device, out_dtype, schedule, true, batch, {}, {m}, {n}, k, static_cast<int>(layout)};
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    bsm_plan plan = nullptr;
+    bsm_status st = cached_plan(std::move(key), [&](bsm_plan* np) {
+        return create_gemm_plan(np, batch, m, n, k, static_cast<int>(layout), out_dtype, schedule,
+                                nullptr, nullptr, device);
+    }, &plan);
+    if (st != BSM_OK) return st;
+    return execute_gemm(plan, a, b, c, alpha, stream, nullptr);
 }
 
 bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,

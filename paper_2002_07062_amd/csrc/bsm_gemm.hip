@@ -1,0 +1,60 @@
+// Host launch wrappers of the batched matrix-product kernels (device code in bsm_gemm.hpp).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "bsm.h"
+#include "bsm_gemm.hpp"
+#include "bsm_launch.hpp"
+
+namespace {
+
+using bsm_mm::Shape;
+
+template <int LAYOUT, bool BF16OUT, bool VEC>
+hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const int32_t* worker_ptr,
+                    const bsm_item* items, int n_wg, int wg_threads, int per_wave, void* trace,
+                    hipStream_t stream) {
+    const uint16_t* a_a = static_cast<const uint16_t*>(a);
+    const uint16_t* a_b = static_cast<const uint16_t*>(b);
+    void* a_c = c;
+    Shape a_s = s;
+    bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
+    void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &per_wave, &a_trace};
+    return hipLaunchKernel(
+        reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<LAYOUT, BF16OUT, VEC, VEC, VEC>),
+        dim3(n_wg), dim3(wg_threads), args, 0, stream);
+}
+
+}  // namespace
+
+namespace bsm {
+
+hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
+                       int n, int k, float alpha, const int32_t* d_worker_ptr,
+                       const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
+                       void* trace, hipStream_t stream) {
+    Shape s;
+    s.m = m;
+    s.n = n;
+    s.k = k;
+    s.a_batch = static_cast<int64_t>(m) * k;
+    s.b_batch = static_cast<int64_t>(n) * k;
+    s.c_batch = static_cast<int64_t>(m) * n;
+    s.alpha = alpha;
+    const uintptr_t ab = reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b);
+    s.vec_a = (k % 8 == 0) && (ab & 15) == 0;
+    s.vec_b = s.vec_a;
+    s.vec_c = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(c) & 15) == 0;
+    const bool vec = s.vec_a && s.vec_c;
+#define BSM_G(L, O, V) launch_g<L, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, wg_threads, per_wave, trace, stream)
+    if (layout == bsm_mm::kNT) {
+        if (bf16_out) return vec ? BSM_G(bsm_mm::kNT, true, true) : BSM_G(bsm_mm::kNT, true, false);
+        return vec ? BSM_G(bsm_mm::kNT, false, true) : BSM_G(bsm_mm::kNT, false, false);
+    }
+    if (bf16_out) return vec ? BSM_G(bsm_mm::kNN, true, true) : BSM_G(bsm_mm::kNN, true, false);
+    return vec ? BSM_G(bsm_mm::kNN, false, true) : BSM_G(bsm_mm::kNN, false, false);
+#undef BSM_G
+}
+
+}  // namespace bsm

@@ -33,6 +33,14 @@ hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool tempo
                                    const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
                                    int lds_floats_per_wave, void* trace, hipStream_t stream);
 
+// Batched matrix product under a table whose slices are the outputs C_b (m x n each, batch
+// after batch): layout 0 (NT) C_b = alpha A_b B_b^T, layout 1 (NN) C_b = alpha A_b B_b; bf16
+// A and B, fp32 or bf16 C.
+hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
+                       int n, int k, float alpha, const int32_t* d_worker_ptr,
+                       const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
+                       void* trace, hipStream_t stream);
+
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
                                size_t dyn_lds_bytes, int* n);

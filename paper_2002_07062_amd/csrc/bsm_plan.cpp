@@ -72,7 +72,9 @@ std::vector<Segment> segments_of(const std::vector<Span>& stream, const Topology
     std::vector<Segment> segs;
     for (const Span& s : stream) {
         const int64_t rc = row_cost_of(t, es, s.cols);
-        const int32_t unit = whole_steps ? std::max(1, wave_step_rows(s.cols, es, kernel_class)) : 1;
+        const int32_t unit = !whole_steps ? 1
+                             : t.row_unit > 0 ? t.row_unit
+                                              : std::max(1, wave_step_rows(s.cols, es, kernel_class));
         const int64_t full = s.nrows / unit, tail = s.nrows % unit;
         if (full > 0) segs.push_back(Segment{s.off, s.cols, unit, full, unit * rc});
         if (tail > 0)

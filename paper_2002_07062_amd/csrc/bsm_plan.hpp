@@ -33,6 +33,9 @@ struct Topology {
     // Weighted load balancing (Section 4.2): relative weight of each XCD's share under the XCD
     // schedule, e.g. in inverse proportion to a measured latency.  Empty = equal weights.
     std::vector<int64_t> xcd_weight;
+    // Rows per cutting unit (0: the softmax register-tile step for the row's length).  The
+    // matrix-product kernels take rows 32 at a time.
+    int32_t row_unit = 0;
     int32_t n_wg() const { return n_cu * wg_per_cu; }
     int32_t waves_per_wg() const { return wg_threads / 64; }
 };

@@ -1,0 +1,132 @@
+"""GPU parity of the batched matrix products (bsm_gemm_*) against the fp64 oracle: Section 6's
+two products at their full size (batch 384) under every schedule, both output types, tails in
+every dimension, alpha, the empty reduction, and the one-shot entry point."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2002_07062_amd as bsm
+import workloads
+from gpu_util import bits_to_f64, to_host_bits
+from oracle import gemm as og
+
+pytestmark = pytest.mark.gpu
+
+SCHEDULES = ("rr", "balanced", "xcd")
+
+
+def _operands(batch, m, n, k, seed):
+    rng = np.random.default_rng(seed)
+    a = workloads._to_bf16_bits(rng.standard_normal(batch * m * k, dtype=np.float32))
+    b = workloads._to_bf16_bits(rng.standard_normal(batch * n * k, dtype=np.float32))
+    return a, b
+
+
+def _dev_bf16(x):
+    return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _check(c_bits, a, b, batch, m, n, k, layout, out, alpha=1.0):
+    ref = og.batched_gemm(a, b, batch, m, n, k, layout, alpha)
+    # fp32 accumulation of k exact products: |err| <= k u sum |a||b| (u = 2^-24), doubled
+    tol = 2.0 * max(k, 1) * 2.0 ** -24 * abs(alpha) * og.abs_product_sums(a, b, batch, m, n, k, layout)
+    if out == "bf16":
+        tol = 2.0 ** -8 * np.abs(ref) + 2.0 * tol
+    got = bits_to_f64(c_bits)
+    err = np.abs(got - ref)
+    bad = err > tol
+    assert not bad.any(), f"{int(bad.sum())} of {err.size} beyond the bound; worst {float(err.max()):.3e}"
+    return float(err.max())
+
+
+def _run(plan_args, a_d, b_d, c, alpha=1.0):
+    p = bsm.bsm_gemm_plan_create(*plan_args, device=0)
+    bsm.bsm_gemm_execute(p, a_d, b_d, c, alpha)
+    torch.cuda.synchronize()
+    p.destroy()
+    return c
+
+
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+@pytest.mark.parametrize("layout,shape", [("nt", (384, 512, 512, 64)), ("nn", (384, 512, 64, 512))],
+                         ids=["scores_QKt", "context_PV"])
+def test_paper_products_all_schedules(layout, shape, out):
+    batch, m, n, k = shape
+    a, b = _operands(batch, m, n, k, seed=70 if layout == "nt" else 71)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    tdt = torch.float32 if out == "f32" else torch.bfloat16
+    first = None
+    for schedule in SCHEDULES:
+        print(f"[gemm {layout} {shape} {out} {schedule}]", flush=True)
+        c = torch.full((batch * m * n,), float("nan"), dtype=tdt, device="cuda")
+        _run((batch, m, n, k, layout, out, schedule), a_d, b_d, c)
+        bits = to_host_bits(c)
+        if first is None:
+            err = _check(bits, a, b, batch, m, n, k, layout, out)
+            print(f"  max abs err {err:.3e}", flush=True)
+            first = bits
+        else:
+            assert np.array_equal(bits, first), schedule
+
+
+@pytest.mark.parametrize("layout", ["nt", "nn"])
+@pytest.mark.parametrize("shape", [(3, 37, 45, 24), (2, 70, 33, 20), (5, 1, 1, 1), (1, 33, 96, 40),
+                                   (4, 64, 200, 136)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_tails_in_every_dimension(layout, shape, out):
+    batch, m, n, k = shape
+    a, b = _operands(batch, m, n, k, seed=72)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    tdt = torch.float32 if out == "f32" else torch.bfloat16
+    for schedule in ("rr", "balanced"):
+        c = torch.full((batch * m * n + 5,), float("nan"), dtype=tdt, device="cuda")
+        _run((batch, m, n, k, layout, out, schedule), a_d, b_d, c, alpha=0.125)
+        bits = to_host_bits(c)
+        _check(bits[: batch * m * n], a, b, batch, m, n, k, layout, out, alpha=0.125)
+        tail = bits_to_f64(bits[batch * m * n:])
+        assert np.all(np.isnan(tail)), "written past C"
+
+
+def test_empty_reduction_stores_zeros_and_noops():
+    a_d = torch.zeros(8, dtype=torch.bfloat16, device="cuda")
+    c = torch.full((2 * 3 * 4,), 7.0, device="cuda")
+    _run((2, 3, 4, 0, "nt", "f32", "balanced"), a_d, a_d, c)
+    assert torch.all(c == 0)
+    c.fill_(7.0)
+    bsm.bsm_gemm(a_d, a_d, c, 0, 3, 4, 5)  # batch 0: nothing
+    torch.cuda.synchronize()
+    assert torch.all(c == 7.0)
+
+
+def test_one_shot_equals_plan_and_rejects_overlap():
+    batch, m, n, k = 24, 512, 512, 64
+    a, b = _operands(batch, m, n, k, seed=73)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    c1 = torch.empty(batch * m * n, device="cuda")
+    c2 = torch.empty_like(c1)
+    _run((batch, m, n, k, "nt", "f32", "xcd"), a_d, b_d, c1)
+    bsm.bsm_gemm(a_d, b_d, c2, batch, m, n, k, "nt", schedule="xcd")
+    bsm.bsm_gemm(a_d, b_d, c2, batch, m, n, k, "nt", schedule="xcd")  # cached plan
+    torch.cuda.synchronize()
+    assert torch.equal(c1.view(torch.int32), c2.view(torch.int32))
+    buf = torch.zeros(batch * m * n, device="cuda")
+    with pytest.raises(bsm.BsmError) as e:  # A is C's memory
+        bsm.bsm_gemm(buf.view(torch.bfloat16), b_d, buf, batch, m, n, k)
+    assert e.value.status == bsm.BSM_ERR_ALIAS
+
+
+def test_trace_counts_every_output_row():
+    batch, m, n, k = 96, 512, 512, 64
+    a, b = _operands(batch, m, n, k, seed=74)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    c = torch.empty(batch * m * n, device="cuda")
+    p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt", "f32", "balanced", device=0)
+    st = bsm.bsm_plan_describe(p)
+    trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
+    bsm.bsm_gemm_execute(p, a_d, b_d, c, trace=trace)
+    torch.cuda.synchronize()
+    p.destroy()
+    rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+    assert int(rec["rows"].sum()) == batch * m
+    assert np.all(rec["xcc_id"] == (rec["wg"] % 8))

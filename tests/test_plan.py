@@ -343,3 +343,46 @@ def test_bad_weights_are_rejected(weights, err):
     w = workloads.generate("c1")
     with pytest.raises(err):
         _weighted_plan(w, "xcd", MI355X, weights)
+
+
+@pytest.mark.parametrize("schedule", ["rr", "balanced", "xcd"])
+@pytest.mark.parametrize("shape", [(384, 512, 512, 64), (384, 512, 64, 512), (7, 45, 33, 20)])
+def test_gemm_plans_cover_every_output_row_in_32_row_blocks(schedule, shape):
+    """Matrix-product plans: the outputs C_b are the slices; every output row is scheduled
+    exactly once; BALANCED cuts whole 32-row blocks (the XCD balancer moves single rows)."""
+    batch, m, n, k = shape
+    p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt", "f32", schedule, topology=MI355X, device=-1)
+    d = bsm.bsm_plan_describe(p)
+    ptr, items, _, _ = bsm.bsm_plan_export(p)
+    p.destroy()
+    offs = np.arange(batch, dtype=np.int64) * m * n
+    assert pc.check_exactly_once(ptr, items, offs, [m] * batch, [n] * batch) == []
+    assert d["algorithmic_bytes"] == batch * (2 * (m * k + n * k) + 4 * m * n)
+    if schedule == "balanced":
+        # pieces are whole 32-row blocks of the row stream (batches follow each other, so a
+        # block may cross into the next batch; the kernel splits it there), the stream's last
+        # piece aside
+        g0 = items["elem_offset"] // n
+        assert np.all(g0 % 32 == 0)
+        assert np.all((items["nrows"] % 32 == 0) | (g0 + items["nrows"] == batch * m))
+
+
+def test_gemm_plan_rejects_bad_arguments():
+    for args in [(-1, 4, 4, 4, 0), (1, -4, 4, 4, 0), (1, 4, 4, 4, 2)]:
+        with pytest.raises(bsm.BsmError) as e:
+            bsm.bsm_gemm_plan_create(*args[:4], layout=args[4], topology=MI355X, device=-1)
+        assert e.value.status == bsm.BSM_ERR_INVALID_ARG
+    # a matrix-product plan does not run as a softmax, nor a softmax plan as a product
+    lib = bsm.load()
+    import ctypes
+    g = bsm.bsm_gemm_plan_create(2, 8, 8, 8, topology=MI355X, device=-1)
+    assert lib.bsm_plan_execute(g.handle, ctypes.c_void_p(16), ctypes.c_void_p(4096), None, None) == bsm.BSM_ERR_UNSUPPORTED
+    g.destroy()
+    s = bsm.bsm_plan_create([4], [4], [0], dtype="f32", topology=MI355X, device=-1)
+    assert lib.bsm_gemm_execute(s.handle, ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.c_void_p(4096),
+                                1.0, None, None) == bsm.BSM_ERR_UNSUPPORTED
+    s.destroy()
+    # one-shot: no-ops and validation before any GPU call
+    assert lib.bsm_gemm(None, None, None, 0, 4, 4, 4, 0, 0, 1.0, 0, None) == bsm.BSM_OK
+    assert lib.bsm_gemm(None, None, None, 2, 4, 4, 4, 0, 0, 1.0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_gemm(None, None, None, 2, 4, 4, 4, 5, 0, 1.0, 0, None) == bsm.BSM_ERR_INVALID_ARG
