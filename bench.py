@@ -203,6 +203,52 @@ def run_backward(name, schedule, steps, warmup, w=None):
                 gbs=nbytes / (ms * 1e-3) / 1e9, buffers_rotated=n_sets)
 
 
+GEMM_SHAPES = {  # Section 6's two batch products of BERT attention (batch, m, n, k, layout)
+    "scores_384x512x512x64": (384, 512, 512, 64, "nt"),
+    "context_384x512x64x512": (384, 512, 64, 512, "nn"),
+}
+
+
+def run_gemm(name, schedule, steps, warmup, out="bf16", topology=None):
+    """Bench one batched product: algorithmic bytes = A and B read once + C written once;
+    flops = 2 batch m n k."""
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    batch, m, n, k, layout = GEMM_SHAPES[name]
+    es = 4 if out == "f32" else 2
+    nbytes = batch * (2 * (m * k + n * k) + es * m * n)
+    n_sets = _rotation(nbytes)
+    rng = np.random.default_rng(5)
+    a0 = torch.from_numpy(rng.standard_normal(batch * m * k, dtype=np.float32)).to(torch.bfloat16).cuda()
+    b0 = torch.from_numpy(rng.standard_normal(batch * n * k, dtype=np.float32)).to(torch.bfloat16).cuda()
+    tdt = torch.float32 if out == "f32" else torch.bfloat16
+    As = [a0] + [a0.clone() for _ in range(n_sets - 1)]
+    Bs = [b0] + [b0.clone() for _ in range(n_sets - 1)]
+    Cs = [torch.empty(batch * m * n, dtype=tdt, device="cuda") for _ in range(n_sets)]
+    plan = bsm.bsm_gemm_plan_create(batch, m, n, k, layout, out, schedule, topology=topology,
+                                    device=0)
+    for i in range(warmup):
+        bsm.bsm_gemm_execute(plan, As[i % n_sets], Bs[i % n_sets], Cs[i % n_sets])
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(steps):
+        bsm.bsm_gemm_execute(plan, As[i % n_sets], Bs[i % n_sets], Cs[i % n_sets])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    plan.destroy()
+    ms = t0.elapsed_time(t1) / steps
+    del As, Bs, Cs, a0, b0
+    torch.cuda.empty_cache()
+    return dict(gbs=nbytes / (ms * 1e-3) / 1e9, tflops=2.0 * batch * m * n * k / (ms * 1e-3) / 1e12,
+                ms_per_step=ms, algorithmic_bytes=nbytes, out=out)
+
+
 def xcd_weight_calibration(name, steps, warmup):
     """Weighted load balancing (Section 4.2) with weights measured on this GPU: one traced
     launch of the unweighted XCD plan gives each XCD's rate (its bytes over the span of its
@@ -467,6 +513,13 @@ def main() -> int:
             r = run_backward(cfg, sch, args.steps, args.warmup)
             extra[f"{cfg}_backward_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "algorithmic_bytes")}
         extra["xcd_weighted_c2"] = xcd_weight_calibration("c2", args.steps, args.warmup)
+        # Section 6's batch products around the softmax, bf16 in and out, per schedule
+        for gname in GEMM_SHAPES:
+            res = {sch: run_gemm(gname, sch, args.steps, args.warmup) for sch in ("rr", "balanced", "xcd")}
+            extra[f"gemm_{gname}"] = {sch: {k: round(v, 4) if isinstance(v, float) else v
+                                            for k, v in r.items()} for sch, r in res.items()}
+            extra[f"gemm_{gname}"]["balanced_over_rr"] = round(res["rr"]["ms_per_step"] /
+                                                               res["balanced"]["ms_per_step"], 3)
         extra["producer_consumer"] = producer_consumer()
         extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region and

@@ -377,10 +377,31 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
                     static_cast<long long>(batch), m, n, k);
     if (static_cast<double>(batch) * std::max({m, n, k}) * std::max({m, n, k}) > 1.0e18)
         return fail(BSM_ERR_INVALID_ARG, "operands too large");
+    // The kernel runs 256-thread workgroups, two per CU by default (its LDS staging takes
+    // gemm_lds_bytes_per_wave() per wave).
+    bsm_topology t{};
+    if (topology) t = *topology;
+    if (t.wg_threads != 0 && t.wg_threads != 256)
+        return fail(BSM_ERR_INVALID_ARG, "matrix-product plans run 256-thread workgroups (got %d)",
+                    t.wg_threads);
+    t.wg_threads = 256;
+    if (t.wg_per_cu == 0) t.wg_per_cu = 2;
+    if (device >= 0) {
+        DeviceGuard g;
+        hipError_t e = g.enter(device);
+        hipDeviceProp_t prop;
+        if (e == hipSuccess) e = hipGetDeviceProperties(&prop, device);
+        if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+        const int64_t per_wg = 4LL * bsm::gemm_lds_bytes_per_wave();
+        if (per_wg > static_cast<int64_t>(prop.sharedMemPerBlock) ||
+            per_wg * t.wg_per_cu > static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor))
+            return fail(BSM_ERR_INVALID_ARG, "wg_per_cu %d: %lld bytes of LDS per workgroup do not fit",
+                        t.wg_per_cu, static_cast<long long>(per_wg));
+    }
     const int32_t rows[1] = {m}, cols[1] = {n};
     bsm_plan p = nullptr;
     bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
-                                schedule, home_xcd, nullptr, topology, device, /*row_unit=*/32);
+                                schedule, home_xcd, nullptr, &t, device, /*row_unit=*/32);
     if (st != BSM_OK) return st;
     p->gemm = true;
     p->gemm_m = m;

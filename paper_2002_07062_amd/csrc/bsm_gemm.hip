@@ -21,14 +21,16 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &per_wave, &a_trace};
-    return hipLaunchKernel(
-        reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<LAYOUT, BF16OUT, VEC, VEC, VEC>),
-        dim3(n_wg), dim3(wg_threads), args, 0, stream);
+    const size_t lds = static_cast<size_t>(bsm_mm::kLdsBytes) * (wg_threads / 64);
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<LAYOUT, BF16OUT, VEC>),
+                           dim3(n_wg), dim3(wg_threads), args, lds, stream);
 }
 
 }  // namespace
 
 namespace bsm {
+
+int gemm_lds_bytes_per_wave() { return bsm_mm::kLdsBytes; }
 
 hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
                        int n, int k, float alpha, const int32_t* d_worker_ptr,
@@ -42,11 +44,12 @@ hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, 
     s.b_batch = static_cast<int64_t>(n) * k;
     s.c_batch = static_cast<int64_t>(m) * n;
     s.alpha = alpha;
-    const uintptr_t ab = reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b);
-    s.vec_a = (k % 8 == 0) && (ab & 15) == 0;
-    s.vec_b = s.vec_a;
-    s.vec_c = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(c) & 15) == 0;
-    const bool vec = s.vec_a && s.vec_c;
+    // 16-byte operand pieces and 4-column stores: rows of A (and NT's B) of k elements, rows of
+    // NN's B and of C of n elements, every base 16-byte aligned
+    const uintptr_t ptrs = reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+                           reinterpret_cast<uintptr_t>(c);
+    const bool vec = (ptrs & 15) == 0 && k % 8 == 0 && n % (layout == bsm_mm::kNN ? 8 : 4) == 0;
+    s.vec_a = s.vec_b = s.vec_c = vec ? 1 : 0;
 #define BSM_G(L, O, V) launch_g<L, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, wg_threads, per_wave, trace, stream)
     if (layout == bsm_mm::kNT) {
         if (bf16_out) return vec ? BSM_G(bsm_mm::kNT, true, true) : BSM_G(bsm_mm::kNT, true, false);

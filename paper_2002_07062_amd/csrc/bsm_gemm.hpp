@@ -7,12 +7,13 @@
 //   layout NN:  C_b = alpha A_b B_b     (A_b: m x k, B_b: k x n; e.g. P V)
 //
 // bf16 operands, fp32 accumulation on the matrix cores (v_mfma_f32_32x32x16_bf16), fp32 or
-// bf16 (round to nearest even) output.  A wave computes 32 output rows at a time, 32 columns
-// per MFMA tile, up to four tiles side by side, as the transposed tile D = B_sub A_sub^T:
-// the MFMA's row operand is 32 rows of B (NT: contiguous 16-byte loads; NN: gathered down
-// B's columns) and its column operand 32 rows of A (contiguous), so each lane ends with four
-// consecutive output columns of one output row -- 16-byte stores.  At these shapes the work
-// is bound by HBM (the 512 x 512 output, or input), not by the matrix cores.
+// bf16 (round to nearest even) output.  A wave computes 32 output rows at a time in blocks of
+// 64 columns (two 32 x 32 MFMA tiles), as the transposed tile D = B_sub A_sub^T so that each
+// lane ends with four consecutive output columns.  Operands are staged in the wave's LDS from
+// 16-byte loads (NN's B transposed on the way in), one step ahead: a step's loads are in
+// flight while the previous step computes; the output block goes through LDS too and is
+// stored as whole rows.  At these shapes the work is bound by HBM (the 512 x 512 output, or
+// input), not by the matrix cores.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,7 +37,7 @@ enum { kNT = 0, kNN = 1 };
 constexpr int kTileM = 32;   // output rows per wave step
 constexpr int kTileN = 32;   // output columns per MFMA tile
 constexpr int kTileK = 16;   // reduction depth per MFMA
-constexpr int kMaxTiles = 4; // tiles a wave accumulates side by side
+constexpr int kMaxTiles = 2; // tiles a wave accumulates side by side
 
 struct Shape {
     int m, n, k;
@@ -46,134 +47,276 @@ struct Shape {
     int vec_c;         // 4-column stores allowed (n % 4 == 0 and aligned)
 };
 
-// Eight bf16 of row `row` of a row-major operand with `len` columns, columns c0 .. c0+7;
-// zeros when !ok or past len.  The vector form requires len % 8 == 0 and 16-byte alignment;
-// its load is unconditional (the caller passes an in-range row, `ok` only selects zeros) so
-// that all of a wave's loads are in flight together.
-template <bool VEC>
-__device__ __forceinline__ bf16x8 row8(const uint16_t* row, int c0, int len, bool ok) {
-    if constexpr (VEC) {
-        const int cc = c0 < len ? c0 : len - 8;
-        u16x8 v = __builtin_nontemporal_load(reinterpret_cast<const u16x8*>(row + cc));
-        if (!ok || c0 >= len) v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        return __builtin_bit_cast(bf16x8, v);
-    } else {
-        u16x8 v;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int cc = c0 + e < len ? c0 + e : len - 1;
-            const uint16_t x = row[cc];
-            v[e] = (ok && c0 + e < len) ? x : static_cast<uint16_t>(0);
-        }
-        return __builtin_bit_cast(bf16x8, v);
-    }
-}
+// One step of a wave's work on a 32-row chunk: the output column block [j0, j0 + 64) (two
+// 32 x 32 MFMA tiles) and the reduction slice [k0, k0 + 64).  Per-wave LDS layout (bf16
+// elements): A block [32][kLdk], B block [64][kLdk] (B's rows for NT, B's columns for NN: the
+// MFMA's row operand either way), rows padded so that a ds_read_b128 of 32 rows spreads over
+// the banks.  After a column block's last step the output block is staged in the same region
+// as [32][kLdc] fp32 and stored as whole rows.
+constexpr int kChunkK = 64;                 // reduction indices per step
+constexpr int kLdk = kChunkK + 8;           // padded LDS row, elements
+constexpr int kBlockN = 64;                 // output columns per block (two tiles)
+constexpr int kBlockTiles = kBlockN / kTileN;
+constexpr int kLdc = kBlockN + 4;           // padded LDS row of the staged output, floats
+constexpr int kLdv = kBlockN + 8;           // padded LDS row of NN's B (rows = reduction index)
+constexpr int kLdsBytes = (kTileM * kLdc * 4 > (kTileM + kBlockN) * kLdk * 2)
+                              ? kTileM * kLdc * 4 : (kTileM + kBlockN) * kLdk * 2;
+static_assert(kChunkK * kLdv <= kBlockN * kLdk, "NN's B fits the B region");
+constexpr int kAPieces = kTileM * kChunkK / 8 / 64;   // 16-byte pieces of A per lane per step
+constexpr int kBPieces = kBlockN * kChunkK / 8 / 64;  // ... of B
+constexpr int kDepth = 1;                             // steps of operands in flight
 
-// Eight bf16 down column j (an in-range column) of a row-major k x n operand, rows r0 .. r0+7
-// (zeros past k or when !ok).
-__device__ __forceinline__ bf16x8 col8(const uint16_t* b, int n, int k, int r0, int j, bool ok) {
-    u16x8 v;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int r = r0 + e < k ? r0 + e : k - 1;
-        const uint16_t x = b[static_cast<int64_t>(r) * n + j];
-        v[e] = (ok && r0 + e < k) ? x : static_cast<uint16_t>(0);
-    }
-    return __builtin_bit_cast(bf16x8, v);
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 __device__ __forceinline__ unsigned pack_bf16(float a, float b) {
     return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
-// Stores the four values of a lane for output row `row` (valid when row_ok), columns
-// j .. j+3 (those below n).
-template <bool BF16OUT, bool VECC>
-__device__ __forceinline__ void store4(void* c_row, int j, int n, bool row_ok, float v0, float v1,
-                                       float v2, float v3) {
-    if (!row_ok || j >= n) return;
-    if constexpr (BF16OUT) {
-        uint16_t* c = static_cast<uint16_t*>(c_row);
-        if (VECC && j + 3 < n) {
-            __builtin_nontemporal_store(u32x2{pack_bf16(v0, v1), pack_bf16(v2, v3)},
-                                        reinterpret_cast<u32x2*>(c + j));
-        } else {
-            const float v[4] = {v0, v1, v2, v3};
-            for (int e = 0; e < 4 && j + e < n; ++e)
-                c[j + e] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v[e]));
+// Eight consecutive bf16 of a row-major operand row (`len` columns) from column c, or from
+// the row's last whole piece when c is past the row (the caller zeroes such pieces when it
+// writes them to LDS).  VEC: one unconditional 16-byte load (len % 8 == 0, 16-byte aligned
+// rows), so that no branch or select on the loaded data sits between a step's loads and the
+// wait before their use; the scalar form (any len) loads element by element.  Ordinary
+// (cache-resident) loads: B is re-read by every row chunk of its batch, A by every column
+// block.
+template <bool VEC>
+__device__ __forceinline__ u16x8 load8(const uint16_t* row, int c, int len) {
+    if constexpr (VEC) {
+        return *reinterpret_cast<const u16x8*>(row + (c < len ? c : len - 8));
+    } else {
+        u16x8 v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = row[c + e < len ? c + e : len - 1];
+        return v;
+    }
+}
+
+// Zeroes the elements of a piece loaded from columns [c, c + 8) that lie past `len`, or all
+// of them when !ok.
+__device__ __forceinline__ u16x8 keep8(u16x8 v, int c, int len, bool ok) {
+    u16x8 z;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z[e] = (ok && c + e < len) ? v[e] : static_cast<unsigned short>(0);
+    return z;
+}
+
+// The operand pieces of one step, held in registers between their loads and their LDS writes
+// so that a step's loads are in flight while earlier steps compute.
+struct Pieces {
+    u16x8 a[kAPieces];
+    u16x8 b[kBPieces];
+};
+
+// Piece q of a lane.  A and NT's B: lanes walk rows 8 pieces (128 bytes) at a time.  NN's B:
+// lane = reduction index, piece q = columns 8q .. 8q+7, so that the transposed LDS writes of
+// consecutive lanes fall in consecutive bytes.
+__device__ __forceinline__ int piece_row(int lane, int q) { return (lane + 64 * q) / (kChunkK / 8); }
+__device__ __forceinline__ int piece_col(int lane, int q) { return ((lane + 64 * q) % (kChunkK / 8)) * 8; }
+// NN's B: rows of kBlockN columns, kBlockN / 8 pieces each
+__device__ __forceinline__ int piece_nn_row(int lane, int q) { return (lane + 64 * q) / (kBlockN / 8); }
+__device__ __forceinline__ int piece_nn_col(int lane, int q) { return ((lane + 64 * q) % (kBlockN / 8)) * 8; }
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// MFMA row operand of NN from row-major B in LDS: lane (li, h) of tile t gets B[kk + 8h + e]
+// [32t + li] for e = 0..7.  ds_read_b64_tr_b16 works on groups of 16 lanes: lane i of a group
+// receives element i % 4 of the 8-byte loads of the group's lanes 4r + i / 4, r = 0..3; so
+// group lane s points at row kb + s / 4, columns jb + 4 (s % 4) .. +3, and lane i ends with
+// column jb + i of rows kb .. kb+3.  Two reads (kb and kb + 4) give the eight rows.
+__device__ __forceinline__ bf16x8 nn_row_operand(const uint16_t* lb, int t, int kk, int lane) {
+    const int g = lane >> 4, sl = lane & 15;
+    const int kb = kk + 8 * (g >> 1), jb = t * kTileN + 16 * (g & 1);
+    const uint16_t* p0 = lb + (kb + (sl >> 2)) * kLdv + jb + 4 * (sl & 3);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 4 * kLdv));
+    u16x8 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[e] = static_cast<unsigned short>(lo[e]);
+        v[e + 4] = static_cast<unsigned short>(hi[e]);
+    }
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int LAYOUT, bool VEC>
+__device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t* b_blk,
+                                          const Shape& s, int rows, int j0, int k0, int lane,
+                                          Pieces& p) {
+    if (s.k == 0) {  // empty reduction: nothing to read (write_step zeroes every piece)
+#pragma unroll
+        for (int q = 0; q < kAPieces; ++q) p.a[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int q = 0; q < kBPieces; ++q) p.b[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        return;
+    }
+#pragma unroll
+    for (int q = 0; q < kAPieces; ++q) {
+        const int r = piece_row(lane, q);
+        p.a[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : rows - 1) * s.k,
+                            k0 + piece_col(lane, q), s.k);
+    }
+    if constexpr (LAYOUT == kNT) {
+#pragma unroll
+        for (int q = 0; q < kBPieces; ++q) {
+            const int j = j0 + piece_row(lane, q);
+            p.b[q] = load8<VEC>(b_blk + static_cast<int64_t>(j < s.n ? j : s.n - 1) * s.k,
+                                k0 + piece_col(lane, q), s.k);
         }
     } else {
-        float* c = static_cast<float*>(c_row);
-        if (VECC && j + 3 < n) {
-            __builtin_nontemporal_store(f32x4{v0, v1, v2, v3}, reinterpret_cast<f32x4*>(c + j));
-        } else {
-            const float v[4] = {v0, v1, v2, v3};
-            for (int e = 0; e < 4 && j + e < n; ++e) c[j + e] = v[e];
+#pragma unroll
+        for (int q = 0; q < kBPieces; ++q) {
+            const int kr = k0 + piece_nn_row(lane, q);
+            p.b[q] = load8<VEC>(b_blk + static_cast<int64_t>(kr < s.k ? kr : s.k - 1) * s.n,
+                                j0 + piece_nn_col(lane, q), s.n);
         }
     }
 }
 
-// Output rows [i0, i0 + rows) (rows <= 32) of batch b: all n columns, tiles of 32 columns,
-// up to kMaxTiles at a time sharing each load of A.
-template <int LAYOUT, bool BF16OUT, bool VECA, bool VECB, bool VECC>
+template <int LAYOUT>
+__device__ __forceinline__ void write_step(const Pieces& p, const Shape& s, int rows, int j0,
+                                           int k0, int lane, uint16_t* la, uint16_t* lb) {
+#pragma unroll
+    for (int q = 0; q < kAPieces; ++q) {
+        const int r = piece_row(lane, q), c = piece_col(lane, q);
+        *reinterpret_cast<u16x8*>(la + r * kLdk + c) = keep8(p.a[q], k0 + c, s.k, r < rows);
+    }
+    if constexpr (LAYOUT == kNT) {
+#pragma unroll
+        for (int q = 0; q < kBPieces; ++q) {
+            const int r = piece_row(lane, q), c = piece_col(lane, q);
+            *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8(p.b[q], k0 + c, s.k, j0 + r < s.n);
+        }
+    } else {
+        // B's rows k0 .. k0+63 as they are (row = reduction index, kLdv elements apart);
+        // the MFMA operand is read back transposed (ds_read_b64_tr_b16)
+#pragma unroll
+        for (int q = 0; q < kBPieces; ++q) {
+            const int kr = piece_nn_row(lane, q), c = piece_nn_col(lane, q);
+            *reinterpret_cast<u16x8*>(lb + kr * kLdv + c) =
+                keep8(p.b[q], j0 + c, s.n, k0 + kr < s.k);
+        }
+    }
+}
+
+// Output rows [i0, i0 + rows) (rows <= 32) of batch b, as a sequence of steps (column block,
+// reduction slice); step t + 1's loads are issued before step t's arithmetic.
+template <int LAYOUT, bool BF16OUT, bool VEC>
 __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, void* c,
-                                       const Shape& s, int64_t bidx, int i0, int rows, int lane) {
-    const int li = lane & 31;  // this lane's output row within the chunk (column operand)
-    const int h = lane >> 5;   // which 8 of the 16 reduction indices this lane carries
-    const bool row_ok = li < rows;
-    const int li_in = row_ok ? li : rows - 1;  // loads stay inside the item's rows
-    const uint16_t* a_row = a + bidx * s.a_batch + static_cast<int64_t>(i0 + li_in) * s.k;
-    const uint16_t* bb = b + bidx * s.b_batch;
-    const int ntiles = (s.n + kTileN - 1) / kTileN;
-    char* c_row = static_cast<char*>(c) +
-                  (bidx * s.c_batch + static_cast<int64_t>(i0 + li_in) * s.n) * (BF16OUT ? 2 : 4);
-    for (int t0 = 0; t0 < ntiles; t0 += kMaxTiles) {
-        const int nt = ntiles - t0 < kMaxTiles ? ntiles - t0 : kMaxTiles;  // wave-uniform
-        f32x16 acc[kMaxTiles];
+                                       const Shape& s, int64_t bidx, int i0, int rows, int lane,
+                                       uint16_t* lds) {
+    const int li = lane & 31;
+    const int h = lane >> 5;
+    uint16_t* const la = lds;
+    uint16_t* const lb = lds + kTileM * kLdk;
+    float* const lc = reinterpret_cast<float*>(lds);
+    const uint16_t* a_blk = a + bidx * s.a_batch + static_cast<int64_t>(i0) * s.k;
+    const uint16_t* b_blk = b + bidx * s.b_batch;
+    const int nk = s.k > 0 ? (s.k + kChunkK - 1) / kChunkK : 1;  // k == 0: one step of zeros
+    const int nj = (s.n + kBlockN - 1) / kBlockN;
+    const int nsteps = nk * nj;
+    f32x16 acc[kBlockTiles];
+    // kDepth steps of operands in flight: step st + kDepth is loaded into the registers step
+    // st has just written to LDS
+    Pieces p[kDepth];
 #pragma unroll
-        for (int t = 0; t < kMaxTiles; ++t) acc[t] = f32x16{};
-        for (int k0 = 0; k0 < s.k; k0 += kTileK) {
-            const int kk = k0 + 8 * h;
-            const bf16x8 av = row8<VECA>(a_row, kk, s.k, row_ok);
+    for (int d = 0; d < kDepth; ++d) {
+        if (d < nsteps) {
+            const int jd = d / nk, kd = d - jd * nk;
+            load_step<LAYOUT, VEC>(a_blk, b_blk, s, rows, jd * kBlockN, kd * kChunkK, lane, p[d]);
+        }
+    }
+    for (int st0 = 0; st0 < nsteps; st0 += kDepth) {
 #pragma unroll
-            for (int t = 0; t < kMaxTiles; ++t) {
-                if (t < nt) {
-                    const int j = (t0 + t) * kTileN + li;  // this lane's row of the row operand
-                    const int jc = j < s.n ? j : s.n - 1;
-                    bf16x8 bv;
-                    if constexpr (LAYOUT == kNT)
-                        bv = row8<VECB>(bb + static_cast<int64_t>(jc) * s.k, kk, s.k, j < s.n);
-                    else
-                        bv = col8(bb, s.n, s.k, kk, jc, j < s.n);
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[t], 0, 0, 0);
+    for (int d = 0; d < kDepth; ++d) {
+        const int st = st0 + d;
+        if (st >= nsteps) break;
+        const int jb = st / nk, kb = st - jb * nk;
+        const int j0 = jb * kBlockN;
+        if (kb == 0) {
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
+        }
+        write_step<LAYOUT>(p[d], s, rows, j0, kb * kChunkK, lane, la, lb);
+        wave_lds_sync();
+        if (st + kDepth < nsteps) {
+            const int jn1 = (st + kDepth) / nk, kn1 = (st + kDepth) - jn1 * nk;
+            load_step<LAYOUT, VEC>(a_blk, b_blk, s, rows, jn1 * kBlockN, kn1 * kChunkK, lane, p[d]);
+        }
+        const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
+#pragma unroll
+        for (int kk = 0; kk < kChunkK; kk += kTileK) {
+            const bf16x8 av = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u16x8*>(la + li * kLdk + kk + 8 * h));
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
+                bf16x8 bv;
+                if constexpr (LAYOUT == kNT)
+                    bv = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u16x8*>(lb + (t * kTileN + li) * kLdk + kk + 8 * h));
+                else
+                    bv = nn_row_operand(lb, t, kk, lane);
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[t], 0, 0, 0);
+            }
+        }
+        wave_lds_sync();  // operands consumed
+        if (kb + 1 < nk) continue;
+        // column block done: tile t, lane (li, h) holds output row li, columns
+        // j0 + 32 t + 8 g + 4 h + 0..3
+#pragma unroll
+        for (int t = 0; t < kBlockTiles; ++t) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<f32x4*>(lc + li * kLdc + t * kTileN + 8 * g + 4 * h) =
+                    f32x4{s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1],
+                          s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3]};
+        }
+        wave_lds_sync();
+        // whole rows: 16 lanes x 4 columns per row, four rows per store instruction
+        const int col = (lane & 15) * 4;
+        const int rq = lane >> 4;
+#pragma unroll
+        for (int r0 = 0; r0 < kTileM; r0 += 4) {
+            const int r = r0 + rq;
+            if (r < rows && col < jn) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(lc + r * kLdc + col);
+                const int64_t off = bidx * s.c_batch + static_cast<int64_t>(i0 + r) * s.n + j0 + col;
+                if constexpr (BF16OUT) {
+                    uint16_t* cp = static_cast<uint16_t*>(c) + off;
+                    if (VEC && col + 3 < jn) {
+                        __builtin_nontemporal_store(u32x2{pack_bf16(v.x, v.y), pack_bf16(v.z, v.w)},
+                                                    reinterpret_cast<u32x2*>(cp));
+                    } else {
+                        for (int e = 0; e < 4 && col + e < jn; ++e)
+                            cp[e] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v[e]));
+                    }
+                } else {
+                    float* cp = static_cast<float*>(c) + off;
+                    if (VEC && col + 3 < jn) {
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
+                    } else {
+                        for (int e = 0; e < 4 && col + e < jn; ++e) cp[e] = v[e];
+                    }
                 }
             }
         }
-        // D[jj][ii]: lane (ii = li, h) holds columns jj = 8 g + 4 h + 0..3 of tile t
-#pragma unroll
-        for (int t = 0; t < kMaxTiles; ++t) {
-            if (t < nt) {
-                const int jbase = (t0 + t) * kTileN;
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int j = jbase + 8 * g + 4 * h;
-                    store4<BF16OUT, VECC>(c_row, j, s.n, row_ok, s.alpha * acc[t][4 * g],
-                                          s.alpha * acc[t][4 * g + 1], s.alpha * acc[t][4 * g + 2],
-                                          s.alpha * acc[t][4 * g + 3]);
-                }
-            }
-        }
+        wave_lds_sync();  // the next step rewrites the region
+    }
     }
 }
 
 // Worker loop: worker v (a workgroup, or one wave when per_wave) runs its items; an item's
 // rows are taken 32 at a time (split where a batch ends), the workgroup's waves splitting
 // them when they share the item.
-template <int LAYOUT, bool BF16OUT, bool VECA, bool VECB, bool VECC>
+template <int LAYOUT, bool BF16OUT, bool VEC>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
                                             const Shape& s, const int32_t* __restrict__ worker_ptr,
                                             const bsm_item* __restrict__ items, int per_wave,
-                                            bsm_trace_rec* __restrict__ trace) {
+                                            bsm_trace_rec* __restrict__ trace, uint16_t* lds_base) {
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int nwaves = static_cast<int>(blockDim.x) >> 6;
@@ -182,6 +325,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     const int worker = per_wave ? w * nwaves + wave : w;
     const int my_wave = per_wave ? 0 : wave;
     const int my_nwaves = per_wave ? 1 : nwaves;
+    uint16_t* const lds = lds_base + wave * (kLdsBytes / 2);
     uint32_t done = 0;
     const int i_begin = worker_ptr[worker];
     const int i_end = worker_ptr[worker + 1];
@@ -201,7 +345,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                     const int64_t bidx = g / s.m;
                     const int i = static_cast<int>(g - bidx * s.m);
                     const int seg = s.m - i < left ? s.m - i : left;
-                    rows32<LAYOUT, BF16OUT, VECA, VECB, VECC>(a, b, c, s, bidx, i, seg, lane);
+                    rows32<LAYOUT, BF16OUT, VEC>(a, b, c, s, bidx, i, seg, lane, lds);
                     done += static_cast<uint32_t>(seg);
                     g += seg;
                     left -= seg;
@@ -221,12 +365,18 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     }
 }
 
-template <int LAYOUT, bool BF16OUT, bool VECA, bool VECB, bool VECC>
-__global__ void __launch_bounds__(1024)
+extern __shared__ uint16_t bsm_gemm_lds[];  // kLdsBytes per wave
+
+// 256-thread workgroups, two waves per SIMD: up to 256 registers per lane (the accumulators
+// and the in-flight operand pieces) and 2 x 4 waves x kLdsBytes of LDS per CU.
+constexpr int kGemmThreads = 256;
+
+template <int LAYOUT, bool BF16OUT, bool VEC>
+__global__ void __launch_bounds__(kGemmThreads, 2)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 int per_wave, bsm_trace_rec* __restrict__ trace) {
-    gemm_worker<LAYOUT, BF16OUT, VECA, VECB, VECC>(a, b, c, s, worker_ptr, items, per_wave, trace);
+    gemm_worker<LAYOUT, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, per_wave, trace, bsm_gemm_lds);
 }
 
 }  // namespace bsm_mm
