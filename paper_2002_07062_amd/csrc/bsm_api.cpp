@@ -385,14 +385,15 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
         return fail(BSM_ERR_INVALID_ARG, "matrix-product plans run 256-thread workgroups (got %d)",
                     t.wg_threads);
     t.wg_threads = 256;
-    if (t.wg_per_cu == 0) t.wg_per_cu = 2;
+    // one workgroup per SIMD's worth of waves the kernel instance is compiled for
+    if (t.wg_per_cu == 0) t.wg_per_cu = bsm::gemm_waves_per_simd(layout, k);
     if (device >= 0) {
         DeviceGuard g;
         hipError_t e = g.enter(device);
         hipDeviceProp_t prop;
         if (e == hipSuccess) e = hipGetDeviceProperties(&prop, device);
         if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
-        const int64_t per_wg = 4LL * bsm::gemm_lds_bytes_per_wave();
+        const int64_t per_wg = 4LL * bsm::gemm_lds_bytes_per_wave(layout, k);
         if (per_wg > static_cast<int64_t>(prop.sharedMemPerBlock) ||
             per_wg * t.wg_per_cu > static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor))
             return fail(BSM_ERR_INVALID_ARG, "wg_per_cu %d: %lld bytes of LDS per workgroup do not fit",

@@ -11,7 +11,7 @@ namespace {
 
 using bsm_mm::Shape;
 
-template <int LAYOUT, bool BF16OUT, bool VEC>
+template <int MODE, bool BF16OUT, bool VEC>
 hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const int32_t* worker_ptr,
                     const bsm_item* items, int n_wg, int wg_threads, int per_wave, void* trace,
                     hipStream_t stream) {
@@ -21,8 +21,8 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &per_wave, &a_trace};
-    const size_t lds = static_cast<size_t>(bsm_mm::kLdsBytes) * (wg_threads / 64);
-    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<LAYOUT, BF16OUT, VEC>),
+    const size_t lds = static_cast<size_t>(bsm_mm::mode_lds_bytes(MODE)) * (wg_threads / 64);
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC>),
                            dim3(n_wg), dim3(wg_threads), args, lds, stream);
 }
 
@@ -30,7 +30,21 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
 
 namespace bsm {
 
-int gemm_lds_bytes_per_wave() { return bsm_mm::kLdsBytes; }
+int gemm_mode(int layout, int /*k*/) { return layout == bsm_mm::kNN ? bsm_mm::kModeNn : bsm_mm::kModeNt; }
+
+int gemm_lds_bytes_per_wave(int layout, int k) {
+    switch (gemm_mode(layout, k)) {
+        case bsm_mm::kModeNt: return bsm_mm::mode_lds_bytes(bsm_mm::kModeNt);
+        default: return bsm_mm::mode_lds_bytes(bsm_mm::kModeNn);
+    }
+}
+
+int gemm_waves_per_simd(int layout, int k) {
+    switch (gemm_mode(layout, k)) {
+        case bsm_mm::kModeNt: return bsm_mm::mode_waves_per_simd(bsm_mm::kModeNt);
+        default: return bsm_mm::mode_waves_per_simd(bsm_mm::kModeNn);
+    }
+}
 
 hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
                        int n, int k, float alpha, const int32_t* d_worker_ptr,
@@ -44,19 +58,21 @@ hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, 
     s.b_batch = static_cast<int64_t>(n) * k;
     s.c_batch = static_cast<int64_t>(m) * n;
     s.alpha = alpha;
-    // 16-byte operand pieces and 4-column stores: rows of A (and NT's B) of k elements, rows of
-    // NN's B and of C of n elements, every base 16-byte aligned
+    // 16-byte operand pieces and 16-byte output stores (4 fp32 or 8 bf16 columns): rows of A
+    // (and NT's B) of k elements, rows of NN's B and of C of n elements, every base 16-byte
+    // aligned
     const uintptr_t ptrs = reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
                            reinterpret_cast<uintptr_t>(c);
-    const bool vec = (ptrs & 15) == 0 && k % 8 == 0 && n % (layout == bsm_mm::kNN ? 8 : 4) == 0;
-    s.vec_a = s.vec_b = s.vec_c = vec ? 1 : 0;
-#define BSM_G(L, O, V) launch_g<L, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, wg_threads, per_wave, trace, stream)
-    if (layout == bsm_mm::kNT) {
-        if (bf16_out) return vec ? BSM_G(bsm_mm::kNT, true, true) : BSM_G(bsm_mm::kNT, true, false);
-        return vec ? BSM_G(bsm_mm::kNT, false, true) : BSM_G(bsm_mm::kNT, false, false);
+    const bool vec = (ptrs & 15) == 0 && k % 8 == 0 &&
+                     n % ((layout == bsm_mm::kNN || bf16_out) ? 8 : 4) == 0;
+#define BSM_G(M, O, V) launch_g<M, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, wg_threads, per_wave, trace, stream)
+#define BSM_G2(M) (bf16_out ? (vec ? BSM_G(M, true, true) : BSM_G(M, true, false)) \
+                            : (vec ? BSM_G(M, false, true) : BSM_G(M, false, false)))
+    switch (gemm_mode(layout, k)) {
+        case bsm_mm::kModeNt: return BSM_G2(bsm_mm::kModeNt);
+        default: return BSM_G2(bsm_mm::kModeNn);
     }
-    if (bf16_out) return vec ? BSM_G(bsm_mm::kNN, true, true) : BSM_G(bsm_mm::kNN, true, false);
-    return vec ? BSM_G(bsm_mm::kNN, false, true) : BSM_G(bsm_mm::kNN, false, false);
+#undef BSM_G2
 #undef BSM_G
 }
 

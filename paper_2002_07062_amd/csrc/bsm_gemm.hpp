@@ -43,8 +43,6 @@ struct Shape {
     int m, n, k;
     int64_t a_batch, b_batch, c_batch;  // elements between consecutive batch indices
     float alpha;
-    int vec_a, vec_b;  // 16-byte operand loads allowed (k % 8 == 0 / n % 8 == 0 and aligned)
-    int vec_c;         // 4-column stores allowed (n % 4 == 0 and aligned)
 };
 
 // One step of a wave's work on a 32-row chunk: the output column block [j0, j0 + 64) (two
@@ -58,13 +56,13 @@ constexpr int kLdk = kChunkK + 8;           // padded LDS row, elements
 constexpr int kBlockN = 64;                 // output columns per block (two tiles)
 constexpr int kBlockTiles = kBlockN / kTileN;
 constexpr int kLdc = kBlockN + 4;           // padded LDS row of the staged output, floats
+constexpr int kLdh = kBlockN + 8;           // ... staged as bf16, elements
 constexpr int kLdv = kBlockN + 8;           // padded LDS row of NN's B (rows = reduction index)
 constexpr int kLdsBytes = (kTileM * kLdc * 4 > (kTileM + kBlockN) * kLdk * 2)
                               ? kTileM * kLdc * 4 : (kTileM + kBlockN) * kLdk * 2;
 static_assert(kChunkK * kLdv <= kBlockN * kLdk, "NN's B fits the B region");
 constexpr int kAPieces = kTileM * kChunkK / 8 / 64;   // 16-byte pieces of A per lane per step
 constexpr int kBPieces = kBlockN * kChunkK / 8 / 64;  // ... of B
-constexpr int kDepth = 1;                             // steps of operands in flight
 
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -96,12 +94,22 @@ __device__ __forceinline__ u16x8 load8(const uint16_t* row, int c, int len) {
 }
 
 // Zeroes the elements of a piece loaded from columns [c, c + 8) that lie past `len`, or all
-// of them when !ok.
+// of them when !ok.  VEC (len % 8 == 0, c % 8 == 0): the piece is wholly in or wholly out,
+// four 32-bit selects.
+template <bool VEC>
 __device__ __forceinline__ u16x8 keep8(u16x8 v, int c, int len, bool ok) {
-    u16x8 z;
+    if constexpr (VEC) {
+        const bool in = ok && c < len;
+        u32x4 w = __builtin_bit_cast(u32x4, v);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) z[e] = (ok && c + e < len) ? v[e] : static_cast<unsigned short>(0);
-    return z;
+        for (int e = 0; e < 4; ++e) w[e] = in ? w[e] : 0u;
+        return __builtin_bit_cast(u16x8, w);
+    } else {
+        u16x8 z;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) z[e] = (ok && c + e < len) ? v[e] : static_cast<unsigned short>(0);
+        return z;
+    }
 }
 
 // The operand pieces of one step, held in registers between their loads and their LDS writes
@@ -143,23 +151,43 @@ __device__ __forceinline__ bf16x8 nn_row_operand(const uint16_t* lb, int t, int 
     return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int LAYOUT, bool VEC>
+// A's pieces of the reduction slice [k0, k0 + 64) of the wave's rows, and their LDS writes
+// (rows past `rows` and columns past k zeroed).
+template <bool VEC>
+__device__ __forceinline__ void load_a(const uint16_t* a_blk, const Shape& s, int rows, int k0,
+                                       int lane, u16x8 (&pa)[kAPieces]) {
+#pragma unroll
+    for (int q = 0; q < kAPieces; ++q) {
+        const int r = piece_row(lane, q);
+        pa[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : rows - 1) * s.k,
+                           k0 + piece_col(lane, q), s.k);
+    }
+}
+
+template <bool VEC>
+__device__ __forceinline__ void write_a(const u16x8 (&pa)[kAPieces], const Shape& s, int rows,
+                                        int k0, int lane, uint16_t* la) {
+#pragma unroll
+    for (int q = 0; q < kAPieces; ++q) {
+        const int r = piece_row(lane, q), c = piece_col(lane, q);
+        *reinterpret_cast<u16x8*>(la + r * kLdk + c) = keep8<VEC>(pa[q], k0 + c, s.k, r < rows);
+    }
+}
+
+template <int LAYOUT, bool VEC, bool WITH_A>
 __device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t* b_blk,
                                           const Shape& s, int rows, int j0, int k0, int lane,
                                           Pieces& p) {
     if (s.k == 0) {  // empty reduction: nothing to read (write_step zeroes every piece)
+        if constexpr (WITH_A) {
 #pragma unroll
-        for (int q = 0; q < kAPieces; ++q) p.a[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+            for (int q = 0; q < kAPieces; ++q) p.a[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        }
 #pragma unroll
         for (int q = 0; q < kBPieces; ++q) p.b[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
         return;
     }
-#pragma unroll
-    for (int q = 0; q < kAPieces; ++q) {
-        const int r = piece_row(lane, q);
-        p.a[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : rows - 1) * s.k,
-                            k0 + piece_col(lane, q), s.k);
-    }
+    if constexpr (WITH_A) load_a<VEC>(a_blk, s, rows, k0, lane, p.a);
     if constexpr (LAYOUT == kNT) {
 #pragma unroll
         for (int q = 0; q < kBPieces; ++q) {
@@ -177,19 +205,15 @@ __device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t*
     }
 }
 
-template <int LAYOUT>
+template <int LAYOUT, bool VEC, bool WITH_A>
 __device__ __forceinline__ void write_step(const Pieces& p, const Shape& s, int rows, int j0,
                                            int k0, int lane, uint16_t* la, uint16_t* lb) {
-#pragma unroll
-    for (int q = 0; q < kAPieces; ++q) {
-        const int r = piece_row(lane, q), c = piece_col(lane, q);
-        *reinterpret_cast<u16x8*>(la + r * kLdk + c) = keep8(p.a[q], k0 + c, s.k, r < rows);
-    }
+    if constexpr (WITH_A) write_a<VEC>(p.a, s, rows, k0, lane, la);
     if constexpr (LAYOUT == kNT) {
 #pragma unroll
         for (int q = 0; q < kBPieces; ++q) {
             const int r = piece_row(lane, q), c = piece_col(lane, q);
-            *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8(p.b[q], k0 + c, s.k, j0 + r < s.n);
+            *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8<VEC>(p.b[q], k0 + c, s.k, j0 + r < s.n);
         }
     } else {
         // B's rows k0 .. k0+63 as they are (row = reduction index, kLdv elements apart);
@@ -198,14 +222,75 @@ __device__ __forceinline__ void write_step(const Pieces& p, const Shape& s, int 
         for (int q = 0; q < kBPieces; ++q) {
             const int kr = piece_nn_row(lane, q), c = piece_nn_col(lane, q);
             *reinterpret_cast<u16x8*>(lb + kr * kLdv + c) =
-                keep8(p.b[q], j0 + c, s.n, k0 + kr < s.k);
+                keep8<VEC>(p.b[q], j0 + c, s.n, k0 + kr < s.k);
+        }
+    }
+}
+
+// Stores the staged output block (rows [i0, i0 + rows), columns [j0, j0 + jn) of batch b)
+// as whole rows: 16 lanes x 4 columns per row, four rows per store instruction.
+// Stores a staged output block (rows [i0, i0 + rows), columns [j0, j0 + jn)) as whole rows:
+// 16 lanes x 4 fp32 columns, four rows per instruction.
+template <bool VEC>
+__device__ __forceinline__ void store_block_f32(float* c, const Shape& s, int64_t bidx, int i0, int rows,
+                                            int j0, int jn, int lane, const float* lc) {
+    const int col = (lane & 15) * 4;
+    const int rq = lane >> 4;
+    // one 64-bit base per lane, advanced by 4 output rows per instruction
+    const int64_t off0 = bidx * s.c_batch + static_cast<int64_t>(i0 + rq) * s.n + j0 + col;
+    const int64_t step = 4 * static_cast<int64_t>(s.n);
+    const bool col_ok = col < jn;
+    const bool whole = VEC && col + 3 < jn;
+#pragma unroll
+    for (int r0 = 0; r0 < kTileM; r0 += 4) {
+        const int r = r0 + rq;
+        if (r < rows && col_ok) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(lc + r * kLdc + col);
+            float* cp = c + off0 + (r0 / 4) * step;
+            if (whole) {
+                __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (col + e < jn) cp[e] = v[e];
+            }
+        }
+    }
+}
+
+// The same for a block staged as bf16 ([32][kLdh]): 8 lanes x 8 columns, eight rows per
+// instruction.
+template <bool VEC>
+__device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, int64_t bidx, int i0,
+                                             int rows, int j0, int jn, int lane, const uint16_t* lh) {
+    const int col = (lane & 7) * 8;
+    const int rq = lane >> 3;
+    const int64_t off0 = bidx * s.c_batch + static_cast<int64_t>(i0 + rq) * s.n + j0 + col;
+    const int64_t step = 8 * static_cast<int64_t>(s.n);
+    const bool col_ok = col < jn;
+    const bool whole = VEC && col + 7 < jn;
+#pragma unroll
+    for (int r0 = 0; r0 < kTileM; r0 += 8) {
+        const int r = r0 + rq;
+        if (r < rows && col_ok) {
+            const u16x8 v = *reinterpret_cast<const u16x8*>(lh + r * kLdh + col);
+            uint16_t* cp = c + off0 + (r0 / 8) * step;
+            if (whole) {
+                __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(cp));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (col + e < jn) cp[e] = v[e];
+            }
         }
     }
 }
 
 // Output rows [i0, i0 + rows) (rows <= 32) of batch b, as a sequence of steps (column block,
-// reduction slice); step t + 1's loads are issued before step t's arithmetic.
-template <int LAYOUT, bool BF16OUT, bool VEC>
+// reduction slice); step t + 1's loads are issued before step t's arithmetic.  AREG (the
+// whole reduction in one step, k <= 64): A's operands are read from LDS once, at the first
+// step, and kept in registers for every column block, so later steps move only B.
+template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG>
 __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, void* c,
                                        const Shape& s, int64_t bidx, int i0, int rows, int lane,
                                        uint16_t* lds) {
@@ -221,14 +306,28 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
     const int nsteps = nk * nj;
     f32x16 acc[kBlockTiles];
     // kDepth steps of operands in flight: step st + kDepth is loaded into the registers step
-    // st has just written to LDS
+    // st has just written to LDS (two for the 16-byte form; the element-wise form's registers
+    // allow one)
+    constexpr int kDepth = VEC ? 2 : 1;
     Pieces p[kDepth];
+    u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
+    if constexpr (AREG) {  // A once, through LDS into its MFMA layout
+        u16x8 pa[kAPieces];
+        load_a<VEC>(a_blk, s, rows, 0, lane, pa);
+        write_a<VEC>(pa, s, rows, 0, lane, la);
+        wave_lds_sync();
+#pragma unroll
+        for (int q = 0; q < kChunkK / kTileK; ++q)
+            a_reg[q] = *reinterpret_cast<const u16x8*>(la + li * kLdk + q * kTileK + 8 * h);
+        wave_lds_sync();
+    }
+    auto load = [&](int st, Pieces& pp) {
+        const int js = st / nk, ks = st - js * nk;
+        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, lane, pp);
+    };
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
-        if (d < nsteps) {
-            const int jd = d / nk, kd = d - jd * nk;
-            load_step<LAYOUT, VEC>(a_blk, b_blk, s, rows, jd * kBlockN, kd * kChunkK, lane, p[d]);
-        }
+        if (d < nsteps) load(d, p[d]);
     }
     for (int st0 = 0; st0 < nsteps; st0 += kDepth) {
 #pragma unroll
@@ -241,17 +340,15 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
         }
-        write_step<LAYOUT>(p[d], s, rows, j0, kb * kChunkK, lane, la, lb);
+        write_step<LAYOUT, VEC, !AREG>(p[d], s, rows, j0, kb * kChunkK, lane, la, lb);
         wave_lds_sync();
-        if (st + kDepth < nsteps) {
-            const int jn1 = (st + kDepth) / nk, kn1 = (st + kDepth) - jn1 * nk;
-            load_step<LAYOUT, VEC>(a_blk, b_blk, s, rows, jn1 * kBlockN, kn1 * kChunkK, lane, p[d]);
-        }
+        if (st + kDepth < nsteps) load(st + kDepth, p[d]);
         const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
 #pragma unroll
         for (int kk = 0; kk < kChunkK; kk += kTileK) {
             const bf16x8 av = __builtin_bit_cast(
-                bf16x8, *reinterpret_cast<const u16x8*>(la + li * kLdk + kk + 8 * h));
+                bf16x8, AREG ? a_reg[AREG ? kk / kTileK : 0]
+                             : *reinterpret_cast<const u16x8*>(la + li * kLdk + kk + 8 * h));
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
                 bf16x8 bv;
@@ -267,42 +364,29 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
         if (kb + 1 < nk) continue;
         // column block done: tile t, lane (li, h) holds output row li, columns
         // j0 + 32 t + 8 g + 4 h + 0..3
+        if constexpr (BF16OUT) {  // rounded to bf16 (nearest even) on the way into LDS
+            uint16_t* const lh = lds;
 #pragma unroll
-        for (int t = 0; t < kBlockTiles; ++t) {
+            for (int t = 0; t < kBlockTiles; ++t) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                *reinterpret_cast<f32x4*>(lc + li * kLdc + t * kTileN + 8 * g + 4 * h) =
-                    f32x4{s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1],
-                          s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3]};
-        }
-        wave_lds_sync();
-        // whole rows: 16 lanes x 4 columns per row, four rows per store instruction
-        const int col = (lane & 15) * 4;
-        const int rq = lane >> 4;
-#pragma unroll
-        for (int r0 = 0; r0 < kTileM; r0 += 4) {
-            const int r = r0 + rq;
-            if (r < rows && col < jn) {
-                const f32x4 v = *reinterpret_cast<const f32x4*>(lc + r * kLdc + col);
-                const int64_t off = bidx * s.c_batch + static_cast<int64_t>(i0 + r) * s.n + j0 + col;
-                if constexpr (BF16OUT) {
-                    uint16_t* cp = static_cast<uint16_t*>(c) + off;
-                    if (VEC && col + 3 < jn) {
-                        __builtin_nontemporal_store(u32x2{pack_bf16(v.x, v.y), pack_bf16(v.z, v.w)},
-                                                    reinterpret_cast<u32x2*>(cp));
-                    } else {
-                        for (int e = 0; e < 4 && col + e < jn; ++e)
-                            cp[e] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v[e]));
-                    }
-                } else {
-                    float* cp = static_cast<float*>(c) + off;
-                    if (VEC && col + 3 < jn) {
-                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
-                    } else {
-                        for (int e = 0; e < 4 && col + e < jn; ++e) cp[e] = v[e];
-                    }
-                }
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<u32x2*>(lh + li * kLdh + t * kTileN + 8 * g + 4 * h) =
+                        u32x2{pack_bf16(s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1]),
+                              pack_bf16(s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3])};
             }
+            wave_lds_sync();
+            store_block_bf16<VEC>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lh);
+        } else {
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<f32x4*>(lc + li * kLdc + t * kTileN + 8 * g + 4 * h) =
+                        f32x4{s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1],
+                              s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3]};
+            }
+            wave_lds_sync();
+            store_block_f32<VEC>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
         }
         wave_lds_sync();  // the next step rewrites the region
     }
@@ -312,7 +396,12 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
 // Worker loop: worker v (a workgroup, or one wave when per_wave) runs its items; an item's
 // rows are taken 32 at a time (split where a batch ends), the workgroup's waves splitting
 // them when they share the item.
-template <int LAYOUT, bool BF16OUT, bool VEC>
+// Kernel modes (one compiled instance each): NT and NN, both with LDS-staged operands.
+enum { kModeNt = 0, kModeNn = 1 };
+constexpr int mode_lds_bytes(int) { return kLdsBytes; }
+constexpr int mode_waves_per_simd(int) { return 2; }
+
+template <int MODE, bool BF16OUT, bool VEC>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
                                             const Shape& s, const int32_t* __restrict__ worker_ptr,
                                             const bsm_item* __restrict__ items, int per_wave,
@@ -325,7 +414,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     const int worker = per_wave ? w * nwaves + wave : w;
     const int my_wave = per_wave ? 0 : wave;
     const int my_nwaves = per_wave ? 1 : nwaves;
-    uint16_t* const lds = lds_base + wave * (kLdsBytes / 2);
+    uint16_t* const lds = lds_base + wave * (mode_lds_bytes(MODE) / 2);
     uint32_t done = 0;
     const int i_begin = worker_ptr[worker];
     const int i_end = worker_ptr[worker + 1];
@@ -345,7 +434,10 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                     const int64_t bidx = g / s.m;
                     const int i = static_cast<int>(g - bidx * s.m);
                     const int seg = s.m - i < left ? s.m - i : left;
-                    rows32<LAYOUT, BF16OUT, VEC>(a, b, c, s, bidx, i, seg, lane, lds);
+                    if (VEC && s.k <= kChunkK && s.n > kBlockN)  // (registers: 16-byte form only)
+                        rows32<MODE == kModeNn ? kNN : kNT, BF16OUT, VEC, true>(a, b, c, s, bidx, i, seg, lane, lds);
+                    else
+                        rows32<MODE == kModeNn ? kNN : kNT, BF16OUT, VEC, false>(a, b, c, s, bidx, i, seg, lane, lds);
                     done += static_cast<uint32_t>(seg);
                     g += seg;
                     left -= seg;
@@ -367,16 +459,16 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
 
 extern __shared__ uint16_t bsm_gemm_lds[];  // kLdsBytes per wave
 
-// 256-thread workgroups, two waves per SIMD: up to 256 registers per lane (the accumulators
-// and the in-flight operand pieces) and 2 x 4 waves x kLdsBytes of LDS per CU.
+// 256-thread workgroups; each mode's instance is compiled for its waves per SIMD (registers:
+// 512 / waves) and takes mode_lds_bytes() of LDS per wave.
 constexpr int kGemmThreads = 256;
 
-template <int LAYOUT, bool BF16OUT, bool VEC>
-__global__ void __launch_bounds__(kGemmThreads, 2)
+template <int MODE, bool BF16OUT, bool VEC>
+__global__ void __launch_bounds__(kGemmThreads, mode_waves_per_simd(MODE))
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 int per_wave, bsm_trace_rec* __restrict__ trace) {
-    gemm_worker<LAYOUT, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, per_wave, trace, bsm_gemm_lds);
+    gemm_worker<MODE, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, per_wave, trace, bsm_gemm_lds);
 }
 
 }  // namespace bsm_mm

@@ -36,8 +36,11 @@ hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool tempo
 // Batched matrix product under a table whose slices are the outputs C_b (m x n each, batch
 // after batch): layout 0 (NT) C_b = alpha A_b B_b^T, layout 1 (NN) C_b = alpha A_b B_b; bf16
 // A and B, fp32 or bf16 C.
-// LDS bytes each wave of a matrix-product launch uses (operand and output staging).
-int gemm_lds_bytes_per_wave();
+// The matrix-product kernel instance (mode) a layout and reduction depth run, the LDS bytes
+// each of its waves uses, and the waves per SIMD it is compiled for.
+int gemm_mode(int layout, int k);
+int gemm_lds_bytes_per_wave(int layout, int k);
+int gemm_waves_per_simd(int layout, int k);
 
 hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
                        int n, int k, float alpha, const int32_t* d_worker_ptr,

@@ -72,7 +72,7 @@ def test_paper_products_all_schedules(layout, shape, out):
 
 @pytest.mark.parametrize("layout", ["nt", "nn"])
 @pytest.mark.parametrize("shape", [(3, 37, 45, 24), (2, 70, 33, 20), (5, 1, 1, 1), (1, 33, 96, 40),
-                                   (4, 64, 200, 136)])
+                                   (4, 64, 200, 136), (2, 40, 36, 16)])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 def test_tails_in_every_dimension(layout, shape, out):
     batch, m, n, k = shape
