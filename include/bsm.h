@@ -236,7 +236,8 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
  * The two batch matrix multiplications of Section 6 that surround the softmax in BERT
  * attention -- scores (512 x 64) x (64 x 512) and context (512 x 512) x (512 x 64), batch 384 --
  * scheduled by the same tables: the outputs C_b are the slices (m rows of n), cut by RR,
- * BALANCED or XCD exactly as for the softmax (pieces of whole 32-row blocks).
+ * BALANCED or XCD as for the softmax, with one worker per workgroup (256 threads) and pieces
+ * of whole 128-row blocks (the rows a workgroup takes per round, 32 per wave).
  *   BSM_GEMM_NT:  C_b = alpha * A_b * B_b^T    A_b m x k,  B_b n x k  (scores Q K^T)
  *   BSM_GEMM_NN:  C_b = alpha * A_b * B_b      A_b m x k,  B_b k x n  (context P V)
  * All operands row-major, batch after batch (A_b at b*m*k, B_b at b*n*k, C_b at b*m*n
@@ -245,7 +246,9 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
 typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1 } bsm_gemm_layout;
 
 /* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
- * bsm_plan_create).  A plan made here runs only with bsm_gemm_execute. */
+ * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 2).  A plan
+ * made here runs only with bsm_gemm_execute.  Its stats report per_wave 0 (worker =
+ * workgroup). */
 bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,
                                 int32_t k, bsm_gemm_layout layout, bsm_dtype out_dtype,
                                 bsm_schedule schedule, const int8_t* home_xcd,

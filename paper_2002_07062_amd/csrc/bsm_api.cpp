@@ -377,33 +377,42 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
                     static_cast<long long>(batch), m, n, k);
     if (static_cast<double>(batch) * std::max({m, n, k}) * std::max({m, n, k}) > 1.0e18)
         return fail(BSM_ERR_INVALID_ARG, "operands too large");
-    // The kernel runs 256-thread workgroups, two per CU by default (its LDS staging takes
-    // gemm_lds_bytes_per_wave() per wave).
+    // The kernel runs workgroups of gemm_wg_threads() threads whose waves share staged operands,
+    // gemm_waves_per_simd() per CU by default; each workgroup is one worker of the table.
     bsm_topology t{};
     if (topology) t = *topology;
-    if (t.wg_threads != 0 && t.wg_threads != 256)
-        return fail(BSM_ERR_INVALID_ARG, "matrix-product plans run 256-thread workgroups (got %d)",
-                    t.wg_threads);
-    t.wg_threads = 256;
-    // one workgroup per SIMD's worth of waves the kernel instance is compiled for
-    if (t.wg_per_cu == 0) t.wg_per_cu = bsm::gemm_waves_per_simd(layout, k);
+    const int wg_threads = bsm::gemm_wg_threads();
+    if (t.wg_threads != 0 && t.wg_threads != wg_threads)
+        return fail(BSM_ERR_INVALID_ARG, "matrix-product plans run %d-thread workgroups (got %d)",
+                    wg_threads, t.wg_threads);
+    if (t.wg_per_cu == 0) t.wg_per_cu = bsm::gemm_waves_per_simd();
+    const bool bf16_out = out_dtype == BSM_BF16;
     if (device >= 0) {
         DeviceGuard g;
         hipError_t e = g.enter(device);
         hipDeviceProp_t prop;
         if (e == hipSuccess) e = hipGetDeviceProperties(&prop, device);
         if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
-        const int64_t per_wg = 4LL * bsm::gemm_lds_bytes_per_wave(layout, k);
+        const int64_t per_wg = bsm::gemm_lds_bytes_per_wg(bf16_out);
         if (per_wg > static_cast<int64_t>(prop.sharedMemPerBlock) ||
             per_wg * t.wg_per_cu > static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor))
             return fail(BSM_ERR_INVALID_ARG, "wg_per_cu %d: %lld bytes of LDS per workgroup do not fit",
                         t.wg_per_cu, static_cast<long long>(per_wg));
     }
+    // planned with one-wave workgroups, so that every worker is a workgroup (same index, same
+    // XCD); the launch then runs the real workgroup size
+    t.wg_threads = 64;
     const int32_t rows[1] = {m}, cols[1] = {n};
     bsm_plan p = nullptr;
     bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
-                                schedule, home_xcd, nullptr, &t, device, /*row_unit=*/32);
+                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg());
     if (st != BSM_OK) return st;
+    p->topo.wg_threads = wg_threads;
+    p->table.per_wave = false;
+    p->table.stats.per_wave = 0;
+    p->table.stats.wg_threads = wg_threads;
+    p->table.stats.trace_bytes = static_cast<int64_t>(p->topo.n_wg()) * (wg_threads / 64) *
+                                 static_cast<int64_t>(sizeof(bsm_trace_rec));
     p->gemm = true;
     p->gemm_m = m;
     p->gemm_n = n;
@@ -445,8 +454,7 @@ bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float
     std::lock_guard<std::mutex> lock(p->mu);
     // k == 0 runs the same kernel: an empty reduction stores zeros
     e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, a, b, c, p->gemm_m, p->gemm_n,
-                         p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(),
-                         p->topo.wg_threads, p->table.per_wave ? 1 : 0, trace, s);
+                         p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(), trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     e = hipEventRecord(p->last_use, s);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");

@@ -13,43 +13,30 @@ using bsm_mm::Shape;
 
 template <int MODE, bool BF16OUT, bool VEC>
 hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const int32_t* worker_ptr,
-                    const bsm_item* items, int n_wg, int wg_threads, int per_wave, void* trace,
-                    hipStream_t stream) {
+                    const bsm_item* items, int n_wg, void* trace, hipStream_t stream) {
     const uint16_t* a_a = static_cast<const uint16_t*>(a);
     const uint16_t* a_b = static_cast<const uint16_t*>(b);
     void* a_c = c;
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
-    void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &per_wave, &a_trace};
-    const size_t lds = static_cast<size_t>(bsm_mm::mode_lds_bytes(MODE)) * (wg_threads / 64);
+    void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &a_trace};
+    const size_t lds = static_cast<size_t>(bsm_mm::wg_lds_bytes(BF16OUT));
     return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC>),
-                           dim3(n_wg), dim3(wg_threads), args, lds, stream);
+                           dim3(n_wg), dim3(bsm_mm::kGemmThreads), args, lds, stream);
 }
 
 }  // namespace
 
 namespace bsm {
 
-int gemm_mode(int layout, int /*k*/) { return layout == bsm_mm::kNN ? bsm_mm::kModeNn : bsm_mm::kModeNt; }
-
-int gemm_lds_bytes_per_wave(int layout, int k) {
-    switch (gemm_mode(layout, k)) {
-        case bsm_mm::kModeNt: return bsm_mm::mode_lds_bytes(bsm_mm::kModeNt);
-        default: return bsm_mm::mode_lds_bytes(bsm_mm::kModeNn);
-    }
-}
-
-int gemm_waves_per_simd(int layout, int k) {
-    switch (gemm_mode(layout, k)) {
-        case bsm_mm::kModeNt: return bsm_mm::mode_waves_per_simd(bsm_mm::kModeNt);
-        default: return bsm_mm::mode_waves_per_simd(bsm_mm::kModeNn);
-    }
-}
+int gemm_wg_threads() { return bsm_mm::kGemmThreads; }
+int gemm_lds_bytes_per_wg(bool bf16_out) { return bsm_mm::wg_lds_bytes(bf16_out); }
+int gemm_waves_per_simd() { return bsm_mm::kWavesPerSimd; }
+int gemm_rows_per_wg() { return bsm_mm::kWaves * bsm_mm::kTileM; }
 
 hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
                        int n, int k, float alpha, const int32_t* d_worker_ptr,
-                       const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
-                       void* trace, hipStream_t stream) {
+                       const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream) {
     Shape s;
     s.m = m;
     s.n = n;
@@ -65,13 +52,11 @@ hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, 
                            reinterpret_cast<uintptr_t>(c);
     const bool vec = (ptrs & 15) == 0 && k % 8 == 0 &&
                      n % ((layout == bsm_mm::kNN || bf16_out) ? 8 : 4) == 0;
-#define BSM_G(M, O, V) launch_g<M, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, wg_threads, per_wave, trace, stream)
+#define BSM_G(M, O, V) launch_g<M, O, V>(a, b, c, s, d_worker_ptr, d_items, n_wg, trace, stream)
 #define BSM_G2(M) (bf16_out ? (vec ? BSM_G(M, true, true) : BSM_G(M, true, false)) \
                             : (vec ? BSM_G(M, false, true) : BSM_G(M, false, false)))
-    switch (gemm_mode(layout, k)) {
-        case bsm_mm::kModeNt: return BSM_G2(bsm_mm::kModeNt);
-        default: return BSM_G2(bsm_mm::kModeNn);
-    }
+    if (layout == bsm_mm::kNN) return BSM_G2(bsm_mm::kModeNn);
+    return BSM_G2(bsm_mm::kModeNt);
 #undef BSM_G2
 #undef BSM_G
 }

@@ -7,13 +7,15 @@
 //   layout NN:  C_b = alpha A_b B_b     (A_b: m x k, B_b: k x n; e.g. P V)
 //
 // bf16 operands, fp32 accumulation on the matrix cores (v_mfma_f32_32x32x16_bf16), fp32 or
-// bf16 (round to nearest even) output.  A wave computes 32 output rows at a time in blocks of
-// 64 columns (two 32 x 32 MFMA tiles), as the transposed tile D = B_sub A_sub^T so that each
-// lane ends with four consecutive output columns.  Operands are staged in the wave's LDS from
-// 16-byte loads (NN's B transposed on the way in), one step ahead: a step's loads are in
-// flight while the previous step computes; the output block goes through LDS too and is
-// stored as whole rows.  At these shapes the work is bound by HBM (the 512 x 512 output, or
-// input), not by the matrix cores.
+// bf16 (round to nearest even) output.  A workgroup of four waves takes up to 128 rows of one
+// batch index at a time, 32 per wave, and walks the output in blocks of 64 columns (two
+// 32 x 32 MFMA tiles per wave) and the reduction in slices of 64.  Each wave computes the
+// transposed tile D = B_sub A_sub^T so that a lane ends with four consecutive output columns.
+// Operands are staged in LDS from 16-byte loads, two steps ahead: a wave's own A rows in its
+// own region, the B block shared by the four waves (each loads a quarter of it; two buffers,
+// one barrier per step); NN's B is stored as it is and read back transposed.  The output
+// block goes through the wave's LDS too and is stored as whole rows.  At these shapes the
+// work is bound by HBM (the 512 x 512 output, or input), not by the matrix cores.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -34,10 +36,10 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 enum { kNT = 0, kNN = 1 };
-constexpr int kTileM = 32;   // output rows per wave step
+constexpr int kWaves = 4;    // waves per workgroup
+constexpr int kTileM = 32;   // output rows per wave
 constexpr int kTileN = 32;   // output columns per MFMA tile
 constexpr int kTileK = 16;   // reduction depth per MFMA
-constexpr int kMaxTiles = 2; // tiles a wave accumulates side by side
 
 struct Shape {
     int m, n, k;
@@ -45,12 +47,11 @@ struct Shape {
     float alpha;
 };
 
-// One step of a wave's work on a 32-row chunk: the output column block [j0, j0 + 64) (two
-// 32 x 32 MFMA tiles) and the reduction slice [k0, k0 + 64).  Per-wave LDS layout (bf16
-// elements): A block [32][kLdk], B block [64][kLdk] (B's rows for NT, B's columns for NN: the
-// MFMA's row operand either way), rows padded so that a ds_read_b128 of 32 rows spreads over
-// the banks.  After a column block's last step the output block is staged in the same region
-// as [32][kLdc] fp32 and stored as whole rows.
+// One step of a workgroup: the output column block [j0, j0 + 64) and the reduction slice
+// [k0, k0 + 64).  LDS (bf16 elements unless noted): per wave, A block [32][kLdk], reused after
+// a column block's last step for the output block, [32][kLdc] fp32 or [32][kLdh] bf16; shared,
+// two B buffers of [64][kLdk] (NT: B's rows) or [64][kLdv] (NN: B's rows k0 .. k0+63 as they
+// are).  Rows are padded so that 16-byte accesses of consecutive rows spread over the banks.
 constexpr int kChunkK = 64;                 // reduction indices per step
 constexpr int kLdk = kChunkK + 8;           // padded LDS row, elements
 constexpr int kBlockN = 64;                 // output columns per block (two tiles)
@@ -58,11 +59,16 @@ constexpr int kBlockTiles = kBlockN / kTileN;
 constexpr int kLdc = kBlockN + 4;           // padded LDS row of the staged output, floats
 constexpr int kLdh = kBlockN + 8;           // ... staged as bf16, elements
 constexpr int kLdv = kBlockN + 8;           // padded LDS row of NN's B (rows = reduction index)
-constexpr int kLdsBytes = (kTileM * kLdc * 4 > (kTileM + kBlockN) * kLdk * 2)
-                              ? kTileM * kLdc * 4 : (kTileM + kBlockN) * kLdk * 2;
-static_assert(kChunkK * kLdv <= kBlockN * kLdk, "NN's B fits the B region");
-constexpr int kAPieces = kTileM * kChunkK / 8 / 64;   // 16-byte pieces of A per lane per step
-constexpr int kBPieces = kBlockN * kChunkK / 8 / 64;  // ... of B
+static_assert(kChunkK * kLdv <= kBlockN * kLdk, "NN's B fits the B buffer");
+constexpr int kBBufElems = kBlockN * kLdk;  // one shared B buffer
+constexpr int kDepth = 2;                   // steps of operands in flight = shared B buffers
+constexpr int wave_lds_bytes(bool bf16_out) {
+    return (bf16_out ? kTileM * kLdh * 2 : kTileM * kLdc * 4) > kTileM * kLdk * 2
+               ? (bf16_out ? kTileM * kLdh * 2 : kTileM * kLdc * 4) : kTileM * kLdk * 2;
+}
+constexpr int wg_lds_bytes(bool bf16_out) { return kWaves * wave_lds_bytes(bf16_out) + kDepth * kBBufElems * 2; }
+constexpr int kAPieces = kTileM * kChunkK / 8 / 64;            // 16-byte pieces of A per lane per step
+constexpr int kBPieces = kBlockN * kChunkK / 8 / 64 / kWaves;  // ... of B per lane (a quarter)
 
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -114,8 +120,9 @@ __device__ __forceinline__ u16x8 keep8(u16x8 v, int c, int len, bool ok) {
 
 // The operand pieces of one step, held in registers between their loads and their LDS writes
 // so that a step's loads are in flight while earlier steps compute.
+template <bool WITH_A>
 struct Pieces {
-    u16x8 a[kAPieces];
+    u16x8 a[WITH_A ? kAPieces : 1];
     u16x8 b[kBPieces];
 };
 
@@ -159,7 +166,7 @@ __device__ __forceinline__ void load_a(const uint16_t* a_blk, const Shape& s, in
 #pragma unroll
     for (int q = 0; q < kAPieces; ++q) {
         const int r = piece_row(lane, q);
-        pa[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : rows - 1) * s.k,
+        pa[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : (rows > 0 ? rows - 1 : 0)) * s.k,
                            k0 + piece_col(lane, q), s.k);
     }
 }
@@ -174,10 +181,12 @@ __device__ __forceinline__ void write_a(const u16x8 (&pa)[kAPieces], const Shape
     }
 }
 
+// The wave's quarter of the B block of step (j0, k0): pieces q = kBPieces * wave + 0, 1, of
+// the block's 64 x 64 as 64 lanes x 8 pieces (B's rows for NT, B's rows k0.. for NN).
 template <int LAYOUT, bool VEC, bool WITH_A>
 __device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t* b_blk,
-                                          const Shape& s, int rows, int j0, int k0, int lane,
-                                          Pieces& p) {
+                                          const Shape& s, int rows, int j0, int k0, int wave,
+                                          int lane, Pieces<WITH_A>& p) {
     if (s.k == 0) {  // empty reduction: nothing to read (write_step zeroes every piece)
         if constexpr (WITH_A) {
 #pragma unroll
@@ -188,47 +197,39 @@ __device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t*
         return;
     }
     if constexpr (WITH_A) load_a<VEC>(a_blk, s, rows, k0, lane, p.a);
-    if constexpr (LAYOUT == kNT) {
 #pragma unroll
-        for (int q = 0; q < kBPieces; ++q) {
-            const int j = j0 + piece_row(lane, q);
+    for (int q = 0; q < kBPieces; ++q) {
+        const int qg = kBPieces * wave + q;
+        if constexpr (LAYOUT == kNT) {
+            const int j = j0 + piece_row(lane, qg);
             p.b[q] = load8<VEC>(b_blk + static_cast<int64_t>(j < s.n ? j : s.n - 1) * s.k,
-                                k0 + piece_col(lane, q), s.k);
-        }
-    } else {
-#pragma unroll
-        for (int q = 0; q < kBPieces; ++q) {
-            const int kr = k0 + piece_nn_row(lane, q);
+                                k0 + piece_col(lane, qg), s.k);
+        } else {
+            const int kr = k0 + piece_nn_row(lane, qg);
             p.b[q] = load8<VEC>(b_blk + static_cast<int64_t>(kr < s.k ? kr : s.k - 1) * s.n,
-                                j0 + piece_nn_col(lane, q), s.n);
+                                j0 + piece_nn_col(lane, qg), s.n);
         }
     }
 }
 
 template <int LAYOUT, bool VEC, bool WITH_A>
-__device__ __forceinline__ void write_step(const Pieces& p, const Shape& s, int rows, int j0,
-                                           int k0, int lane, uint16_t* la, uint16_t* lb) {
+__device__ __forceinline__ void write_step(const Pieces<WITH_A>& p, const Shape& s, int rows,
+                                           int j0, int k0, int wave, int lane, uint16_t* la,
+                                           uint16_t* lb) {
     if constexpr (WITH_A) write_a<VEC>(p.a, s, rows, k0, lane, la);
-    if constexpr (LAYOUT == kNT) {
 #pragma unroll
-        for (int q = 0; q < kBPieces; ++q) {
-            const int r = piece_row(lane, q), c = piece_col(lane, q);
+    for (int q = 0; q < kBPieces; ++q) {
+        const int qg = kBPieces * wave + q;
+        if constexpr (LAYOUT == kNT) {
+            const int r = piece_row(lane, qg), c = piece_col(lane, qg);
             *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8<VEC>(p.b[q], k0 + c, s.k, j0 + r < s.n);
-        }
-    } else {
-        // B's rows k0 .. k0+63 as they are (row = reduction index, kLdv elements apart);
-        // the MFMA operand is read back transposed (ds_read_b64_tr_b16)
-#pragma unroll
-        for (int q = 0; q < kBPieces; ++q) {
-            const int kr = piece_nn_row(lane, q), c = piece_nn_col(lane, q);
-            *reinterpret_cast<u16x8*>(lb + kr * kLdv + c) =
-                keep8<VEC>(p.b[q], j0 + c, s.n, k0 + kr < s.k);
+        } else {
+            const int kr = piece_nn_row(lane, qg), c = piece_nn_col(lane, qg);
+            *reinterpret_cast<u16x8*>(lb + kr * kLdv + c) = keep8<VEC>(p.b[q], j0 + c, s.n, k0 + kr < s.k);
         }
     }
 }
 
-// Stores the staged output block (rows [i0, i0 + rows), columns [j0, j0 + jn) of batch b)
-// as whole rows: 16 lanes x 4 columns per row, four rows per store instruction.
 // Stores a staged output block (rows [i0, i0 + rows), columns [j0, j0 + jn)) as whole rows:
 // 16 lanes x 4 fp32 columns, four rows per instruction.
 template <bool VEC>
@@ -286,34 +287,35 @@ __device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, in
     }
 }
 
-// Output rows [i0, i0 + rows) (rows <= 32) of batch b, as a sequence of steps (column block,
-// reduction slice); step t + 1's loads are issued before step t's arithmetic.  AREG (the
-// whole reduction in one step, k <= 64): A's operands are read from LDS once, at the first
-// step, and kept in registers for every column block, so later steps move only B.
+// A workgroup's round: output rows [i0, i0 + rows) of batch bidx for this wave (rows <= 32;
+// 0 for a wave past the round's end, which still loads its quarter of B and meets every
+// barrier), as a sequence of steps (column block, reduction slice) that all four waves take
+// together; step t + kDepth's loads are issued before step t's arithmetic.  AREG (the whole
+// reduction in one step, k <= 64): A's operands are read from LDS once and kept in registers
+// for every column block, so later steps move only B.
 template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG>
-__device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, void* c,
-                                       const Shape& s, int64_t bidx, int i0, int rows, int lane,
-                                       uint16_t* lds) {
+__device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b, void* c,
+                                           const Shape& s, int64_t bidx, int i0, int rows,
+                                           int wave, int lane, uint16_t* lw, uint16_t* lbs) {
     const int li = lane & 31;
     const int h = lane >> 5;
-    uint16_t* const la = lds;
-    uint16_t* const lb = lds + kTileM * kLdk;
-    float* const lc = reinterpret_cast<float*>(lds);
-    const uint16_t* a_blk = a + bidx * s.a_batch + static_cast<int64_t>(i0) * s.k;
+    uint16_t* const la = lw;
+    const uint16_t* a_blk = rows > 0 ? a + bidx * s.a_batch + static_cast<int64_t>(i0) * s.k : a;
     const uint16_t* b_blk = b + bidx * s.b_batch;
     const int nk = s.k > 0 ? (s.k + kChunkK - 1) / kChunkK : 1;  // k == 0: one step of zeros
     const int nj = (s.n + kBlockN - 1) / kBlockN;
     const int nsteps = nk * nj;
     f32x16 acc[kBlockTiles];
-    // kDepth steps of operands in flight: step st + kDepth is loaded into the registers step
-    // st has just written to LDS (two for the 16-byte form; the element-wise form's registers
-    // allow one)
-    constexpr int kDepth = VEC ? 2 : 1;
-    Pieces p[kDepth];
+    Pieces<!AREG> p[kDepth];
     u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
-    if constexpr (AREG) {  // A once, through LDS into its MFMA layout
+    if constexpr (AREG) {  // A once, through the wave's LDS into its MFMA layout
         u16x8 pa[kAPieces];
-        load_a<VEC>(a_blk, s, rows, 0, lane, pa);
+        if (s.k > 0) {
+            load_a<VEC>(a_blk, s, rows, 0, lane, pa);
+        } else {
+#pragma unroll
+            for (int q = 0; q < kAPieces; ++q) pa[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        }
         write_a<VEC>(pa, s, rows, 0, lane, la);
         wave_lds_sync();
 #pragma unroll
@@ -321,9 +323,9 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
             a_reg[q] = *reinterpret_cast<const u16x8*>(la + li * kLdk + q * kTileK + 8 * h);
         wave_lds_sync();
     }
-    auto load = [&](int st, Pieces& pp) {
+    auto load = [&](int st, Pieces<!AREG>& pp) {
         const int js = st / nk, ks = st - js * nk;
-        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, lane, pp);
+        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane, pp);
     };
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
@@ -336,36 +338,41 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
         if (st >= nsteps) break;
         const int jb = st / nk, kb = st - jb * nk;
         const int j0 = jb * kBlockN;
+        uint16_t* const lb = lbs + d * kBBufElems;  // buffer st % kDepth
         if (kb == 0) {
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
         }
-        write_step<LAYOUT, VEC, !AREG>(p[d], s, rows, j0, kb * kChunkK, lane, la, lb);
-        wave_lds_sync();
+        // Buffer st % kDepth was last read at step st - kDepth; every wave finished that step
+        // before the barrier of step st - kDepth + 1, so one barrier per step orders both uses.
+        write_step<LAYOUT, VEC, !AREG>(p[d], s, rows, j0, kb * kChunkK, wave, lane, la, lb);
+        __syncthreads();
         if (st + kDepth < nsteps) load(st + kDepth, p[d]);
-        const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
+        if (rows > 0) {  // wave-uniform
 #pragma unroll
-        for (int kk = 0; kk < kChunkK; kk += kTileK) {
-            const bf16x8 av = __builtin_bit_cast(
-                bf16x8, AREG ? a_reg[AREG ? kk / kTileK : 0]
-                             : *reinterpret_cast<const u16x8*>(la + li * kLdk + kk + 8 * h));
+            for (int kk = 0; kk < kChunkK; kk += kTileK) {
+                const bf16x8 av = __builtin_bit_cast(
+                    bf16x8, AREG ? a_reg[AREG ? kk / kTileK : 0]
+                                 : *reinterpret_cast<const u16x8*>(la + li * kLdk + kk + 8 * h));
 #pragma unroll
-            for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
-                bf16x8 bv;
-                if constexpr (LAYOUT == kNT)
-                    bv = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const u16x8*>(lb + (t * kTileN + li) * kLdk + kk + 8 * h));
-                else
-                    bv = nn_row_operand(lb, t, kk, lane);
-                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[t], 0, 0, 0);
+                for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
+                    bf16x8 bv;
+                    if constexpr (LAYOUT == kNT)
+                        bv = __builtin_bit_cast(
+                            bf16x8, *reinterpret_cast<const u16x8*>(lb + (t * kTileN + li) * kLdk + kk + 8 * h));
+                    else
+                        bv = nn_row_operand(lb, t, kk, lane);
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[t], 0, 0, 0);
+                }
             }
         }
-        wave_lds_sync();  // operands consumed
-        if (kb + 1 < nk) continue;
+        wave_lds_sync();  // the wave's A consumed
+        if (kb + 1 < nk || rows == 0) continue;
         // column block done: tile t, lane (li, h) holds output row li, columns
         // j0 + 32 t + 8 g + 4 h + 0..3
+        const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
         if constexpr (BF16OUT) {  // rounded to bf16 (nearest even) on the way into LDS
-            uint16_t* const lh = lds;
+            uint16_t* const lh = lw;
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) {
 #pragma unroll
@@ -377,6 +384,7 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
             wave_lds_sync();
             store_block_bf16<VEC>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lh);
         } else {
+            float* const lc = reinterpret_cast<float*>(lw);
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) {
 #pragma unroll
@@ -393,31 +401,29 @@ __device__ __forceinline__ void rows32(const uint16_t* a, const uint16_t* b, voi
     }
 }
 
-// Worker loop: worker v (a workgroup, or one wave when per_wave) runs its items; an item's
-// rows are taken 32 at a time (split where a batch ends), the workgroup's waves splitting
-// them when they share the item.
-// Kernel modes (one compiled instance each): NT and NN, both with LDS-staged operands.
+// Kernel modes (one compiled instance each): NT and NN.
 enum { kModeNt = 0, kModeNn = 1 };
-constexpr int mode_lds_bytes(int) { return kLdsBytes; }
-constexpr int mode_waves_per_simd(int) { return 2; }
+constexpr int kWavesPerSimd = 3;
 
+// Worker loop: workgroup w runs its items; an item's rows are taken up to 128 at a time (cut
+// where a batch ends), 32 per wave.  Every bound of these loops is the same for the four
+// waves, so they meet the same barriers.
 template <int MODE, bool BF16OUT, bool VEC>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
                                             const Shape& s, const int32_t* __restrict__ worker_ptr,
-                                            const bsm_item* __restrict__ items, int per_wave,
+                                            const bsm_item* __restrict__ items,
                                             bsm_trace_rec* __restrict__ trace, uint16_t* lds_base) {
+    constexpr int kLayout = MODE == kModeNn ? kNN : kNT;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
-    const int nwaves = static_cast<int>(blockDim.x) >> 6;
     const int lane = static_cast<int>(threadIdx.x) & 63;
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
-    const int worker = per_wave ? w * nwaves + wave : w;
-    const int my_wave = per_wave ? 0 : wave;
-    const int my_nwaves = per_wave ? 1 : nwaves;
-    uint16_t* const lds = lds_base + wave * (mode_lds_bytes(MODE) / 2);
+    uint16_t* const lw = lds_base + wave * (wave_lds_bytes(BF16OUT) / 2);
+    uint16_t* const lbs = lds_base + kWaves * (wave_lds_bytes(BF16OUT) / 2);
+    const bool areg = VEC && s.k <= kChunkK && s.n > kBlockN;  // (registers: 16-byte form only)
     uint32_t done = 0;
-    const int i_begin = worker_ptr[worker];
-    const int i_end = worker_ptr[worker + 1];
+    const int i_begin = worker_ptr[w];
+    const int i_end = worker_ptr[w + 1];
     for (int it = i_begin; it < i_end; ++it) {
         const int64_t e0 = items[it].elem_offset;
         const int nrows = items[it].nrows;
@@ -425,23 +431,25 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
         const int64_t stride = static_cast<int64_t>(items[it].rep_stride) * s.n;
         for (int r = 0; r < reps; ++r) {
             // Output rows are numbered batch after batch (row G = b m + i); a run may cross
-            // from one batch into the next, so each 32-row chunk is split at batch ends.
-            const int64_t g0 = (e0 + r * stride) / s.n;
-            for (int q = my_wave * kTileM; q < nrows; q += my_nwaves * kTileM) {
-                int64_t g = g0 + q;
-                int left = nrows - q < kTileM ? nrows - q : kTileM;
-                while (left > 0) {
-                    const int64_t bidx = g / s.m;
-                    const int i = static_cast<int>(g - bidx * s.m);
-                    const int seg = s.m - i < left ? s.m - i : left;
-                    if (VEC && s.k <= kChunkK && s.n > kBlockN)  // (registers: 16-byte form only)
-                        rows32<MODE == kModeNn ? kNN : kNT, BF16OUT, VEC, true>(a, b, c, s, bidx, i, seg, lane, lds);
-                    else
-                        rows32<MODE == kModeNn ? kNN : kNT, BF16OUT, VEC, false>(a, b, c, s, bidx, i, seg, lane, lds);
-                    done += static_cast<uint32_t>(seg);
-                    g += seg;
-                    left -= seg;
-                }
+            // from one batch into the next.
+            int64_t g = (e0 + r * stride) / s.n;
+            int left = nrows;
+            while (left > 0) {
+                const int64_t bidx = g / s.m;
+                const int i = static_cast<int>(g - bidx * s.m);
+                int seg = s.m - i < left ? s.m - i : left;
+                if (seg > kWaves * kTileM) seg = kWaves * kTileM;
+                int mine = seg - wave * kTileM;
+                mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
+                if (areg)
+                    round_rows<kLayout, BF16OUT, VEC, true>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                                                            wave, lane, lw, lbs);
+                else
+                    round_rows<kLayout, BF16OUT, VEC, false>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                                                             wave, lane, lw, lbs);
+                done += static_cast<uint32_t>(mine);
+                g += seg;
+                left -= seg;
             }
         }
     }
@@ -453,22 +461,22 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
         rec.rows = done;
         rec.t_start = t0;
         rec.t_end = __builtin_amdgcn_s_memrealtime();
-        trace[static_cast<int64_t>(w) * nwaves + wave] = rec;
+        trace[static_cast<int64_t>(w) * kWaves + wave] = rec;
     }
 }
 
-extern __shared__ uint16_t bsm_gemm_lds[];  // kLdsBytes per wave
+extern __shared__ uint16_t bsm_gemm_lds[];  // wg_lds_bytes() per workgroup
 
-// 256-thread workgroups; each mode's instance is compiled for its waves per SIMD (registers:
-// 512 / waves) and takes mode_lds_bytes() of LDS per wave.
-constexpr int kGemmThreads = 256;
+constexpr int kGemmThreads = 64 * kWaves;
 
+// The element-wise (unaligned / odd-size) form is compiled for two waves per SIMD: its
+// registers do not fit three.
 template <int MODE, bool BF16OUT, bool VEC>
-__global__ void __launch_bounds__(kGemmThreads, mode_waves_per_simd(MODE))
+__global__ void __launch_bounds__(kGemmThreads, VEC ? kWavesPerSimd : 2)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
-                int per_wave, bsm_trace_rec* __restrict__ trace) {
-    gemm_worker<MODE, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, per_wave, trace, bsm_gemm_lds);
+                bsm_trace_rec* __restrict__ trace) {
+    gemm_worker<MODE, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, trace, bsm_gemm_lds);
 }
 
 }  // namespace bsm_mm

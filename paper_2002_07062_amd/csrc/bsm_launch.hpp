@@ -36,16 +36,18 @@ hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool tempo
 // Batched matrix product under a table whose slices are the outputs C_b (m x n each, batch
 // after batch): layout 0 (NT) C_b = alpha A_b B_b^T, layout 1 (NN) C_b = alpha A_b B_b; bf16
 // A and B, fp32 or bf16 C.
-// The matrix-product kernel instance (mode) a layout and reduction depth run, the LDS bytes
-// each of its waves uses, and the waves per SIMD it is compiled for.
-int gemm_mode(int layout, int k);
-int gemm_lds_bytes_per_wave(int layout, int k);
-int gemm_waves_per_simd(int layout, int k);
+// Matrix-product launches: threads per workgroup, LDS bytes per workgroup, the waves per SIMD
+// the kernel is compiled for, and the output rows a workgroup takes per round.
+int gemm_wg_threads();
+int gemm_lds_bytes_per_wg(bool bf16_out);
+int gemm_waves_per_simd();
+int gemm_rows_per_wg();
 
+// Worker w of the table is workgroup w (gemm_wg_threads() threads, gemm_rows_per_wg() rows
+// per round).
 hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
                        int n, int k, float alpha, const int32_t* d_worker_ptr,
-                       const bsm_item* d_items, int n_wg, int wg_threads, int per_wave,
-                       void* trace, hipStream_t stream);
+                       const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream);
 
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,

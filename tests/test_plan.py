@@ -347,9 +347,10 @@ def test_bad_weights_are_rejected(weights, err):
 
 @pytest.mark.parametrize("schedule", ["rr", "balanced", "xcd"])
 @pytest.mark.parametrize("shape", [(384, 512, 512, 64), (384, 512, 64, 512), (7, 45, 33, 20)])
-def test_gemm_plans_cover_every_output_row_in_32_row_blocks(schedule, shape):
+def test_gemm_plans_cover_every_output_row_in_128_row_blocks(schedule, shape):
     """Matrix-product plans: the outputs C_b are the slices; every output row is scheduled
-    exactly once; BALANCED cuts whole 32-row blocks (the XCD balancer moves single rows)."""
+    exactly once; workers are workgroups (512 on MI355X at two per CU), and BALANCED cuts whole
+    128-row blocks, the rows a workgroup takes per round (the XCD balancer moves single rows)."""
     batch, m, n, k = shape
     p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt", "f32", schedule, topology=MI355X, device=-1)
     d = bsm.bsm_plan_describe(p)
@@ -358,13 +359,19 @@ def test_gemm_plans_cover_every_output_row_in_32_row_blocks(schedule, shape):
     offs = np.arange(batch, dtype=np.int64) * m * n
     assert pc.check_exactly_once(ptr, items, offs, [m] * batch, [n] * batch) == []
     assert d["algorithmic_bytes"] == batch * (2 * (m * k + n * k) + 4 * m * n)
+    assert d["per_wave"] == 0 and d["n_workers"] == 512 and d["wg_threads"] == 256
+    assert d["trace_bytes"] == 512 * 4 * bsm.TRACE_DTYPE.itemsize
     if schedule == "balanced":
-        # pieces are whole 32-row blocks of the row stream (batches follow each other, so a
+        # pieces are whole 128-row blocks of the row stream (batches follow each other, so a
         # block may cross into the next batch; the kernel splits it there), the stream's last
         # piece aside
         g0 = items["elem_offset"] // n
-        assert np.all(g0 % 32 == 0)
-        assert np.all((items["nrows"] % 32 == 0) | (g0 + items["nrows"] == batch * m))
+        assert np.all(g0 % 128 == 0)
+        assert np.all((items["nrows"] % 128 == 0) | (g0 + items["nrows"] == batch * m))
+    if shape[0] == 384 and schedule != "rr":
+        # Section 6's products: 196608 output rows are 384 per workgroup, three rounds each
+        rows = np.add.reduceat(items["nrows"] * items["reps"], ptr[:-1]) if len(items) else []
+        assert np.all(np.asarray(rows) == 384)
 
 
 def test_gemm_plan_rejects_bad_arguments():
