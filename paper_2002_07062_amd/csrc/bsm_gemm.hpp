@@ -85,12 +85,14 @@ __device__ __forceinline__ unsigned pack_bf16(float a, float b) {
 // writes them to LDS).  VEC: one unconditional 16-byte load (len % 8 == 0, 16-byte aligned
 // rows), so that no branch or select on the loaded data sits between a step's loads and the
 // wait before their use; the scalar form (any len) loads element by element.  Ordinary
-// (cache-resident) loads: B is re-read by every row chunk of its batch, A by every column
-// block.
-template <bool VEC>
+// (cache-resident) loads where the data is read again (B by every row round of its batch, A
+// by every column block), nontemporal (STREAM) where it is read once.
+template <bool VEC, bool STREAM = false>
 __device__ __forceinline__ u16x8 load8(const uint16_t* row, int c, int len) {
     if constexpr (VEC) {
-        return *reinterpret_cast<const u16x8*>(row + (c < len ? c : len - 8));
+        const u16x8* p = reinterpret_cast<const u16x8*>(row + (c < len ? c : len - 8));
+        if constexpr (STREAM) return __builtin_nontemporal_load(p);
+        return *p;
     } else {
         u16x8 v;
 #pragma unroll
@@ -162,12 +164,13 @@ __device__ __forceinline__ bf16x8 nn_row_operand(const uint16_t* lb, int t, int 
 // (rows past `rows` and columns past k zeroed).
 template <bool VEC>
 __device__ __forceinline__ void load_a(const uint16_t* a_blk, const Shape& s, int rows, int k0,
-                                       int lane, u16x8 (&pa)[kAPieces]) {
+                                       int lane, bool stream, u16x8 (&pa)[kAPieces]) {
 #pragma unroll
     for (int q = 0; q < kAPieces; ++q) {
         const int r = piece_row(lane, q);
-        pa[q] = load8<VEC>(a_blk + static_cast<int64_t>(r < rows ? r : (rows > 0 ? rows - 1 : 0)) * s.k,
-                           k0 + piece_col(lane, q), s.k);
+        const uint16_t* row = a_blk + static_cast<int64_t>(r < rows ? r : (rows > 0 ? rows - 1 : 0)) * s.k;
+        const int c = k0 + piece_col(lane, q);
+        pa[q] = stream ? load8<VEC, true>(row, c, s.k) : load8<VEC, false>(row, c, s.k);
     }
 }
 
@@ -186,17 +189,8 @@ __device__ __forceinline__ void write_a(const u16x8 (&pa)[kAPieces], const Shape
 template <int LAYOUT, bool VEC, bool WITH_A>
 __device__ __forceinline__ void load_step(const uint16_t* a_blk, const uint16_t* b_blk,
                                           const Shape& s, int rows, int j0, int k0, int wave,
-                                          int lane, Pieces<WITH_A>& p) {
-    if (s.k == 0) {  // empty reduction: nothing to read (write_step zeroes every piece)
-        if constexpr (WITH_A) {
-#pragma unroll
-            for (int q = 0; q < kAPieces; ++q) p.a[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        }
-#pragma unroll
-        for (int q = 0; q < kBPieces; ++q) p.b[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        return;
-    }
-    if constexpr (WITH_A) load_a<VEC>(a_blk, s, rows, k0, lane, p.a);
+                                          int lane, bool stream_a, Pieces<WITH_A>& p) {
+    if constexpr (WITH_A) load_a<VEC>(a_blk, s, rows, k0, lane, stream_a, p.a);
 #pragma unroll
     for (int q = 0; q < kBPieces; ++q) {
         const int qg = kBPieces * wave + q;
@@ -302,7 +296,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     uint16_t* const la = lw;
     const uint16_t* a_blk = rows > 0 ? a + bidx * s.a_batch + static_cast<int64_t>(i0) * s.k : a;
     const uint16_t* b_blk = b + bidx * s.b_batch;
-    const int nk = s.k > 0 ? (s.k + kChunkK - 1) / kChunkK : 1;  // k == 0: one step of zeros
+    const int nk = (s.k + kChunkK - 1) / kChunkK;  // k > 0 here
     const int nj = (s.n + kBlockN - 1) / kBlockN;
     const int nsteps = nk * nj;
     f32x16 acc[kBlockTiles];
@@ -310,12 +304,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
     if constexpr (AREG) {  // A once, through the wave's LDS into its MFMA layout
         u16x8 pa[kAPieces];
-        if (s.k > 0) {
-            load_a<VEC>(a_blk, s, rows, 0, lane, pa);
-        } else {
-#pragma unroll
-            for (int q = 0; q < kAPieces; ++q) pa[q] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        }
+        load_a<VEC>(a_blk, s, rows, 0, lane, true, pa);  // read once
         write_a<VEC>(pa, s, rows, 0, lane, la);
         wave_lds_sync();
 #pragma unroll
@@ -325,29 +314,29 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     }
     auto load = [&](int st, Pieces<!AREG>& pp) {
         const int js = st / nk, ks = st - js * nk;
-        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane, pp);
+        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane,
+                                      nj == 1, pp);  // A read once when one column block
     };
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-        if (d < nsteps) load(d, p[d]);
-    }
-    for (int st0 = 0; st0 < nsteps; st0 += kDepth) {
-#pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-        const int st = st0 + d;
-        if (st >= nsteps) break;
+    for (int d = 0; d < kDepth; ++d) load(d < nsteps ? d : nsteps - 1, p[d]);
+    static_assert(kDepth == 2, "the step loop below is written for two buffers");
+    // One step: st's operands (in pp, loaded kDepth steps ago) go to LDS buffer lb, then
+    // step st + kDepth's loads are issued into pp, then st's arithmetic and, at a column
+    // block's end, its output.
+    auto step = [&](int st, Pieces<!AREG>& pp, uint16_t* lb) {
         const int jb = st / nk, kb = st - jb * nk;
         const int j0 = jb * kBlockN;
-        uint16_t* const lb = lbs + d * kBBufElems;  // buffer st % kDepth
         if (kb == 0) {
 #pragma unroll
             for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
         }
-        // Buffer st % kDepth was last read at step st - kDepth; every wave finished that step
-        // before the barrier of step st - kDepth + 1, so one barrier per step orders both uses.
-        write_step<LAYOUT, VEC, !AREG>(p[d], s, rows, j0, kb * kChunkK, wave, lane, la, lb);
+        // lb (buffer st % 2) was last read at step st - 2; every wave finished that step
+        // before the barrier of step st - 1, so one barrier per step orders both uses.
+        write_step<LAYOUT, VEC, !AREG>(pp, s, rows, j0, kb * kChunkK, wave, lane, la, lb);
         __syncthreads();
-        if (st + kDepth < nsteps) load(st + kDepth, p[d]);
+        // issued on every step (past the last step: the last step's operands again, cache
+        // hits, unused), so that every path has the same loads in flight
+        load(st + kDepth < nsteps ? st + kDepth : nsteps - 1, pp);
         if (rows > 0) {  // wave-uniform
 #pragma unroll
             for (int kk = 0; kk < kChunkK; kk += kTileK) {
@@ -367,7 +356,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
             }
         }
         wave_lds_sync();  // the wave's A consumed
-        if (kb + 1 < nk || rows == 0) continue;
+        if (kb + 1 < nk || rows == 0) return;
         // column block done: tile t, lane (li, h) holds output row li, columns
         // j0 + 32 t + 8 g + 4 h + 0..3
         const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
@@ -397,7 +386,30 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
             store_block_f32<VEC>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
         }
         wave_lds_sync();  // the next step rewrites the region
+    };
+    // Two steps per iteration and the odd one after the loop, so that every path around the
+    // loop issues the same loads (a step waits for its own loads only, not for the next
+    // step's, which the wait-count insertion would otherwise have to assume).
+    int st = 0;
+    for (; st + 1 < nsteps; st += 2) {
+        step(st, p[0], lbs);
+        step(st + 1, p[1], lbs + kBBufElems);
     }
+    if (st < nsteps) step(st, p[0], lbs);
+}
+
+// An empty reduction (k == 0): the wave's output rows are zeros.
+template <bool BF16OUT>
+__device__ __forceinline__ void zero_rows(void* c, const Shape& s, int64_t bidx, int i0, int rows,
+                                          int lane) {
+    for (int r = 0; r < rows; ++r) {
+        const int64_t off = bidx * s.c_batch + static_cast<int64_t>(i0 + r) * s.n;
+        for (int j = lane; j < s.n; j += 64) {
+            if constexpr (BF16OUT)
+                static_cast<uint16_t*>(c)[off + j] = 0;
+            else
+                static_cast<float*>(c)[off + j] = 0.0f;
+        }
     }
 }
 
@@ -441,7 +453,9 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 if (seg > kWaves * kTileM) seg = kWaves * kTileM;
                 int mine = seg - wave * kTileM;
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
-                if (areg)
+                if (s.k == 0)
+                    zero_rows<BF16OUT>(c, s, bidx, i + wave * kTileM, mine, lane);
+                else if (areg)
                     round_rows<kLayout, BF16OUT, VEC, true>(a, b, c, s, bidx, i + wave * kTileM, mine,
                                                             wave, lane, lw, lbs);
                 else
