@@ -275,9 +275,10 @@ bsm_status bsm_plan_describe(bsm_plan plan, bsm_plan_stats* stats);
 bsm_status bsm_plan_export(bsm_plan plan, int32_t* worker_ptr, bsm_item* items, int8_t* home,
                            uint8_t* overlap);
 
-/* Free a plan.  Waits for the plan's executions to finish first (its last stream's event, or
- * the whole device when the plan ran on more than one stream).  A plan may be executed from
- * several threads and streams, but must not be destroyed while another thread executes it. */
+/* Free a plan.  A plan that has been executed waits for its device to finish all queued work
+ * first (executions record nothing per launch, so the wait is device-wide).  A plan may be
+ * executed from several threads and streams, but must not be destroyed while another thread
+ * executes it. */
 bsm_status bsm_plan_destroy(bsm_plan plan);
 
 bsm_status bsm_device_info(int device, bsm_device_props* info);

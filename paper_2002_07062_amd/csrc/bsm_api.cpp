@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -37,11 +38,7 @@ struct bsm_plan_s {
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
     const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
-    hipEvent_t last_use = nullptr;  // recorded after every execution
-    bool used = false;
-    hipStream_t last_stream = nullptr;
-    bool many_streams = false;      // executed on more than one stream since creation
-    std::mutex mu;                  // guards the launch + event bookkeeping above
+    std::atomic<bool> used{false};  // executed at least once (destroy then waits for the device)
 };
 
 namespace {
@@ -204,14 +201,10 @@ void free_device(bsm_plan p) {
     if (p->device < 0) return;
     DeviceGuard g;
     if (g.enter(p->device) != hipSuccess) return;
-    if (p->last_use) {
-        // The event marks the last execution on the last stream; executions on other streams
-        // may still be reading the table, so then wait for the whole device.
-        if (p->many_streams) (void)hipDeviceSynchronize();
-        else if (p->used) (void)hipEventSynchronize(p->last_use);
-        (void)hipEventDestroy(p->last_use);
-        p->last_use = nullptr;
-    }
+    // Executions on any stream may still be reading the table.  (Nothing is recorded per
+    // execution: an event after every launch costs the stream a gap of several microseconds
+    // between kernels.)
+    if (p->used) (void)hipDeviceSynchronize();
     if (p->d_table) {
         (void)hipFree(p->d_table);
         p->d_table = nullptr;
@@ -304,7 +297,6 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         if (e == hipSuccess && !p->table.items.empty())
             e = hipMemcpy(base + items_at, p->table.items.data(),
                           p->table.items.size() * sizeof(bsm_item), hipMemcpyHostToDevice);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->last_use, hipEventDisableTiming);
         if (e != hipSuccess) {
             bsm_status st = hip_fail(e, "uploading the work table");
             free_device(p.get());
@@ -345,7 +337,6 @@ bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b,
     hipError_t e = g.enter(p->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    std::lock_guard<std::mutex> lock(p->mu);
     const bool temporal = (p->flags & BSM_FLAG_TEMPORAL) != 0;
     if (backward)
         e = bsm::launch_softmax_backward(p->dtype, p->kernel_class, temporal, a, b, out,
@@ -357,10 +348,6 @@ bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b,
                                 p->d_items, p->topo.n_wg(), p->topo.wg_threads,
                                 p->table.per_wave ? 1 : 0, p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    e = hipEventRecord(p->last_use, s);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if (p->used && s != p->last_stream) p->many_streams = true;
-    p->last_stream = s;
     p->used = true;
     return BSM_OK;
 }
@@ -451,15 +438,10 @@ bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float
     hipError_t e = g.enter(p->device);
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    std::lock_guard<std::mutex> lock(p->mu);
     // k == 0 runs the same kernel: an empty reduction stores zeros
     e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, a, b, c, p->gemm_m, p->gemm_n,
                          p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(), trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    e = hipEventRecord(p->last_use, s);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if (p->used && s != p->last_stream) p->many_streams = true;
-    p->last_stream = s;
     p->used = true;
     return BSM_OK;
 }
