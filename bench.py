@@ -422,9 +422,12 @@ def main() -> int:
     ap.add_argument("--schedule", default="balanced", choices=["rr", "balanced", "xcd"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="headline line only")
-    ap.add_argument("--op", default="forward", choices=["forward", "backward"],
+    ap.add_argument("--op", default="forward", choices=["forward", "backward", "gemm"],
                     help="backward: time the gradient kernel alone on --workload and print its "
-                         "line (not the headline metric)")
+                         "line; gemm: time one batched product (--gemm, --out) alone (neither "
+                         "is the headline metric)")
+    ap.add_argument("--gemm", default="scores_384x512x512x64", choices=list(GEMM_SHAPES))
+    ap.add_argument("--out", default="bf16", choices=["bf16", "f32"], help="--op gemm: C's type")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -464,6 +467,29 @@ def main() -> int:
             "pct_of_peak": round(100 * r["gbs"] / PEAK_HBM_GBS, 2),
             "algorithmic_bytes": r["algorithmic_bytes"],
             "copy_reference_gbs": round(wb.algorithmic_bytes / (copy_ms * 1e-3) / 1e9, 1)}))
+        return 0
+
+    if args.op == "gemm":
+        # one batched product alone, with the copy reference (half the bytes each way) for
+        # the counters' scale factors
+        r = run_gemm(args.gemm, args.schedule, args.steps, args.warmup, out=args.out)
+        batch, m, n, k, layout = GEMM_SHAPES[args.gemm]
+        half = r["algorithmic_bytes"] // 2 // 16 * 16
+        n_pairs = _rotation(2 * half)
+        xs = [torch.empty(half // 4, device="cuda") for _ in range(n_pairs)]
+        outs = [torch.empty_like(x) for x in xs]
+        copy_ms = time_copy(xs, outs, half, args.steps, args.warmup)
+        print(json.dumps({
+            "metric": f"batched matrix product HBM GB/s ({args.gemm}, {layout}, bf16 in, {args.out} out)",
+            "value": round(r["gbs"], 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(r["ms_per_step"], 5),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": args.gemm, "batch": batch, "m": m, "n": n, "k": k,
+                       "layout": layout, "out": args.out, "schedule": args.schedule, "op": "gemm"},
+            "tflops": round(r["tflops"], 2), "pct_of_peak": round(100 * r["gbs"] / PEAK_HBM_GBS, 2),
+            "algorithmic_bytes": r["algorithmic_bytes"], "copy_bytes_each_way": half,
+            "copy_reference_gbs": round(2 * half / (copy_ms * 1e-3) / 1e9, 1)}))
         return 0
 
     head, w = run_workload(args.workload, args.schedule, args.steps, args.warmup)
