@@ -274,7 +274,9 @@ def xcd_weight_calibration(name, steps, warmup):
         torch.cuda.synchronize()
         rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
         for xc in range(st["n_xcd"]):
-            r = rec[rec["xcc_id"] == xc]
+            # the waves of the workers planned for XCD xc (workgroups w mod n_xcd == xc: the
+            # bytes of xcd_bytes[xc]; dispatch may rotate which XCD runs them, uniformly)
+            r = rec[rec["wg"] % st["n_xcd"] == xc]
             span = float(r["t_end"].max() - r["t_start"].min())
             rates[xc] += st["xcd_bytes"][xc] / max(span, 1.0)
     plan.destroy()

@@ -129,4 +129,6 @@ def test_trace_counts_every_output_row():
     p.destroy()
     rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
     assert int(rec["rows"].sum()) == batch * m
-    assert np.all(rec["xcc_id"] == (rec["wg"] % 8))
+    # one XCD per residue of the workgroup index (dispatch may rotate the grid as a whole)
+    rot = (rec["xcc_id"].astype(np.int64) - rec["wg"].astype(np.int64)) % 8
+    assert len(set(rot.tolist())) == 1
