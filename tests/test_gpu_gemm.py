@@ -132,3 +132,55 @@ def test_trace_counts_every_output_row():
     # one XCD per residue of the workgroup index (dispatch may rotate the grid as a whole)
     rot = (rec["xcc_id"].astype(np.int64) - rec["wg"].astype(np.int64)) % 8
     assert len(set(rot.tolist())) == 1
+
+
+@pytest.mark.parametrize("layout,shape", [("nt", (12, 200, 130, 72)), ("nn", (12, 200, 72, 136))])
+def test_occupancy_and_homes_do_not_change_bits(layout, shape):
+    """Plans for one, two or three workgroups per CU, and an XCD plan with caller-given homes,
+    cut the rows differently; every output bit is the same (a row's result depends only on
+    its operands)."""
+    batch, m, n, k = shape
+    a, b = _operands(batch, m, n, k, seed=75)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    outs = []
+    for topo, sched, homes in [(dict(wg_per_cu=1), "balanced", None), (dict(wg_per_cu=2), "rr", None),
+                               (dict(wg_per_cu=3), "xcd", None),
+                               (None, "xcd", np.arange(batch, dtype=np.int8) % 8 // 3)]:
+        print(f"[gemm {layout} {shape} {topo} {sched} homes={homes is not None}]", flush=True)
+        p = bsm.bsm_gemm_plan_create(batch, m, n, k, layout, "f32", sched, home_xcd=homes,
+                                     topology=topo, device=0)
+        c = torch.full((batch * m * n,), float("nan"), device="cuda")
+        bsm.bsm_gemm_execute(p, a_d, b_d, c)
+        torch.cuda.synchronize()
+        p.destroy()
+        outs.append(to_host_bits(c))
+    _check(outs[0], a, b, batch, m, n, k, layout, "f32")
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+@pytest.mark.parametrize("layout", ["nt", "nn"])
+@pytest.mark.parametrize("which", ["a", "b", "c"])
+def test_misaligned_operand_takes_the_elementwise_path(layout, which):
+    """An operand 2 bytes (or C 4 bytes) off a 16-byte boundary cannot use 16-byte accesses;
+    the element-wise instance gives the same results as the aligned one."""
+    batch, m, n, k = 5, 96, 80, 72
+    a, b = _operands(batch, m, n, k, seed=76)
+    a_buf = torch.zeros(a.size + 8, dtype=torch.bfloat16, device="cuda")
+    b_buf = torch.zeros(b.size + 8, dtype=torch.bfloat16, device="cuda")
+    c_buf = torch.full((batch * m * n + 8,), float("nan"), device="cuda")
+    oa, ob, oc = (1 if which == "a" else 0), (1 if which == "b" else 0), (1 if which == "c" else 0)
+    a_d, b_d, c = a_buf[oa: oa + a.size], b_buf[ob: ob + b.size], c_buf[oc: oc + batch * m * n]
+    a_d.copy_(_dev_bf16(a))
+    b_d.copy_(_dev_bf16(b))
+    _run((batch, m, n, k, layout, "f32", "balanced"), a_d, b_d, c)
+    got = to_host_bits(c)
+    ref_c = torch.empty(batch * m * n, device="cuda")
+    _run((batch, m, n, k, layout, "f32", "balanced"), _dev_bf16(a), _dev_bf16(b), ref_c)
+    want = to_host_bits(ref_c)
+    _check(got, a, b, batch, m, n, k, layout, "f32")
+    # same products, same fp32 accumulation order per MFMA: the aligned and element-wise
+    # instances differ only in how operands reach LDS
+    assert np.array_equal(got, want)
+    rest = bits_to_f64(to_host_bits(c_buf))
+    assert np.all(np.isnan(rest[:oc])) and np.all(np.isnan(rest[oc + batch * m * n:])), "written outside C"
