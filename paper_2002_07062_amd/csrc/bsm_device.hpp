@@ -486,11 +486,15 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
 #define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     if (nvec <= 16) return BSM_RUN(16, 1);
     if (nvec <= 32) return BSM_RUN(32, 1);
-    if (nvec <= 64) return BSM_RUN(64, 1);
     // Larger register tiles only for aligned rows; unaligned longer rows take the two-pass path.
+    // Rows of 33..64 vectors: 32 lanes x 2 vectors rather than 64 x 1 (a shorter butterfly and
+    // half the per-row work per value: +7% on 384 x 512 x 512 bf16); the host gives such rows
+    // kernel class 1, so the tile depends on the row length only.
     if constexpr (VEC && KCLASS >= 1) {
+        if (nvec <= 64) return BSM_RUN(32, 2);
         if (nvec <= 128) return BSM_RUN(64, 2);
     }
+    if (nvec <= 64) return BSM_RUN(64, 1);
     if constexpr (VEC && KCLASS >= 2) {
         if (nvec <= 256) return BSM_RUN(64, 4);
     }
@@ -660,6 +664,8 @@ __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
                                                       int lane64, float* lds, int cap) {
     const int nvec = (cols + E::kEPV - 1) / E::kEPV;
 #define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    // (Rows of 33..64 vectors keep 64 lanes x 1 vector here: with two input streams the
+    // forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x 512 bf16.)
     if (nvec <= 16) return BSM_RUN_BWD(16, 1);
     if (nvec <= 32) return BSM_RUN_BWD(32, 1);
     if (nvec <= 64) return BSM_RUN_BWD(64, 1);

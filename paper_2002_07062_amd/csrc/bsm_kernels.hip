@@ -77,8 +77,8 @@ namespace bsm {
 
 int kernel_class_for(int32_t max_cols, int elem_bytes) {
     const int64_t nvec = (static_cast<int64_t>(max_cols) * elem_bytes + kVecBytes - 1) / kVecBytes;
-    if (nvec <= 64) return 0;
-    if (nvec <= 128) return 1;
+    if (nvec <= 32) return 0;
+    if (nvec <= 128) return 1;  // rows of 33..64 vectors run 32 lanes x 2 vectors
     if (nvec <= 256) return 2;
     if (nvec <= 512) return 3;
     return 4;

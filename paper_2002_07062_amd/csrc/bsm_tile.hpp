@@ -20,6 +20,7 @@ struct Tile {
 constexpr Tile tile_for(int64_t nvec, int max_v) {
     if (nvec <= 16) return Tile{16, 1};
     if (nvec <= 32) return Tile{32, 1};
+    if (max_v >= 2 && nvec <= 64) return Tile{32, 2};  // (kernel class >= 1 for such rows)
     if (nvec <= 64) return Tile{64, 1};
     if (max_v >= 2 && nvec <= 128) return Tile{64, 2};
     if (max_v >= 4 && nvec <= 256) return Tile{64, 4};
