@@ -49,8 +49,13 @@ __device__ __forceinline__ float dpp(float v) {
         float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
 }
 
+// The row max uses IEEE 754-2019 maximum (NaN in, NaN out: gfx950's v_maximum3_f32), not
+// fmaxf: fmaxf's NaN-ignoring form makes the compiler canonicalize every operand first (one
+// extra instruction per value and per butterfly stage).  A NaN anywhere in the row makes the
+// whole row NaN either way (through the max here, through the exponentials with fmaxf), and a
+// max of -0 or +0 gives the same exponentials.
 struct OpMax {
-    __device__ __forceinline__ static float f(float a, float b) { return __builtin_fmaxf(a, b); }
+    __device__ __forceinline__ static float f(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 };
 struct OpAdd {
     __device__ __forceinline__ static float f(float a, float b) { return a + b; }
@@ -105,10 +110,13 @@ struct F32 {
     using T = float;
     static constexpr int kBytes = 4;
     static constexpr int kEPV = 4;  // elements per 16-byte vector
-    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const f32x4 v = load16<NT>(reinterpret_cast<const f32x4*>(p));
+    using R = f32x4;  // one 16-byte vector as loaded
+    __device__ __forceinline__ static R load_raw(const T* p) { return load16<NT>(reinterpret_cast<const R*>(p)); }
+    __device__ __forceinline__ static R raw_fill(float f) { return R{f, f, f, f}; }
+    __device__ __forceinline__ static void unpack(R v, float* x) {
         x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
     }
+    __device__ __forceinline__ static void load_vec(const T* p, float* x) { unpack(load_raw(p), x); }
     __device__ __forceinline__ static void store_vec(T* p, const float* y) {
         store16<NT>(reinterpret_cast<f32x4*>(p), f32x4{y[0], y[1], y[2], y[3]});
     }
@@ -121,14 +129,21 @@ struct BF16 {
     using T = uint16_t;  // raw bf16 bit pattern
     static constexpr int kBytes = 2;
     static constexpr int kEPV = 8;
-    __device__ __forceinline__ static void load_vec(const T* p, float* x) {
-        const u32x4 v = load16<NT>(reinterpret_cast<const u32x4*>(p));
+    using R = u32x4;  // one 16-byte vector as loaded: eight bf16 bit patterns
+    __device__ __forceinline__ static R load_raw(const T* p) { return load16<NT>(reinterpret_cast<const R*>(p)); }
+    // f's bf16 pattern twice per dword (exact for the fills used: -inf and 0)
+    __device__ __forceinline__ static R raw_fill(float f) {
+        const unsigned h = f_bits(f) >> 16;
+        return R{h | (h << 16), h | (h << 16), h | (h << 16), h | (h << 16)};
+    }
+    __device__ __forceinline__ static void unpack(R v, float* x) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             x[2 * i] = bits_f(v[i] << 16);
             x[2 * i + 1] = bits_f(v[i] & 0xFFFF0000u);
         }
     }
+    __device__ __forceinline__ static void load_vec(const T* p, float* x) { unpack(load_raw(p), x); }
     __device__ __forceinline__ static unsigned pack(float a, float b) {
         // round to nearest even, NaN stays NaN (v_cvt_pk_bf16_f32)
         return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
@@ -153,6 +168,7 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
     constexpr int EPV = E::kEPV;
     constexpr int K = V * EPV;
     float x[U][K];
+    typename E::R raw[U][V];
     bool act[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -160,16 +176,16 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
         act[u] = r < nrows;
         const typename E::T* src = in + base + static_cast<int64_t>(r) * cols;
         if constexpr (VEC) {
+            // the vectors as loaded (a lane's loads all issued before any use; unpacking
+            // inside each conditional load would make every load wait for the previous one)
             const int nvec = cols / EPV;
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
-                if (act[u] && vi < nvec) {
-                    E::load_vec(src + vi * EPV, &x[u][v * EPV]);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < EPV; ++i) x[u][v * EPV + i] = kNegInf;
-                }
+                if (act[u] && vi < nvec)
+                    raw[u][v] = E::load_raw(src + vi * EPV);
+                else
+                    raw[u][v] = E::raw_fill(kNegInf);
             }
         } else {
 #pragma unroll
@@ -178,6 +194,12 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
                 x[u][k] = (act[u] && j < cols) ? E::load1(src + j) : kNegInf;
             }
         }
+    }
+    if constexpr (VEC) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int v = 0; v < V; ++v) E::unpack(raw[u][v], &x[u][v * EPV]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -364,7 +386,7 @@ __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T
         for (int first = lane; first < n; first += step) {
             float x[K];
             L::load(src, cols, first, x);
-            m = __builtin_fmaxf(m, lane_reduce<K, OpMax>(x));
+            m = OpMax::f(m, lane_reduce<K, OpMax>(x));
             if constexpr (VEC) {
 #pragma unroll
                 for (int c = 0; c < L::CH; ++c) {
@@ -532,6 +554,7 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
     constexpr int EPV = E::kEPV;
     constexpr int K = V * EPV;
     float a[U][K], g[U][K];
+    typename E::R ra[U][V], rg[U][V];
     bool act[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -544,11 +567,10 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
                 if (act[u] && vi < nvec) {
-                    E::load_vec(y + o + vi * EPV, &a[u][v * EPV]);
-                    E::load_vec(dy + o + vi * EPV, &g[u][v * EPV]);
+                    ra[u][v] = E::load_raw(y + o + vi * EPV);
+                    rg[u][v] = E::load_raw(dy + o + vi * EPV);
                 } else {
-#pragma unroll
-                    for (int i = 0; i < EPV; ++i) a[u][v * EPV + i] = g[u][v * EPV + i] = 0.0f;
+                    ra[u][v] = rg[u][v] = E::raw_fill(0.0f);
                 }
             }
         } else {
@@ -560,6 +582,15 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
                 g[u][k] = in ? E::load1(dy + o + j) : 0.0f;
             }
         }
+    }
+    if constexpr (VEC) {  // unpacked after every load is issued
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                E::unpack(ra[u][v], &a[u][v * EPV]);
+                E::unpack(rg[u][v], &g[u][v * EPV]);
+            }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
