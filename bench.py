@@ -406,13 +406,19 @@ def cpu_baseline(w):
     import oracle
 
     threads = min(16, len(os.sched_getaffinity(0)))
+    out = None
+    reps = 0
     t0 = time.perf_counter()
-    oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=threads)
-    dt = time.perf_counter() - t0
+    # the whole workload, repeated until at least 3 s have passed (at least three times)
+    while reps < 3 or time.perf_counter() - t0 < 3.0:
+        out = oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=threads,
+                             out=out)
+        reps += 1
+    dt = (time.perf_counter() - t0) / reps
     return {"value": round(w.algorithmic_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt, 3),
-            "sample": f"all {w.batch} slices of {w.name} once (fp64 reference, {threads} threads, "
-                      "bytes counted as the fp32 read-once + write-once of the GPU path)"}
+            "kind": "oracle", "seconds": round(dt * reps, 3),
+            "sample": f"all {w.batch} slices of {w.name}, {reps} times (fp64 reference, {threads} "
+                      "threads, bytes counted as the fp32 read-once + write-once of the GPU path)"}
 
 
 def main() -> int:
