@@ -284,17 +284,19 @@ struct LongRow {
     __device__ __forceinline__ static void load(const T* src, int cols, int first, float* x,
                                                 float pad = kNegInf) {
         if constexpr (VEC) {
+            // every load of the chunk issued before any is unpacked (as in rows_u)
             const int nvec = cols / EPV;
+            typename E::R raw[CH];
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 const int vi = first + c * 64;
-                if (vi < nvec) {
-                    E::load_vec(src + vi * EPV, x + c * EPV);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < EPV; ++i) x[c * EPV + i] = pad;
-                }
+                if (vi < nvec)
+                    raw[c] = E::load_raw(src + vi * EPV);
+                else
+                    raw[c] = E::raw_fill(pad);
             }
+#pragma unroll
+            for (int c = 0; c < CH; ++c) E::unpack(raw[c], x + c * EPV);
         } else {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
