@@ -556,9 +556,10 @@ def main() -> int:
                                                                res["balanced"]["ms_per_step"], 3)
         extra["producer_consumer"] = producer_consumer()
         extra["l2_locality_16MB_us"] = l2_locality()
-        # rows longer than the register tile: 4096-element rows fit a wave's LDS region and
-        # are read once; 8192-element rows take the two-pass path (1.25x the traffic)
-        for name in ("long4k", "long"):
+        # rows longer than the register tile: 4096-element rows fit a wave's LDS region at 8
+        # waves/CU, 8192-element rows at 4 (the plan picks 4), both read once; 16384-element
+        # rows take the two-pass path (1.5x the traffic)
+        for name in ("long4k", "long", "long16k"):
             r, _ = run_workload(name, "balanced", args.steps, args.warmup)
             extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "lds_bytes_per_wave")}
 

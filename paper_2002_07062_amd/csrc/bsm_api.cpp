@@ -86,8 +86,14 @@ struct DeviceGuard {
 // 4096-element rows 4.29 TB/s staged at 8 waves vs 3.77 two-pass; staging 8192-element rows at
 // 4 waves/CU, 3.0 TB/s, loses to two-pass at 8 waves, 3.8).
 constexpr int kLongRowClass = 4;
-int default_waves_per_cu(bsm_dtype d, int kclass) {
-    if (kclass >= kLongRowClass) return 8;
+// Waves per CU a plan runs by default, by element type, kernel class and longest row.  Long
+// rows run 8 waves per CU (each wave stages up to 5120 floats in LDS), except fp32 plans whose
+// longest row is 5121..10240 elements: those run 4, so that every row fits a wave's 40 KiB and
+// is read once (8192-element rows: 4.6 TB/s staged against 3.8 two-pass at 8 waves; bf16 keeps
+// 8, its arithmetic needs the waves: 3.5 staged against 3.7).
+int default_waves_per_cu(bsm_dtype d, int kclass, int32_t max_cols) {
+    if (kclass >= kLongRowClass)
+        return (d == BSM_F32 && max_cols > 5120 && max_cols <= 10240) ? 4 : 8;
     return d == BSM_BF16 ? 16 : 8;
 }
 
@@ -136,7 +142,7 @@ bsm_status default_topology(int device, bsm_topology* t) {
 }
 
 bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtype, int kclass,
-                            bsm::Topology* out) {
+                            int32_t max_cols, bsm::Topology* out) {
     bsm_topology t;
     if (device >= 0) {
         bsm_status st = default_topology(device, &t);
@@ -165,7 +171,7 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
     }
     if (t.wg_per_cu <= 0 && t.wg_threads >= 64) {
-        const int want = std::max(1, default_waves_per_cu(dtype, kclass) / (t.wg_threads / 64));
+        const int want = std::max(1, default_waves_per_cu(dtype, kclass, max_cols) / (t.wg_threads / 64));
         t.wg_per_cu = want;
         if (device >= 0 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
             int n = 0;
@@ -250,7 +256,8 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         std::string err = bsm::make_geometry(offs, rows, cols, batch, elem_bytes_of(dtype), &p->geo);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
         p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
-        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
+        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, p->geo.max_cols,
+                                         &p->topo);
         if (st != BSM_OK) return st;
         st = resolve_weights(xcd_weight, &p->topo);
         if (st != BSM_OK) return st;

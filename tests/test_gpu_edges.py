@@ -420,3 +420,20 @@ def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
     assert rec["rows"][rec["xcc_id"] == (7 + rot.pop()) % 8].sum() == 0
     assert rec["rows"].sum() == int(w.rows.sum())
     assert st["xcd_bytes"][7] == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fp32_rows_up_to_10240_are_staged_at_four_waves_per_cu(dtype):
+    """An fp32 plan whose longest row is 5121..10240 elements runs 4 waves per CU, so every
+    row fits a wave's LDS region (read once); bf16 plans keep 8 waves per CU. Both against the
+    oracle."""
+    cols = [5000, 6144, 8192, 10240, 7003]
+    w = workloads.custom([3, 2, 2, 2, 3], cols, dtype=dtype, sigma=3.0, seed=12, gap=8)
+    print(f"[mid-long {dtype}]", flush=True)
+    _, st = _check_ragged(w, "balanced")
+    assert st["kernel_class"] == 4
+    waves_per_cu = st["n_wg"] * (st["wg_threads"] // 64) // bsm.bsm_device_info(0)["n_cu"]
+    if dtype == "f32":
+        assert waves_per_cu == 4 and st["lds_bytes_per_wave"] // 4 >= max(cols)
+    else:
+        assert waves_per_cu == 8

@@ -62,14 +62,17 @@ SPECS = {
         doc="128 slices x 64x4096 fp32, N(0,9): rows that fit a wave's LDS region"),
     "long_64x64x8192_f32": Spec(
         "long_64x64x8192_f32", 64, 64, 8192, F32, 3.0, 6,
-        doc="64 slices x 64x8192 fp32, N(0,9): rows longer than one wave's register tile"),
+        doc="64 slices x 64x8192 fp32, N(0,9): rows that fit a wave's LDS region at 4 waves/CU"),
+    "long_32x64x16384_f32": Spec(
+        "long_32x64x16384_f32", 32, 64, 16384, F32, 3.0, 8,
+        doc="32 slices x 64x16384 fp32, N(0,9): rows longer than any wave's LDS region"),
 }
 
 # Short aliases used by the bench and the tests.
 ALIASES = {"c1": "c1_8x64x64_f32", "c2": "c2_384x512x512_f32",
            "c3": "c3_384x512x512_bf16_mask", "c4": "c4_16384x128x128_f32",
            "c5": "c5_384_ragged_f32", "long": "long_64x64x8192_f32",
-           "long4k": "long_128x64x4096_f32"}
+           "long4k": "long_128x64x4096_f32", "long16k": "long_32x64x16384_f32"}
 
 
 @dataclasses.dataclass
