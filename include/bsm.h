@@ -246,7 +246,7 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
 typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1 } bsm_gemm_layout;
 
 /* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
- * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 2).  A plan
+ * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 3).  A plan
  * made here runs only with bsm_gemm_execute.  Its stats report per_wave 0 (worker =
  * workgroup). */
 bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,
