@@ -65,7 +65,9 @@ typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1 } bsm_dtype;
  *             largest share of its elements, ties to the lowest index, or the caller's
  *             home_xcd[]); the load balancer moves the fewest rows it must from XCDs above
  *             their share to XCDs below it; each XCD's rows are then cut into rounds over the
- *             waves of that XCD's workgroups (workgroup w runs on XCD w mod n_xcd). */
+ *             waves of that XCD's workgroups (workgroup w is planned for XCD w mod n_xcd:
+ *             the dispatch order of MI355X, which now and then starts a launch on another
+ *             XCD and so rotates the whole grid; results never depend on it). */
 typedef enum bsm_schedule {
     BSM_SCHED_RR = 0,
     BSM_SCHED_BALANCED = 1,
