@@ -393,3 +393,26 @@ def test_gemm_plan_rejects_bad_arguments():
     assert lib.bsm_gemm(None, None, None, 0, 4, 4, 4, 0, 0, 1.0, 0, None) == bsm.BSM_OK
     assert lib.bsm_gemm(None, None, None, 2, 4, 4, 4, 0, 0, 1.0, 0, None) == bsm.BSM_ERR_INVALID_ARG
     assert lib.bsm_gemm(None, None, None, 2, 4, 4, 4, 5, 0, 1.0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_geometries_every_row_exactly_once(seed):
+    """Randomized geometries (slices in random order with gaps, empty slices, widths from 1 to
+    9000) on random topologies, under every schedule and with random homes for XCD: every row
+    is scheduled exactly once and the plan's totals are the geometry's."""
+    from random_geometry import geometry, topology
+
+    w = geometry(seed)
+    topo = topology(seed)
+    rng = np.random.default_rng(20_000 + seed)
+    for schedule in ("rr", "balanced", "xcd"):
+        home = None
+        if schedule == "xcd" and rng.random() < 0.5 and w.batch:
+            home = rng.integers(0, topo["n_xcd"], size=w.batch).astype(np.int8)
+        d, ptr, items, _, _ = _plan(w, schedule, topo, home=home)
+        assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == [], (seed, schedule)
+        assert d["total_rows"] == int(w.rows.sum())
+        assert d["algorithmic_bytes"] == 2 * 4 * int(np.sum(w.rows.astype(np.int64) * w.cols))
+        assert d["n_wg"] == topo["n_cu"] * topo["wg_per_cu"]
+        if schedule == "xcd":
+            assert sum(d["xcd_bytes"][: topo["n_xcd"]]) == d["algorithmic_bytes"]
