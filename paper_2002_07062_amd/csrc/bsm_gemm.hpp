@@ -287,10 +287,23 @@ __device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, in
 // together; step t + kDepth's loads are issued before step t's arithmetic.  AREG (the whole
 // reduction in one step, k <= 64): A's operands are read from LDS once and kept in registers
 // for every column block, so later steps move only B.
+// Wave priority 0..3 (s_setprio takes an immediate).  The three workgroups on a CU get the
+// same rows, but the SQ favours older waves, so without this the first one dispatched finishes
+// far ahead of the last (31 vs 47 us on the context product) and the CU ends on one
+// workgroup's waves; each workgroup therefore lowers its priority as its own share gets done,
+// and the ones behind catch up.
+__device__ __forceinline__ void set_prio(int p) {
+    if (p >= 3) __builtin_amdgcn_s_setprio(3);
+    else if (p == 2) __builtin_amdgcn_s_setprio(2);
+    else if (p == 1) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+}
+
 template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG>
 __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b, void* c,
                                            const Shape& s, int64_t bidx, int i0, int rows,
-                                           int wave, int lane, uint16_t* lw, uint16_t* lbs) {
+                                           int wave, int lane, uint16_t* lw, uint16_t* lbs,
+                                           int done_rows, int round_rows_n, int total_rows) {
     const int li = lane & 31;
     const int h = lane >> 5;
     uint16_t* const la = lw;
@@ -324,6 +337,13 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     // step st + kDepth's loads are issued into pp, then st's arithmetic and, at a column
     // block's end, its output.
     auto step = [&](int st, Pieces<!AREG>& pp, uint16_t* lb) {
+        if constexpr (!AREG) {  // priority 3 .. 0 by the workgroup's own progress (rows done,
+                                // steps of this round); measured: -2.5% time on the context
+                                // product, no gain on the one-step scores product
+            const int64_t prog = static_cast<int64_t>(done_rows) * nsteps + static_cast<int64_t>(round_rows_n) * st;
+            const int64_t tot = static_cast<int64_t>(total_rows) * nsteps;
+            set_prio(3 - static_cast<int>((4 * prog) / (tot > 0 ? tot : 1)));
+        }
         const int jb = st / nk, kb = st - jb * nk;
         const int j0 = jb * kBlockN;
         if (kb == 0) {
@@ -436,6 +456,8 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     uint32_t done = 0;
     const int i_begin = worker_ptr[w];
     const int i_end = worker_ptr[w + 1];
+    int total_rows = 0, wg_done = 0;
+    for (int it = i_begin; it < i_end; ++it) total_rows += items[it].nrows * items[it].reps;
     for (int it = i_begin; it < i_end; ++it) {
         const int64_t e0 = items[it].elem_offset;
         const int nrows = items[it].nrows;
@@ -457,10 +479,11 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                     zero_rows<BF16OUT>(c, s, bidx, i + wave * kTileM, mine, lane);
                 else if (areg)
                     round_rows<kLayout, BF16OUT, VEC, true>(a, b, c, s, bidx, i + wave * kTileM, mine,
-                                                            wave, lane, lw, lbs);
+                                                            wave, lane, lw, lbs, wg_done, seg, total_rows);
                 else
                     round_rows<kLayout, BF16OUT, VEC, false>(a, b, c, s, bidx, i + wave * kTileM, mine,
-                                                             wave, lane, lw, lbs);
+                                                             wave, lane, lw, lbs, wg_done, seg, total_rows);
+                wg_done += seg;
                 done += static_cast<uint32_t>(mine);
                 g += seg;
                 left -= seg;
