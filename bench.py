@@ -362,6 +362,73 @@ def producer_consumer(iters=20):
     return res
 
 
+def attention_pipeline(steps=30, warmup=5, batch=384, seq=512, d=64):
+    """Section 6's attention flow end to end, unfused: scores S = Q K^T / sqrt(d) (bf16 out),
+    softmax of S in place (bf16), context O = P V (bf16 out), all under BALANCED, Q K V O rotated
+    over enough sets to stay out of the Infinity Cache. Compares the default streaming
+    (nontemporal) accesses with BSM_FLAG_TEMPORAL on all three plans, so that the 201 MB score
+    tensor written by the first product can be served from the 256 MB Infinity Cache to the
+    softmax and then to the second product. Returns microseconds per pipeline and per stage
+    (each stage alone, same buffers) and algorithmic bytes."""
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    mk, ms = batch * seq * d, batch * seq * seq
+    n_sets = max(2, math.ceil(4 * MALL_BYTES / (4 * mk * 2)) + 1)
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    Q = [torch.randn(mk, device="cuda", generator=gen).bfloat16() for _ in range(n_sets)]
+    K = [torch.randn(mk, device="cuda", generator=gen).bfloat16() for _ in range(n_sets)]
+    V = [torch.randn(mk, device="cuda", generator=gen).bfloat16() for _ in range(n_sets)]
+    O = [torch.empty(mk, device="cuda", dtype=torch.bfloat16) for _ in range(n_sets)]
+    S = torch.empty(ms, device="cuda", dtype=torch.bfloat16)
+    scale = 1.0 / math.sqrt(d)
+    res = {"algorithmic_bytes": {"scores": batch * (2 * 2 * seq * d + 2 * seq * seq),
+                                 "softmax": 2 * 2 * ms,
+                                 "context": batch * (2 * seq * seq + 2 * seq * d + 2 * seq * d)}}
+
+    def timed(fn):
+        for i in range(warmup):
+            fn(i % n_sets)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(steps):
+            fn(i % n_sets)
+        e1.record()
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / steps * 1e3, 2)
+
+    for label, flags in (("streaming", 0), ("temporal", bsm.BSM_FLAG_TEMPORAL)):
+        topo = {"flags": flags}
+        p_s = bsm.bsm_gemm_plan_create(batch, seq, seq, d, "nt", "bf16", "balanced", topology=topo, device=0)
+        p_c = bsm.bsm_gemm_plan_create(batch, seq, d, seq, "nn", "bf16", "balanced", topology=topo, device=0)
+        p_m = bsm.bsm_plan_create([seq], [seq], None, dtype="bf16", schedule="balanced",
+                                  topology=topo, device=0, batch=batch)
+
+        def scores(i):
+            bsm.bsm_gemm_execute(p_s, Q[i], K[i], S, scale)
+
+        def soft(i):
+            bsm.bsm_plan_execute(p_m, S, S)
+
+        def context(i):
+            bsm.bsm_gemm_execute(p_c, S, V[i], O[i])
+
+        def pipe(i):
+            scores(i)
+            soft(i)
+            context(i)
+
+        res[label] = {"pipeline_us": timed(pipe), "scores_us": timed(scores),
+                      "softmax_us": timed(soft), "context_us": timed(context)}
+        for p in (p_s, p_c, p_m):
+            p.destroy()
+    del Q, K, V, O, S
+    torch.cuda.empty_cache()
+    return res
+
+
 def l2_locality(nslices=16, iters=30):
     """Producer on each slice's home XCD, then the consumer on the same XCD or on the next one
     (XCD schedule with explicit homes), 16 MB working set: does the consumer find the
@@ -555,6 +622,7 @@ def main() -> int:
             extra[f"gemm_{gname}"]["balanced_over_rr"] = round(res["rr"]["ms_per_step"] /
                                                                res["balanced"]["ms_per_step"], 3)
         extra["producer_consumer"] = producer_consumer()
+        extra["attention_pipeline"] = attention_pipeline()
         extra["l2_locality_16MB_us"] = l2_locality()
         # rows longer than the register tile: 4096-element rows fit a wave's LDS region at 8
         # waves/CU, 8192-element rows at 4 (the plan picks 4), both read once; 16384-element

@@ -90,7 +90,8 @@ typedef struct bsm_topology {
  * for data that is not in any cache).  BSM_FLAG_TEMPORAL uses ordinary accesses instead, so
  * input that a producer kernel just wrote is served from the memory-side Infinity Cache
  * (256 MB on MI355X) and the output stays there for the consumer; use it when the batch fits.
- * The output bits are the same under both policies. */
+ * Matrix-product plans take the same flag (C's stores and A's loads).  The output bits are the
+ * same under both policies. */
 #define BSM_FLAG_TEMPORAL 1
 
 /* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): `reps`

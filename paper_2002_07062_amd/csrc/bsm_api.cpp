@@ -446,7 +446,8 @@ bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float
     if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
     // k == 0 runs the same kernel: an empty reduction stores zeros
-    e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, a, b, c, p->gemm_m, p->gemm_n,
+    e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, (p->flags & BSM_FLAG_TEMPORAL) != 0,
+                         a, b, c, p->gemm_m, p->gemm_n,
                          p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(), trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     p->used = true;

@@ -34,8 +34,8 @@ int gemm_lds_bytes_per_wg(bool bf16_out) { return bsm_mm::wg_lds_bytes(bf16_out)
 int gemm_waves_per_simd() { return bsm_mm::kWavesPerSimd; }
 int gemm_rows_per_wg() { return bsm_mm::kWaves * bsm_mm::kTileM; }
 
-hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
-                       int n, int k, float alpha, const int32_t* d_worker_ptr,
+hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, const void* b,
+                       void* c, int m, int n, int k, float alpha, const int32_t* d_worker_ptr,
                        const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream) {
     Shape s;
     s.m = m;
@@ -45,6 +45,7 @@ hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, 
     s.b_batch = static_cast<int64_t>(n) * k;
     s.c_batch = static_cast<int64_t>(m) * n;
     s.alpha = alpha;
+    s.temporal = temporal ? 1 : 0;
     // 16-byte operand pieces and 16-byte output stores (4 fp32 or 8 bf16 columns): rows of A
     // (and NT's B) of k elements, rows of NN's B and of C of n elements, every base 16-byte
     // aligned

@@ -45,6 +45,8 @@ struct Shape {
     int m, n, k;
     int64_t a_batch, b_batch, c_batch;  // elements between consecutive batch indices
     float alpha;
+    int temporal;  // 1: ordinary stores of C and loads of A (a consumer finds C in the
+                   // Infinity Cache); 0: nontemporal (streaming)
 };
 
 // One step of a workgroup: the output column block [j0, j0 + 64) and the reduction slice
@@ -243,7 +245,10 @@ __device__ __forceinline__ void store_block_f32(float* c, const Shape& s, int64_
             const f32x4 v = *reinterpret_cast<const f32x4*>(lc + r * kLdc + col);
             float* cp = c + off0 + (r0 / 4) * step;
             if (whole) {
-                __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
+                if (s.temporal)
+                    *reinterpret_cast<f32x4*>(cp) = v;
+                else
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -271,7 +276,10 @@ __device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, in
             const u16x8 v = *reinterpret_cast<const u16x8*>(lh + r * kLdh + col);
             uint16_t* cp = c + off0 + (r0 / 8) * step;
             if (whole) {
-                __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(cp));
+                if (s.temporal)
+                    *reinterpret_cast<u32x4*>(cp) = __builtin_bit_cast(u32x4, v);
+                else
+                    __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(cp));
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
@@ -317,7 +325,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
     if constexpr (AREG) {  // A once, through the wave's LDS into its MFMA layout
         u16x8 pa[kAPieces];
-        load_a<VEC>(a_blk, s, rows, 0, lane, true, pa);  // read once
+        load_a<VEC>(a_blk, s, rows, 0, lane, !s.temporal, pa);  // read once
         write_a<VEC>(pa, s, rows, 0, lane, la);
         wave_lds_sync();
 #pragma unroll
@@ -328,7 +336,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     auto load = [&](int st, Pieces<!AREG>& pp) {
         const int js = st / nk, ks = st - js * nk;
         load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane,
-                                      nj == 1, pp);  // A read once when one column block
+                                      nj == 1 && !s.temporal, pp);  // A read once when one column block
     };
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) load(d < nsteps ? d : nsteps - 1, p[d]);

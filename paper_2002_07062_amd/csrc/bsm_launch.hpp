@@ -44,9 +44,9 @@ int gemm_waves_per_simd();
 int gemm_rows_per_wg();
 
 // Worker w of the table is workgroup w (gemm_wg_threads() threads, gemm_rows_per_wg() rows
-// per round).
-hipError_t launch_gemm(int layout, bool bf16_out, const void* a, const void* b, void* c, int m,
-                       int n, int k, float alpha, const int32_t* d_worker_ptr,
+// per round).  temporal: ordinary instead of nontemporal stores of C and loads of A.
+hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, const void* b,
+                       void* c, int m, int n, int k, float alpha, const int32_t* d_worker_ptr,
                        const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream);
 
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).

@@ -184,3 +184,23 @@ def test_misaligned_operand_takes_the_elementwise_path(layout, which):
     assert np.array_equal(got, want)
     rest = bits_to_f64(to_host_bits(c_buf))
     assert np.all(np.isnan(rest[:oc])) and np.all(np.isnan(rest[oc + batch * m * n:])), "written outside C"
+
+
+@pytest.mark.parametrize("layout,shape", [("nt", (16, 256, 512, 64)), ("nn", (16, 256, 64, 512))])
+def test_temporal_flag_gives_the_same_bits(layout, shape):
+    """BSM_FLAG_TEMPORAL only changes the cache hints of C's stores and A's loads."""
+    batch, m, n, k = shape
+    a, b = _operands(batch, m, n, k, seed=77)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    outs = []
+    for flags in (0, bsm.BSM_FLAG_TEMPORAL):
+        p = bsm.bsm_gemm_plan_create(batch, m, n, k, layout, "bf16", "balanced",
+                                     topology={"flags": flags}, device=0)
+        assert bsm.bsm_plan_describe(p)["flags"] == flags
+        c = torch.empty(batch * m * n, dtype=torch.bfloat16, device="cuda")
+        bsm.bsm_gemm_execute(p, a_d, b_d, c)
+        torch.cuda.synchronize()
+        p.destroy()
+        outs.append(to_host_bits(c))
+    _check(outs[0], a, b, batch, m, n, k, layout, "bf16")
+    assert np.array_equal(outs[0], outs[1])
