@@ -45,8 +45,6 @@ struct Shape {
     int m, n, k;
     int64_t a_batch, b_batch, c_batch;  // elements between consecutive batch indices
     float alpha;
-    int temporal;  // 1: ordinary stores of C and loads of A (a consumer finds C in the
-                   // Infinity Cache); 0: nontemporal (streaming)
 };
 
 // One step of a workgroup: the output column block [j0, j0 + 64) and the reduction slice
@@ -228,7 +226,7 @@ __device__ __forceinline__ void write_step(const Pieces<WITH_A>& p, const Shape&
 
 // Stores a staged output block (rows [i0, i0 + rows), columns [j0, j0 + jn)) as whole rows:
 // 16 lanes x 4 fp32 columns, four rows per instruction.
-template <bool VEC>
+template <bool VEC, bool TEMPORAL>
 __device__ __forceinline__ void store_block_f32(float* c, const Shape& s, int64_t bidx, int i0, int rows,
                                             int j0, int jn, int lane, const float* lc) {
     const int col = (lane & 15) * 4;
@@ -245,7 +243,7 @@ __device__ __forceinline__ void store_block_f32(float* c, const Shape& s, int64_
             const f32x4 v = *reinterpret_cast<const f32x4*>(lc + r * kLdc + col);
             float* cp = c + off0 + (r0 / 4) * step;
             if (whole) {
-                if (s.temporal)
+                if constexpr (TEMPORAL)
                     *reinterpret_cast<f32x4*>(cp) = v;
                 else
                     __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(cp));
@@ -260,7 +258,7 @@ __device__ __forceinline__ void store_block_f32(float* c, const Shape& s, int64_
 
 // The same for a block staged as bf16 ([32][kLdh]): 8 lanes x 8 columns, eight rows per
 // instruction.
-template <bool VEC>
+template <bool VEC, bool TEMPORAL>
 __device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, int64_t bidx, int i0,
                                              int rows, int j0, int jn, int lane, const uint16_t* lh) {
     const int col = (lane & 7) * 8;
@@ -276,7 +274,7 @@ __device__ __forceinline__ void store_block_bf16(uint16_t* c, const Shape& s, in
             const u16x8 v = *reinterpret_cast<const u16x8*>(lh + r * kLdh + col);
             uint16_t* cp = c + off0 + (r0 / 8) * step;
             if (whole) {
-                if (s.temporal)
+                if constexpr (TEMPORAL)
                     *reinterpret_cast<u32x4*>(cp) = __builtin_bit_cast(u32x4, v);
                 else
                     __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(cp));
@@ -307,7 +305,7 @@ __device__ __forceinline__ void set_prio(int p) {
     else __builtin_amdgcn_s_setprio(0);
 }
 
-template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG>
+template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG, bool TEMPORAL>
 __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b, void* c,
                                            const Shape& s, int64_t bidx, int i0, int rows,
                                            int wave, int lane, uint16_t* lw, uint16_t* lbs,
@@ -325,7 +323,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
     if constexpr (AREG) {  // A once, through the wave's LDS into its MFMA layout
         u16x8 pa[kAPieces];
-        load_a<VEC>(a_blk, s, rows, 0, lane, !s.temporal, pa);  // read once
+        load_a<VEC>(a_blk, s, rows, 0, lane, !TEMPORAL, pa);  // read once
         write_a<VEC>(pa, s, rows, 0, lane, la);
         wave_lds_sync();
 #pragma unroll
@@ -336,7 +334,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     auto load = [&](int st, Pieces<!AREG>& pp) {
         const int js = st / nk, ks = st - js * nk;
         load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane,
-                                      nj == 1 && !s.temporal, pp);  // A read once when one column block
+                                      !TEMPORAL && nj == 1, pp);  // A read once when one column block
     };
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) load(d < nsteps ? d : nsteps - 1, p[d]);
@@ -399,7 +397,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
                               pack_bf16(s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3])};
             }
             wave_lds_sync();
-            store_block_bf16<VEC>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lh);
+            store_block_bf16<VEC, TEMPORAL>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lh);
         } else {
             float* const lc = reinterpret_cast<float*>(lw);
 #pragma unroll
@@ -411,7 +409,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
                               s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3]};
             }
             wave_lds_sync();
-            store_block_f32<VEC>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
+            store_block_f32<VEC, TEMPORAL>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
         }
         wave_lds_sync();  // the next step rewrites the region
     };
@@ -448,7 +446,7 @@ constexpr int kWavesPerSimd = 3;
 // Worker loop: workgroup w runs its items; an item's rows are taken up to 128 at a time (cut
 // where a batch ends), 32 per wave.  Every bound of these loops is the same for the four
 // waves, so they meet the same barriers.
-template <int MODE, bool BF16OUT, bool VEC>
+template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
                                             const Shape& s, const int32_t* __restrict__ worker_ptr,
                                             const bsm_item* __restrict__ items,
@@ -486,10 +484,10 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 if (s.k == 0)
                     zero_rows<BF16OUT>(c, s, bidx, i + wave * kTileM, mine, lane);
                 else if (areg)
-                    round_rows<kLayout, BF16OUT, VEC, true>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                    round_rows<kLayout, BF16OUT, VEC, true, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
                                                             wave, lane, lw, lbs, wg_done, seg, total_rows);
                 else
-                    round_rows<kLayout, BF16OUT, VEC, false>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                    round_rows<kLayout, BF16OUT, VEC, false, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
                                                              wave, lane, lw, lbs, wg_done, seg, total_rows);
                 wg_done += seg;
                 done += static_cast<uint32_t>(mine);
@@ -516,12 +514,15 @@ constexpr int kGemmThreads = 64 * kWaves;
 
 // The element-wise (unaligned / odd-size) form is compiled for two waves per SIMD: its
 // registers do not fit three.
-template <int MODE, bool BF16OUT, bool VEC>
+// TEMPORAL: ordinary stores of C and loads of A (a consumer finds C in the Infinity Cache)
+// instead of nontemporal ones; a compile-time choice, so the default instance carries no
+// branch for it.
+template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL>
 __global__ void __launch_bounds__(kGemmThreads, VEC ? kWavesPerSimd : 2)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 bsm_trace_rec* __restrict__ trace) {
-    gemm_worker<MODE, BF16OUT, VEC>(a, b, c, s, worker_ptr, items, trace, bsm_gemm_lds);
+    gemm_worker<MODE, BF16OUT, VEC, TEMPORAL>(a, b, c, s, worker_ptr, items, trace, bsm_gemm_lds);
 }
 
 }  // namespace bsm_mm
