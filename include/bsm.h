@@ -42,16 +42,20 @@ extern "C" {
 #define BSM_ABI_VERSION 1
 #define BSM_MAX_XCD 16
 
+/* The enumerations' *_MAX_ENUM entries are not values: they make each enum a 32-bit type whose
+ * range covers every int, so a caller passing any value is well-defined (and rejected with
+ * BSM_ERR_INVALID_ARG when it names nothing). */
 typedef enum bsm_status {
     BSM_OK = 0,
     BSM_ERR_INVALID_ARG = 1, /* bad pointer, size, enum, geometry or overlapping slices */
     BSM_ERR_UNSUPPORTED = 2, /* valid request this build cannot serve (e.g. host-only plan) */
     BSM_ERR_ALIAS = 3,       /* in and out overlap without being equal */
     BSM_ERR_OOM = 4,         /* host or device allocation failed */
-    BSM_ERR_HIP = 5          /* a HIP runtime call failed; bsm_last_error() has its string */
+    BSM_ERR_HIP = 5,         /* a HIP runtime call failed; bsm_last_error() has its string */
+    BSM_STATUS_MAX_ENUM = 0x7FFFFFFF
 } bsm_status;
 
-typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1 } bsm_dtype;
+typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1, BSM_DTYPE_MAX_ENUM = 0x7FFFFFFF } bsm_dtype;
 
 /* Which worker processes which rows.
  *   RR        Section 3's prior solution: whole slice s goes to workgroup (s mod n_wg), whose
@@ -71,7 +75,8 @@ typedef enum bsm_dtype { BSM_F32 = 0, BSM_BF16 = 1 } bsm_dtype;
 typedef enum bsm_schedule {
     BSM_SCHED_RR = 0,
     BSM_SCHED_BALANCED = 1,
-    BSM_SCHED_XCD = 2
+    BSM_SCHED_XCD = 2,
+    BSM_SCHED_MAX_ENUM = 0x7FFFFFFF
 } bsm_schedule;
 
 /* Launch geometry and cost model used by the planner.  Zero-filled fields take defaults. */
@@ -246,7 +251,7 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
  * All operands row-major, batch after batch (A_b at b*m*k, B_b at b*n*k, C_b at b*m*n
  * elements).  A and B are bf16; C is fp32 or bf16 (round to nearest even); accumulation in
  * fp32 on the matrix cores. */
-typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1 } bsm_gemm_layout;
+typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1, BSM_GEMM_LAYOUT_MAX_ENUM = 0x7FFFFFFF } bsm_gemm_layout;
 
 /* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
  * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 3).  A plan

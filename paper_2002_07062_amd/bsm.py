@@ -16,7 +16,9 @@ import numpy as np
 # the same SONAME), so tensors, streams and kernels share one runtime.
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbsm.so")
+# the in-tree build; BSM_LIB names another build of the same library (e.g. one with host-side
+# sanitizers for the CPU tests)
+LIB_PATH = os.environ.get("BSM_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbsm.so")
 
 BSM_OK, BSM_ERR_INVALID_ARG, BSM_ERR_UNSUPPORTED, BSM_ERR_ALIAS, BSM_ERR_OOM, BSM_ERR_HIP = range(6)
 BSM_F32, BSM_BF16 = 0, 1
