@@ -19,6 +19,7 @@
 #include "bsm.h"
 #include "bsm_launch.hpp"
 #include "bsm_plan.hpp"
+#include "bsm_tile.hpp"
 
 struct bsm_plan_s {
     int device = -1;  // -1: host-only plan
@@ -80,32 +81,26 @@ struct DeviceGuard {
 
 // Waves per CU that measured fastest on MI355X: 8 for fp32 rows (more waves only add DRAM
 // page conflicts), 16 for bf16 rows, which carry twice the ALU work per byte and need the
-// extra waves to overlap it with memory.  Plans with rows beyond the register tile also run 8
-// waves per CU, each staging rows of up to an eighth of the CU's LDS (20 KiB: 5120 fp32): with
-// fewer waves the staged rows' LDS passes leave HBM idle and the two-pass path wins (measured:
-// 4096-element rows 4.29 TB/s staged at 8 waves vs 3.77 two-pass; staging 8192-element rows at
-// 4 waves/CU, 3.0 TB/s, loses to two-pass at 8 waves, 3.8).
+// extra waves to overlap it with memory.  Plans with rows beyond the register tile run two
+// 256-thread workgroups per CU (8 waves), each holding one or two rows in its registers.
 constexpr int kLongRowClass = 4;
-// Waves per CU a plan runs by default, by element type, kernel class and longest row.  Long
-// rows run 8 waves per CU (each wave stages up to 5120 floats in LDS), except fp32 plans whose
-// longest row is 5121..10240 elements: those run 4, so that every row fits a wave's 40 KiB and
-// is read once (8192-element rows: 4.6 TB/s staged against 3.8 two-pass at 8 waves; bf16 keeps
-// 8, its arithmetic needs the waves: 3.5 staged against 3.7).
-int default_waves_per_cu(bsm_dtype d, int kclass, int32_t max_cols) {
-    if (kclass >= kLongRowClass)
-        return (d == BSM_F32 && max_cols > 5120 && max_cols <= 10240) ? 4 : 8;
+int default_waves_per_cu(bsm_dtype d, int kclass) {
+    if (kclass >= kLongRowClass) return 8;
     return d == BSM_BF16 ? 16 : 8;
 }
 
 // Smallest LDS region worth staging a row in (shorter rows never reach the long-row path).
 constexpr int64_t kMinStageBytes = 8192;
 
-// LDS per wave for long-row staging: the CU's LDS split over its resident waves, capped by the
-// per-workgroup limit, rounded down to 64 bytes.
-int64_t lds_bytes_per_wave(const hipDeviceProp_t& prop, const bsm::Topology& t) {
+// LDS per wave for long-row staging: the CU's LDS split over its resident workgroups, capped
+// by the per-workgroup limit, less the kernels' own static LDS (`static_bytes` per workgroup),
+// split over the waves and rounded down to 64 bytes.
+int64_t lds_bytes_per_wave(const hipDeviceProp_t& prop, const bsm::Topology& t,
+                           int64_t static_bytes) {
     const int64_t per_cu = static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor);
     const int64_t per_wg = std::min<int64_t>(per_cu / std::max(1, t.wg_per_cu),
-                                             static_cast<int64_t>(prop.sharedMemPerBlock));
+                                             static_cast<int64_t>(prop.sharedMemPerBlock)) -
+                           static_bytes;
     const int64_t per_wave = (per_wg / t.waves_per_wg()) & ~static_cast<int64_t>(63);
     return per_wave >= kMinStageBytes ? per_wave : 0;
 }
@@ -142,7 +137,7 @@ bsm_status default_topology(int device, bsm_topology* t) {
 }
 
 bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtype, int kclass,
-                            int32_t max_cols, bsm::Topology* out) {
+                            bsm::Topology* out) {
     bsm_topology t;
     if (device >= 0) {
         bsm_status st = default_topology(device, &t);
@@ -171,7 +166,7 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         if (user->row_cost > 0.0f) t.row_cost = user->row_cost;
     }
     if (t.wg_per_cu <= 0 && t.wg_threads >= 64) {
-        const int want = std::max(1, default_waves_per_cu(dtype, kclass, max_cols) / (t.wg_threads / 64));
+        const int want = std::max(1, default_waves_per_cu(dtype, kclass) / (t.wg_threads / 64));
         t.wg_per_cu = want;
         if (device >= 0 && t.wg_threads <= 1024 && t.wg_threads % 64 == 0) {
             int n = 0;
@@ -184,7 +179,11 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
                 bsm::Topology probe;
                 probe.wg_per_cu = want;
                 probe.wg_threads = t.wg_threads;
-                lds = static_cast<size_t>(lds_bytes_per_wave(prop, probe)) * (t.wg_threads / 64);
+                int static_bytes = 0;
+                e = bsm::static_lds_bytes(dtype, kclass, &static_bytes);
+                if (e == hipSuccess)
+                    lds = static_cast<size_t>(lds_bytes_per_wave(prop, probe, static_bytes)) *
+                          (t.wg_threads / 64);
             }
             if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, lds, &n);
             if (e != hipSuccess) return hip_fail(e, "occupancy query");
@@ -237,7 +236,8 @@ bsm_status resolve_weights(const float* w, bsm::Topology* t) {
 bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* rows,
                        const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
                        const int8_t* home_xcd, const float* xcd_weight,
-                       const bsm_topology* topology, int device, int32_t row_unit = 0) {
+                       const bsm_topology* topology, int device, int32_t row_unit = 0,
+                       bool product = false) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
@@ -252,20 +252,40 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
     }
     std::unique_ptr<bsm_plan_s> p(new (std::nothrow) bsm_plan_s);
     if (!p) return fail(BSM_ERR_OOM, "plan allocation failed");
+    bsm_topology tu{};  // the caller's topology with a long-row plan's workgroup size
     try {
         std::string err = bsm::make_geometry(offs, rows, cols, batch, elem_bytes_of(dtype), &p->geo);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
         p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
-        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, p->geo.max_cols,
-                                         &p->topo);
+        // Rows beyond the register tile are worked by whole workgroups of kTeamThreads threads,
+        // one row at a time: such plans run that workgroup size whatever the topology asks (a
+        // row's bits depend on it), and every worker of their table is a workgroup.
+        const bool team = !product && p->kernel_class >= kLongRowClass;
+        if (team) {
+            if (topology) tu = *topology;
+            tu.wg_threads = bsm::kTeamThreads;
+            topology = &tu;
+        }
+        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
         if (st != BSM_OK) return st;
         st = resolve_weights(xcd_weight, &p->topo);
         if (st != BSM_OK) return st;
         p->topo.row_unit = row_unit;
         err = bsm::check_topology(p->topo);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "topology: %s", err.c_str());
-        err = bsm::build_table(p->geo, schedule, p->topo, home_xcd, p->kernel_class, &p->table);
+        // planned with one-wave workgroups, so that worker w is workgroup w (on XCD w mod n_xcd)
+        bsm::Topology tt = p->topo;
+        if (team) tt.wg_threads = 64;
+        err = bsm::build_table(p->geo, schedule, tt, home_xcd, p->kernel_class, &p->table);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "plan: %s", err.c_str());
+        if (team) {
+            p->table.per_wave = false;
+            p->table.stats.per_wave = 0;
+            p->table.stats.wg_threads = bsm::kTeamThreads;
+            p->table.stats.trace_bytes = static_cast<int64_t>(p->topo.n_wg()) *
+                                         (bsm::kTeamThreads / 64) *
+                                         static_cast<int64_t>(sizeof(bsm_trace_rec));
+        }
     } catch (const std::bad_alloc&) {
         return fail(BSM_ERR_OOM, "host allocation failed while planning");
     }
@@ -285,7 +305,10 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             hipDeviceProp_t prop;
             e = hipGetDeviceProperties(&prop, device);
             if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
-            const int64_t b = lds_bytes_per_wave(prop, p->topo);
+            int static_bytes = 0;
+            e = bsm::static_lds_bytes(dtype, p->kernel_class, &static_bytes);
+            if (e != hipSuccess) return hip_fail(e, "hipFuncGetAttributes");
+            const int64_t b = lds_bytes_per_wave(prop, p->topo, static_bytes);
             p->lds_floats_per_wave = static_cast<int>(b / static_cast<int64_t>(sizeof(float)));
             p->table.stats.lds_bytes_per_wave = static_cast<int32_t>(b);
         }
@@ -399,7 +422,7 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
     const int32_t rows[1] = {m}, cols[1] = {n};
     bsm_plan p = nullptr;
     bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
-                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg());
+                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg(), true);
     if (st != BSM_OK) return st;
     p->topo.wg_threads = wg_threads;
     p->table.per_wave = false;
@@ -720,6 +743,7 @@ const char* bsm_status_string(bsm_status status) {
         case BSM_ERR_ALIAS: return "BSM_ERR_ALIAS";
         case BSM_ERR_OOM: return "BSM_ERR_OOM";
         case BSM_ERR_HIP: return "BSM_ERR_HIP";
+        default: break;  // any other value, BSM_STATUS_MAX_ENUM included
     }
     return "BSM_ERR_UNKNOWN";
 }

@@ -83,6 +83,7 @@ __device__ __forceinline__ float group_reduce(float v) {
 // In-lane pairwise reduction of K values (K a power of two).
 template <int K, class Op>
 __device__ __forceinline__ float lane_reduce(const float* x) {
+    static_assert(K > 0 && (K & (K - 1)) == 0, "lane_reduce needs a power of two");
     if constexpr (K == 1) {
         return x[0];
     } else {
@@ -500,12 +501,235 @@ __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T
     }
 }
 
+// ------------------------------------------------------------------------ workgroup rows
+// Aligned rows beyond the register tile, one row at a time per workgroup: all of its
+// nt = 64 * nwaves lanes share the row, lane t holding vectors t, t + nt, ..., t + (L-1) nt (so
+// each load instruction of a wave covers 1 KiB of consecutive bytes).  The row is read once
+// into registers; max and sum are the in-lane tree, the wave's butterfly, then the waves'
+// values combined in wave order through LDS (two barriers per row), so every lane of the
+// workgroup ends with the same bits and a row's result depends on its values, its length and
+// the workgroup size only.  Rows beyond L vectors per lane take two passes over HBM with a
+// per-lane running max and rescaled sum (as in long_row), combined the same way.
+constexpr int kTeamMaxRows = 2;  // rows a workgroup keeps in flight
+__shared__ float team_slots[2][kTeamMaxRows][16];  // [max, sum][row][wave]: lane 0 of each wave
+
+// Combine U values per wave (one per row) in wave order; slot set `which` is reused by the next
+// rows only after the other set's barrier, which every wave reaches after reading this one.
+template <class Op, int U>
+__device__ __forceinline__ void team_combine(float (&v)[U], int which, int wave, int nwaves,
+                                             int lane) {
+    if (lane == 0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) team_slots[which][u][wave] = v[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float r = team_slots[which][u][0];
+        for (int i = 1; i < nwaves; ++i) r = Op::f(r, team_slots[which][u][i]);
+        v[u] = r;
+    }
+}
+
+// Vectors past the row (or of an inactive row) read as `pad`.
+template <class E, int L>
+__device__ __forceinline__ void team_load(const typename E::T* src, int nvec, int first, int nt,
+                                          bool act, typename E::R* raw, float pad = kNegInf) {
+    constexpr int EPV = E::kEPV;
+#pragma unroll
+    for (int c = 0; c < L; ++c) {
+        const int vi = first + c * nt;
+        raw[c] = (act && vi < nvec) ? E::load_raw(src + vi * EPV) : E::raw_fill(pad);
+    }
+}
+
+template <class E, int L>
+__device__ __forceinline__ void team_unpack(const typename E::R* raw, float* x) {
+#pragma unroll
+    for (int c = 0; c < L; ++c) E::unpack(raw[c], x + c * E::kEPV);
+}
+
+template <class E, int L>
+__device__ __forceinline__ void team_store(typename E::T* dst, int nvec, int first, int nt,
+                                           bool act, const float* y) {
+    constexpr int EPV = E::kEPV;
+#pragma unroll
+    for (int c = 0; c < L; ++c) {
+        const int vi = first + c * nt;
+        if (act && vi < nvec) E::store_vec(dst + vi * EPV, y + c * EPV);
+    }
+}
+
+// Up to U rows (those with act[u], starting at elements off[u]) held in registers: L vectors
+// per lane cover nt * L vectors of a row.  A row's arithmetic does not depend on U.
+template <class E, int L, int U>
+__device__ __forceinline__ void team_rows(const typename E::T* in, typename E::T* out,
+                                          const int64_t (&off)[U], const bool (&act)[U], int nvec,
+                                          int t, int nt, int wave, int nwaves, int lane) {
+    constexpr int K = L * E::kEPV;
+    float x[U][K];
+    typename E::R raw[U][L];
+#pragma unroll
+    for (int u = 0; u < U; ++u) team_load<E, L>(in + off[u], nvec, t, nt, act[u], raw[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) team_unpack<E, L>(raw[u], x[u]);
+    float m[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) m[u] = group_reduce<64, OpMax>(lane_reduce<K, OpMax>(x[u]));
+    team_combine<OpMax, U>(m, 0, wave, nwaves, lane);
+    float s[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float ms = (m[u] == kNegInf) ? 0.0f : m[u];
+#pragma unroll
+        for (int k = 0; k < K; ++k) x[u][k] = __builtin_amdgcn_exp2f((x[u][k] - ms) * kLog2e);
+        s[u] = group_reduce<64, OpAdd>(lane_reduce<K, OpAdd>(x[u]));
+    }
+    team_combine<OpAdd, U>(s, 1, wave, nwaves, lane);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float inv = (s[u] == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(s[u]);
+#pragma unroll
+        for (int k = 0; k < K; ++k) x[u][k] *= inv;
+        team_store<E, L>(out + off[u], nvec, t, nt, act[u], x[u]);
+    }
+}
+
+// The rows of an item, reps ranges of nrows rows, as one sequence j = 0, 1, ... (U at a time,
+// across ranges: a balanced table often gives long rows as ranges of one row).
+// The trace counts row j of an item's sequence for wave j mod nwaves.
+__device__ __forceinline__ uint32_t team_rows_of_wave(int nrows, int reps, int wave, int nwaves) {
+    const int64_t total = static_cast<int64_t>(nrows) * reps;
+    return total > wave ? static_cast<uint32_t>((total - wave + nwaves - 1) / nwaves) : 0u;
+}
+
+template <int U>
+struct RowWalk {
+    int64_t base, stride, total, j = 0;
+    int cols, nrows, k = 0, r = 0;
+    __device__ RowWalk(int64_t b, int c, int n, int reps, int64_t st)
+        : base(b), stride(st), total(static_cast<int64_t>(n) * reps), cols(c), nrows(n) {}
+    __device__ bool more() const { return j < total; }
+    __device__ void next(int64_t (&off)[U], bool (&act)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            act[u] = j < total;
+            off[u] = base + k * stride + static_cast<int64_t>(r) * cols;
+            if (act[u]) {
+                ++j;
+                if (++r == nrows) {
+                    r = 0;
+                    ++k;
+                }
+            }
+        }
+    }
+};
+
+// A row longer than nt * L vectors: chunks of nt * L vectors, read twice.
+template <class E, int L>
+__device__ __forceinline__ void team_row_two_pass(const typename E::T* src, typename E::T* dst,
+                                                  int nvec, int t, int nt, int wave, int nwaves,
+                                                  int lane) {
+    constexpr int K = L * E::kEPV;
+    float m = kNegInf, s = 0.0f;
+    for (int first = t; first - t < nvec; first += nt * L) {
+        float x[K];
+        typename E::R raw[L];
+        team_load<E, L>(src, nvec, first, nt, true, raw);
+        team_unpack<E, L>(raw, x);
+        const float cm = lane_reduce<K, OpMax>(x);
+        if (cm > m) {
+            s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
+            m = cm;
+        }
+        if (m != kNegInf) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - m) * kLog2e);
+            s += lane_reduce<K, OpAdd>(x);
+        }
+    }
+    float M[1] = {group_reduce<64, OpMax>(m)};
+    team_combine<OpMax, 1>(M, 0, wave, nwaves, lane);
+    const float Ms = (M[0] == kNegInf) ? 0.0f : M[0];
+    const float scale = (m == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f((m - Ms) * kLog2e);
+    float S[1] = {group_reduce<64, OpAdd>(s * scale)};
+    team_combine<OpAdd, 1>(S, 1, wave, nwaves, lane);
+    const float inv = (S[0] == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S[0]);
+    for (int first = t; first - t < nvec; first += nt * L) {
+        float x[K];
+        typename E::R raw[L];
+        team_load<E, L>(src, nvec, first, nt, true, raw);
+        team_unpack<E, L>(raw, x);
+#pragma unroll
+        for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - Ms) * kLog2e) * inv;
+        team_store<E, L>(dst, nvec, first, nt, true, x);
+    }
+}
+
+// Vectors per lane (and per input stream) of a register-held row: bsm::kTeamValues values per
+// lane in kernel class 4, twice that in class 5.
+template <class E, int KCLASS>
+constexpr int kTeamMaxL = (KCLASS >= 5 ? 2 : 1) * bsm::kTeamValues / E::kEPV;
+
+// Every row of an item, each by the whole workgroup.  The trace counts row r for wave
+// r mod nwaves.
+template <class E, int KCLASS>
+__device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename E::T* out,
+                                              int64_t base, int cols, int nrows, int reps,
+                                              int64_t stride, int wave, int nwaves, int lane) {
+    constexpr int EPV = E::kEPV;
+    const int nvec = cols / EPV;
+    const int nt = nwaves * 64;
+    const int t = wave * 64 + lane;
+    const int per_lane = (nvec + nt - 1) / nt;
+    constexpr int kMaxL = kTeamMaxL<E, KCLASS>;  // 4 or 8 (class 4), 8 or 16 (class 5)
+    // two rows of 4 vectors per lane in flight where that is within kTeamValues values (fp32)
+    constexpr bool kPair = 2 * 4 * E::kEPV <= bsm::kTeamValues;
+    if (kPair && per_lane <= 3) {
+        // the shortest rows (at most 3 of the 4 vectors per lane): two in flight, so that a lane
+        // keeps 5-6 loads outstanding (measured: 2500-element fp32 rows 5.7 TB/s against 4.9 one
+        // at a time; rows filling 4 vectors per lane are 2% faster one at a time)
+        RowWalk<2> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[2];
+            bool act[2];
+            w.next(off, act);
+            team_rows<E, 4, 2>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+        }
+    } else if (per_lane <= kMaxL) {
+        RowWalk<1> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[1];
+            bool act[1];
+            w.next(off, act);
+            if (per_lane <= 4)
+                team_rows<E, 4, 1>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+            else if (kMaxL > 8 && per_lane <= 8)
+                team_rows<E, (kMaxL > 8 ? 8 : kMaxL), 1>(in, out, off, act, nvec, t, nt, wave,
+                                                         nwaves, lane);
+            else
+                team_rows<E, kMaxL, 1>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+        }
+    } else {
+        RowWalk<1> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[1];
+            bool act[1];
+            w.next(off, act);
+            team_row_two_pass<E, kMaxL>(in + off[0], out + off[0], nvec, t, nt, wave, nwaves,
+                                        lane);
+        }
+    }
+    return team_rows_of_wave(nrows, reps, wave, nwaves);
+}
+
 // Register-tile choice per item (wave-uniform branch); the thresholds are bsm::tile_for's.
 template <class E, int KCLASS, bool VEC>
 __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
                                                   int64_t base, int cols, int nrows, int reps,
                                                   int64_t stride, int wave, int nwaves,
-                                                  int lane64, float* lds, int cap) {
+                                                  int lane64, float* lds, int cap, bool team) {
     const int nvec = (cols + E::kEPV - 1) / E::kEPV;
 #define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     if (nvec <= 16) return BSM_RUN(16, 1);
@@ -526,6 +750,11 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
         if (nvec <= 512) return BSM_RUN(64, 8);
     }
 #undef BSM_RUN
+    if constexpr (VEC && KCLASS >= 4) {
+        // the host gives long-row plans workgroup workers (team != 0): the waves share each row
+        if (team)
+            return team_item<E, KCLASS>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64);
+    }
     if constexpr (!VEC || KCLASS >= 4) {
         uint32_t done = 0;
         for (int k = 0; k < reps; ++k) {
@@ -689,13 +918,134 @@ __device__ __forceinline__ void long_row_bwd(const typename E::T* y, const typen
     }
 }
 
+// Backward rows beyond the register tile, one (or two) at a time per workgroup, laid out as
+// in team_rows: y and dy held in registers, d = sum dy * y formed by the in-lane tree, the
+// wave's butterfly and the waves' values in wave order; one barrier per rows, alternating the
+// slot set (`which`), so a set is rewritten only after every wave has passed the next barrier.
+template <class E, int L, int U>
+__device__ __forceinline__ void team_rows_bwd(const typename E::T* y, const typename E::T* dy,
+                                              typename E::T* dx, const int64_t (&off)[U],
+                                              const bool (&act)[U], int nvec, int t, int nt,
+                                              int wave, int nwaves, int lane, int which) {
+    constexpr int K = L * E::kEPV;
+    float a[U][K], g[U][K];
+    typename E::R ra[U][L], rg[U][L];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        team_load<E, L>(y + off[u], nvec, t, nt, act[u], ra[u], 0.0f);  // padding: products 0
+        team_load<E, L>(dy + off[u], nvec, t, nt, act[u], rg[u], 0.0f);
+    }
+    float d[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        team_unpack<E, L>(ra[u], a[u]);
+        team_unpack<E, L>(rg[u], g[u]);
+        float p[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) p[k] = a[u][k] * g[u][k];
+        d[u] = group_reduce<64, OpAdd>(lane_reduce<K, OpAdd>(p));
+    }
+    team_combine<OpAdd, U>(d, which, wave, nwaves, lane);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) a[u][k] = a[u][k] * (g[u][k] - d[u]);
+        team_store<E, L>(dx + off[u], nvec, t, nt, act[u], a[u]);
+    }
+}
+
+// A backward row longer than nt * L vectors: d over chunks, then y and dy read again.
+template <class E, int L>
+__device__ __forceinline__ void team_row_bwd_two_pass(const typename E::T* y,
+                                                      const typename E::T* dy, typename E::T* dx,
+                                                      int nvec, int t, int nt, int wave,
+                                                      int nwaves, int lane, int which) {
+    constexpr int K = L * E::kEPV;
+    float s = 0.0f;
+    for (int first = t; first - t < nvec; first += nt * L) {
+        float a[K], g[K];
+        typename E::R ra[L], rg[L];
+        team_load<E, L>(y, nvec, first, nt, true, ra, 0.0f);
+        team_load<E, L>(dy, nvec, first, nt, true, rg, 0.0f);
+        team_unpack<E, L>(ra, a);
+        team_unpack<E, L>(rg, g);
+#pragma unroll
+        for (int k = 0; k < K; ++k) g[k] *= a[k];
+        s += lane_reduce<K, OpAdd>(g);
+    }
+    float d[1] = {group_reduce<64, OpAdd>(s)};
+    team_combine<OpAdd, 1>(d, which, wave, nwaves, lane);
+    for (int first = t; first - t < nvec; first += nt * L) {
+        float a[K], g[K];
+        typename E::R ra[L], rg[L];
+        team_load<E, L>(y, nvec, first, nt, true, ra, 0.0f);
+        team_load<E, L>(dy, nvec, first, nt, true, rg, 0.0f);
+        team_unpack<E, L>(ra, a);
+        team_unpack<E, L>(rg, g);
+#pragma unroll
+        for (int k = 0; k < K; ++k) a[k] = a[k] * (g[k] - d[0]);
+        team_store<E, L>(dx, nvec, first, nt, true, a);
+    }
+}
+
+template <class E, int KCLASS>
+__device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const typename E::T* dy,
+                                                  typename E::T* dx, int64_t base, int cols,
+                                                  int nrows, int reps, int64_t stride, int wave,
+                                                  int nwaves, int lane) {
+    const int nvec = cols / E::kEPV;
+    const int nt = nwaves * 64;
+    const int t = wave * 64 + lane;
+    const int per_lane = (nvec + nt - 1) / nt;
+    constexpr int kMaxL = kTeamMaxL<E, KCLASS>;  // vectors per lane and stream
+    constexpr bool kPair = 2 * 4 * E::kEPV <= bsm::kTeamValues;  // as in team_item
+    int which = 0;
+    if (kPair && per_lane <= 4) {
+        RowWalk<2> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[2];
+            bool act[2];
+            w.next(off, act);
+            team_rows_bwd<E, 4, 2>(y, dy, dx, off, act, nvec, t, nt, wave, nwaves, lane, which);
+            which ^= 1;
+        }
+    } else if (per_lane <= kMaxL) {
+        RowWalk<1> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[1];
+            bool act[1];
+            w.next(off, act);
+            team_rows_bwd<E, kMaxL, 1>(y, dy, dx, off, act, nvec, t, nt, wave, nwaves, lane,
+                                       which);
+            which ^= 1;
+        }
+    } else {
+        RowWalk<1> w(base, cols, nrows, reps, stride);
+        while (w.more()) {
+            int64_t off[1];
+            bool act[1];
+            w.next(off, act);
+            team_row_bwd_two_pass<E, kMaxL>(y + off[0], dy + off[0], dx + off[0], nvec, t, nt,
+                                            wave, nwaves, lane, which);
+            which ^= 1;
+        }
+    }
+    return team_rows_of_wave(nrows, reps, wave, nwaves);
+}
+
 template <class E, int KCLASS, bool VEC>
 __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
                                                       const typename E::T* dy, typename E::T* dx,
                                                       int64_t base, int cols, int nrows, int reps,
                                                       int64_t stride, int wave, int nwaves,
-                                                      int lane64, float* lds, int cap) {
+                                                      int lane64, float* lds, int cap, bool team) {
     const int nvec = (cols + E::kEPV - 1) / E::kEPV;
+    if constexpr (VEC && KCLASS >= 4) {
+        // rows beyond the forward register tile: the workgroup's waves share each row
+        if (team && nvec > 512)
+            return team_item_bwd<E, KCLASS>(y, dy, dx, base, cols, nrows, reps, stride, wave,
+                                            nwaves, lane64);
+    }
 #define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     // (Rows of 33..64 vectors keep 64 lanes x 1 vector here: with two input streams the
     // forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x 512 bf16.)
@@ -756,20 +1106,20 @@ __device__ __forceinline__ void worker_loop(const typename E::T* a, const typena
             if (vec)
                 rows += dispatch_item_bwd<E, KCLASS, true>(a, b, out, base, cols, nrows, reps, stride,
                                                            my_wave, my_nwaves, lane64, lds,
-                                                           lds_floats_per_wave);
+                                                           lds_floats_per_wave, !per_wave);
             else
                 rows += dispatch_item_bwd<E, KCLASS, false>(a, b, out, base, cols, nrows, reps, stride,
                                                             my_wave, my_nwaves, lane64, lds,
-                                                            lds_floats_per_wave);
+                                                            lds_floats_per_wave, !per_wave);
         } else {
             if (vec)
                 rows += dispatch_item<E, KCLASS, true>(a, out, base, cols, nrows, reps, stride,
                                                        my_wave, my_nwaves, lane64, lds,
-                                                       lds_floats_per_wave);
+                                                       lds_floats_per_wave, !per_wave);
             else
                 rows += dispatch_item<E, KCLASS, false>(a, out, base, cols, nrows, reps, stride,
                                                         my_wave, my_nwaves, lane64, lds,
-                                                        lds_floats_per_wave);
+                                                        lds_floats_per_wave, !per_wave);
         }
     }
     if (trace && lane64 == 0) {
@@ -787,8 +1137,15 @@ __device__ __forceinline__ void worker_loop(const typename E::T* a, const typena
 
 extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
 
+// Launch bounds: any workgroup size up to 1024 threads; long-row plans (class 4) always run
+// 256-thread workgroups, two or more per CU, so their rows may hold up to 256 VGPRs per lane.
+template <int KCLASS>
+constexpr int kMaxThreads = KCLASS >= 4 ? 256 : 1024;
+template <int KCLASS>
+constexpr int kMinWavesPerSimd = KCLASS >= 4 ? 2 : 1;
+
 template <class E, int KCLASS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
 bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
                    const bsm_item* __restrict__ items, int base_aligned, int per_wave,
                    int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
@@ -798,7 +1155,7 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
 
 // dx = softmax backward of (y, dy) under the same work table.
 template <class E, int KCLASS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
 bsm_softmax_bwd_kernel(const typename E::T* y, const typename E::T* dy, typename E::T* dx,
                        const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                        int base_aligned, int per_wave, int lds_floats_per_wave,

@@ -36,7 +36,8 @@ hipError_t launch_class(int kclass, const void* in, void* out, const int32_t* wo
         case 1: return BSM_LAUNCH(1);
         case 2: return BSM_LAUNCH(2);
         case 3: return BSM_LAUNCH(3);
-        default: return BSM_LAUNCH(4);
+        case 4: return BSM_LAUNCH(4);
+        default: return BSM_LAUNCH(5);
     }
 #undef BSM_LAUNCH
 }
@@ -66,7 +67,8 @@ hipError_t launch_class_bwd(int kclass, const void* y, const void* dy, void* dx,
         case 1: return BSM_LAUNCH(1);
         case 2: return BSM_LAUNCH(2);
         case 3: return BSM_LAUNCH(3);
-        default: return BSM_LAUNCH(4);
+        case 4: return BSM_LAUNCH(4);
+        default: return BSM_LAUNCH(5);
     }
 #undef BSM_LAUNCH
 }
@@ -81,7 +83,8 @@ int kernel_class_for(int32_t max_cols, int elem_bytes) {
     if (nvec <= 128) return 1;  // rows of 33..64 vectors run 32 lanes x 2 vectors
     if (nvec <= 256) return 2;
     if (nvec <= 512) return 3;
-    return 4;
+    // longer rows: workgroup-held, up to kTeamValues values per lane in class 4
+    return max_cols <= kTeamThreads * kTeamValues ? 4 : 5;
 }
 
 hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool temporal, const void* in,
@@ -109,6 +112,51 @@ hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool tempo
 #undef BSM_ARGS
 }
 
+namespace {
+template <class E>
+hipError_t static_lds_of(int kernel_class, int* bytes) {
+    const void* fns[2] = {nullptr, nullptr};
+    switch (kernel_class) {
+#define BSM_FNS(K)                                                              \
+    case K:                                                                     \
+        fns[0] = reinterpret_cast<const void*>(&bsm_softmax_kernel<E, K>);     \
+        fns[1] = reinterpret_cast<const void*>(&bsm_softmax_bwd_kernel<E, K>); \
+        break;
+        BSM_FNS(0)
+        BSM_FNS(1)
+        BSM_FNS(2)
+        BSM_FNS(3)
+        BSM_FNS(4)
+        default:
+            fns[0] = reinterpret_cast<const void*>(&bsm_softmax_kernel<E, 5>);
+            fns[1] = reinterpret_cast<const void*>(&bsm_softmax_bwd_kernel<E, 5>);
+            break;
+#undef BSM_FNS
+    }
+    *bytes = 0;
+    for (const void* fn : fns) {
+        hipFuncAttributes a;
+        const hipError_t e = hipFuncGetAttributes(&a, fn);
+        if (e != hipSuccess) return e;
+        if (static_cast<int>(a.sharedSizeBytes) > *bytes) *bytes = static_cast<int>(a.sharedSizeBytes);
+    }
+    return hipSuccess;
+}
+}  // namespace
+
+// Static LDS is the same for the streaming and the cache-resident instances; both are checked
+// anyway, as they are separate functions.
+hipError_t static_lds_bytes(bsm_dtype dtype, int kernel_class, int* bytes) {
+    int a = 0, b = 0;
+    hipError_t e = dtype == BSM_BF16 ? static_lds_of<BF16<true>>(kernel_class, &a)
+                                     : static_lds_of<F32<true>>(kernel_class, &a);
+    if (e == hipSuccess)
+        e = dtype == BSM_BF16 ? static_lds_of<BF16<false>>(kernel_class, &b)
+                              : static_lds_of<F32<false>>(kernel_class, &b);
+    *bytes = a > b ? a : b;
+    return e;
+}
+
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
                                size_t dyn_lds_bytes, int* n) {
     const void* fn = nullptr;
@@ -118,7 +166,8 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads
             case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 1>); break;
             case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 2>); break;
             case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 3>); break;
-            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 4>); break;
+            case 4: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 4>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<BF16<true>, 5>); break;
         }
     } else {
         switch (kernel_class) {
@@ -126,7 +175,8 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads
             case 1: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 1>); break;
             case 2: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 2>); break;
             case 3: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 3>); break;
-            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 4>); break;
+            case 4: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 4>); break;
+            default: fn = reinterpret_cast<const void*>(&bsm_softmax_kernel<F32<true>, 5>); break;
         }
     }
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(n, fn, wg_threads, dyn_lds_bytes);

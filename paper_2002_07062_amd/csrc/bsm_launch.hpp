@@ -50,6 +50,8 @@ hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, 
                        const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream);
 
 // Workgroups of the kernel instance that fit on one CU at once (registers and LDS decide).
+// Largest static LDS (bytes per workgroup) of the forward and backward kernels of a class.
+hipError_t static_lds_bytes(bsm_dtype dtype, int kernel_class, int* bytes);
 hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, int wg_threads,
                                size_t dyn_lds_bytes, int* n);
 

@@ -28,6 +28,13 @@ constexpr Tile tile_for(int64_t nvec, int max_v) {
     return Tile{64, 0};
 }
 
+// Rows beyond the register tile are held in the registers of a whole workgroup of kTeamThreads
+// threads: up to kTeamValues values per lane in kernel class 4 (rows of up to
+// kTeamThreads * kTeamValues elements), twice that in class 5, whose instances need twice the
+// registers.
+constexpr int kTeamThreads = 256;
+constexpr int kTeamValues = 32;
+
 // Rows per group a wave keeps in flight: enough rows that each lane has kVecsInFlight 16-byte
 // loads outstanding (one row for the element-wise and two-pass paths).
 constexpr int rows_per_group_in_flight(int V, bool vec_path) {

@@ -58,20 +58,37 @@ def test_backward_ragged_odd_cols_with_gaps(dtype, schedule):
     _check(w, schedule, y, dy)
 
 
+# Rows past the backward register tile (256 vectors): 16-byte aligned rows first, then
+# unaligned ones.  Class 3 (one wave per row: staged in LDS or read twice), class 4 (a
+# workgroup holds y and dy: two rows of 4 vectors per lane (fp32), or up to 32 values per lane
+# and stream) and class 5 (up to 64 values; longer rows read twice).
+BWD_LONG_COLS = {
+    ("f32", 3): [1028, 1500, 2048, 1030],
+    ("f32", 4): [2052, 3000, 4096, 6000, 8192, 2050, 5003],
+    ("f32", 5): [8196, 16384, 16388, 40000, 10001],
+    ("bf16", 3): [2056, 3000, 4096, 2050],
+    ("bf16", 4): [4104, 6000, 8192, 4098, 5003],
+    ("bf16", 5): [8200, 16384, 16392, 40000, 10001],
+}
+
+
+@pytest.mark.parametrize("kclass", [3, 4, 5])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("schedule", ["rr", "balanced"])
-def test_backward_long_rows_staged_and_two_pass(dtype, schedule):
-    """Rows past the register tile: both y and dy staged in the wave's LDS when 2 C fits it,
-    otherwise a second read of both; aligned and unaligned rows."""
-    cols = [1028, 2048, 2052, 3000, 4096, 6000, 10000, 40000]
-    rows = [3, 2, 2, 3, 2, 2, 1, 1]
+def test_backward_long_rows(dtype, kclass):
+    """Rows past the backward register tile under every schedule, against the oracle, with the
+    same bits under all three."""
+    cols = BWD_LONG_COLS[(dtype, kclass)]
+    rows = [3, 2, 5, 3, 2, 3, 1][: len(cols)]
     w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=43, gap=8)
     y, dy = backward_inputs(w)
-    print(f"[backward long {dtype} {schedule}]", flush=True)
-    _, st, _ = _check(w, schedule, y, dy)
-    assert st["kernel_class"] == 4
-    cap = st["lds_bytes_per_wave"] // 4
-    assert any(2 * c <= cap for c in cols) and any(2 * c > cap for c in cols)
+    first = None
+    for schedule in SCHEDULES:
+        print(f"[backward long {dtype} class {kclass} {schedule}] cols {cols}", flush=True)
+        bits, st, _ = _check(w, schedule, y, dy)
+        assert st["kernel_class"] == kclass
+        if first is None:
+            first = bits
+        assert np.array_equal(bits, first), schedule
 
 
 def test_backward_in_place_equals_out_of_place():

@@ -44,21 +44,34 @@ def test_ragged_odd_cols_with_gaps(dtype, schedule):
     _check_ragged(w, schedule)
 
 
-@pytest.mark.parametrize("schedule", SCHEDULES)
+# Rows beyond the register tile, by kernel class: 16-byte aligned rows first (each tile of the
+# workgroup-held path: two rows of <= 3 vectors per lane (fp32), 4, 8 or 16 vectors per lane,
+# and the two-pass path past 64 values per lane), an unaligned row last (element-wise, one
+# wave per row), so that every earlier slice starts 16-byte aligned.
+LONG_COLS = {
+    ("f32", 4): [2052, 2500, 3072, 4096, 4100, 6000, 8192, 4095],
+    ("bf16", 4): [4104, 5000, 6144, 8192, 4200, 8000, 4097],
+    ("f32", 5): [8196, 12000, 16384, 16388, 40000, 100003],
+    ("bf16", 5): [8200, 12000, 16384, 16392, 40000, 100003],
+}
+
+
+@pytest.mark.parametrize("kclass", [4, 5])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_long_rows_lds_staged_and_two_pass(dtype, schedule):
-    """Rows beyond the register tile: those that fit a wave's LDS region are staged there (read
-    once), longer ones take the two-pass path; both against the oracle."""
-    cols = [2049, 4095, 4096, 4100, 8192, 10000, 40000, 100003]
-    rows = [3, 2, 2, 3, 2, 2, 1, 1]
+def test_long_rows_workgroup_held_and_two_pass(dtype, kclass):
+    """Rows beyond the register tile, held by a 256-thread workgroup (up to 8192 elements in
+    kernel class 4, 16384 in class 5) or, longer, read twice; odd row counts (rows are paired
+    across ranges); against the oracle under every schedule, with the same bits under all."""
+    cols = LONG_COLS[(dtype, kclass)]
+    rows = [3, 5, 2, 3, 2, 3, 2, 3][: len(cols)]
     w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=9, gap=8)
-    print(f"[long {dtype} {schedule}]", flush=True)
-    bits, st = _check_ragged(w, schedule)
-    assert st["kernel_class"] == 4
-    cap = st["lds_bytes_per_wave"] // 4
-    print(f"  LDS per wave {st['lds_bytes_per_wave']} B = rows up to {cap} staged", flush=True)
-    assert cap >= 2048
-    assert any(c <= cap for c in cols) and any(c > cap for c in cols)
+    results = []
+    for schedule in SCHEDULES:
+        print(f"[long {dtype} class {kclass} {schedule}] cols {cols}", flush=True)
+        bits, st = _check_ragged(w, schedule)
+        assert st["kernel_class"] == kclass and st["wg_threads"] == 256 and st["per_wave"] == 0
+        results.append(bits)
+    assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
 
 
 # Aligned rows whose 16-byte vector count n = cols * elem_bytes / 16 is not a power of two
@@ -423,17 +436,33 @@ def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_fp32_rows_up_to_10240_are_staged_at_four_waves_per_cu(dtype):
-    """An fp32 plan whose longest row is 5121..10240 elements runs 4 waves per CU, so every
-    row fits a wave's LDS region (read once); bf16 plans keep 8 waves per CU. Both against the
-    oracle."""
-    cols = [5000, 6144, 8192, 10240, 7003]
-    w = workloads.custom([3, 2, 2, 2, 3], cols, dtype=dtype, sigma=3.0, seed=12, gap=8)
-    print(f"[mid-long {dtype}]", flush=True)
-    _, st = _check_ragged(w, "balanced")
-    assert st["kernel_class"] == 4
-    waves_per_cu = st["n_wg"] * (st["wg_threads"] // 64) // bsm.bsm_device_info(0)["n_cu"]
-    if dtype == "f32":
-        assert waves_per_cu == 4 and st["lds_bytes_per_wave"] // 4 >= max(cols)
-    else:
-        assert waves_per_cu == 8
+def test_long_row_plans_run_256_thread_workgroups(dtype):
+    """A plan with rows beyond the register tile runs 256-thread workgroups whatever workgroup
+    size the topology asks for (a row's bits depend on it): same bits for 64, 256 and 512, and
+    the per-wave trace counts every row once."""
+    cols = [5000, 6144, 8192, 7000]
+    w = workloads.custom([3, 2, 5, 3], cols, dtype=dtype, sigma=3.0, seed=12, gap=8)
+    first = None
+    for threads in (64, 256, 512):
+        print(f"[long-row workgroups {dtype} asked {threads}]", flush=True)
+        n = int(w.offsets[-1])
+        x = to_device(w.x, dtype)
+        out = sentinel_like(n, dtype)
+        plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=dtype,
+                                   schedule="balanced", device=0,
+                                   topology=dict(wg_threads=threads))
+        st = bsm.bsm_plan_describe(plan)
+        trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
+        bsm.bsm_plan_execute(plan, x, out, trace=trace)
+        torch.cuda.synchronize()
+        plan.destroy()
+        assert st["wg_threads"] == 256 and st["per_wave"] == 0
+        rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+        assert int(rec["rows"].sum()) == int(w.rows.sum())
+        bits = to_host_bits(out)
+        if first is None:
+            first = bits
+            mask = covered_mask(w.offsets[: w.batch], w.rows, w.cols, n)
+            compare(bits, oracle.softmax(w.x, dtype, w.offsets[: w.batch], w.rows, w.cols),
+                    dtype, mask)
+        assert np.array_equal(bits, first), threads

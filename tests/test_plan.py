@@ -59,12 +59,17 @@ def test_every_row_scheduled_exactly_once(name, schedule, topo):
     assert pc.check_exactly_once(ptr, items, w.offsets[: w.batch], w.rows, w.cols) == []
     t = TOPOLOGIES[topo]
     n_wg = t["n_cu"] * t["wg_per_cu"]
-    assert d["n_wg"] == n_wg
-    assert d["n_workers"] == (n_wg if schedule == "rr" else n_wg * t["wg_threads"] // 64)
-    assert d["per_wave"] == (0 if schedule == "rr" else 1)
+    # rows beyond the register tile (kernel class >= 4): 256-thread workgroups share each row,
+    # so every worker is a workgroup under every schedule
+    team = d["kernel_class"] >= 4
+    threads = 256 if team else t["wg_threads"]
+    assert d["n_wg"] == n_wg and d["wg_threads"] == threads
+    per_wave = schedule != "rr" and not team
+    assert d["n_workers"] == (n_wg * threads // 64 if per_wave else n_wg)
+    assert d["per_wave"] == int(per_wave)
     assert d["total_rows"] == int(w.rows.sum())
     assert d["algorithmic_bytes"] == w.algorithmic_bytes
-    assert d["trace_bytes"] == n_wg * (t["wg_threads"] // 64) * 32
+    assert d["trace_bytes"] == n_wg * (threads // 64) * 32
 
 
 @pytest.mark.parametrize("name", list(WL))
