@@ -624,12 +624,14 @@ def main() -> int:
         extra["producer_consumer"] = producer_consumer()
         extra["attention_pipeline"] = attention_pipeline()
         extra["l2_locality_16MB_us"] = l2_locality()
-        # rows longer than the register tile: 4096-element rows fit a wave's LDS region at 8
-        # waves/CU, 8192-element rows at 4 (the plan picks 4), both read once; 16384-element
-        # rows take the two-pass path (1.5x the traffic)
+        # rows longer than the register tile, held in the registers of a 256-thread workgroup
+        # (up to 8192 elements in kernel class 4, 16384 in class 5) and read once, forward and
+        # backward
         for name in ("long4k", "long", "long16k"):
             r, _ = run_workload(name, "balanced", args.steps, args.warmup)
-            extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "lds_bytes_per_wave")}
+            extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}
+            r = run_backward(name, "balanced", args.steps, args.warmup)
+            extra[f"{name}_backward_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step")}
 
     head_trace = None if args.no_extra else trace_stats(w, args.schedule)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)

@@ -84,7 +84,9 @@ typedef struct bsm_topology {
     int32_t n_cu;        /* compute units (MI355X: 256) */
     int32_t n_xcd;       /* XCDs (MI355X: 8); workgroup w is taken to run on XCD w mod n_xcd */
     int32_t wg_per_cu;   /* persistent workgroups per CU; the grid has n_cu * wg_per_cu */
-    int32_t wg_threads;  /* threads per workgroup, a multiple of 64 in [64, 1024] */
+    int32_t wg_threads;  /* threads per workgroup, a multiple of 64 in [64, 1024]; plans with
+                            rows longer than 2048 fp32 / 4096 bf16 elements run 256 whatever
+                            is asked (the workgroup's waves share each such row) */
     int32_t piece_bytes; /* BALANCED / XCD: traffic of one worker's piece of a round */
     float item_cost;     /* planner cost of one work item, in byte equivalents (<= 0: default) */
     float row_cost;      /* planner cost of one row on top of its bytes (<= 0: default) */
@@ -123,7 +125,8 @@ typedef struct bsm_plan_stats {
     int64_t trace_bytes;       /* size a trace buffer passed to bsm_plan_execute must have */
     int64_t n_rounds;          /* BALANCED / XCD: rounds the largest team's stream was cut into */
     int32_t n_workers;         /* entries of the work table's row pointer minus one */
-    int32_t per_wave;          /* 1: workers are waves (w * waves_per_wg + wave); 0: workgroups */
+    int32_t per_wave;          /* 1: workers are waves (w * waves_per_wg + wave); 0: workgroups
+                                  (RR, and every plan with rows beyond the register tile) */
     int32_t n_wg;              /* persistent workgroups in the grid */
     int32_t n_xcd;
     int32_t wg_threads;
@@ -132,7 +135,9 @@ typedef struct bsm_plan_stats {
     int32_t n_overlap;         /* XCD: slices straddling two or more virtual banks */
     int32_t max_cols;          /* longest row */
     int32_t kernel_class;      /* which kernel instance the plan launches (internal) */
-    int32_t lds_bytes_per_wave; /* LDS each wave stages long rows in (0: two-pass path only) */
+    int32_t lds_bytes_per_wave; /* LDS each wave may stage a row in (rows beyond the register
+                                   tile whose start or length is not 16-byte aligned, and
+                                   backward rows of 257..512 16-byte vectors; 0: none) */
     int32_t flags;             /* the BSM_FLAG_* bits the plan runs with */
     double max_worker_cost;    /* planner cost of the most loaded worker */
     double mean_worker_cost;   /* total planner cost / n_workers */

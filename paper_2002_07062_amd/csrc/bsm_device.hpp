@@ -3,8 +3,9 @@
 // One launch runs a grid of n_wg persistent workgroups.  Each worker -- a workgroup, or a
 // single wave when the table is per-wave -- walks its items [worker_ptr[v], worker_ptr[v+1])
 // of the host-built work table (the mapping table of the paper's Section 5: geometry is read
-// per item, the instructions are the same for every patch).  No barrier is ever needed: every
-// row is owned by one group of lanes of one wave.
+// per item, the instructions are the same for every patch).  A row up to the register tile is
+// owned by one group of lanes of one wave (no barrier); a longer row is shared by all the
+// waves of a 256-thread workgroup, which combine their partial max and sum through LDS.
 //
 // Per row (softmax over the row, the operation of the problem statement, Section 2):
 //   128-bit loads (fp32, or bf16 widened to fp32; nontemporal unless the plan asks for cache-
@@ -17,10 +18,11 @@
 //
 // A group of G lanes (16, 32 or 64) owns one row and holds V 16-byte vectors per lane, so a
 // wave covers 64/G rows at a time, with four 16-byte loads per lane in flight.  Rows longer
-// than the kernel class's register tile are staged in the wave's LDS region (read once) or,
-// when too long for it, take a two-pass online max/sum.  Rows whose start or length is not
-// 16-byte aligned use element loads with the same lane layout.  This is bandwidth-bound work:
-// no MFMA.
+// than the largest register tile (512 vectors) are held in the registers of a whole workgroup
+// (up to 32 values per lane in kernel class 4, 64 in class 5) and read once, or, longer still,
+// read twice with an online max/sum.  Rows whose start or length is not 16-byte aligned use
+// element loads with the same lane layout, or one wave per row (staged in the wave's LDS
+// region, else two passes).  This is bandwidth-bound work: no MFMA.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -261,9 +263,11 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
     return done;
 }
 
-// Rows longer than the register tile, one wave per row, in chunks of CH 16-byte vectors per
-// lane (VALS values: 32 for one input stream, 16 for two) so each lane keeps CH loads in flight; the rare element-wise path (rows not
-// 16-byte aligned) uses chunks of 8 elements, whose per-element addresses cost registers.
+// One wave per row, for rows that neither a register tile nor the workgroup path takes: rows
+// whose start or length is not 16-byte aligned, beyond 64 vectors (element-wise, in chunks of
+// 8 elements, whose per-element addresses cost registers), and in the backward pass aligned
+// rows of 257..512 vectors (chunks of CH 16-byte vectors per lane, VALS values: 32 for one
+// input stream, 16 for two, so each lane keeps CH loads in flight).
 //
 // When the row fits the wave's LDS region (`cap` floats, given to plans with long rows), it is
 // read from HBM once: pass 1 keeps a per-lane max while staging the values in LDS, pass 2

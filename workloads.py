@@ -59,13 +59,13 @@ SPECS = {
     # long rows (beyond the register tile): long-context attention scores
     "long_128x64x4096_f32": Spec(
         "long_128x64x4096_f32", 128, 64, 4096, F32, 3.0, 7,
-        doc="128 slices x 64x4096 fp32, N(0,9): rows that fit a wave's LDS region"),
+        doc="128 slices x 64x4096 fp32, N(0,9): 4 vectors per lane of a 256-thread workgroup"),
     "long_64x64x8192_f32": Spec(
         "long_64x64x8192_f32", 64, 64, 8192, F32, 3.0, 6,
-        doc="64 slices x 64x8192 fp32, N(0,9): rows that fit a wave's LDS region at 4 waves/CU"),
+        doc="64 slices x 64x8192 fp32, N(0,9): the longest rows of kernel class 4 (8 vectors per lane)"),
     "long_32x64x16384_f32": Spec(
         "long_32x64x16384_f32", 32, 64, 16384, F32, 3.0, 8,
-        doc="32 slices x 64x16384 fp32, N(0,9): rows longer than any wave's LDS region"),
+        doc="32 slices x 64x16384 fp32, N(0,9): the longest register-held rows (class 5, 16 vectors per lane)"),
 }
 
 # Short aliases used by the bench and the tests.
