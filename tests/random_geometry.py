@@ -1,13 +1,14 @@
 """Seeded random slice geometries for the randomized planner and parity tests: slices in a
-random order with random gaps, empty slices, widths across every register-tile class and a
-few long rows. Input generation only (no softmax arithmetic)."""
+random order with random gaps (in half the geometries every slice start and row length a
+multiple of 8 elements, so aligned paths run), empty slices, widths across every
+register-tile class and long rows of both long-row kernel classes. Input generation only (no softmax arithmetic)."""
 
 import numpy as np
 
 import workloads
 
 WIDTHS = [1, 3, 7, 8, 15, 16, 17, 31, 33, 64, 72, 100, 128, 129, 200, 256, 260, 511, 512, 513,
-          700, 1000, 1024, 1100, 2048, 2051, 3000, 4096, 5000, 9000]
+          700, 1000, 1024, 1100, 2048, 2051, 3000, 4096, 5000, 8192, 9000, 12000, 16384, 20000]
 
 
 def geometry(seed: int, max_batch: int = 40, max_rows: int = 120, dtype: str = "f32",
@@ -20,6 +21,9 @@ def geometry(seed: int, max_batch: int = 40, max_rows: int = 120, dtype: str = "
     rows[rng.random(batch) < 0.1] = 0  # some empty slices
     base = int(rng.integers(0, 40))
     gaps = rng.integers(0, 50, size=batch)
+    if rng.random() < 0.5:  # every slice start 16-byte aligned (for fp32 and bf16)
+        base, gaps = 8 * base, 8 * gaps
+        cols = np.where(cols % 8 == 0, cols, cols - cols % 8 + 8).astype(np.int32)
     order = rng.permutation(batch)
     offsets = np.zeros(batch + 1, dtype=np.int64)
     pos = base
