@@ -29,12 +29,13 @@ struct bsm_plan_s {
     bsm::Geometry geo;
     bsm::Table table;
     int kernel_class = 0;
+    bool shifted = false;  // some slice's rows do not start and end on 16-byte vectors
     // A matrix-product plan (bsm_gemm_plan_create) instead of a softmax plan: the slices are
     // the outputs C_b (gemm_m x gemm_n), A_b is gemm_m x gemm_k, layout 0 = NT, 1 = NN.
     bool gemm = false;
     int gemm_m = 0, gemm_n = 0, gemm_k = 0, gemm_layout = 0;
     int64_t gemm_batch = 0;
-    int lds_floats_per_wave = 0;  // long-row staging (kernel class 4 on a device)
+    int lds_floats_per_wave = 0;  // one-wave long-row staging (kernel classes 4, 5 on a device)
     int32_t flags = 0;            // BSM_FLAG_* bits
     void* d_table = nullptr;  // device copy: worker_ptr, then items (256-byte aligned)
     const int32_t* d_worker_ptr = nullptr;
@@ -110,6 +111,15 @@ constexpr float kDefaultRowCost = 64.0f;
 
 int elem_bytes_of(bsm_dtype d) { return d == BSM_BF16 ? 2 : 4; }
 
+// Whether some non-empty slice's rows do not all start and end on 16-byte vectors.
+bool any_shifted(const bsm::Geometry& g) {
+    const int64_t epv = bsm::kVecBytes / g.elem_bytes;
+    for (int64_t s = 0; s < g.batch; ++s)
+        if (g.R[s] > 0 && g.C[s] > 0 && ((g.off[s] | static_cast<int64_t>(g.C[s])) % epv) != 0)
+            return true;
+    return false;
+}
+
 bool valid_dtype(int d) { return d == BSM_F32 || d == BSM_BF16; }
 bool valid_schedule(int s) { return s == BSM_SCHED_RR || s == BSM_SCHED_BALANCED || s == BSM_SCHED_XCD; }
 
@@ -137,7 +147,7 @@ bsm_status default_topology(int device, bsm_topology* t) {
 }
 
 bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtype, int kclass,
-                            bsm::Topology* out) {
+                            bool shifted, bsm::Topology* out) {
     bsm_topology t;
     if (device >= 0) {
         bsm_status st = default_topology(device, &t);
@@ -180,12 +190,13 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
                 probe.wg_per_cu = want;
                 probe.wg_threads = t.wg_threads;
                 int static_bytes = 0;
-                e = bsm::static_lds_bytes(dtype, kclass, &static_bytes);
+                e = bsm::static_lds_bytes(dtype, kclass, shifted, &static_bytes);
                 if (e == hipSuccess)
                     lds = static_cast<size_t>(lds_bytes_per_wave(prop, probe, static_bytes)) *
                           (t.wg_threads / 64);
             }
-            if (e == hipSuccess) e = bsm::resident_wgs_per_cu(dtype, kclass, t.wg_threads, lds, &n);
+            if (e == hipSuccess)
+                e = bsm::resident_wgs_per_cu(dtype, kclass, shifted, t.wg_threads, lds, &n);
             if (e != hipSuccess) return hip_fail(e, "occupancy query");
             t.wg_per_cu = std::max(1, std::min(want, n));
         }
@@ -256,7 +267,8 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
     try {
         std::string err = bsm::make_geometry(offs, rows, cols, batch, elem_bytes_of(dtype), &p->geo);
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
-        p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype));
+        p->shifted = any_shifted(p->geo);
+        p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype), p->shifted);
         // Rows beyond the register tile are worked by whole workgroups of kTeamThreads threads,
         // one row at a time: such plans run that workgroup size whatever the topology asks (a
         // row's bits depend on it), and every worker of their table is a workgroup.
@@ -266,7 +278,8 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             tu.wg_threads = bsm::kTeamThreads;
             topology = &tu;
         }
-        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, &p->topo);
+        bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, p->shifted,
+                                         &p->topo);
         if (st != BSM_OK) return st;
         st = resolve_weights(xcd_weight, &p->topo);
         if (st != BSM_OK) return st;
@@ -306,7 +319,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             e = hipGetDeviceProperties(&prop, device);
             if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
             int static_bytes = 0;
-            e = bsm::static_lds_bytes(dtype, p->kernel_class, &static_bytes);
+            e = bsm::static_lds_bytes(dtype, p->kernel_class, p->shifted, &static_bytes);
             if (e != hipSuccess) return hip_fail(e, "hipFuncGetAttributes");
             const int64_t b = lds_bytes_per_wave(prop, p->topo, static_bytes);
             p->lds_floats_per_wave = static_cast<int>(b / static_cast<int64_t>(sizeof(float)));
@@ -369,12 +382,12 @@ bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b,
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool temporal = (p->flags & BSM_FLAG_TEMPORAL) != 0;
     if (backward)
-        e = bsm::launch_softmax_backward(p->dtype, p->kernel_class, temporal, a, b, out,
+        e = bsm::launch_softmax_backward(p->dtype, p->kernel_class, p->shifted, temporal, a, b, out,
                                          p->d_worker_ptr, p->d_items, p->topo.n_wg(),
                                          p->topo.wg_threads, p->table.per_wave ? 1 : 0,
                                          p->lds_floats_per_wave, trace, s);
     else
-        e = bsm::launch_softmax(p->dtype, p->kernel_class, temporal, a, out, p->d_worker_ptr,
+        e = bsm::launch_softmax(p->dtype, p->kernel_class, p->shifted, temporal, a, out, p->d_worker_ptr,
                                 p->d_items, p->topo.n_wg(), p->topo.wg_threads,
                                 p->table.per_wave ? 1 : 0, p->lds_floats_per_wave, trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");

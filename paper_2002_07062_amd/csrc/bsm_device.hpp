@@ -165,7 +165,61 @@ struct BF16 {
 
 // Softmax of U rows per group, all loads first (U rows x V vectors in flight per lane).
 //   row r of the item starts at element base + r * cols; rows r0, r0 + step, ...
-template <class E, int G, int V, int U, bool VEC>
+// The 16-byte vectors of one row.  An aligned row (SHIFT false: its start and length whole
+// vectors) holds cols / EPV of them from its start.  A shifted row -- start or length not a
+// whole number of vectors, the buffers themselves 16-byte aligned -- is covered by the aligned
+// vectors from the one holding its first element: the first `ph` elements of vector 0 precede
+// the row and the last vector may run past its end.  Those outside elements are read with the
+// vector (a 16-byte vector never crosses a page, so it is mapped wherever one of its elements
+// is) and replaced by `pad`, and never written: the row's first and last vectors are stored
+// element by element, every other one as a whole.
+template <class E, bool SHIFT>
+struct RowVecs {
+    static constexpr int EPV = E::kEPV;
+    int64_t start;  // element offset of vector 0
+    int ph;         // elements of vector 0 before the row
+    int cols;
+    int nv;         // vectors covering the row
+    __device__ __forceinline__ RowVecs(int64_t row_start, int c) : cols(c) {
+        ph = SHIFT ? static_cast<int>(row_start & (EPV - 1)) : 0;
+        start = row_start - ph;
+        nv = SHIFT ? (ph + c + EPV - 1) / EPV : c / EPV;
+    }
+    // Elements [lo, hi) of vector vi belong to the row.
+    __device__ __forceinline__ int lo(int vi) const { return ph - vi * EPV; }
+    __device__ __forceinline__ int hi(int vi) const { return cols + ph - vi * EPV; }
+    __device__ __forceinline__ void mask(int vi, float* x, float pad) const {
+        if constexpr (SHIFT) {
+            const int l = lo(vi), h = hi(vi);
+            if (l > 0 || h < EPV) {
+#pragma unroll
+                for (int e = 0; e < EPV; ++e)
+                    if (e < l || e >= h) x[e] = pad;
+            }
+        }
+    }
+    __device__ __forceinline__ void store(typename E::T* out, int vi, const float* y) const {
+        typename E::T* p = out + start + vi * EPV;
+        if constexpr (SHIFT) {
+            const int l = lo(vi), h = hi(vi);
+            if (l > 0 || h < EPV) {
+#pragma unroll
+                for (int e = 0; e < EPV; ++e)
+                    if (e >= l && e < h) E::store1(p + e, y[e]);
+                return;
+            }
+        }
+        E::store_vec(p, y);
+    }
+};
+
+// Vectors a row of `cols` elements may span: one more than its length in vectors when shifted.
+template <class E, bool SHIFT>
+__device__ __forceinline__ int span_vecs(int cols) {
+    return (cols + E::kEPV - 1) / E::kEPV + (SHIFT ? 1 : 0);
+}
+
+template <class E, int G, int V, int U, bool VEC, bool SHIFT = false>
 __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* out, int64_t base,
                                        int cols, int nrows, int r0, int step, int lane) {
     constexpr int EPV = E::kEPV;
@@ -177,16 +231,16 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
     for (int u = 0; u < U; ++u) {
         const int r = r0 + u * step;
         act[u] = r < nrows;
-        const typename E::T* src = in + base + static_cast<int64_t>(r) * cols;
+        const int64_t o = base + static_cast<int64_t>(r) * cols;
         if constexpr (VEC) {
             // the vectors as loaded (a lane's loads all issued before any use; unpacking
             // inside each conditional load would make every load wait for the previous one)
-            const int nvec = cols / EPV;
+            const RowVecs<E, SHIFT> rv(o, cols);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
-                if (act[u] && vi < nvec)
-                    raw[u][v] = E::load_raw(src + vi * EPV);
+                if (act[u] && vi < rv.nv)
+                    raw[u][v] = E::load_raw(in + rv.start + vi * EPV);
                 else
                     raw[u][v] = E::raw_fill(kNegInf);
             }
@@ -194,15 +248,20 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const int j = lane + k * G;
-                x[u][k] = (act[u] && j < cols) ? E::load1(src + j) : kNegInf;
+                x[u][k] = (act[u] && j < cols) ? E::load1(in + o + j) : kNegInf;
             }
         }
     }
     if constexpr (VEC) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; ++u) {
+            const RowVecs<E, SHIFT> rv(base + static_cast<int64_t>(r0 + u * step) * cols, cols);
 #pragma unroll
-            for (int v = 0; v < V; ++v) E::unpack(raw[u][v], &x[u][v * EPV]);
+            for (int v = 0; v < V; ++v) {
+                E::unpack(raw[u][v], &x[u][v * EPV]);
+                rv.mask(lane + v * G, &x[u][v * EPV], kNegInf);
+            }
+        }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -215,19 +274,19 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
 #pragma unroll
         for (int k = 0; k < K; ++k) x[u][k] *= inv;
         const int r = r0 + u * step;
-        typename E::T* dst = out + base + static_cast<int64_t>(r) * cols;
+        const int64_t o = base + static_cast<int64_t>(r) * cols;
         if constexpr (VEC) {
-            const int nvec = cols / EPV;
+            const RowVecs<E, SHIFT> rv(o, cols);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
-                if (act[u] && vi < nvec) E::store_vec(dst + vi * EPV, &x[u][v * EPV]);
+                if (act[u] && vi < rv.nv) rv.store(out, vi, &x[u][v * EPV]);
             }
         } else {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const int j = lane + k * G;
-                if (act[u] && j < cols) E::store1(dst + j, x[u][k]);
+                if (act[u] && j < cols) E::store1(out + o + j, x[u][k]);
             }
         }
     }
@@ -237,7 +296,7 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
 // base + k * stride.  Within a range the worker's rows are wave*RPW + sub + j*step, j = 0, 1,
 // ... (RPW = 64/G rows per wave, step = rows covered by all the worker's waves at once); loop
 // trip counts depend on the wave only, so lanes never diverge across iterations.
-template <class E, int G, int V, bool VEC>
+template <class E, int G, int V, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E::T* out,
                                              int64_t base, int cols, int nrows, int reps,
                                              int64_t stride, int wave, int nwaves, int lane64) {
@@ -252,7 +311,7 @@ __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E
     for (int k = 0; k < reps; ++k) {
         const int64_t b = base + k * stride;
         for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
-            rows_u<E, G, V, U, VEC>(in, out, b, cols, nrows, r0 + sub, step, lane);
+            rows_u<E, G, V, U, VEC, SHIFT>(in, out, b, cols, nrows, r0 + sub, step, lane);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int left = nrows - (r0 + u * step);
@@ -535,48 +594,56 @@ __device__ __forceinline__ void team_combine(float (&v)[U], int which, int wave,
     }
 }
 
-// Vectors past the row (or of an inactive row) read as `pad`.
-template <class E, int L>
-__device__ __forceinline__ void team_load(const typename E::T* src, int nvec, int first, int nt,
-                                          bool act, typename E::R* raw, float pad = kNegInf) {
+// Lane t's vectors t + c nt, c < L, of row rv; vectors past the row (or of an inactive row)
+// read as `pad`, and so do a shifted row's outside elements (after team_unpack).
+template <class E, int L, bool SHIFT>
+__device__ __forceinline__ void team_load(const typename E::T* in, const RowVecs<E, SHIFT>& rv,
+                                          int first, int nt, bool act, typename E::R* raw,
+                                          float pad = kNegInf) {
     constexpr int EPV = E::kEPV;
 #pragma unroll
     for (int c = 0; c < L; ++c) {
         const int vi = first + c * nt;
-        raw[c] = (act && vi < nvec) ? E::load_raw(src + vi * EPV) : E::raw_fill(pad);
+        raw[c] = (act && vi < rv.nv) ? E::load_raw(in + rv.start + vi * EPV) : E::raw_fill(pad);
     }
 }
 
-template <class E, int L>
-__device__ __forceinline__ void team_unpack(const typename E::R* raw, float* x) {
+template <class E, int L, bool SHIFT>
+__device__ __forceinline__ void team_unpack(const RowVecs<E, SHIFT>& rv, int first, int nt,
+                                            const typename E::R* raw, float* x,
+                                            float pad = kNegInf) {
 #pragma unroll
-    for (int c = 0; c < L; ++c) E::unpack(raw[c], x + c * E::kEPV);
+    for (int c = 0; c < L; ++c) {
+        E::unpack(raw[c], x + c * E::kEPV);
+        rv.mask(first + c * nt, x + c * E::kEPV, pad);
+    }
 }
 
-template <class E, int L>
-__device__ __forceinline__ void team_store(typename E::T* dst, int nvec, int first, int nt,
-                                           bool act, const float* y) {
-    constexpr int EPV = E::kEPV;
+template <class E, int L, bool SHIFT>
+__device__ __forceinline__ void team_store(typename E::T* out, const RowVecs<E, SHIFT>& rv,
+                                           int first, int nt, bool act, const float* y) {
 #pragma unroll
     for (int c = 0; c < L; ++c) {
         const int vi = first + c * nt;
-        if (act && vi < nvec) E::store_vec(dst + vi * EPV, y + c * EPV);
+        if (act && vi < rv.nv) rv.store(out, vi, y + c * E::kEPV);
     }
 }
 
 // Up to U rows (those with act[u], starting at elements off[u]) held in registers: L vectors
 // per lane cover nt * L vectors of a row.  A row's arithmetic does not depend on U.
-template <class E, int L, int U>
+template <class E, int L, int U, bool SHIFT>
 __device__ __forceinline__ void team_rows(const typename E::T* in, typename E::T* out,
-                                          const int64_t (&off)[U], const bool (&act)[U], int nvec,
+                                          const int64_t (&off)[U], const bool (&act)[U], int cols,
                                           int t, int nt, int wave, int nwaves, int lane) {
     constexpr int K = L * E::kEPV;
     float x[U][K];
     typename E::R raw[U][L];
 #pragma unroll
-    for (int u = 0; u < U; ++u) team_load<E, L>(in + off[u], nvec, t, nt, act[u], raw[u]);
+    for (int u = 0; u < U; ++u)
+        team_load<E, L, SHIFT>(in, RowVecs<E, SHIFT>(off[u], cols), t, nt, act[u], raw[u]);
 #pragma unroll
-    for (int u = 0; u < U; ++u) team_unpack<E, L>(raw[u], x[u]);
+    for (int u = 0; u < U; ++u)
+        team_unpack<E, L, SHIFT>(RowVecs<E, SHIFT>(off[u], cols), t, nt, raw[u], x[u]);
     float m[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) m[u] = group_reduce<64, OpMax>(lane_reduce<K, OpMax>(x[u]));
@@ -595,12 +662,10 @@ __device__ __forceinline__ void team_rows(const typename E::T* in, typename E::T
         const float inv = (s[u] == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(s[u]);
 #pragma unroll
         for (int k = 0; k < K; ++k) x[u][k] *= inv;
-        team_store<E, L>(out + off[u], nvec, t, nt, act[u], x[u]);
+        team_store<E, L, SHIFT>(out, RowVecs<E, SHIFT>(off[u], cols), t, nt, act[u], x[u]);
     }
 }
 
-// The rows of an item, reps ranges of nrows rows, as one sequence j = 0, 1, ... (U at a time,
-// across ranges: a balanced table often gives long rows as ranges of one row).
 // The trace counts row j of an item's sequence for wave j mod nwaves.
 __device__ __forceinline__ uint32_t team_rows_of_wave(int nrows, int reps, int wave, int nwaves) {
     const int64_t total = static_cast<int64_t>(nrows) * reps;
@@ -631,17 +696,18 @@ struct RowWalk {
 };
 
 // A row longer than nt * L vectors: chunks of nt * L vectors, read twice.
-template <class E, int L>
-__device__ __forceinline__ void team_row_two_pass(const typename E::T* src, typename E::T* dst,
-                                                  int nvec, int t, int nt, int wave, int nwaves,
-                                                  int lane) {
+template <class E, int L, bool SHIFT>
+__device__ __forceinline__ void team_row_two_pass(const typename E::T* in, typename E::T* out,
+                                                  int64_t off, int cols, int t, int nt, int wave,
+                                                  int nwaves, int lane) {
     constexpr int K = L * E::kEPV;
+    const RowVecs<E, SHIFT> rv(off, cols);
     float m = kNegInf, s = 0.0f;
-    for (int first = t; first - t < nvec; first += nt * L) {
+    for (int first = t; first - t < rv.nv; first += nt * L) {
         float x[K];
         typename E::R raw[L];
-        team_load<E, L>(src, nvec, first, nt, true, raw);
-        team_unpack<E, L>(raw, x);
+        team_load<E, L, SHIFT>(in, rv, first, nt, true, raw);
+        team_unpack<E, L, SHIFT>(rv, first, nt, raw, x);
         const float cm = lane_reduce<K, OpMax>(x);
         if (cm > m) {
             s *= __builtin_amdgcn_exp2f((m - cm) * kLog2e);
@@ -660,14 +726,14 @@ __device__ __forceinline__ void team_row_two_pass(const typename E::T* src, type
     float S[1] = {group_reduce<64, OpAdd>(s * scale)};
     team_combine<OpAdd, 1>(S, 1, wave, nwaves, lane);
     const float inv = (S[0] == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S[0]);
-    for (int first = t; first - t < nvec; first += nt * L) {
+    for (int first = t; first - t < rv.nv; first += nt * L) {
         float x[K];
         typename E::R raw[L];
-        team_load<E, L>(src, nvec, first, nt, true, raw);
-        team_unpack<E, L>(raw, x);
+        team_load<E, L, SHIFT>(in, rv, first, nt, true, raw);
+        team_unpack<E, L, SHIFT>(rv, first, nt, raw, x);
 #pragma unroll
         for (int k = 0; k < K; ++k) x[k] = __builtin_amdgcn_exp2f((x[k] - Ms) * kLog2e) * inv;
-        team_store<E, L>(dst, nvec, first, nt, true, x);
+        team_store<E, L, SHIFT>(out, rv, first, nt, true, x);
     }
 }
 
@@ -678,15 +744,13 @@ constexpr int kTeamMaxL = (KCLASS >= 5 ? 2 : 1) * bsm::kTeamValues / E::kEPV;
 
 // Every row of an item, each by the whole workgroup.  The trace counts row r for wave
 // r mod nwaves.
-template <class E, int KCLASS>
+template <class E, int KCLASS, bool SHIFT>
 __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename E::T* out,
                                               int64_t base, int cols, int nrows, int reps,
                                               int64_t stride, int wave, int nwaves, int lane) {
-    constexpr int EPV = E::kEPV;
-    const int nvec = cols / EPV;
     const int nt = nwaves * 64;
     const int t = wave * 64 + lane;
-    const int per_lane = (nvec + nt - 1) / nt;
+    const int per_lane = (span_vecs<E, SHIFT>(cols) + nt - 1) / nt;
     constexpr int kMaxL = kTeamMaxL<E, KCLASS>;  // 4 or 8 (class 4), 8 or 16 (class 5)
     // two rows of 4 vectors per lane in flight where that is within kTeamValues values (fp32)
     constexpr bool kPair = 2 * 4 * E::kEPV <= bsm::kTeamValues;
@@ -699,7 +763,7 @@ __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename 
             int64_t off[2];
             bool act[2];
             w.next(off, act);
-            team_rows<E, 4, 2>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+            team_rows<E, 4, 2, SHIFT>(in, out, off, act, cols, t, nt, wave, nwaves, lane);
         }
     } else if (per_lane <= kMaxL) {
         RowWalk<1> w(base, cols, nrows, reps, stride);
@@ -708,12 +772,12 @@ __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename 
             bool act[1];
             w.next(off, act);
             if (per_lane <= 4)
-                team_rows<E, 4, 1>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+                team_rows<E, 4, 1, SHIFT>(in, out, off, act, cols, t, nt, wave, nwaves, lane);
             else if (kMaxL > 8 && per_lane <= 8)
-                team_rows<E, (kMaxL > 8 ? 8 : kMaxL), 1>(in, out, off, act, nvec, t, nt, wave,
-                                                         nwaves, lane);
+                team_rows<E, (kMaxL > 8 ? 8 : kMaxL), 1, SHIFT>(in, out, off, act, cols, t, nt,
+                                                                wave, nwaves, lane);
             else
-                team_rows<E, kMaxL, 1>(in, out, off, act, nvec, t, nt, wave, nwaves, lane);
+                team_rows<E, kMaxL, 1, SHIFT>(in, out, off, act, cols, t, nt, wave, nwaves, lane);
         }
     } else {
         RowWalk<1> w(base, cols, nrows, reps, stride);
@@ -721,27 +785,32 @@ __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename 
             int64_t off[1];
             bool act[1];
             w.next(off, act);
-            team_row_two_pass<E, kMaxL>(in + off[0], out + off[0], nvec, t, nt, wave, nwaves,
-                                        lane);
+            team_row_two_pass<E, kMaxL, SHIFT>(in, out, off[0], cols, t, nt, wave, nwaves, lane);
         }
     }
     return team_rows_of_wave(nrows, reps, wave, nwaves);
 }
 
-// Register-tile choice per item (wave-uniform branch); the thresholds are bsm::tile_for's.
-template <class E, int KCLASS, bool VEC>
+// Vectors the largest register tile of a kernel class covers (classes 4 and 5: any row).
+template <int KCLASS>
+constexpr int kClassMaxVecs = KCLASS == 0 ? 64 : KCLASS == 1 ? 128 : KCLASS == 2 ? 256
+                              : KCLASS == 3 ? 512 : 0x7FFFFFFF;
+
+// Register-tile choice per item (wave-uniform branch); the thresholds are bsm::tile_for's.  A
+// shifted item's tile covers the vectors its rows may span (one more than their length).
+template <class E, int KCLASS, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typename E::T* out,
                                                   int64_t base, int cols, int nrows, int reps,
                                                   int64_t stride, int wave, int nwaves,
                                                   int lane64, float* lds, int cap, bool team) {
-    const int nvec = (cols + E::kEPV - 1) / E::kEPV;
-#define BSM_RUN(G, V) run_item<E, G, V, VEC>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    const int nvec = VEC ? span_vecs<E, SHIFT>(cols) : (cols + E::kEPV - 1) / E::kEPV;
+#define BSM_RUN(G, V) run_item<E, G, V, VEC, SHIFT>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     if (nvec <= 16) return BSM_RUN(16, 1);
     if (nvec <= 32) return BSM_RUN(32, 1);
-    // Larger register tiles only for aligned rows; unaligned longer rows take the two-pass path.
-    // Rows of 33..64 vectors: 32 lanes x 2 vectors rather than 64 x 1 (a shorter butterfly and
-    // half the per-row work per value: +7% on 384 x 512 x 512 bf16); the host gives such rows
-    // kernel class 1, so the tile depends on the row length only.
+    // Larger register tiles only for 16-byte vectors; longer element-wise rows take the one-wave
+    // path.  Rows of 33..64 vectors: 32 lanes x 2 vectors rather than 64 x 1 (a shorter
+    // butterfly and half the per-row work per value: +7% on 384 x 512 x 512 bf16); the host
+    // gives such rows kernel class 1, so the tile depends on the row length only.
     if constexpr (VEC && KCLASS >= 1) {
         if (nvec <= 64) return BSM_RUN(32, 2);
         if (nvec <= 128) return BSM_RUN(64, 2);
@@ -757,21 +826,22 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
     if constexpr (VEC && KCLASS >= 4) {
         // the host gives long-row plans workgroup workers (team != 0): the waves share each row
         if (team)
-            return team_item<E, KCLASS>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64);
+            return team_item<E, KCLASS, SHIFT>(in, out, base, cols, nrows, reps, stride, wave,
+                                               nwaves, lane64);
     }
     if constexpr (!VEC || KCLASS >= 4) {
         uint32_t done = 0;
         for (int k = 0; k < reps; ++k) {
             for (int r = wave; r < nrows; r += nwaves) {
                 const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
-                // only the long-row class is launched with LDS to stage rows in
-                long_row<E, VEC, (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
+                // only the long-row classes are launched with LDS to stage rows in
+                long_row<E, (VEC && !SHIFT), (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
                 ++done;
             }
         }
         return done;
     }
-    return 0;  // unreachable: the host picks a class that covers the plan's longest row
+    return 0;  // unreachable: the item's access path is chosen so that its class covers it
 }
 
 // ------------------------------------------------------------------------------- backward
@@ -782,7 +852,7 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
 // input streams: half as many rows per group in flight, and tiles up to 4 vectors per lane
 // (longer rows take the long-row path).
 
-template <class E, int G, int V, int U, bool VEC>
+template <class E, int G, int V, int U, bool VEC, bool SHIFT = false>
 __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typename E::T* dy,
                                            typename E::T* dx, int64_t base, int cols, int nrows,
                                            int r0, int step, int lane) {
@@ -797,13 +867,13 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
         act[u] = r < nrows;
         const int64_t o = base + static_cast<int64_t>(r) * cols;
         if constexpr (VEC) {
-            const int nvec = cols / EPV;
+            const RowVecs<E, SHIFT> rv(o, cols);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
-                if (act[u] && vi < nvec) {
-                    ra[u][v] = E::load_raw(y + o + vi * EPV);
-                    rg[u][v] = E::load_raw(dy + o + vi * EPV);
+                if (act[u] && vi < rv.nv) {
+                    ra[u][v] = E::load_raw(y + rv.start + vi * EPV);
+                    rg[u][v] = E::load_raw(dy + rv.start + vi * EPV);
                 } else {
                     ra[u][v] = rg[u][v] = E::raw_fill(0.0f);
                 }
@@ -818,14 +888,18 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
             }
         }
     }
-    if constexpr (VEC) {  // unpacked after every load is issued
+    if constexpr (VEC) {  // unpacked after every load is issued; outside elements are 0
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; ++u) {
+            const RowVecs<E, SHIFT> rv(base + static_cast<int64_t>(r0 + u * step) * cols, cols);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 E::unpack(ra[u][v], &a[u][v * EPV]);
                 E::unpack(rg[u][v], &g[u][v * EPV]);
+                rv.mask(lane + v * G, &a[u][v * EPV], 0.0f);
+                rv.mask(lane + v * G, &g[u][v * EPV], 0.0f);
             }
+        }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -836,25 +910,25 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
 #pragma unroll
         for (int k = 0; k < K; ++k) a[u][k] = a[u][k] * (g[u][k] - d);
         const int r = r0 + u * step;
-        typename E::T* dst = dx + base + static_cast<int64_t>(r) * cols;
+        const int64_t o = base + static_cast<int64_t>(r) * cols;
         if constexpr (VEC) {
-            const int nvec = cols / EPV;
+            const RowVecs<E, SHIFT> rv(o, cols);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int vi = lane + v * G;
-                if (act[u] && vi < nvec) E::store_vec(dst + vi * EPV, &a[u][v * EPV]);
+                if (act[u] && vi < rv.nv) rv.store(dx, vi, &a[u][v * EPV]);
             }
         } else {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const int j = lane + k * G;
-                if (act[u] && j < cols) E::store1(dst + j, a[u][k]);
+                if (act[u] && j < cols) E::store1(dx + o + j, a[u][k]);
             }
         }
     }
 }
 
-template <class E, int G, int V, bool VEC>
+template <class E, int G, int V, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t run_item_bwd(const typename E::T* y, const typename E::T* dy,
                                                  typename E::T* dx, int64_t base, int cols,
                                                  int nrows, int reps, int64_t stride, int wave,
@@ -869,7 +943,7 @@ __device__ __forceinline__ uint32_t run_item_bwd(const typename E::T* y, const t
     for (int k = 0; k < reps; ++k) {
         const int64_t b = base + k * stride;
         for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
-            rows_u_bwd<E, G, V, U, VEC>(y, dy, dx, b, cols, nrows, r0 + sub, step, lane);
+            rows_u_bwd<E, G, V, U, VEC, SHIFT>(y, dy, dx, b, cols, nrows, r0 + sub, step, lane);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int left = nrows - (r0 + u * step);
@@ -926,24 +1000,26 @@ __device__ __forceinline__ void long_row_bwd(const typename E::T* y, const typen
 // in team_rows: y and dy held in registers, d = sum dy * y formed by the in-lane tree, the
 // wave's butterfly and the waves' values in wave order; one barrier per rows, alternating the
 // slot set (`which`), so a set is rewritten only after every wave has passed the next barrier.
-template <class E, int L, int U>
+template <class E, int L, int U, bool SHIFT>
 __device__ __forceinline__ void team_rows_bwd(const typename E::T* y, const typename E::T* dy,
                                               typename E::T* dx, const int64_t (&off)[U],
-                                              const bool (&act)[U], int nvec, int t, int nt,
+                                              const bool (&act)[U], int cols, int t, int nt,
                                               int wave, int nwaves, int lane, int which) {
     constexpr int K = L * E::kEPV;
     float a[U][K], g[U][K];
     typename E::R ra[U][L], rg[U][L];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        team_load<E, L>(y + off[u], nvec, t, nt, act[u], ra[u], 0.0f);  // padding: products 0
-        team_load<E, L>(dy + off[u], nvec, t, nt, act[u], rg[u], 0.0f);
+        const RowVecs<E, SHIFT> rv(off[u], cols);
+        team_load<E, L, SHIFT>(y, rv, t, nt, act[u], ra[u], 0.0f);  // padding: products 0
+        team_load<E, L, SHIFT>(dy, rv, t, nt, act[u], rg[u], 0.0f);
     }
     float d[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        team_unpack<E, L>(ra[u], a[u]);
-        team_unpack<E, L>(rg[u], g[u]);
+        const RowVecs<E, SHIFT> rv(off[u], cols);
+        team_unpack<E, L, SHIFT>(rv, t, nt, ra[u], a[u], 0.0f);
+        team_unpack<E, L, SHIFT>(rv, t, nt, rg[u], g[u], 0.0f);
         float p[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) p[k] = a[u][k] * g[u][k];
@@ -954,53 +1030,53 @@ __device__ __forceinline__ void team_rows_bwd(const typename E::T* y, const type
     for (int u = 0; u < U; ++u) {
 #pragma unroll
         for (int k = 0; k < K; ++k) a[u][k] = a[u][k] * (g[u][k] - d[u]);
-        team_store<E, L>(dx + off[u], nvec, t, nt, act[u], a[u]);
+        team_store<E, L, SHIFT>(dx, RowVecs<E, SHIFT>(off[u], cols), t, nt, act[u], a[u]);
     }
 }
 
 // A backward row longer than nt * L vectors: d over chunks, then y and dy read again.
-template <class E, int L>
+template <class E, int L, bool SHIFT>
 __device__ __forceinline__ void team_row_bwd_two_pass(const typename E::T* y,
                                                       const typename E::T* dy, typename E::T* dx,
-                                                      int nvec, int t, int nt, int wave,
-                                                      int nwaves, int lane, int which) {
+                                                      int64_t off, int cols, int t, int nt,
+                                                      int wave, int nwaves, int lane, int which) {
     constexpr int K = L * E::kEPV;
+    const RowVecs<E, SHIFT> rv(off, cols);
     float s = 0.0f;
-    for (int first = t; first - t < nvec; first += nt * L) {
+    for (int first = t; first - t < rv.nv; first += nt * L) {
         float a[K], g[K];
         typename E::R ra[L], rg[L];
-        team_load<E, L>(y, nvec, first, nt, true, ra, 0.0f);
-        team_load<E, L>(dy, nvec, first, nt, true, rg, 0.0f);
-        team_unpack<E, L>(ra, a);
-        team_unpack<E, L>(rg, g);
+        team_load<E, L, SHIFT>(y, rv, first, nt, true, ra, 0.0f);
+        team_load<E, L, SHIFT>(dy, rv, first, nt, true, rg, 0.0f);
+        team_unpack<E, L, SHIFT>(rv, first, nt, ra, a, 0.0f);
+        team_unpack<E, L, SHIFT>(rv, first, nt, rg, g, 0.0f);
 #pragma unroll
         for (int k = 0; k < K; ++k) g[k] *= a[k];
         s += lane_reduce<K, OpAdd>(g);
     }
     float d[1] = {group_reduce<64, OpAdd>(s)};
     team_combine<OpAdd, 1>(d, which, wave, nwaves, lane);
-    for (int first = t; first - t < nvec; first += nt * L) {
+    for (int first = t; first - t < rv.nv; first += nt * L) {
         float a[K], g[K];
         typename E::R ra[L], rg[L];
-        team_load<E, L>(y, nvec, first, nt, true, ra, 0.0f);
-        team_load<E, L>(dy, nvec, first, nt, true, rg, 0.0f);
-        team_unpack<E, L>(ra, a);
-        team_unpack<E, L>(rg, g);
+        team_load<E, L, SHIFT>(y, rv, first, nt, true, ra, 0.0f);
+        team_load<E, L, SHIFT>(dy, rv, first, nt, true, rg, 0.0f);
+        team_unpack<E, L, SHIFT>(rv, first, nt, ra, a, 0.0f);
+        team_unpack<E, L, SHIFT>(rv, first, nt, rg, g, 0.0f);
 #pragma unroll
         for (int k = 0; k < K; ++k) a[k] = a[k] * (g[k] - d[0]);
-        team_store<E, L>(dx, nvec, first, nt, true, a);
+        team_store<E, L, SHIFT>(dx, rv, first, nt, true, a);
     }
 }
 
-template <class E, int KCLASS>
+template <class E, int KCLASS, bool SHIFT>
 __device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const typename E::T* dy,
                                                   typename E::T* dx, int64_t base, int cols,
                                                   int nrows, int reps, int64_t stride, int wave,
                                                   int nwaves, int lane) {
-    const int nvec = cols / E::kEPV;
     const int nt = nwaves * 64;
     const int t = wave * 64 + lane;
-    const int per_lane = (nvec + nt - 1) / nt;
+    const int per_lane = (span_vecs<E, SHIFT>(cols) + nt - 1) / nt;
     constexpr int kMaxL = kTeamMaxL<E, KCLASS>;  // vectors per lane and stream
     constexpr bool kPair = 2 * 4 * E::kEPV <= bsm::kTeamValues;  // as in team_item
     int which = 0;
@@ -1010,7 +1086,8 @@ __device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const 
             int64_t off[2];
             bool act[2];
             w.next(off, act);
-            team_rows_bwd<E, 4, 2>(y, dy, dx, off, act, nvec, t, nt, wave, nwaves, lane, which);
+            team_rows_bwd<E, 4, 2, SHIFT>(y, dy, dx, off, act, cols, t, nt, wave, nwaves, lane,
+                                          which);
             which ^= 1;
         }
     } else if (per_lane <= kMaxL) {
@@ -1019,8 +1096,8 @@ __device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const 
             int64_t off[1];
             bool act[1];
             w.next(off, act);
-            team_rows_bwd<E, kMaxL, 1>(y, dy, dx, off, act, nvec, t, nt, wave, nwaves, lane,
-                                       which);
+            team_rows_bwd<E, kMaxL, 1, SHIFT>(y, dy, dx, off, act, cols, t, nt, wave, nwaves,
+                                              lane, which);
             which ^= 1;
         }
     } else {
@@ -1029,28 +1106,117 @@ __device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const 
             int64_t off[1];
             bool act[1];
             w.next(off, act);
-            team_row_bwd_two_pass<E, kMaxL>(y + off[0], dy + off[0], dx + off[0], nvec, t, nt,
-                                            wave, nwaves, lane, which);
+            team_row_bwd_two_pass<E, kMaxL, SHIFT>(y, dy, dx, off[0], cols, t, nt, wave, nwaves,
+                                                   lane, which);
             which ^= 1;
         }
     }
     return team_rows_of_wave(nrows, reps, wave, nwaves);
 }
 
-template <class E, int KCLASS, bool VEC>
+// long_row_bwd for a shifted row: the same two passes over the vectors that cover it (outside
+// elements read as 0, never written), staged when both streams' vectors fit the wave's LDS
+// region.
+template <class E, bool STAGE>
+__device__ __forceinline__ void long_row_bwd_shift(const typename E::T* y, const typename E::T* dy,
+                                                   typename E::T* dx, int64_t o, int cols,
+                                                   int lane, float* lds, int cap) {
+    constexpr int EPV = E::kEPV;
+    constexpr int CH = 16 / EPV;  // vectors per lane and stream per chunk (16 values)
+    constexpr int K = CH * EPV;
+    const RowVecs<E, true> rv(o, cols);
+    const int n = rv.nv;
+    const int span = n * EPV;  // floats of one stream staged
+    const bool stage = STAGE && 2 * span <= cap;
+    float s = 0.0f;
+    for (int first = lane; first < n; first += CH * 64) {
+        float a[K], g[K];
+        typename E::R ra[CH], rg[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int vi = first + c * 64;
+            ra[c] = vi < n ? E::load_raw(y + rv.start + vi * EPV) : E::raw_fill(0.0f);
+            rg[c] = vi < n ? E::load_raw(dy + rv.start + vi * EPV) : E::raw_fill(0.0f);
+        }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int vi = first + c * 64;
+            E::unpack(ra[c], a + c * EPV);
+            E::unpack(rg[c], g + c * EPV);
+            rv.mask(vi, a + c * EPV, 0.0f);
+            rv.mask(vi, g + c * EPV, 0.0f);
+            if (stage && vi < n) {
+#pragma unroll
+                for (int i = 0; i < EPV; i += 4) {
+                    *reinterpret_cast<f32x4*>(lds + vi * EPV + i) =
+                        f32x4{a[c * EPV + i], a[c * EPV + i + 1], a[c * EPV + i + 2], a[c * EPV + i + 3]};
+                    *reinterpret_cast<f32x4*>(lds + span + vi * EPV + i) =
+                        f32x4{g[c * EPV + i], g[c * EPV + i + 1], g[c * EPV + i + 2], g[c * EPV + i + 3]};
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) g[k] *= a[k];
+        s += lane_reduce<K, OpAdd>(g);
+    }
+    const float d = group_reduce<64, OpAdd>(s);
+    for (int first = lane; first < n; first += CH * 64) {
+        float a[K], g[K];
+        if (stage) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+#pragma unroll
+                for (int i = 0; i < EPV; i += 4) {
+                    f32x4 va = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, vg = va;
+                    if (vi < n) {
+                        va = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
+                        vg = *reinterpret_cast<const f32x4*>(lds + span + vi * EPV + i);
+                    }
+                    a[c * EPV + i] = va.x; a[c * EPV + i + 1] = va.y;
+                    a[c * EPV + i + 2] = va.z; a[c * EPV + i + 3] = va.w;
+                    g[c * EPV + i] = vg.x; g[c * EPV + i + 1] = vg.y;
+                    g[c * EPV + i + 2] = vg.z; g[c * EPV + i + 3] = vg.w;
+                }
+            }
+        } else {
+            typename E::R ra[CH], rg[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int vi = first + c * 64;
+                ra[c] = vi < n ? E::load_raw(y + rv.start + vi * EPV) : E::raw_fill(0.0f);
+                rg[c] = vi < n ? E::load_raw(dy + rv.start + vi * EPV) : E::raw_fill(0.0f);
+            }
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                E::unpack(ra[c], a + c * EPV);
+                E::unpack(rg[c], g + c * EPV);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) a[k] = a[k] * (g[k] - d);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int vi = first + c * 64;
+            if (vi < n) rv.store(dx, vi, a + c * EPV);
+        }
+    }
+}
+
+template <class E, int KCLASS, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
                                                       const typename E::T* dy, typename E::T* dx,
                                                       int64_t base, int cols, int nrows, int reps,
                                                       int64_t stride, int wave, int nwaves,
                                                       int lane64, float* lds, int cap, bool team) {
-    const int nvec = (cols + E::kEPV - 1) / E::kEPV;
+    const int nvec = VEC ? span_vecs<E, SHIFT>(cols) : (cols + E::kEPV - 1) / E::kEPV;
     if constexpr (VEC && KCLASS >= 4) {
         // rows beyond the forward register tile: the workgroup's waves share each row
         if (team && nvec > 512)
-            return team_item_bwd<E, KCLASS>(y, dy, dx, base, cols, nrows, reps, stride, wave,
-                                            nwaves, lane64);
+            return team_item_bwd<E, KCLASS, SHIFT>(y, dy, dx, base, cols, nrows, reps, stride,
+                                                   wave, nwaves, lane64);
     }
-#define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+#define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC, SHIFT>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
     // (Rows of 33..64 vectors keep 64 lanes x 1 vector here: with two input streams the
     // forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x 512 bf16.)
     if (nvec <= 16) return BSM_RUN_BWD(16, 1);
@@ -1068,19 +1234,23 @@ __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
         for (int k = 0; k < reps; ++k) {
             for (int r = wave; r < nrows; r += nwaves) {
                 const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
-                long_row_bwd<E, VEC, (KCLASS >= 4)>(y + o, dy + o, dx + o, cols, lane64, lds, cap);
+                if constexpr (VEC && SHIFT)
+                    long_row_bwd_shift<E, (KCLASS >= 4)>(y, dy, dx, o, cols, lane64, lds, cap);
+                else
+                    long_row_bwd<E, VEC, (KCLASS >= 4)>(y + o, dy + o, dx + o, cols, lane64, lds,
+                                                        cap);
                 ++done;
             }
         }
         return done;
     }
-    return 0;  // unreachable: the host picks a class that covers the plan's longest row
+    return 0;  // unreachable: the item's access path is chosen so that its class covers it
 }
 
 // Worker w of the table is workgroup w (all its waves share each item) or, when per_wave is
 // set, wave (w * waves_per_workgroup + wave), which then runs its own items alone.  BWD selects
 // the backward op (a = y, b = dy, out = dx); the forward op reads a only.
-template <class E, int KCLASS, bool BWD>
+template <class E, int KCLASS, bool BWD, bool SHIFTED>
 __device__ __forceinline__ void worker_loop(const typename E::T* a, const typename E::T* b,
                                             typename E::T* out, const int32_t* __restrict__ worker_ptr,
                                             const bsm_item* __restrict__ items, int base_aligned,
@@ -1104,27 +1274,32 @@ __device__ __forceinline__ void worker_loop(const typename E::T* a, const typena
         const int nrows = items[i].nrows;
         const int reps = items[i].reps;
         const int64_t stride = static_cast<int64_t>(items[i].rep_stride) * cols;
-        const bool vec = base_aligned && ((base * E::kBytes) & 15) == 0 &&
-                         ((static_cast<int64_t>(cols) * E::kBytes) & 15) == 0;
+        // Access path: whole 16-byte vectors when every row of the item starts and ends on
+        // one; shifted vectors when the buffers are aligned but the rows are not (in the
+        // instances for plans with such slices, SHIFTED, and as long as the kernel class has a
+        // tile or path for the extra vector); else element by element.
+        const bool rows_whole = ((base | static_cast<int64_t>(cols)) & (E::kEPV - 1)) == 0;
+        const int span = span_vecs<E, true>(cols);
+        const bool shift_fits = SHIFTED && (BWD ? (KCLASS >= 3 || span <= kClassMaxVecs<KCLASS>)
+                                                : span <= kClassMaxVecs<KCLASS>);
+        const int path = !base_aligned ? 0 : rows_whole ? 1 : shift_fits ? 2 : 0;
+#define BSM_ARGS_TAIL cols, nrows, reps, stride, my_wave, my_nwaves, lane64, lds, lds_floats_per_wave, !per_wave
         if constexpr (BWD) {
-            if (vec)
-                rows += dispatch_item_bwd<E, KCLASS, true>(a, b, out, base, cols, nrows, reps, stride,
-                                                           my_wave, my_nwaves, lane64, lds,
-                                                           lds_floats_per_wave, !per_wave);
+            if (path == 1)
+                rows += dispatch_item_bwd<E, KCLASS, true, false>(a, b, out, base, BSM_ARGS_TAIL);
+            else if (SHIFTED && path == 2)
+                rows += dispatch_item_bwd<E, KCLASS, true, SHIFTED>(a, b, out, base, BSM_ARGS_TAIL);
             else
-                rows += dispatch_item_bwd<E, KCLASS, false>(a, b, out, base, cols, nrows, reps, stride,
-                                                            my_wave, my_nwaves, lane64, lds,
-                                                            lds_floats_per_wave, !per_wave);
+                rows += dispatch_item_bwd<E, KCLASS, false, false>(a, b, out, base, BSM_ARGS_TAIL);
         } else {
-            if (vec)
-                rows += dispatch_item<E, KCLASS, true>(a, out, base, cols, nrows, reps, stride,
-                                                       my_wave, my_nwaves, lane64, lds,
-                                                       lds_floats_per_wave, !per_wave);
+            if (path == 1)
+                rows += dispatch_item<E, KCLASS, true, false>(a, out, base, BSM_ARGS_TAIL);
+            else if (SHIFTED && path == 2)
+                rows += dispatch_item<E, KCLASS, true, SHIFTED>(a, out, base, BSM_ARGS_TAIL);
             else
-                rows += dispatch_item<E, KCLASS, false>(a, out, base, cols, nrows, reps, stride,
-                                                        my_wave, my_nwaves, lane64, lds,
-                                                        lds_floats_per_wave, !per_wave);
+                rows += dispatch_item<E, KCLASS, false, false>(a, out, base, BSM_ARGS_TAIL);
         }
+#undef BSM_ARGS_TAIL
     }
     if (trace && lane64 == 0) {
         bsm_trace_rec rec;
@@ -1148,24 +1323,26 @@ constexpr int kMaxThreads = KCLASS >= 4 ? 256 : 1024;
 template <int KCLASS>
 constexpr int kMinWavesPerSimd = KCLASS >= 4 ? 2 : 1;
 
-template <class E, int KCLASS>
+// SHIFTED: the instance for plans with slices whose rows do not start and end on 16-byte
+// vectors (kept apart so that the other plans' instances carry none of its registers).
+template <class E, int KCLASS, bool SHIFTED>
 __global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
 bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
                    const bsm_item* __restrict__ items, int base_aligned, int per_wave,
                    int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
-    worker_loop<E, KCLASS, false>(in, nullptr, out, worker_ptr, items, base_aligned, per_wave,
-                                  lds_floats_per_wave, trace, bsm_lds);
+    worker_loop<E, KCLASS, false, SHIFTED>(in, nullptr, out, worker_ptr, items, base_aligned,
+                                           per_wave, lds_floats_per_wave, trace, bsm_lds);
 }
 
 // dx = softmax backward of (y, dy) under the same work table.
-template <class E, int KCLASS>
+template <class E, int KCLASS, bool SHIFTED>
 __global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
 bsm_softmax_bwd_kernel(const typename E::T* y, const typename E::T* dy, typename E::T* dx,
                        const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                        int base_aligned, int per_wave, int lds_floats_per_wave,
                        bsm_trace_rec* __restrict__ trace) {
-    worker_loop<E, KCLASS, true>(y, dy, dx, worker_ptr, items, base_aligned, per_wave,
-                                 lds_floats_per_wave, trace, bsm_lds);
+    worker_loop<E, KCLASS, true, SHIFTED>(y, dy, dx, worker_ptr, items, base_aligned, per_wave,
+                                          lds_floats_per_wave, trace, bsm_lds);
 }
 
 // Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the

@@ -11,8 +11,9 @@ import torch
 import oracle
 import paper_2002_07062_amd as bsm
 import workloads
-from gpu_util import (SENTINEL_BF16, SENTINEL_F32, compare, covered_mask, run_plan,
-                      sentinel_like, to_device, to_host_bits)
+from gpu_util import (SENTINEL_BF16, SENTINEL_F32, backward_inputs, compare, compare_backward,
+                      covered_mask, run_plan, run_plan_backward, sentinel_like, to_device,
+                      to_host_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -46,11 +47,12 @@ def test_ragged_odd_cols_with_gaps(dtype, schedule):
 
 # Rows beyond the register tile, by kernel class: 16-byte aligned rows first (each tile of the
 # workgroup-held path: two rows of <= 3 vectors per lane (fp32), 4, 8 or 16 vectors per lane,
-# and the two-pass path past 64 values per lane), an unaligned row last (element-wise, one
-# wave per row), so that every earlier slice starts 16-byte aligned.
+# and the two-pass path past 64 values per lane), an unaligned row last (shifted vectors; it
+# makes the plan count one more vector per row for its kernel class), so that every earlier
+# slice starts 16-byte aligned.
 LONG_COLS = {
-    ("f32", 4): [2052, 2500, 3072, 4096, 4100, 6000, 8192, 4095],
-    ("bf16", 4): [4104, 5000, 6144, 8192, 4200, 8000, 4097],
+    ("f32", 4): [2052, 2500, 3072, 4096, 4100, 6000, 8188, 4095],
+    ("bf16", 4): [4104, 5000, 6144, 8184, 4200, 8000, 4097],
     ("f32", 5): [8196, 12000, 16384, 16388, 40000, 100003],
     ("bf16", 5): [8200, 12000, 16384, 16392, 40000, 100003],
 }
@@ -178,6 +180,46 @@ def test_unaligned_base_pointer(shift):
     out_t, _ = run_plan(w, "xcd", x=x, out=out)
     ref = oracle.softmax(w.x, "f32", w.offsets[:-1], w.rows, w.cols)
     compare(to_host_bits(out_t), ref, "f32")
+
+
+# Rows whose start or length is not a whole number of 16-byte vectors (aligned buffers): read
+# as the aligned vectors that cover them, outside elements masked, the first and last vectors
+# stored element by element.  Contiguous rows then share their boundary vectors.
+SHIFTED_COLS = [1, 2, 3, 5, 7, 9, 13, 30, 77, 129, 333, 1001, 2047, 2051, 4097, 8193, 12001]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_shifted_rows_all_schedules_in_place(dtype):
+    """Every width and every start phase (odd gaps): against the oracle, bytes outside the
+    slices untouched, the same bits under every schedule, in place equal to out of place, and
+    the backward pass against its oracle."""
+    rng = np.random.default_rng(31)
+    rows = [int(r) for r in rng.integers(1, 12, size=len(SHIFTED_COLS))]
+    w = workloads.custom(rows, SHIFTED_COLS, dtype=dtype, sigma=3.0, seed=32, gap=1, base=3)
+    x = to_device(w.x, dtype)
+    results = []
+    for schedule in SCHEDULES:
+        print(f"[shifted {dtype} {schedule}]", flush=True)
+        bits, st = _check_ragged(w, schedule)
+        results.append(bits)
+    assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
+    y = x.clone()
+    run_plan(w, "balanced", x=y, out=y)
+    n = int(w.offsets[-1])
+    mask = covered_mask(w.offsets[: w.batch], w.rows, w.cols, n)
+    assert np.array_equal(to_host_bits(y)[mask], results[0][mask])
+    assert np.array_equal(to_host_bits(y)[~mask], to_host_bits(x)[~mask])
+    yb, dyb = backward_inputs(w)
+    ref = oracle.softmax_backward(yb, dyb, dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=16)
+    first = None
+    for schedule in SCHEDULES:
+        dx, _ = run_plan_backward(w, to_device(yb, dtype), to_device(dyb, dtype), schedule)
+        bits = to_host_bits(dx)
+        compare_backward(bits, ref, yb, dyb, dtype, w.offsets[: w.batch], w.rows, w.cols, mask)
+        sentinel = SENTINEL_F32 if dtype == "f32" else SENTINEL_BF16
+        assert np.all(bits[:n][~mask] == sentinel), "a byte outside every slice was written"
+        first = bits if first is None else first
+        assert np.array_equal(bits, first), schedule
 
 
 def test_in_place_equals_out_of_place():
