@@ -184,7 +184,10 @@ typedef struct bsm_plan_s* bsm_plan;
  *                  and slice s starts at element s*R*C.  Otherwise [batch] element offsets:
  *                  slice s occupies elements [slice_offsets[s], slice_offsets[s] + R_s*C_s).
  *                  Slices may sit in any order with gaps between them, but must not overlap;
- *                  gaps are never read or written.
+ *                  gaps are never written.  A row that starts or ends inside a 16-byte
+ *                  vector (buffers 16-byte aligned) is read as the aligned vectors that
+ *                  cover it: up to 15 bytes before and after it are read and ignored (a
+ *                  16-byte vector never crosses a page, so this cannot fault).
  *   rows, cols     [batch] (or [1] when uniform), each >= 0; an empty slice is skipped
  *   schedule       see bsm_schedule
  *   stream         hipStream_t as void*

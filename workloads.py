@@ -183,7 +183,7 @@ def custom(rows, cols, dtype=F32, sigma=1.0, seed=0, gap=0, base=0) -> Workload:
 
 def gradient(w: Workload, seed: int = 1000) -> np.ndarray:
     """Upstream gradient dy for the backward pass of workload `w`: N(0, 1) at every element of
-    `w.x` (gaps included, never read), in w's dtype (bf16 as raw bit patterns, rounded to
+    `w.x` (gaps included; their values never affect dx), in w's dtype (bf16 as raw bit patterns, rounded to
     nearest even). Drawn from its own seed so the forward inputs are unaffected."""
     rng = np.random.default_rng(seed)
     g = rng.standard_normal(w.x.shape[0], dtype=np.float32)
