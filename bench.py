@@ -632,6 +632,11 @@ def main() -> int:
             extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}
             r = run_backward(name, "balanced", args.steps, args.warmup)
             extra[f"{name}_backward_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step")}
+        # rows that do not start or end on a 16-byte vector (1001 fp32): shifted vectors
+        r, _ = run_workload("odd", "balanced", args.steps, args.warmup)
+        extra["odd_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}
+        r = run_backward("odd", "balanced", args.steps, args.warmup)
+        extra["odd_backward_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step")}
 
     head_trace = None if args.no_extra else trace_stats(w, args.schedule)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)

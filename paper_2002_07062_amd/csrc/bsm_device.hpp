@@ -1345,22 +1345,4 @@ bsm_softmax_bwd_kernel(const typename E::T* y, const typename E::T* dy, typename
                                           lds_floats_per_wave, trace, bsm_lds);
 }
 
-// Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the
-// whole grid sweeps one compact window (the fastest copy layout measured on MI355X); a byte
-// loop handles an unaligned remainder.
-__global__ void __launch_bounds__(256) bsm_copy_kernel(const u32x4* __restrict__ src,
-                                                       u32x4* __restrict__ dst, int64_t n_vec) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n_vec; i += stride)
-        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
-}
-
-__global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char* __restrict__ src,
-                                                             unsigned char* __restrict__ dst,
-                                                             int64_t n) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += stride)
-        dst[i] = src[i];
-}
-
 }  // namespace bsm_dev

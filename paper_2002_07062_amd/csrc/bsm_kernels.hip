@@ -1,37 +1,34 @@
-// Host launch wrappers of the persistent softmax and copy kernels (device code in
-// bsm_device.hpp).
+// Host launch wrappers of the persistent softmax kernels (device code in bsm_device.hpp,
+// instances in bsm_kernels_*.hip) and the streaming copy kernel, defined here.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 #include "bsm.h"
 #include "bsm_device.hpp"
+#include "bsm_kernel_set.hpp"
 #include "bsm_launch.hpp"
 
 namespace {
 
 using namespace bsm_dev;
 
-// The kernel instance for (element type, class, shifted), forward or backward.
-template <class E, bool SHIFTED>
-const void* softmax_fn(int kclass, bool bwd) {
-#define BSM_FN(K)                                                                               \
-    return bwd ? reinterpret_cast<const void*>(&bsm_softmax_bwd_kernel<E, K, SHIFTED>)          \
-               : reinterpret_cast<const void*>(&bsm_softmax_kernel<E, K, SHIFTED>)
-    switch (kclass) {
-        case 0: BSM_FN(0);
-        case 1: BSM_FN(1);
-        case 2: BSM_FN(2);
-        case 3: BSM_FN(3);
-        case 4: BSM_FN(4);
-        default: BSM_FN(5);
-    }
-#undef BSM_FN
+// Streaming copy, the bandwidth reference: nontemporal 16-byte accesses, grid-stride, so the
+// whole grid sweeps one compact window (the fastest copy layout measured on MI355X); a byte
+// loop handles an unaligned remainder.
+__global__ void __launch_bounds__(256) bsm_copy_kernel(const u32x4* __restrict__ src,
+                                                       u32x4* __restrict__ dst, int64_t n_vec) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n_vec; i += stride)
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
-template <class E>
-const void* softmax_fn(int kclass, bool shifted, bool bwd) {
-    return shifted ? softmax_fn<E, true>(kclass, bwd) : softmax_fn<E, false>(kclass, bwd);
+__global__ void __launch_bounds__(256) bsm_copy_bytes_kernel(const unsigned char* __restrict__ src,
+                                                             unsigned char* __restrict__ dst,
+                                                             int64_t n) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += stride)
+        dst[i] = src[i];
 }
 
 // Both ops take (a, [b,] out, worker_ptr, items, aligned, per_wave, lds_floats, trace); the
@@ -47,12 +44,13 @@ hipError_t launch_fn(const void* fn, bool bwd, const void* a, const void* b, voi
                            stream);
 }
 
+// The instances live in four sources (element type x access set) that compile in parallel.
 const void* fn_for(bsm_dtype dtype, bool temporal, int kclass, bool shifted, bool bwd) {
     if (dtype == BSM_BF16)
-        return temporal ? softmax_fn<BF16<false>>(kclass, shifted, bwd)
-                        : softmax_fn<BF16<true>>(kclass, shifted, bwd);
-    return temporal ? softmax_fn<F32<false>>(kclass, shifted, bwd)
-                    : softmax_fn<F32<true>>(kclass, shifted, bwd);
+        return shifted ? bsm::softmax_fn_bf16_shifted(kclass, temporal, bwd)
+                       : bsm::softmax_fn_bf16(kclass, temporal, bwd);
+    return shifted ? bsm::softmax_fn_f32_shifted(kclass, temporal, bwd)
+                   : bsm::softmax_fn_f32(kclass, temporal, bwd);
 }
 
 }  // namespace

@@ -1,0 +1,13 @@
+// Softmax kernel instances, fp32, for plans whose rows all start and end on 16-byte vectors
+// (and for any plan on buffers that are not 16-byte aligned).
+#include <hip/hip_runtime.h>
+
+#include "bsm_kernel_set.hpp"
+
+namespace bsm {
+
+const void* softmax_fn_f32(int kclass, bool temporal, bool bwd) {
+    return kernel_set<bsm_dev::F32, false>(kclass, temporal, bwd);
+}
+
+}  // namespace bsm

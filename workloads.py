@@ -63,6 +63,11 @@ SPECS = {
     "long_64x64x8192_f32": Spec(
         "long_64x64x8192_f32", 64, 64, 8192, F32, 3.0, 6,
         doc="64 slices x 64x8192 fp32, N(0,9): the longest rows of kernel class 4 (8 vectors per lane)"),
+    # rows that do not start or end on a 16-byte vector (shifted rows)
+    "odd_64x768x1001_f32": Spec(
+        "odd_64x768x1001_f32", 64, 768, 1001, F32, 3.0, 9,
+        doc="64 slices x 768x1001 fp32, N(0,9): every row starts at a different phase of the "
+            "16-byte vectors"),
     "long_32x64x16384_f32": Spec(
         "long_32x64x16384_f32", 32, 64, 16384, F32, 3.0, 8,
         doc="32 slices x 64x16384 fp32, N(0,9): the longest register-held rows (class 5, 16 vectors per lane)"),
@@ -72,7 +77,8 @@ SPECS = {
 ALIASES = {"c1": "c1_8x64x64_f32", "c2": "c2_384x512x512_f32",
            "c3": "c3_384x512x512_bf16_mask", "c4": "c4_16384x128x128_f32",
            "c5": "c5_384_ragged_f32", "long": "long_64x64x8192_f32",
-           "long4k": "long_128x64x4096_f32", "long16k": "long_32x64x16384_f32"}
+           "long4k": "long_128x64x4096_f32", "long16k": "long_32x64x16384_f32",
+           "odd": "odd_64x768x1001_f32"}
 
 
 @dataclasses.dataclass
