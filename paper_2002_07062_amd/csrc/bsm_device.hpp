@@ -752,9 +752,7 @@ __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename 
     const int t = wave * 64 + lane;
     const int per_lane = (span_vecs<E, SHIFT>(cols) + nt - 1) / nt;
     constexpr int kMaxL = kTeamMaxL<E, KCLASS>;  // 4 or 8 (class 4), 8 or 16 (class 5)
-    // two rows of 4 vectors per lane in flight where that is within kTeamValues values (fp32)
-    constexpr bool kPair = 2 * 4 * E::kEPV <= bsm::kTeamValues;
-    if (kPair && per_lane <= 3) {
+    if (per_lane <= 3) {
         // the shortest rows (at most 3 of the 4 vectors per lane): two in flight, so that a lane
         // keeps 5-6 loads outstanding (measured: 2500-element fp32 rows 5.7 TB/s against 4.9 one
         // at a time; rows filling 4 vectors per lane are 2% faster one at a time)
@@ -1111,6 +1109,9 @@ __device__ __forceinline__ uint32_t team_item_bwd(const typename E::T* y, const 
             which ^= 1;
         }
     }
+    // The next item starts again with slot set 0, which this item's last rows may have used:
+    // every wave has read its slots before any wave goes on.
+    __syncthreads();
     return team_rows_of_wave(nrows, reps, wave, nwaves);
 }
 

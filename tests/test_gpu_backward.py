@@ -91,6 +91,18 @@ def test_backward_long_rows(dtype, kclass):
         assert np.array_equal(bits, first), schedule
 
 
+@pytest.mark.parametrize("schedule", ["rr", "balanced"])
+def test_backward_consecutive_workgroup_items(schedule):
+    """Many slices of 3 rows of 6000 fp32 (one row at a time per workgroup, so a slice ends on
+    the slot set the next one starts with): a workgroup runs several such items back to back
+    (RR: slices s, s + 512, ...), against the oracle."""
+    w = workloads.custom([3] * 1100, [6000] * 1100, dtype="f32", sigma=3.0, seed=45)
+    y, dy = backward_inputs(w)
+    print(f"[backward consecutive items {schedule}]", flush=True)
+    _, st, _ = _check(w, schedule, y, dy)
+    assert st["kernel_class"] == 4 and st["n_wg"] < w.batch
+
+
 def test_backward_in_place_equals_out_of_place():
     w = workloads.generate("c5", batch=32)
     y, dy = backward_inputs(w)
