@@ -437,106 +437,49 @@ struct LongRow {
     __device__ __forceinline__ static int extent(int cols) { return VEC ? cols / EPV : cols; }
 };
 
-template <class E, bool VEC, bool STAGE>
+// Forward one-wave path: element by element (rows in buffers that are not 16-byte aligned;
+// aligned buffers take the register tiles, shifted vectors or the workgroup path).
+template <class E, bool STAGE>
 __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T* dst, int cols,
                                          int lane, float* lds, int cap) {
-    using L = LongRow<E, VEC>;
+    using L = LongRow<E, false>;
     constexpr int K = L::K;
-    const int n = L::extent(cols);
     const int step = L::kStep;
     if (STAGE && cols <= cap) {
-        // LDS holds the row as floats at their element index; aligned rows move whole 16-byte
-        // vectors (consecutive lanes on consecutive 16 bytes: no bank conflicts).
-        constexpr int EPV = E::kEPV;
+        // LDS holds the row as floats at their element index
         float m = kNegInf;
-        for (int first = lane; first < n; first += step) {
+        for (int first = lane; first < cols; first += step) {
             float x[K];
             L::load(src, cols, first, x);
             m = OpMax::f(m, lane_reduce<K, OpMax>(x));
-            if constexpr (VEC) {
-#pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-                    if (vi < n) {
-#pragma unroll
-                        for (int i = 0; i < EPV; i += 4)
-                            *reinterpret_cast<f32x4*>(lds + vi * EPV + i) =
-                                f32x4{x[c * EPV + i], x[c * EPV + i + 1], x[c * EPV + i + 2], x[c * EPV + i + 3]};
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    if (j < cols) lds[j] = x[k];
-                }
-            }
+            L::to_lds(lds, cols, first, x);
         }
         const float M = group_reduce<64, OpMax>(m);
         const float Ms = (M == kNegInf) ? 0.0f : M;
         float s = 0.0f;
-        for (int first = lane; first < n; first += step) {
+        for (int first = lane; first < cols; first += step) {
             float e[K];
-            if constexpr (VEC) {
 #pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-#pragma unroll
-                    for (int i = 0; i < EPV; i += 4) {
-                        f32x4 v = f32x4{kNegInf, kNegInf, kNegInf, kNegInf};
-                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
-                        v.x = __builtin_amdgcn_exp2f((v.x - Ms) * kLog2e);
-                        v.y = __builtin_amdgcn_exp2f((v.y - Ms) * kLog2e);
-                        v.z = __builtin_amdgcn_exp2f((v.z - Ms) * kLog2e);
-                        v.w = __builtin_amdgcn_exp2f((v.w - Ms) * kLog2e);
-                        e[c * EPV + i] = v.x;
-                        e[c * EPV + i + 1] = v.y;
-                        e[c * EPV + i + 2] = v.z;
-                        e[c * EPV + i + 3] = v.w;
-                        if (vi < n) *reinterpret_cast<f32x4*>(lds + vi * EPV + i) = v;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    e[k] = j < cols ? __builtin_amdgcn_exp2f((lds[j] - Ms) * kLog2e) : 0.0f;
-                    if (j < cols) lds[j] = e[k];
-                }
+            for (int k = 0; k < K; ++k) {
+                const int j = first + k * 64;
+                e[k] = j < cols ? __builtin_amdgcn_exp2f((lds[j] - Ms) * kLog2e) : 0.0f;
+                if (j < cols) lds[j] = e[k];
             }
             s += lane_reduce<K, OpAdd>(e);
         }
         const float S = group_reduce<64, OpAdd>(s);
         const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
-        for (int first = lane; first < n; first += step) {
+        for (int first = lane; first < cols; first += step) {
             float y[K];
-            if constexpr (VEC) {
+            L::from_lds(lds, cols, first, y, 0.0f);
 #pragma unroll
-                for (int c = 0; c < L::CH; ++c) {
-                    const int vi = first + c * 64;
-#pragma unroll
-                    for (int i = 0; i < EPV; i += 4) {
-                        f32x4 v = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                        if (vi < n) v = *reinterpret_cast<const f32x4*>(lds + vi * EPV + i);
-                        y[c * EPV + i] = v.x * inv;
-                        y[c * EPV + i + 1] = v.y * inv;
-                        y[c * EPV + i + 2] = v.z * inv;
-                        y[c * EPV + i + 3] = v.w * inv;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const int j = first + k * 64;
-                    y[k] = j < cols ? lds[j] * inv : 0.0f;
-                }
-            }
+            for (int k = 0; k < K; ++k) y[k] *= inv;
             L::store(dst, cols, first, y);
         }
         return;
     }
     float m = kNegInf, s = 0.0f;
-    for (int first = lane; first < n; first += step) {
+    for (int first = lane; first < cols; first += step) {
         float x[K];
         L::load(src, cols, first, x);
         const float cm = lane_reduce<K, OpMax>(x);
@@ -555,7 +498,7 @@ __device__ __forceinline__ void long_row(const typename E::T* src, typename E::T
     const float scale = (m == kNegInf) ? 0.0f : __builtin_amdgcn_exp2f((m - Ms) * kLog2e);
     const float S = group_reduce<64, OpAdd>(s * scale);
     const float inv = (S == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(S);
-    for (int first = lane; first < n; first += step) {
+    for (int first = lane; first < cols; first += step) {
         float x[K];
         L::load(src, cols, first, x);
 #pragma unroll
@@ -832,8 +775,10 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
         for (int k = 0; k < reps; ++k) {
             for (int r = wave; r < nrows; r += nwaves) {
                 const int64_t o = base + k * stride + static_cast<int64_t>(r) * cols;
-                // only the long-row classes are launched with LDS to stage rows in
-                long_row<E, (VEC && !SHIFT), (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
+                // element by element (an aligned item gets here only in a per-wave table of a
+                // long-row class, which the host never builds); only the long-row classes are
+                // launched with LDS to stage rows in
+                long_row<E, (KCLASS >= 4)>(in + o, out + o, cols, lane64, lds, cap);
                 ++done;
             }
         }
