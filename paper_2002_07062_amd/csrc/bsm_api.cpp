@@ -269,13 +269,13 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
         p->shifted = any_shifted(p->geo);
         p->kernel_class = bsm::kernel_class_for(p->geo.max_cols, elem_bytes_of(dtype), p->shifted);
-        // Rows beyond the register tile are worked by whole workgroups of kTeamThreads threads,
-        // one row at a time: such plans run that workgroup size whatever the topology asks (a
-        // row's bits depend on it), and every worker of their table is a workgroup.
+        // Rows beyond the register tile are worked by whole workgroups (team_threads of the
+        // class), one row at a time: such plans run that workgroup size whatever the topology
+        // asks (a row's bits depend on it), and every worker of their table is a workgroup.
         const bool team = !product && p->kernel_class >= kLongRowClass;
         if (team) {
             if (topology) tu = *topology;
-            tu.wg_threads = bsm::kTeamThreads;
+            tu.wg_threads = bsm::team_threads(p->kernel_class);
             topology = &tu;
         }
         bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, p->shifted,
@@ -294,9 +294,9 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
         if (team) {
             p->table.per_wave = false;
             p->table.stats.per_wave = 0;
-            p->table.stats.wg_threads = bsm::kTeamThreads;
+            p->table.stats.wg_threads = p->topo.wg_threads;
             p->table.stats.trace_bytes = static_cast<int64_t>(p->topo.n_wg()) *
-                                         (bsm::kTeamThreads / 64) *
+                                         (p->topo.wg_threads / 64) *
                                          static_cast<int64_t>(sizeof(bsm_trace_rec));
         }
     } catch (const std::bad_alloc&) {

@@ -683,7 +683,7 @@ __device__ __forceinline__ void team_row_two_pass(const typename E::T* in, typen
 // Vectors per lane (and per input stream) of a register-held row: bsm::kTeamValues values per
 // lane in kernel class 4, twice that in class 5.
 template <class E, int KCLASS>
-constexpr int kTeamMaxL = (KCLASS >= 5 ? 2 : 1) * bsm::kTeamValues / E::kEPV;
+constexpr int kTeamMaxL = (KCLASS >= 5 ? 2 : 1) * bsm::kTeamValues / E::kEPV;  // 6 as 5
 
 // Every row of an item, each by the whole workgroup.  The trace counts row r for wave
 // r mod nwaves.
@@ -1262,10 +1262,11 @@ __device__ __forceinline__ void worker_loop(const typename E::T* a, const typena
 
 extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
 
-// Launch bounds: any workgroup size up to 1024 threads; long-row plans (class 4) always run
-// 256-thread workgroups, two or more per CU, so their rows may hold up to 256 VGPRs per lane.
+// Launch bounds: any workgroup size up to 1024 threads; long-row plans run workgroups of
+// bsm::team_threads(class) threads (classes 4 and 5: 256, two or more per CU; class 6: 512, one
+// per CU), so their rows may hold up to 256 VGPRs per lane.
 template <int KCLASS>
-constexpr int kMaxThreads = KCLASS >= 4 ? 256 : 1024;
+constexpr int kMaxThreads = KCLASS >= 4 ? bsm::team_threads(KCLASS) : 1024;
 template <int KCLASS>
 constexpr int kMinWavesPerSimd = KCLASS >= 4 ? 2 : 1;
 

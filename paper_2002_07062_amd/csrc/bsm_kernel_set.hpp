@@ -18,7 +18,8 @@ const void* softmax_fn(int kclass, bool bwd) {
         case 2: BSM_FN(2);
         case 3: BSM_FN(3);
         case 4: BSM_FN(4);
-        default: BSM_FN(5);
+        case 5: BSM_FN(5);
+        default: BSM_FN(6);
     }
 #undef BSM_FN
 }

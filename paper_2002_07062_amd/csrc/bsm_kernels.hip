@@ -65,7 +65,9 @@ int kernel_class_for(int32_t max_cols, int elem_bytes, bool shifted) {
     if (nvec <= 256) return 2;
     if (nvec <= 512) return 3;
     // longer rows: workgroup-held, up to kTeamValues values per lane in class 4
-    return nvec * (kVecBytes / elem_bytes) <= kTeamThreads * kTeamValues ? 4 : 5;
+    const int64_t elems = nvec * (kVecBytes / elem_bytes);
+    if (elems <= kTeamThreads * kTeamValues) return 4;
+    return elems <= 2 * kTeamThreads * kTeamValues ? 5 : kLongestClass;
 }
 
 hipError_t launch_softmax(bsm_dtype dtype, int kernel_class, bool shifted, bool temporal,

@@ -28,12 +28,18 @@ constexpr Tile tile_for(int64_t nvec, int max_v) {
     return Tile{64, 0};
 }
 
-// Rows beyond the register tile are held in the registers of a whole workgroup of kTeamThreads
-// threads: up to kTeamValues values per lane in kernel class 4 (rows of up to
+// Rows beyond the register tile are held in the registers of a whole workgroup: kTeamThreads
+// threads with up to kTeamValues values per lane in kernel class 4 (rows of up to
 // kTeamThreads * kTeamValues elements), twice that in class 5, whose instances need twice the
-// registers.
+// registers, and in class 6 (longer rows) workgroups of 2 * kTeamThreads threads with twice
+// the values, one workgroup per CU.
 constexpr int kTeamThreads = 256;
 constexpr int kTeamValues = 32;
+constexpr int kLongestClass = 6;
+// Threads of the workgroup that holds a row, by kernel class (>= 4).
+constexpr int team_threads(int kernel_class) {
+    return kernel_class >= kLongestClass ? 2 * kTeamThreads : kTeamThreads;
+}
 
 // Rows per group a wave keeps in flight: enough rows that each lane has kVecsInFlight 16-byte
 // loads outstanding (one row for the element-wise and two-pass paths).

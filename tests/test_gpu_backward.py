@@ -59,20 +59,23 @@ def test_backward_ragged_odd_cols_with_gaps(dtype, schedule):
 
 
 # Rows past the backward register tile (256 vectors): 16-byte aligned rows first, then
-# unaligned ones (which make the plan count one more vector per row for its kernel class).  Class 3 (one wave per row: staged in LDS or read twice), class 4 (a
-# workgroup holds y and dy: two rows of 4 vectors per lane (fp32), or up to 32 values per lane
-# and stream) and class 5 (up to 64 values; longer rows read twice).
+# unaligned ones (which make the plan count one more vector per row for its kernel class).
+# Class 3: one wave per row, staged in LDS or read twice.  Class 4: a workgroup holds y and
+# dy, two rows of 4 vectors per lane or up to 32 values per lane and stream.  Class 5: up to
+# 64 values.  Class 6: a 512-thread workgroup, up to 64 values per lane; longer rows read twice.
 BWD_LONG_COLS = {
     ("f32", 3): [1028, 1500, 2044, 1030],
     ("f32", 4): [2052, 3000, 4096, 6000, 8188, 2050, 5003],
-    ("f32", 5): [8196, 16384, 16388, 40000, 10001],
+    ("f32", 5): [8196, 16380, 10001],
+    ("f32", 6): [16392, 32768, 32772, 40000, 20001],
     ("bf16", 3): [2056, 3000, 4088, 2050],
     ("bf16", 4): [4104, 6000, 8184, 4098, 5003],
-    ("bf16", 5): [8200, 16384, 16392, 40000, 10001],
+    ("bf16", 5): [8200, 16376, 10001],
+    ("bf16", 6): [16392, 32768, 32776, 40000, 20001],
 }
 
 
-@pytest.mark.parametrize("kclass", [3, 4, 5])
+@pytest.mark.parametrize("kclass", [3, 4, 5, 6])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_backward_long_rows(dtype, kclass):
     """Rows past the backward register tile under every schedule, against the oracle, with the

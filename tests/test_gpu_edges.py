@@ -53,17 +53,20 @@ def test_ragged_odd_cols_with_gaps(dtype, schedule):
 LONG_COLS = {
     ("f32", 4): [2052, 2500, 3072, 4096, 4100, 6000, 8188, 4095],
     ("bf16", 4): [4104, 5000, 6144, 8184, 4200, 8000, 4097],
-    ("f32", 5): [8196, 12000, 16384, 16388, 40000, 100003],
-    ("bf16", 5): [8200, 12000, 16384, 16392, 40000, 100003],
+    ("f32", 5): [8196, 12000, 16380, 9001],
+    ("bf16", 5): [8200, 12000, 16376, 9001],
+    ("f32", 6): [16392, 20000, 32768, 32772, 70000, 20001],
+    ("bf16", 6): [16392, 24000, 32768, 32776, 70000, 20001],
 }
 
 
-@pytest.mark.parametrize("kclass", [4, 5])
+@pytest.mark.parametrize("kclass", [4, 5, 6])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_long_rows_workgroup_held_and_two_pass(dtype, kclass):
     """Rows beyond the register tile, held by a 256-thread workgroup (up to 8192 elements in
-    kernel class 4, 16384 in class 5) or, longer, read twice; odd row counts (rows are paired
-    across ranges); against the oracle under every schedule, with the same bits under all."""
+    kernel class 4, 16384 in class 5) or a 512-thread one (32768, class 6), or, longer, read
+    twice; odd row counts (rows are paired across ranges); against the oracle under every
+    schedule, with the same bits under all."""
     cols = LONG_COLS[(dtype, kclass)]
     rows = [3, 5, 2, 3, 2, 3, 2, 3][: len(cols)]
     w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=9, gap=8)
@@ -71,7 +74,8 @@ def test_long_rows_workgroup_held_and_two_pass(dtype, kclass):
     for schedule in SCHEDULES:
         print(f"[long {dtype} class {kclass} {schedule}] cols {cols}", flush=True)
         bits, st = _check_ragged(w, schedule)
-        assert st["kernel_class"] == kclass and st["wg_threads"] == 256 and st["per_wave"] == 0
+        threads = 512 if kclass == 6 else 256
+        assert st["kernel_class"] == kclass and st["wg_threads"] == threads and st["per_wave"] == 0
         results.append(bits)
     assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
 
