@@ -624,10 +624,10 @@ def main() -> int:
         extra["producer_consumer"] = producer_consumer()
         extra["attention_pipeline"] = attention_pipeline()
         extra["l2_locality_16MB_us"] = l2_locality()
-        # rows longer than the register tile, held in the registers of a 256-thread workgroup
-        # (up to 8192 elements in kernel class 4, 16384 in class 5) and read once, forward and
-        # backward
-        for name in ("long4k", "long", "long16k"):
+        # rows longer than the register tile, held in the registers of a workgroup (256 threads:
+        # up to 8192 elements in kernel class 4, 16384 in class 5; 512 threads: up to 32768 in
+        # class 6) and read once, forward and backward
+        for name in ("long4k", "long", "long16k", "long32k"):
             r, _ = run_workload(name, "balanced", args.steps, args.warmup)
             extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}
             r = run_backward(name, "balanced", args.steps, args.warmup)

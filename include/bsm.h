@@ -85,8 +85,9 @@ typedef struct bsm_topology {
     int32_t n_xcd;       /* XCDs (MI355X: 8); workgroup w is taken to run on XCD w mod n_xcd */
     int32_t wg_per_cu;   /* persistent workgroups per CU; the grid has n_cu * wg_per_cu */
     int32_t wg_threads;  /* threads per workgroup, a multiple of 64 in [64, 1024]; plans with
-                            rows longer than 2048 fp32 / 4096 bf16 elements run 256 whatever
-                            is asked (the workgroup's waves share each such row) */
+                            rows longer than 2048 fp32 / 4096 bf16 elements run 256 (512 when
+                            a row spans more than 16384 elements) whatever is asked: the
+                            workgroup's waves share each such row */
     int32_t piece_bytes; /* BALANCED / XCD: traffic of one worker's piece of a round */
     float item_cost;     /* planner cost of one work item, in byte equivalents (<= 0: default) */
     float row_cost;      /* planner cost of one row on top of its bytes (<= 0: default) */

@@ -5,7 +5,8 @@
 // of the host-built work table (the mapping table of the paper's Section 5: geometry is read
 // per item, the instructions are the same for every patch).  A row up to the register tile is
 // owned by one group of lanes of one wave (no barrier); a longer row is shared by all the
-// waves of a 256-thread workgroup, which combine their partial max and sum through LDS.
+// waves of its workgroup (256 or 512 threads), which combine their partial max and sum through
+// LDS.
 //
 // Per row (softmax over the row, the operation of the problem statement, Section 2):
 //   128-bit loads (fp32, or bf16 widened to fp32; nontemporal unless the plan asks for cache-
@@ -19,8 +20,8 @@
 // A group of G lanes (16, 32 or 64) owns one row and holds V 16-byte vectors per lane, so a
 // wave covers 64/G rows at a time, with four 16-byte loads per lane in flight.  Rows longer
 // than the largest register tile (512 vectors) are held in the registers of a whole workgroup
-// (up to 32 values per lane in kernel class 4, 64 in class 5) and read once, or, longer still,
-// read twice with an online max/sum.  Rows whose start or length is not 16-byte aligned use
+// (up to 32 values per lane in kernel class 4, 64 in classes 5 and 6, whose workgroups have 256
+// and 512 threads) and read once, or, longer still, read twice with an online max/sum.  Rows whose start or length is not 16-byte aligned use
 // element loads with the same lane layout, or one wave per row (staged in the wave's LDS
 // region, else two passes).  This is bandwidth-bound work: no MFMA.
 #pragma once

@@ -16,7 +16,8 @@ namespace bsm {
 //   2: <= 256 vectors                  (fp32 C <= 1024, bf16 C <= 2048)
 //   3: <= 512 vectors                  (fp32 C <= 2048, bf16 C <= 4096)
 //   4: <= 8192 elements, held by a 256-thread workgroup (up to 32 values per lane)
-//   5: any length (up to 64 values per lane held, longer rows read twice)
+//   5: <= 16384 elements, held by a 256-thread workgroup (up to 64 values per lane)
+//   6: any length (a 512-thread workgroup holds up to 32768 elements, longer rows read twice)
 // Kernel instance for a plan whose longest row is max_cols elements; `shifted`: some slice's
 // rows do not start and end on 16-byte vectors (they may span one vector more).
 int kernel_class_for(int32_t max_cols, int elem_bytes, bool shifted);

@@ -68,6 +68,9 @@ SPECS = {
         "odd_64x768x1001_f32", 64, 768, 1001, F32, 3.0, 9,
         doc="64 slices x 768x1001 fp32, N(0,9): every row starts at a different phase of the "
             "16-byte vectors"),
+    "long_16x64x32768_f32": Spec(
+        "long_16x64x32768_f32", 16, 64, 32768, F32, 3.0, 10,
+        doc="16 slices x 64x32768 fp32, N(0,9): rows held by a 512-thread workgroup (class 6)"),
     "long_32x64x16384_f32": Spec(
         "long_32x64x16384_f32", 32, 64, 16384, F32, 3.0, 8,
         doc="32 slices x 64x16384 fp32, N(0,9): the longest register-held rows (class 5, 16 vectors per lane)"),
@@ -78,7 +81,7 @@ ALIASES = {"c1": "c1_8x64x64_f32", "c2": "c2_384x512x512_f32",
            "c3": "c3_384x512x512_bf16_mask", "c4": "c4_16384x128x128_f32",
            "c5": "c5_384_ragged_f32", "long": "long_64x64x8192_f32",
            "long4k": "long_128x64x4096_f32", "long16k": "long_32x64x16384_f32",
-           "odd": "odd_64x768x1001_f32"}
+           "odd": "odd_64x768x1001_f32", "long32k": "long_16x64x32768_f32"}
 
 
 @dataclasses.dataclass
