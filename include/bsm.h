@@ -102,6 +102,16 @@ typedef struct bsm_topology {
  * same under both policies. */
 #define BSM_FLAG_TEMPORAL 1
 
+/* Virtual banks of the XCD schedule (Section 4.1's memory banks; MI355X in NPS1 interleaves HBM
+ * over all stacks, so a bank is a planning construct).  By default the span of the non-empty
+ * slices is cut into chunks dealt to the n_xcd banks in turn: a chunk is the mean slice extent
+ * times the smallest factor that makes it at least 256 KiB, so uniform slices of 256 KiB or more
+ * are homed on XCD s mod n_xcd.  The XCDs then stream neighbouring memory at any moment.  When the
+ * span holds no more than n_xcd chunks, or with BSM_FLAG_CONTIGUOUS_BANKS, the banks are n_xcd
+ * equal contiguous ranges (the layout of Section 4.1's batch-to-bank table).  Homes change only
+ * who computes a row: the output bits are the same. */
+#define BSM_FLAG_CONTIGUOUS_BANKS 2
+
 /* One entry of the work table (the paper's Patch<->Cluster mapping table, Section 5): `reps`
  * ranges of `nrows` rows each; range k starts at element elem_offset + k*rep_stride*cols.
  * Every row lies inside a slice of row length `cols` (a range may run on into the next slice
@@ -202,9 +212,9 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets,
 /* Build a reusable plan: the work table of the HW batch scheduler of Section 5, built once
  * up front and reused for every execution.
  *   home_xcd   optional [batch] home XCD per slice in [0, n_xcd) for the XCD schedule (the
- *              bank each slice was created on); NULL = virtual banks, i.e. n_xcd equal
- *              contiguous element ranges over the span of the slices.  Ignored by RR and
- *              BALANCED.
+ *              bank each slice was created on); NULL = virtual banks over the span of the
+ *              slices, interleaved chunks or contiguous ranges (BSM_FLAG_CONTIGUOUS_BANKS).
+ *              Ignored by RR and BALANCED.
  *   topology   NULL = the device's defaults (bsm_default_topology).
  *   device     HIP device ordinal; -1 builds a host-only plan (topology required) that can
  *              be described and exported but not executed; it touches no GPU. */

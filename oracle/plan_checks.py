@@ -6,8 +6,9 @@ clarity rather than speed, and shares no code with the library's host planner:
 * exactly-once coverage of every row of every slice by a work table (the mapping table of
   Section 5 must schedule every patch, and no patch twice), with the slice's row length;
 * the batch-to-bank table of Section 4.1, computed by counting the elements of each slice that
-  fall in each bank (OVERLAP flag, the counts N_x with overlaps, the max-proportion home with
-  ties to the lowest bank, the counts L_x after resolution);
+  fall in each bank, for contiguous or interleaved virtual banks (OVERLAP flag, the counts N_x
+  with overlaps, the max-proportion home with ties to the lowest bank, the counts L_x after
+  resolution);
 * the MINIMAX objective of Section 4.2 (min over partitions of the patches of the max summed
   execution time per core), solved by enumerating every assignment for tiny instances;
 * longest-processing-time-first list scheduling, a textbook 4/3-approximation of it;
@@ -117,14 +118,37 @@ def bank_bounds(lo: int, hi: int, n_banks: int):
     return [lo + (b * span) // n_banks for b in range(n_banks + 1)]
 
 
-def bank_table(offsets, rows, cols, n_banks: int):
+def interleave_chunk(offsets, rows, cols, n_banks: int, elem_bytes: int,
+                     min_chunk_bytes: int = 256 * 1024) -> int:
+    """Chunk (elements) of the interleaved virtual banks: the span [lo, hi) of the non-empty
+    slices divided by their number (floor, at least 1) is the mean slice extent m; the chunk is
+    the smallest multiple of m holding at least min_chunk_bytes. Returns 0 (contiguous banks)
+    when n_banks chunks cover the span or there is no non-empty slice."""
+    sizes = [int(rows[s]) * int(cols[s]) for s in range(len(rows))]
+    live = [s for s in range(len(rows)) if sizes[s] > 0]
+    if not live:
+        return 0
+    lo = min(int(offsets[s]) for s in live)
+    hi = max(int(offsets[s]) + sizes[s] for s in live)
+    m = max(1, (hi - lo) // len(live))
+    k = 1
+    while k * m * elem_bytes < min_chunk_bytes:
+        k += 1
+    chunk = k * m
+    return 0 if chunk * n_banks >= hi - lo else chunk
+
+
+def bank_table(offsets, rows, cols, n_banks: int, layout: str = "contiguous",
+               elem_bytes: int = 4):
     """Batch-to-bank table by counting, element by element, which bank holds each element.
 
-    Banks are n_banks equal contiguous ranges over the elements spanned by the non-empty
-    slices. Returns dict with per-slice `counts` [B, n_banks], `overlap` [B] (0/1), `home` [B]
-    (bank holding the largest share; ties go to the lowest bank; -1 for an empty slice),
-    `N` [n_banks] (slices touching each bank, overlaps counted in every bank they touch) and
-    `L` [n_banks] (slices homed on each bank)."""
+    The banks partition the elements spanned by the non-empty slices, [lo, hi). layout
+    "contiguous": n_banks equal contiguous ranges. layout "interleaved": element e lies in bank
+    floor((e - lo) / chunk) mod n_banks, chunk = interleave_chunk(...), falling back to the
+    contiguous ranges where that is 0. Returns dict with per-slice `counts` [B, n_banks],
+    `overlap` [B] (0/1), `home` [B] (bank holding the largest share; ties go to the lowest bank;
+    -1 for an empty slice), `N` [n_banks] (slices touching each bank, overlaps counted in every
+    bank they touch) and `L` [n_banks] (slices homed on each bank)."""
     B = len(rows)
     sizes = [int(rows[s]) * int(cols[s]) for s in range(B)]
     live = [s for s in range(B) if sizes[s] > 0]
@@ -136,13 +160,23 @@ def bank_table(offsets, rows, cols, n_banks: int):
                     N=np.zeros(n_banks, np.int64), L=np.zeros(n_banks, np.int64))
     lo = min(int(offsets[s]) for s in live)
     hi = max(int(offsets[s]) + sizes[s] for s in live)
+    chunk = 0
+    if layout == "interleaved":
+        chunk = interleave_chunk(offsets, rows, cols, n_banks, elem_bytes)
+    elif layout != "contiguous":
+        raise ValueError(layout)
     bound = bank_bounds(lo, hi, n_banks)
     for s in live:
-        for e in range(int(offsets[s]), int(offsets[s]) + sizes[s]):
-            b = 0
-            while not (bound[b] <= e < bound[b + 1]):
-                b += 1
-            counts[s, b] += 1
+        if chunk:
+            # every element's bank, counted with numpy (the same count as a Python loop)
+            e = np.arange(int(offsets[s]), int(offsets[s]) + sizes[s], dtype=np.int64)
+            counts[s] = np.bincount(((e - lo) // chunk) % n_banks, minlength=n_banks)
+        else:
+            for e in range(int(offsets[s]), int(offsets[s]) + sizes[s]):
+                b = 0
+                while not (bound[b] <= e < bound[b + 1]):
+                    b += 1
+                counts[s, b] += 1
         nz = [b for b in range(n_banks) if counts[s, b] > 0]
         overlap[s] = 1 if len(nz) > 1 else 0
         best = max(counts[s])

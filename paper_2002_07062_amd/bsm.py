@@ -25,6 +25,7 @@ BSM_F32, BSM_BF16 = 0, 1
 BSM_SCHED_RR, BSM_SCHED_BALANCED, BSM_SCHED_XCD = 0, 1, 2
 BSM_MAX_XCD = 16
 BSM_FLAG_TEMPORAL = 1
+BSM_FLAG_CONTIGUOUS_BANKS = 2
 
 SCHEDULES = {"rr": BSM_SCHED_RR, "balanced": BSM_SCHED_BALANCED, "xcd": BSM_SCHED_XCD}
 BSM_GEMM_NT, BSM_GEMM_NN = 0, 1

@@ -162,7 +162,7 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
         t.row_cost = kDefaultRowCost;
     }
     if (user) {
-        if ((user->flags & ~BSM_FLAG_TEMPORAL) != 0)
+        if ((user->flags & ~(BSM_FLAG_TEMPORAL | BSM_FLAG_CONTIGUOUS_BANKS)) != 0)
             return fail(BSM_ERR_INVALID_ARG, "topology.flags has unknown bits 0x%x", user->flags);
         if (user->n_cu < 0 || user->n_xcd < 0 || user->wg_per_cu < 0 || user->wg_threads < 0 ||
             user->piece_bytes < 0)
@@ -208,6 +208,7 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
     out->piece_bytes = t.piece_bytes;
     out->item_cost = t.item_cost;
     out->row_cost = t.row_cost;
+    out->contiguous_banks = user && (user->flags & BSM_FLAG_CONTIGUOUS_BANKS) != 0;
     std::string err = bsm::check_topology(*out);
     if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "topology: %s", err.c_str());
     return BSM_OK;

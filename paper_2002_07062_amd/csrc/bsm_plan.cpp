@@ -185,10 +185,50 @@ int64_t assign_rounds(const std::vector<Span>& stream, const std::vector<int32_t
     return n_rounds;
 }
 
-// Homes of Section 4.1.  Virtual banks: n equal contiguous element ranges over the span of the
-// non-empty slices; a slice's home is the bank holding its largest share (lowest index on a
-// tie), and OVERLAP is set when it has elements in two or more banks.
-void assign_homes(const Geometry& g, int n, const int8_t* user, Table* tab) {
+// Elements of [a, b) (relative to the span's start) that fall in each of n banks when the
+// span is cut into chunks of g elements dealt to the banks in turn (chunk k -> bank k mod n).
+void interleaved_shares(int64_t a, int64_t b, int64_t g, int n, std::vector<int64_t>* share) {
+    share->assign(static_cast<size_t>(n), 0);
+    const int64_t ka = a / g, kb = (b - 1) / g;
+    if (ka == kb) {
+        (*share)[ka % n] += b - a;
+        return;
+    }
+    (*share)[ka % n] += (ka + 1) * g - a;
+    (*share)[kb % n] += b - kb * g;
+    const int64_t whole = kb - ka - 1;  // full chunks between the two partial ones
+    for (int j = 0; j < n; ++j) (*share)[j] += (whole / n) * g;
+    for (int64_t j = 0; j < whole % n; ++j) (*share)[(ka + 1 + j) % n] += g;
+}
+
+}  // namespace
+
+int64_t bank_chunk_elems(const Geometry& g, int n, bool contiguous) {
+    int64_t lo = std::numeric_limits<int64_t>::max(), hi = 0, live = 0;
+    for (int64_t s = 0; s < g.batch; ++s) {
+        const int64_t sz = static_cast<int64_t>(g.R[s]) * g.C[s];
+        if (sz == 0) continue;
+        lo = std::min(lo, g.off[s]);
+        hi = std::max(hi, g.off[s] + sz);
+        ++live;
+    }
+    if (contiguous || live == 0 || hi <= lo) return 0;
+    const int64_t span = hi - lo;
+    const int64_t mean = std::max<int64_t>(1, span / live);
+    const int64_t min_elems = (kBankChunkBytes + g.elem_bytes - 1) / g.elem_bytes;
+    const int64_t chunk = mean * ((min_elems + mean - 1) / mean);
+    // a span of no more than n chunks keeps the contiguous banks (one range per bank)
+    if (static_cast<i128>(chunk) * n >= span) return 0;
+    return chunk;
+}
+
+namespace {
+
+// Homes of Section 4.1 over virtual banks that partition the span [lo, hi) of the non-empty
+// slices: chunks of bank_chunk_elems() elements dealt to the banks in turn, or n equal
+// contiguous ranges (chunk 0).  A slice's home is the bank holding its largest share (lowest
+// index on a tie), and OVERLAP is set when it has elements in two or more banks.
+void assign_homes(const Geometry& g, int n, bool contiguous, const int8_t* user, Table* tab) {
     const int64_t B = g.batch;
     tab->home.assign(static_cast<size_t>(B), -1);
     tab->overlap.assign(static_cast<size_t>(B), 0);
@@ -210,25 +250,26 @@ void assign_homes(const Geometry& g, int n, const int8_t* user, Table* tab) {
         hi = std::max(hi, g.off[s] + sz);
     }
     if (hi <= lo) return;
+    const int64_t chunk = bank_chunk_elems(g, n, contiguous);
     std::vector<int64_t> bound(static_cast<size_t>(n) + 1);
     for (int b = 0; b <= n; ++b)
         bound[b] = lo + static_cast<int64_t>(static_cast<i128>(b) * (hi - lo) / n);
+    std::vector<int64_t> share(static_cast<size_t>(n));
     for (int64_t s = 0; s < B; ++s) {
         const int64_t o = g.off[s], e = o + static_cast<int64_t>(g.R[s]) * g.C[s];
         if (e == o) continue;
-        const int b0 = static_cast<int>(std::upper_bound(bound.begin() + 1, bound.end(), o) -
-                                        (bound.begin() + 1));
+        if (chunk > 0) {
+            interleaved_shares(o - lo, e - lo, chunk, n, &share);
+        } else {
+            for (int b = 0; b < n; ++b)
+                share[b] = std::max<int64_t>(0, std::min(e, bound[b + 1]) - std::max(o, bound[b]));
+        }
         int best = -1, touched = 0;
-        int64_t best_share = -1;
-        for (int b = b0; b < n && bound[b] < e; ++b) {
-            const int64_t share = std::min(e, bound[b + 1]) - std::max(o, bound[b]);
-            if (share <= 0) continue;
+        for (int b = 0; b < n; ++b) {
+            if (share[b] <= 0) continue;
             ++touched;
             st.bank_touch[b] += 1;
-            if (share > best_share) {
-                best_share = share;
-                best = b;
-            }
+            if (best < 0 || share[b] > share[best]) best = b;
         }
         tab->home[s] = static_cast<int8_t>(best);
         tab->overlap[s] = touched > 1 ? 1 : 0;
@@ -249,7 +290,7 @@ std::vector<std::vector<Span>> xcd_streams(const Geometry& g, const Topology& t,
     const int n = t.n_xcd;
     const int P = t.n_wg();
     const int es = g.elem_bytes;
-    assign_homes(g, n, user_home, tab);
+    assign_homes(g, n, t.contiguous_banks, user_home, tab);
 
     std::vector<int64_t> Px(static_cast<size_t>(n), 0);
     for (int w = 0; w < P; ++w) Px[w % n] += 1;

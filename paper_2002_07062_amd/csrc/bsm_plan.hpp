@@ -36,6 +36,8 @@ struct Topology {
     // Rows per cutting unit (0: the softmax register-tile step for the row's length).  The
     // matrix-product kernels take rows 32 at a time.
     int32_t row_unit = 0;
+    // XCD schedule: virtual banks as n_xcd equal contiguous ranges instead of interleaved chunks
+    bool contiguous_banks = false;
     int32_t n_wg() const { return n_cu * wg_per_cu; }
     int32_t waves_per_wg() const { return wg_threads / 64; }
 };
@@ -48,6 +50,17 @@ struct Table {
     bool per_wave = false;
     bsm_plan_stats stats{};
 };
+
+// Smallest chunk of the interleaved virtual banks of the XCD schedule.  Measured on MI355X: with
+// chunks of at least this size (and at least one mean slice) the eight XCDs stream neighbouring
+// memory at any moment and the XCD schedule runs as fast as BALANCED on cold data, where eight
+// contiguous banks, one window per XCD ~1/8 of the batch apart, cost 4-13%.
+constexpr int64_t kBankChunkBytes = 256 * 1024;
+
+// Chunk, in elements, of the interleaved virtual banks for `g` over n banks: the mean extent of a
+// non-empty slice times the smallest factor that makes it at least kBankChunkBytes.  0 means n
+// equal contiguous ranges: asked for, or the span of the slices holds no more than n chunks.
+int64_t bank_chunk_elems(const Geometry& g, int n, bool contiguous);
 
 // Checks the geometry (sizes, overflow, slices not overlapping) and fills `g`.  Returns an
 // empty string on success, else what is wrong.

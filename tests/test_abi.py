@@ -67,7 +67,7 @@ def test_plan_create_rejects_bad_geometry(kwargs, msg):
 
 @pytest.mark.parametrize("topo", [
     dict(n_cu=-1), dict(wg_threads=100), dict(wg_threads=2048), dict(n_xcd=17),
-    dict(wg_per_cu=65), dict(flags=2), dict(flags=-1), dict(piece_bytes=-5),
+    dict(wg_per_cu=65), dict(flags=4), dict(flags=-1), dict(piece_bytes=-5),
 ])
 def test_plan_create_rejects_bad_topology(topo):
     t = dict(TOPO)

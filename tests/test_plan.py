@@ -144,7 +144,8 @@ def test_paper_bank_table_through_the_library():
     R = np.array([r["R"] for r in rows], np.int32)
     C = np.array([r["C"] for r in rows], np.int32)
     p = bsm.bsm_plan_create(R, C, off, dtype="f32", schedule="xcd", device=-1,
-                            topology=dict(n_cu=4, n_xcd=banks, wg_per_cu=1, wg_threads=64))
+                            topology=dict(n_cu=4, n_xcd=banks, wg_per_cu=1, wg_threads=64,
+                                          flags=bsm.BSM_FLAG_CONTIGUOUS_BANKS))
     d = bsm.bsm_plan_describe(p)
     _, _, home, ov = bsm.bsm_plan_export(p)
     p.destroy()
@@ -157,19 +158,41 @@ def test_paper_bank_table_through_the_library():
     assert d["n_overlap"] == 1
 
 
-@pytest.mark.parametrize("name", ["c1", "c5", "ragged_gaps"])
+@pytest.mark.parametrize("layout,name", [("contiguous", "c1"), ("contiguous", "c5"),
+                                         ("contiguous", "ragged_gaps"), ("interleaved", "c1"),
+                                         ("interleaved", "c2"), ("interleaved", "c3"),
+                                         ("interleaved", "c4"), ("interleaved", "c5"),
+                                         ("interleaved", "ragged_gaps")])
 @pytest.mark.parametrize("n_xcd", [2, 3, 8])
-def test_homes_match_bruteforce_bank_table(name, n_xcd):
+def test_homes_match_bruteforce_bank_table(layout, name, n_xcd):
     w = WL[name]
-    if w.n_elements > 2_000_000:
+    if w.n_elements > 2_000_000 and (layout == "contiguous" or name == "c5"):
         w = workloads.generate("c5", batch=40)
-    topo = dict(n_cu=8 * n_xcd, n_xcd=n_xcd, wg_per_cu=1, wg_threads=64)
+    flags = bsm.BSM_FLAG_CONTIGUOUS_BANKS if layout == "contiguous" else 0
+    topo = dict(n_cu=8 * n_xcd, n_xcd=n_xcd, wg_per_cu=1, wg_threads=64, flags=flags)
     d, ptr, items, home, ov = _plan(w, "xcd", topo)
-    t = pc.bank_table(w.offsets[: w.batch], w.rows, w.cols, n_xcd)
+    t = pc.bank_table(w.offsets[: w.batch], w.rows, w.cols, n_xcd, layout=layout,
+                      elem_bytes=2 if w.dtype == "bf16" else 4)
     assert home.tolist() == t["home"].tolist()
     assert ov.tolist() == t["overlap"].tolist()
     assert d["bank_touch"] == t["N"].tolist()
     assert d["bank_home"] == t["L"].tolist()
+
+
+@pytest.mark.parametrize("name,group", [("c2", 1), ("c3", 1), ("c4", 4)])
+def test_default_banks_deal_uniform_slices_to_xcds_in_turn(name, group):
+    """Interleaved banks on uniform batches: slices of 256 KiB or more (C2's 1 MiB fp32, C3's
+    512 KiB bf16) are homed on XCD s mod 8 with no overlap, and 64 KiB slices (C4) in groups of
+    four (a 256 KiB chunk); the contiguous layout homes slice s on bank floor(8 s / B)."""
+    w = WL[name]
+    d, _, _, home, ov = _plan(w, "xcd", MI355X)
+    s = np.arange(w.batch)
+    assert home.tolist() == ((s // group) % 8).tolist()
+    assert not ov.any() and d["n_overlap"] == 0
+    assert d["moved_bytes"] == 0  # uniform slices dealt evenly: every XCD already has its share
+    d, _, _, home, _ = _plan(w, "xcd", dict(MI355X, flags=bsm.BSM_FLAG_CONTIGUOUS_BANKS))
+    assert home.tolist() == ((8 * s) // w.batch).tolist()
+    assert d["flags"] == bsm.BSM_FLAG_CONTIGUOUS_BANKS
 
 
 def _xcd_loads(w, d, ptr, items, topo, home):
