@@ -454,6 +454,31 @@ def test_temporal_cache_policy_gives_the_same_bits(cfg):
     assert torch.equal(a.view(view), b.view(view))
 
 
+@pytest.mark.parametrize("cfg,batch", [("c2", 64), ("c4", 2048), ("c5", 96)])
+def test_bank_layouts_give_the_same_bits(cfg, batch):
+    """Interleaved (default) and contiguous virtual banks home the slices on different XCDs;
+    the outputs are identical to each other and to BALANCED, and the default homes of a uniform
+    batch follow the interleaving (C2: slice s on XCD s mod 8; C4: groups of four)."""
+    w = workloads.generate(cfg, batch=batch)
+    print(f"[{cfg}] batch {batch}", flush=True)
+    x = to_device(w.x, w.dtype)
+    a, st_a = run_plan(w, "xcd", x=x)
+    b, st_b = run_plan(w, "xcd", x=x, topology={"flags": bsm.BSM_FLAG_CONTIGUOUS_BANKS})
+    c, _ = run_plan(w, "balanced", x=x)
+    assert st_b["flags"] == bsm.BSM_FLAG_CONTIGUOUS_BANKS and st_a["flags"] == 0
+    view = torch.int16 if w.dtype == "bf16" else torch.int32
+    assert torch.equal(a.view(view), b.view(view))
+    assert torch.equal(a.view(view), c.view(view))
+    if cfg != "c5":
+        plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                                   schedule="xcd", device=0)
+        _, _, home, _ = bsm.bsm_plan_export(plan)
+        plan.destroy()
+        s = np.arange(w.batch)
+        group = 1 if cfg == "c2" else 4
+        assert home.tolist() == ((s // group) % st_a["n_xcd"]).tolist()
+
+
 def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
     """Weighted load balancing moves rows between XCDs but never changes a result; an XCD of
     weight 0 runs no rows (per-wave trace)."""
