@@ -25,7 +25,13 @@
  *     rejected with BSM_ERR_ALIAS.
  *   - Errors: every call returns a bsm_status; nothing is thrown, printed or aborted.  After a
  *     failure bsm_last_error() gives a thread-local description.  A failed call leaves its
- *     outputs untouched (no kernel is launched).
+ *     outputs untouched (no kernel is launched).  For tests of the failure paths, the
+ *     environment variable BSM_TEST_ALLOC_FAIL makes every plan creation fail with
+ *     BSM_ERR_OOM as if an allocation had failed: "host" after the table is built on the host,
+ *     "device" at the device allocation of the work table (read at each plan creation).
+ *   - Graph capture: an execution is one kernel launch that reads the plan's device table, so
+ *     executions can be captured in a HIP graph; a plan must outlive every graph that captured
+ *     one of its executions.
  *   - Element values: fp32, or bf16 (stored as raw 16-bit patterns); input and output share
  *     the type; arithmetic is fp32.  A row of all -inf (fully masked) yields zeros; a NaN or
  *     +inf entry makes its whole row NaN.
@@ -202,15 +208,24 @@ typedef struct bsm_plan_s* bsm_plan;
  *   rows, cols     [batch] (or [1] when uniform), each >= 0; an empty slice is skipped
  *   schedule       see bsm_schedule
  *   stream         hipStream_t as void*
- * Plans are built on first use of a geometry (host work plus a synchronous table upload) and
- * cached per device; later calls with the same geometry only launch the kernel.
+ * Arguments are checked before any HIP call.  Plans are built on first use of a geometry and
+ * cached per device (the 32 most recently used, plus any pinned by a graph capture); a later
+ * call with the same arrays hashes and compares them and only launches the kernel.  No call
+ * waits for the device: on a miss the plan is built on the host and its table uploaded with
+ * hipMemcpyAsync on `stream` from pinned staging into a device buffer, both recycled by the
+ * cache (evictions free nothing; a recycled buffer is ordered after its last readers by stream
+ * waits on events, not by host waits).  Streams passed here must not be destroyed while work
+ * they hold is still running.  Under stream capture a cached geometry is launched into the
+ * graph and its plan is pinned until bsm_cache_clear; a geometry not in the cache returns
+ * BSM_ERR_UNSUPPORTED (building a plan allocates and copies): run it once first.
  * batch == 0, or only empty slices, returns BSM_OK without touching the GPU. */
 bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets,
                        const int32_t* rows, const int32_t* cols, int64_t batch,
                        bsm_dtype dtype, bsm_schedule schedule, void* stream);
 
 /* Build a reusable plan: the work table of the HW batch scheduler of Section 5, built once
- * up front and reused for every execution.
+ * up front and reused for every execution.  The table is uploaded to the device before this
+ * returns (synchronously).
  *   home_xcd   optional [batch] home XCD per slice in [0, n_xcd) for the XCD schedule (the
  *              bank each slice was created on); NULL = virtual banks over the span of the
  *              slices, interleaved chunks or contiguous ranges (BSM_FLAG_CONTIGUOUS_BANKS).
@@ -317,7 +332,9 @@ bsm_status bsm_default_topology(int device, bsm_topology* topology);
  * streaming reference the softmax bandwidth is compared with.  src and dst must not overlap. */
 bsm_status bsm_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
-/* Drop every cached one-shot plan (waits for their last use). */
+/* Drop every cached one-shot plan and free the cache's device and pinned buffers: waits for
+ * one-shot calls in other threads to finish launching, then for the device.  Graphs that
+ * captured a one-shot call must not be replayed afterwards. */
 bsm_status bsm_cache_clear(void);
 
 const char* bsm_status_string(bsm_status status);

@@ -8,12 +8,14 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <list>
 #include <memory>
 #include <mutex>
 #include <new>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "bsm.h"
@@ -41,6 +43,16 @@ struct bsm_plan_s {
     const int32_t* d_worker_ptr = nullptr;
     const bsm_item* d_items = nullptr;
     std::atomic<bool> used{false};  // executed at least once (destroy then waits for the device)
+    // One-shot cache plans only (all under the cache lock except `inflight`):
+    bool pooled = false;              // d_table is a buffer of the cache's pool, not owned
+    size_t table_cap = 0;             // bytes of that buffer
+    std::atomic<int> inflight{0};     // calls between lookup and the end of their launch
+    std::vector<hipStream_t> streams; // streams the plan ran on (up to kMaxTrackedStreams)
+    bool many_streams = false;        // ran on more streams than are tracked
+    bool captured = false;            // launched into a graph capture: never evicted
+    hipStream_t upload_stream = nullptr;
+    hipEvent_t upload_done = nullptr; // recorded after the table upload
+    bool uploaded = false;            // upload_done seen complete
 };
 
 namespace {
@@ -215,7 +227,7 @@ bsm_status resolve_topology(const bsm_topology* user, int device, bsm_dtype dtyp
 }
 
 void free_device(bsm_plan p) {
-    if (p->device < 0) return;
+    if (p->device < 0 || p->pooled) return;  // a pooled table belongs to the one-shot cache
     DeviceGuard g;
     if (g.enter(p->device) != hipSuccess) return;
     // Executions on any stream may still be reading the table.  (Nothing is recorded per
@@ -245,11 +257,43 @@ bsm_status resolve_weights(const float* w, bsm::Topology* t) {
     return BSM_OK;
 }
 
+// Device layout of a work table: the worker row pointer, then the items at the next 256-byte
+// boundary.
+size_t table_items_at(const bsm::Table& t) {
+    return (t.worker_ptr.size() * sizeof(int32_t) + 255) & ~static_cast<size_t>(255);
+}
+size_t table_bytes(const bsm::Table& t) {
+    return table_items_at(t) + std::max<size_t>(t.items.size(), 1) * sizeof(bsm_item);
+}
+
+// Test hook for the allocation-failure paths: the environment variable BSM_TEST_ALLOC_FAIL set
+// to "host" makes plan creation fail as if a host allocation had failed (after the table is
+// built, so everything built so far must be released), "device" as if the work table's device
+// allocation had failed.  Read at every plan creation.
+enum class AllocFail { none, host, device };
+AllocFail alloc_fail_hook() {
+    const char* v = std::getenv("BSM_TEST_ALLOC_FAIL");
+    if (!v) return AllocFail::none;
+    if (std::strcmp(v, "host") == 0) return AllocFail::host;
+    if (std::strcmp(v, "device") == 0) return AllocFail::device;
+    return AllocFail::none;
+}
+
+hipError_t table_malloc(void** ptr, size_t bytes) {
+    if (alloc_fail_hook() == AllocFail::device) {
+        *ptr = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    return hipMalloc(ptr, bytes);
+}
+
+// upload == false (one-shot cache misses): the table stays on the host; the cache uploads it
+// asynchronously into a buffer of its pool.
 bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* rows,
                        const int32_t* cols, int64_t batch, bsm_dtype dtype, bsm_schedule schedule,
                        const int8_t* home_xcd, const float* xcd_weight,
                        const bsm_topology* topology, int device, int32_t row_unit = 0,
-                       bool product = false) {
+                       bool product = false, bool upload = true) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
@@ -300,6 +344,7 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
                                          (p->topo.wg_threads / 64) *
                                          static_cast<int64_t>(sizeof(bsm_trace_rec));
         }
+        if (alloc_fail_hook() == AllocFail::host) throw std::bad_alloc();
     } catch (const std::bad_alloc&) {
         return fail(BSM_ERR_OOM, "host allocation failed while planning");
     }
@@ -326,10 +371,14 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             p->lds_floats_per_wave = static_cast<int>(b / static_cast<int64_t>(sizeof(float)));
             p->table.stats.lds_bytes_per_wave = static_cast<int32_t>(b);
         }
+        if (!upload) {
+            *out_plan = p.release();
+            return BSM_OK;
+        }
         const size_t ptr_bytes = p->table.worker_ptr.size() * sizeof(int32_t);
-        const size_t items_at = (ptr_bytes + 255) & ~static_cast<size_t>(255);
-        const size_t bytes = items_at + std::max<size_t>(p->table.items.size(), 1) * sizeof(bsm_item);
-        e = hipMalloc(&p->d_table, bytes);
+        const size_t items_at = table_items_at(p->table);
+        const size_t bytes = table_bytes(p->table);
+        e = table_malloc(&p->d_table, bytes);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             p->d_table = nullptr;
@@ -399,7 +448,8 @@ bsm_status execute_plan(bsm_plan p, bool backward, const void* a, const void* b,
 // --------------------------------------------------------------------- matrix products
 bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n, int32_t k,
                             int layout, bsm_dtype out_dtype, bsm_schedule schedule,
-                            const int8_t* home_xcd, const bsm_topology* topology, int device) {
+                            const int8_t* home_xcd, const bsm_topology* topology, int device,
+                            bool upload = true) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
     if (layout != 0 && layout != 1) return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", layout);
@@ -436,7 +486,8 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
     const int32_t rows[1] = {m}, cols[1] = {n};
     bsm_plan p = nullptr;
     bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
-                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg(), true);
+                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg(), true,
+                                upload);
     if (st != BSM_OK) return st;
     p->topo.wg_threads = wg_threads;
     p->table.per_wave = false;
@@ -492,104 +543,469 @@ bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float
 }
 
 // ---------------------------------------------------------------------------- plan cache
-struct CacheKey {
-    int device;
-    int dtype;
-    int schedule;
-    bool uniform;
-    int64_t batch;
-    std::vector<int64_t> off;
-    std::vector<int32_t> R, C;
-    int gemm_k = -1;  // >= 0: a matrix-product plan with this reduction depth
-    int gemm_layout = 0;
-    bool operator==(const CacheKey& o) const {
-        return device == o.device && dtype == o.dtype && schedule == o.schedule &&
-               uniform == o.uniform && batch == o.batch && off == o.off && R == o.R && C == o.C &&
-               gemm_k == o.gemm_k && gemm_layout == o.gemm_layout;
+// The one-shot calls (bsm_softmax, bsm_softmax_backward, bsm_gemm) run plans from a cache keyed
+// by device, op, element type, schedule and the exact geometry.
+//
+// A hit hashes the caller's geometry arrays, compares them exactly with the stored key and
+// launches: no allocation, copy, event or synchronisation, and the launch itself runs outside
+// the lock.  A miss builds the plan on the host outside the lock, then uploads its table with
+// hipMemcpyAsync on the caller's stream, from a pinned staging buffer into a device buffer,
+// both taken from pools that the cache recycles.  Nothing is freed while the cache runs
+// (hipFree and hipHostFree synchronise the device): an evicted plan's device buffer goes back
+// to the pool tagged with the streams the plan ran on, and whoever takes it next on stream T
+// first makes T wait (hipStreamWaitEvent) on an event recorded then on each other tagged
+// stream, so the reuse is ordered after every kernel that read the old table while the host
+// never waits.  A staging buffer is reused once the event recorded after its copy has
+// completed.  A plan that another stream runs before its upload is seen complete makes that
+// stream wait on the upload's event.
+//
+// Graph capture: a hit on a capturing stream pins its plan (never evicted; only
+// bsm_cache_clear frees it) once its upload has completed; a miss is refused
+// (BSM_ERR_UNSUPPORTED), since building a plan allocates and copies.
+constexpr size_t kCacheMax = 32;
+constexpr size_t kMaxTrackedStreams = 8;
+constexpr size_t kMinPoolBytes = 64 * 1024;
+
+// The caller's geometry, not copied (uniform: R and C have one entry).
+struct KeyView {
+    int device = 0, kind = 0, dtype = 0, schedule = 0;  // kind 0: softmax, 1: product
+    bool uniform = true;
+    int64_t batch = 0;
+    const int64_t* off = nullptr;
+    const int32_t* R = nullptr;
+    const int32_t* C = nullptr;
+    int32_t gm = 0, gn = 0, gk = 0, glayout = 0;  // products
+    int64_t n_entries() const { return uniform ? 1 : batch; }
+};
+
+// 64-bit multiply-xorshift over 8-byte words: enough to tell geometries apart before the exact
+// comparison.
+struct Hasher {
+    uint64_t h = 0x9E3779B97F4A7C15ull;
+    void word(uint64_t v) {
+        h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+        h *= 0xBF58476D1CE4E5B9ull;
+        h ^= h >> 31;
+    }
+    void bytes(const void* p, size_t n) {
+        const unsigned char* c = static_cast<const unsigned char*>(p);
+        size_t i = 0;
+        for (; i + 8 <= n; i += 8) {
+            uint64_t v;
+            std::memcpy(&v, c + i, 8);
+            word(v);
+        }
+        uint64_t tail = 0;
+        std::memcpy(&tail, c + i, n - i);
+        word(tail ^ (static_cast<uint64_t>(n) << 56));
     }
 };
 
-// Looks up (or builds and inserts) the cached plan for `key`; the caller holds g_cache_mu.
-template <class Build>
-bsm_status cached_plan(CacheKey key, Build build, bsm_plan* out);
+uint64_t hash_key(const KeyView& k) {
+    Hasher h;
+    h.word(static_cast<uint64_t>(k.device) | (static_cast<uint64_t>(k.kind) << 16) |
+           (static_cast<uint64_t>(k.dtype) << 24) | (static_cast<uint64_t>(k.schedule) << 32) |
+           (static_cast<uint64_t>(k.uniform) << 40) | (static_cast<uint64_t>(k.glayout) << 48));
+    h.word(static_cast<uint64_t>(k.batch));
+    h.word(static_cast<uint64_t>(static_cast<uint32_t>(k.gm)) |
+           (static_cast<uint64_t>(static_cast<uint32_t>(k.gn)) << 32));
+    h.word(static_cast<uint64_t>(static_cast<uint32_t>(k.gk)));
+    const size_t n = static_cast<size_t>(k.n_entries());
+    if (k.off) h.bytes(k.off, n * sizeof(int64_t));
+    if (k.R) h.bytes(k.R, n * sizeof(int32_t));
+    if (k.C) h.bytes(k.C, n * sizeof(int32_t));
+    return h.h;
+}
+
+struct CacheKey {
+    uint64_t hash = 0;
+    int device = 0, kind = 0, dtype = 0, schedule = 0;
+    bool uniform = true;
+    int64_t batch = 0;
+    std::vector<int64_t> off;
+    std::vector<int32_t> R, C;
+    int32_t gm = 0, gn = 0, gk = 0, glayout = 0;
+    CacheKey(const KeyView& k, uint64_t h)
+        : hash(h), device(k.device), kind(k.kind), dtype(k.dtype), schedule(k.schedule),
+          uniform(k.uniform), batch(k.batch), gm(k.gm), gn(k.gn), gk(k.gk), glayout(k.glayout) {
+        const size_t n = static_cast<size_t>(k.n_entries());
+        if (k.off) off.assign(k.off, k.off + n);
+        if (k.R) R.assign(k.R, k.R + n);
+        if (k.C) C.assign(k.C, k.C + n);
+    }
+    bool matches(const KeyView& k, uint64_t h) const {
+        if (h != hash || k.device != device || k.kind != kind || k.dtype != dtype ||
+            k.schedule != schedule || k.uniform != uniform || k.batch != batch || k.gm != gm ||
+            k.gn != gn || k.gk != gk || k.glayout != glayout)
+            return false;
+        const size_t n = static_cast<size_t>(k.n_entries());
+        auto same = [n](const auto& v, const auto* p) {
+            if (!p) return v.empty();
+            return v.size() == n && (n == 0 || std::memcmp(v.data(), p, n * sizeof(*p)) == 0);
+        };
+        return same(off, k.off) && same(R, k.R) && same(C, k.C);
+    }
+};
 
 struct CacheEntry {
     CacheKey key;
     bsm_plan plan;
 };
 
+struct DevBuf {  // a device table buffer of the pool
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    std::vector<hipStream_t> after;  // its last reader ran on these streams
+};
+
+struct PinBuf {  // a pinned staging buffer of the pool
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    hipEvent_t done = nullptr;  // recorded after the copy that reads it
+    bool pending = false;
+};
+
+struct DeviceCache {
+    std::list<CacheEntry> lru;           // most recently used first
+    std::vector<bsm_plan> graveyard;     // evicted, until no call is launching them
+    std::vector<DevBuf> free_bufs;       // reusable after stream waits
+    std::vector<void*> stale_bufs;       // readers not trackable: freed by bsm_cache_clear only
+    std::vector<PinBuf> pins;
+};
+
 std::mutex g_cache_mu;
-std::list<CacheEntry> g_cache;  // most recently used first
-constexpr size_t kCacheMax = 32;
+std::vector<std::unique_ptr<DeviceCache>> g_cache;  // by device ordinal
+
+DeviceCache& cache_of(int device) {
+    if (static_cast<size_t>(device) >= g_cache.size()) g_cache.resize(device + 1);
+    if (!g_cache[device]) g_cache[device].reset(new DeviceCache);
+    return *g_cache[device];
+}
+
+size_t pool_size(size_t need) {
+    size_t b = kMinPoolBytes;
+    while (b < need) b *= 2;
+    return b;
+}
 
 void destroy_plan(bsm_plan p) {
     if (!p) return;
     free_device(p);
+    if (p->upload_done) (void)hipEventDestroy(p->upload_done);
     delete p;
 }
 
-template <class Build>
-bsm_status cached_plan(CacheKey key, Build build, bsm_plan* out) {
-    for (auto it = g_cache.begin(); it != g_cache.end(); ++it) {
-        if (it->key == key) {
-            *out = it->plan;
-            g_cache.splice(g_cache.begin(), g_cache, it);
+bool is_capturing(hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &st) != hipSuccess || st != hipStreamCaptureStatusNone;
+}
+
+// Evicted plans no call is launching any more give their buffers back to the pool.
+void reclaim(DeviceCache& dc) {
+    auto it = dc.graveyard.begin();
+    while (it != dc.graveyard.end()) {
+        bsm_plan p = *it;
+        if (p->inflight.load(std::memory_order_acquire) != 0) {
+            ++it;
+            continue;
+        }
+        if (p->d_table) {
+            if (p->many_streams)
+                dc.stale_bufs.push_back(p->d_table);
+            else
+                dc.free_bufs.push_back(DevBuf{p->d_table, p->table_cap, p->streams});
+        }
+        p->d_table = nullptr;
+        destroy_plan(p);
+        it = dc.graveyard.erase(it);
+    }
+}
+
+// A device buffer of at least `need` bytes whose reuse is ordered on `stream` after its last
+// readers; the stream waits on events recorded on the other streams (no host wait).
+bsm_status take_device_buffer(DeviceCache& dc, size_t need, hipStream_t stream, DevBuf* out) {
+    reclaim(dc);
+    for (;;) {
+        int best = -1;
+        for (size_t i = 0; i < dc.free_bufs.size(); ++i) {
+            const DevBuf& b = dc.free_bufs[i];
+            if (b.bytes >= need && b.bytes <= 4 * pool_size(need) &&
+                (best < 0 || b.bytes < dc.free_bufs[best].bytes))
+                best = static_cast<int>(i);
+        }
+        if (best < 0) break;
+        DevBuf b = dc.free_bufs[best];
+        dc.free_bufs.erase(dc.free_bufs.begin() + best);
+        bool ok = true;
+        for (hipStream_t s : b.after) {
+            if (s == stream) continue;
+            // a stream that is capturing would take the event into its graph: not now
+            if (is_capturing(s)) {
+                ok = false;
+                break;
+            }
+            hipEvent_t ev = nullptr;
+            if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+                (void)hipGetLastError();
+                ok = false;
+                break;
+            }
+            const bool waited = hipEventRecord(ev, s) == hipSuccess &&
+                                hipStreamWaitEvent(stream, ev, 0) == hipSuccess;
+            (void)hipEventDestroy(ev);
+            if (!waited) {
+                (void)hipGetLastError();
+                ok = false;
+                break;
+            }
+        }
+        if (ok) {
+            *out = b;
             return BSM_OK;
         }
+        dc.stale_bufs.push_back(b.ptr);
     }
-    bsm_plan plan = nullptr;
-    bsm_status st = build(&plan);
-    if (st != BSM_OK) return st;
-    g_cache.push_front(CacheEntry{std::move(key), plan});
-    while (g_cache.size() > kCacheMax) {
-        destroy_plan(g_cache.back().plan);
-        g_cache.pop_back();
+    DevBuf b;
+    b.bytes = pool_size(need);
+    hipError_t e = table_malloc(&b.ptr, b.bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(e == hipErrorOutOfMemory ? BSM_ERR_OOM : BSM_ERR_HIP,
+                    "hipMalloc(%zu) for the work table: %s", b.bytes, hipGetErrorString(e));
     }
-    *out = plan;
+    *out = b;
     return BSM_OK;
 }
 
-// One-shot call: validates the geometry (no HIP call for bad arguments or no-ops), then runs a
-// plan from the per-device cache (built on a miss; plans do not depend on the op).
+bsm_status take_pinned_buffer(DeviceCache& dc, size_t need, PinBuf** out) {
+    PinBuf* best = nullptr;
+    for (PinBuf& pb : dc.pins) {
+        if (pb.bytes < need || !pb.done) continue;
+        if (pb.pending) {
+            hipError_t q = hipEventQuery(pb.done);
+            if (q == hipErrorNotReady) {
+                (void)hipGetLastError();  // not an error: leave no state behind for the caller
+                continue;
+            }
+            if (q != hipSuccess) return hip_fail(q, "hipEventQuery");
+            pb.pending = false;
+        }
+        if (!best || pb.bytes < best->bytes) best = &pb;
+    }
+    if (!best) {
+        PinBuf pb;
+        pb.bytes = pool_size(need);
+        hipError_t e = hipHostMalloc(&pb.ptr, pb.bytes, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(e == hipErrorOutOfMemory ? BSM_ERR_OOM : BSM_ERR_HIP,
+                        "hipHostMalloc(%zu) for table staging: %s", pb.bytes, hipGetErrorString(e));
+        }
+        e = hipEventCreateWithFlags(&pb.done, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            dc.pins.push_back(pb);  // the buffer is kept (freeing it would synchronise)
+            dc.pins.back().done = nullptr;
+            return hip_fail(e, "hipEventCreateWithFlags");
+        }
+        dc.pins.push_back(pb);
+        best = &dc.pins.back();
+    }
+    *out = best;
+    return BSM_OK;
+}
+
+// Uploads a freshly built plan's table on `stream` (caller holds the lock).
+bsm_status upload_pooled(DeviceCache& dc, bsm_plan p, hipStream_t stream) {
+    const size_t need = table_bytes(p->table);
+    const size_t items_at = table_items_at(p->table);
+    DevBuf buf;
+    bsm_status st = take_device_buffer(dc, need, stream, &buf);
+    if (st != BSM_OK) return st;
+    PinBuf* pin = nullptr;
+    st = take_pinned_buffer(dc, need, &pin);
+    if (st != BSM_OK || !pin->done) {
+        dc.free_bufs.push_back(DevBuf{buf.ptr, buf.bytes, {stream}});
+        return st != BSM_OK ? st : fail(BSM_ERR_HIP, "no staging event");
+    }
+    char* h = static_cast<char*>(pin->ptr);
+    std::memcpy(h, p->table.worker_ptr.data(), p->table.worker_ptr.size() * sizeof(int32_t));
+    if (!p->table.items.empty())
+        std::memcpy(h + items_at, p->table.items.data(), p->table.items.size() * sizeof(bsm_item));
+    hipEvent_t up = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&up, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipMemcpyAsync(buf.ptr, h, need, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipEventRecord(pin->done, stream);
+    if (e == hipSuccess) {
+        pin->pending = true;
+        e = hipEventRecord(up, stream);
+    }
+    if (e != hipSuccess) {
+        if (up) (void)hipEventDestroy(up);
+        dc.free_bufs.push_back(DevBuf{buf.ptr, buf.bytes, {stream}});
+        return hip_fail(e, "uploading the work table");
+    }
+    p->pooled = true;
+    p->d_table = buf.ptr;
+    p->table_cap = buf.bytes;
+    p->d_worker_ptr = static_cast<const int32_t*>(buf.ptr);
+    p->d_items = reinterpret_cast<const bsm_item*>(static_cast<char*>(buf.ptr) + items_at);
+    p->upload_stream = stream;
+    p->upload_done = up;
+    p->uploaded = false;
+    return BSM_OK;
+}
+
+// Hit bookkeeping (caller holds the lock): order the call after the table upload, track the
+// stream, pin a captured plan.
+bsm_status prepare_call(bsm_plan p, hipStream_t stream, bool capturing) {
+    if (!p->uploaded) {
+        hipError_t q = p->upload_done ? hipEventQuery(p->upload_done) : hipSuccess;
+        if (q == hipSuccess) {
+            p->uploaded = true;
+        } else if (capturing) {
+            (void)hipGetLastError();
+            return fail(BSM_ERR_UNSUPPORTED,
+                        "one-shot call under stream capture while its plan's table upload is "
+                        "still in flight; synchronise once before capturing");
+        } else if (q == hipErrorNotReady) {
+            (void)hipGetLastError();  // not an error: leave no state behind for the caller
+            if (stream != p->upload_stream) {
+                hipError_t e = hipStreamWaitEvent(stream, p->upload_done, 0);
+                if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+            }
+        } else {
+            return hip_fail(q, "hipEventQuery");
+        }
+    }
+    if (std::find(p->streams.begin(), p->streams.end(), stream) == p->streams.end()) {
+        if (p->streams.size() < kMaxTrackedStreams)
+            p->streams.push_back(stream);
+        else
+            p->many_streams = true;
+    }
+    if (capturing) p->captured = true;
+    p->inflight.fetch_add(1, std::memory_order_acq_rel);
+    return BSM_OK;
+}
+
+bsm_plan lookup(DeviceCache& dc, const KeyView& kv, uint64_t h) {
+    for (auto it = dc.lru.begin(); it != dc.lru.end(); ++it) {
+        if (it->key.matches(kv, h)) {
+            if (it != dc.lru.begin()) dc.lru.splice(dc.lru.begin(), dc.lru, it);
+            return dc.lru.front().plan;
+        }
+    }
+    return nullptr;
+}
+
+void evict(DeviceCache& dc) {
+    auto it = dc.lru.end();
+    while (dc.lru.size() > kCacheMax && it != dc.lru.begin()) {
+        --it;
+        if (it->plan->captured) continue;
+        dc.graveyard.push_back(it->plan);
+        it = dc.lru.erase(it);
+    }
+}
+
+// Runs `launch(plan)` on the cached plan for `kv`, building it with `build(&plan)` (a plan
+// with its table on the host only) on a miss.
+template <class Build, class Launch>
+bsm_status run_cached(const KeyView& kv, hipStream_t stream, Build build, Launch launch) {
+    const uint64_t h = hash_key(kv);
+    const bool capturing = is_capturing(stream);
+    bsm_plan plan = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        DeviceCache& dc = cache_of(kv.device);
+        plan = lookup(dc, kv, h);
+        if (plan) {
+            bsm_status st = prepare_call(plan, stream, capturing);
+            if (st != BSM_OK) return st;
+        }
+    }
+    if (!plan) {
+        if (capturing)
+            return fail(BSM_ERR_UNSUPPORTED,
+                        "one-shot call under stream capture with a geometry not in the plan cache "
+                        "(building a plan allocates and copies); run it once before capturing, "
+                        "or capture a plan's execution");
+        bsm_plan fresh = nullptr;
+        bsm_status st = build(&fresh);
+        if (st != BSM_OK) return st;
+        std::unique_ptr<bsm_plan_s> owner(fresh);  // no device memory yet
+        DeviceGuard g;
+        hipError_t e = g.enter(kv.device);
+        if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        DeviceCache& dc = cache_of(kv.device);
+        plan = lookup(dc, kv, h);  // another thread may have built it meanwhile
+        if (!plan) {
+            try {
+                dc.lru.push_front(CacheEntry{CacheKey(kv, h), fresh});
+            } catch (const std::bad_alloc&) {
+                return fail(BSM_ERR_OOM, "host allocation failed (plan cache)");
+            }
+            st = upload_pooled(dc, fresh, stream);
+            if (st != BSM_OK) {
+                dc.lru.pop_front();
+                return st;
+            }
+            plan = owner.release();
+            evict(dc);
+        }
+        st = prepare_call(plan, stream, false);
+        if (st != BSM_OK) return st;
+    }
+    bsm_status st = launch(plan);
+    plan->inflight.fetch_sub(1, std::memory_order_acq_rel);
+    return st;
+}
+
+// One-shot call: the arguments are checked before any HIP call (allocation-free in the
+// common case of slices in ascending order), then a cached plan for the geometry runs.
 bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
                     const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
                     int64_t batch, bsm_dtype dtype, bsm_schedule schedule, void* stream) {
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
     if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
-    bsm::Geometry geo;
-    std::string err;
-    try {
-        err = bsm::make_geometry(slice_offsets, rows, cols, batch, elem_bytes_of(dtype), &geo);
-    } catch (const std::bad_alloc&) {
-        return fail(BSM_ERR_OOM, "host allocation failed");
+    int64_t extent = 0;
+    if (!bsm::quick_geometry(slice_offsets, rows, cols, batch, &extent)) {
+        bsm::Geometry geo;
+        std::string err;
+        try {
+            err = bsm::make_geometry(slice_offsets, rows, cols, batch, elem_bytes_of(dtype), &geo);
+        } catch (const std::bad_alloc&) {
+            return fail(BSM_ERR_OOM, "host allocation failed");
+        }
+        if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
+        extent = geo.extent;
     }
-    if (!err.empty()) return fail(BSM_ERR_INVALID_ARG, "geometry: %s", err.c_str());
-    if (geo.total_elems == 0) return BSM_OK;
+    if (extent == 0) return BSM_OK;  // no element: nothing to do
     if (!a || !out || (backward && !b)) return fail(BSM_ERR_INVALID_ARG, "an input or the output is NULL");
-    const int64_t extent_bytes = geo.extent * elem_bytes_of(dtype);
+    const int64_t extent_bytes = extent * elem_bytes_of(dtype);
     if (partial_overlap(a, out, extent_bytes) || (backward && partial_overlap(b, out, extent_bytes)))
         return fail(BSM_ERR_ALIAS, "an input and the output overlap without being equal");
-
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    CacheKey key{device, dtype, schedule, slice_offsets == nullptr, batch, {}, {}, {}};
-    if (slice_offsets) {
-        key.off.assign(slice_offsets, slice_offsets + batch);
-        key.R.assign(rows, rows + batch);
-        key.C.assign(cols, cols + batch);
-    } else {
-        key.R.assign(rows, rows + 1);
-        key.C.assign(cols, cols + 1);
-    }
-    std::lock_guard<std::mutex> lock(g_cache_mu);
-    bsm_plan plan = nullptr;
-    bsm_status st = cached_plan(std::move(key), [&](bsm_plan* np) {
-        return create_plan(np, slice_offsets, rows, cols, batch, dtype, schedule, nullptr, nullptr,
-                           nullptr, device);
-    }, &plan);
-    if (st != BSM_OK) return st;
-    return execute_plan(plan, backward, a, b, out, stream, nullptr);
+    KeyView kv;
+    kv.device = device;
+    kv.kind = 0;
+    kv.dtype = dtype;
+    kv.schedule = schedule;
+    kv.uniform = slice_offsets == nullptr;
+    kv.batch = batch;
+    kv.off = slice_offsets;
+    kv.R = rows;
+    kv.C = cols;
+    return run_cached(
+        kv, static_cast<hipStream_t>(stream),
+        [&](bsm_plan* np) {
+            return create_plan(np, slice_offsets, rows, cols, batch, dtype, schedule, nullptr,
+                               nullptr, nullptr, device, 0, false, false);
+        },
+        [&](bsm_plan p) { return execute_plan(p, backward, a, b, out, stream, nullptr); });
 }
 
 }  // namespace
@@ -678,15 +1094,23 @@ bsm_status bsm_gemm(const void* a, const void* b, void* c, int64_t batch, int32_
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    CacheKey key{device, out_dtype, schedule, true, batch, {}, {m}, {n}, k, static_cast<int>(layout)};
-    std::lock_guard<std::mutex> lock(g_cache_mu);
-    bsm_plan plan = nullptr;
-    bsm_status st = cached_plan(std::move(key), [&](bsm_plan* np) {
-        return create_gemm_plan(np, batch, m, n, k, static_cast<int>(layout), out_dtype, schedule,
-                                nullptr, nullptr, device);
-    }, &plan);
-    if (st != BSM_OK) return st;
-    return execute_gemm(plan, a, b, c, alpha, stream, nullptr);
+    KeyView kv;
+    kv.device = device;
+    kv.kind = 1;
+    kv.dtype = out_dtype;
+    kv.schedule = schedule;
+    kv.batch = batch;
+    kv.gm = m;
+    kv.gn = n;
+    kv.gk = k;
+    kv.glayout = static_cast<int>(layout);
+    return run_cached(
+        kv, static_cast<hipStream_t>(stream),
+        [&](bsm_plan* np) {
+            return create_gemm_plan(np, batch, m, n, k, static_cast<int>(layout), out_dtype,
+                                    schedule, nullptr, nullptr, device, false);
+        },
+        [&](bsm_plan p) { return execute_gemm(p, a, b, c, alpha, stream, nullptr); });
 }
 
 bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
@@ -698,8 +1122,29 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
 
 bsm_status bsm_cache_clear(void) {
     std::lock_guard<std::mutex> lock(g_cache_mu);
-    for (auto& ent : g_cache) destroy_plan(ent.plan);
-    g_cache.clear();
+    for (size_t d = 0; d < g_cache.size(); ++d) {
+        if (!g_cache[d]) continue;
+        DeviceCache& dc = *g_cache[d];
+        // calls that found their plan before the lock was taken finish their launch first
+        for (bool busy = true; busy;) {
+            busy = false;
+            for (auto& ent : dc.lru) busy = busy || ent.plan->inflight.load() != 0;
+            for (bsm_plan p : dc.graveyard) busy = busy || p->inflight.load() != 0;
+            if (busy) std::this_thread::yield();
+        }
+        DeviceGuard g;
+        if (g.enter(static_cast<int>(d)) == hipSuccess) (void)hipDeviceSynchronize();
+        for (auto& ent : dc.lru) dc.graveyard.push_back(ent.plan);
+        dc.lru.clear();
+        reclaim(dc);
+        for (DevBuf& b : dc.free_bufs) (void)hipFree(b.ptr);
+        for (void* ptr : dc.stale_bufs) (void)hipFree(ptr);
+        for (PinBuf& pb : dc.pins) {
+            (void)hipHostFree(pb.ptr);
+            if (pb.done) (void)hipEventDestroy(pb.done);
+        }
+        g_cache[d].reset();
+    }
     return BSM_OK;
 }
 

@@ -490,6 +490,33 @@ std::string make_geometry(const int64_t* slice_offsets, const int32_t* rows, con
     return "";
 }
 
+bool quick_geometry(const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
+                    int64_t batch, int64_t* extent) {
+    *extent = 0;
+    if (batch < 0 || batch > std::numeric_limits<int32_t>::max()) return false;
+    if (batch == 0) return true;
+    if (!rows || !cols) return false;
+    if (!slice_offsets) {
+        const int64_t R = rows[0], C = cols[0];
+        if (R < 0 || C < 0) return false;
+        const int64_t per = R * C;
+        if (per > 0 && batch > kMaxElems / per) return false;
+        *extent = per * batch;
+        return true;
+    }
+    int64_t end = 0;  // end of the previous non-empty slice
+    for (int64_t s = 0; s < batch; ++s) {
+        if (rows[s] < 0 || cols[s] < 0 || slice_offsets[s] < 0) return false;
+        const int64_t sz = static_cast<int64_t>(rows[s]) * cols[s];
+        if (sz > kMaxElems || slice_offsets[s] > kMaxElems - sz) return false;
+        if (sz == 0) continue;
+        if (slice_offsets[s] < end) return false;  // out of order, or overlapping
+        end = slice_offsets[s] + sz;
+    }
+    *extent = end;
+    return true;
+}
+
 std::string check_topology(const Topology& t) {
     if (t.n_cu < 1 || t.n_cu > 65536) return "n_cu out of range";
     if (t.n_xcd < 1 || t.n_xcd > BSM_MAX_XCD) return "n_xcd out of range [1, 16]";

@@ -67,6 +67,12 @@ int64_t bank_chunk_elems(const Geometry& g, int n, bool contiguous);
 std::string make_geometry(const int64_t* slice_offsets, const int32_t* rows,
                           const int32_t* cols, int64_t batch, int elem_bytes, Geometry* g);
 
+// Allocation-free check of the common case, for calls that repeat a geometry: true, with the
+// extent, when the geometry is valid and its non-empty slices lie in ascending offset order;
+// false when make_geometry must decide (an error, or slices out of order).
+bool quick_geometry(const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
+                    int64_t batch, int64_t* extent);
+
 std::string check_topology(const Topology& t);
 
 // Builds the table for `schedule`.  home_xcd may be null.  kernel_class is the register-tile

@@ -157,3 +157,88 @@ def test_backward_validation_happens_before_any_gpu_call():
     assert lib.bsm_plan_execute_backward(p.handle, V(16), V(4096), V(8192), None, None) == bsm.BSM_ERR_UNSUPPORTED
     p.destroy()
     assert lib.bsm_plan_execute_backward(None, V(16), V(16), V(16), None, None) == bsm.BSM_ERR_INVALID_ARG
+
+
+def _rss_bytes():
+    with open("/proc/self/statm") as f:
+        return int(f.read().split()[1]) * os.sysconf("SC_PAGE_SIZE")
+
+
+def test_host_allocation_failure_reports_oom_frees_everything_and_recovers(monkeypatch):
+    """BSM_ERR_OOM path of plan creation: with the test hook BSM_TEST_ALLOC_FAIL=host, plan
+    creation fails after the whole table is built, as if a host allocation had failed. The call
+    returns BSM_ERR_OOM with a message, releases what it built (200 failed creations of a
+    16384-slice ragged plan, ~3 MB of table each, leave the resident set within 64 MB), and the
+    next creation without the hook succeeds with the same table as before."""
+    B = 16384
+    rows = np.full(B, 8, np.int32)
+    cols = np.full(B, 128, np.int32)
+    offs = (np.arange(B, dtype=np.int64) * (8 * 128 + 64))
+    args = dict(dtype="f32", schedule="balanced", topology=TOPO, device=-1)
+    ok = bsm.bsm_plan_create(rows, cols, offs, **args)
+    want = bsm.bsm_plan_export(ok)
+    ok.destroy()
+    monkeypatch.setenv("BSM_TEST_ALLOC_FAIL", "host")
+    st, msg = _status(bsm.bsm_plan_create, rows, cols, offs, **args)
+    assert st == bsm.BSM_ERR_OOM and "allocation" in msg, (st, msg)
+    base = _rss_bytes()
+    for _ in range(200):
+        st, _ = _status(bsm.bsm_plan_create, rows, cols, offs, **args)
+        assert st == bsm.BSM_ERR_OOM
+    grown = _rss_bytes() - base
+    assert grown < 64 << 20, f"resident set grew by {grown >> 20} MB over 200 failed creations"
+    monkeypatch.delenv("BSM_TEST_ALLOC_FAIL")
+    again = bsm.bsm_plan_create(rows, cols, offs, **args)
+    got = bsm.bsm_plan_export(again)
+    again.destroy()
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+def test_device_allocation_hook_needs_a_device_plan(monkeypatch):
+    """BSM_TEST_ALLOC_FAIL=device fails only the device table allocation: a host-only plan
+    (device -1) has none and is built as usual."""
+    monkeypatch.setenv("BSM_TEST_ALLOC_FAIL", "device")
+    p = bsm.bsm_plan_create([4], [64], [0], dtype="f32", schedule="balanced", topology=TOPO,
+                            device=-1)
+    assert bsm.bsm_plan_describe(p)["n_items"] > 0
+    p.destroy()
+
+
+def test_one_shot_argument_check_agrees_with_plan_validation():
+    """One-shot calls check a repeated geometry without building it (ascending slices), and fall
+    back to the full validation otherwise. On seeded random ragged geometries -- ordered,
+    shuffled, overlapping, with empty and negative entries -- the one-shot call rejects exactly
+    the geometries plan creation rejects (INVALID_ARG before any HIP call; a valid geometry goes
+    on to the device, which this machine does not have)."""
+    lib = bsm.load()
+    rng = np.random.default_rng(77)
+    seen = {"ok": 0, "bad": 0}
+    for t in range(300):
+        B = int(rng.integers(1, 9))
+        rows = rng.integers(0, 6, B)
+        cols = rng.integers(0, 40, B)
+        sizes = rows * cols
+        offs = np.concatenate([[0], np.cumsum(sizes + rng.integers(0, 8, B))])[:B]
+        kind = t % 5
+        if kind == 1:
+            offs = offs[rng.permutation(B)]
+        elif kind == 2 and B > 1:
+            i = int(rng.integers(1, B))
+            offs[i] = max(0, offs[i] - int(rng.integers(1, 30)))
+        elif kind == 3:
+            rows[int(rng.integers(0, B))] = -1
+        elif kind == 4:
+            offs[int(rng.integers(0, B))] = -int(rng.integers(1, 5))
+        r, c, o, rp, cp, op = _c_arrays(rows, cols, offs)
+        st_plan, _ = _status(bsm.bsm_plan_create, rows, cols, offs, dtype="f32",
+                             schedule="balanced", topology=TOPO, device=-1)
+        st_one = lib.bsm_softmax(ctypes.c_void_p(1 << 40), ctypes.c_void_p(1 << 41), op, rp, cp,
+                                 B, 0, 1, None)
+        if st_plan == bsm.BSM_ERR_INVALID_ARG:
+            assert st_one == bsm.BSM_ERR_INVALID_ARG, (t, rows, cols, offs)
+            seen["bad"] += 1
+        else:
+            assert st_plan == bsm.BSM_OK
+            assert st_one != bsm.BSM_ERR_INVALID_ARG, (t, rows, cols, offs, bsm.bsm_last_error())
+            seen["ok"] += 1
+    assert seen["ok"] > 50 and seen["bad"] > 50, seen

@@ -12,8 +12,8 @@ import oracle
 import paper_2002_07062_amd as bsm
 import workloads
 from gpu_util import (SENTINEL_BF16, SENTINEL_F32, backward_inputs, compare, compare_backward,
-                      covered_mask, run_plan, run_plan_backward, sentinel_like, to_device,
-                      to_host_bits)
+                      covered_mask, oracle_full, run_plan, run_plan_backward, sentinel_like,
+                      to_device, to_host_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -479,31 +479,82 @@ def test_bank_layouts_give_the_same_bits(cfg, batch):
         assert home.tolist() == ((s // group) % st_a["n_xcd"]).tolist()
 
 
-def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
-    """Weighted load balancing moves rows between XCDs but never changes a result; an XCD of
-    weight 0 runs no rows (per-wave trace)."""
-    w = workloads.generate("c5", batch=96)
-    x = to_device(w.x, "f32")
-    ref, _ = run_plan(w, "xcd", x=x)
+def _run_weighted(w, weights, pad=64):
+    """Runs w under the weighted XCD plan into a sentinel-filled output `pad` elements longer
+    than the slices' extent, with a per-wave trace; returns (output bits, stats, trace)."""
     n = int(w.offsets[-1])
-    out = sentinel_like(n, "f32")
-    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype="f32", schedule="xcd",
-                               device=0, xcd_weight=[1, 1, 1, 1, 1, 1, 1, 0])
+    x = to_device(w.x, w.dtype)
+    out = sentinel_like(n + pad, w.dtype)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule="xcd", device=0, xcd_weight=weights)
     st = bsm.bsm_plan_describe(plan)
     trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
     bsm.bsm_plan_execute(plan, x, out, trace=trace)
     torch.cuda.synchronize()
     plan.destroy()
-    assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
-    rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
-    # the workers planned for XCD 7 (w mod 8 == 7) run nothing, and so does the XCD that runs
-    # them (dispatch may rotate the whole grid by r XCDs)
+    return to_host_bits(out), st, trace.cpu().numpy().view(bsm.TRACE_DTYPE)
+
+
+def _check_weighted_against_oracle(w, bits, pad):
+    """Element by element against the fp64 oracle inside the slices; the sentinel untouched in
+    every element outside them (gaps and the tail past the extent)."""
+    n = int(w.offsets[-1])
+    mask = np.concatenate([covered_mask(w.offsets[: w.batch], w.rows, w.cols, n),
+                           np.zeros(pad, bool)])
+    ref = np.concatenate([oracle_full(w), np.zeros(pad)])
+    compare(bits, ref, w.dtype, mask)
+    sentinel = SENTINEL_F32 if w.dtype == "f32" else SENTINEL_BF16
+    assert np.all(bits[~mask] == sentinel), "an element outside the slices was written"
+
+
+def _rotation(rec):
     rot = set(((rec["xcc_id"].astype(np.int64) - rec["wg"].astype(np.int64)) % 8).tolist())
     assert len(rot) == 1, sorted(rot)
+    return rot.pop()
+
+
+def test_weighted_xcd_plan_same_bits_and_weight_zero_xcd_idle():
+    """Weighted load balancing (Section 4.2) moves rows between XCDs but never changes a result:
+    the output matches the fp64 oracle element by element and the unweighted plan bit for bit,
+    the sentinel survives outside the slices, and an XCD of weight 0 runs no rows (per-wave
+    trace)."""
+    w = workloads.generate("c5", batch=96)
+    ref, _ = run_plan(w, "xcd", x=to_device(w.x, "f32"))
+    pad = 64
+    bits, st, rec = _run_weighted(w, [1, 1, 1, 1, 1, 1, 1, 0], pad)
+    _check_weighted_against_oracle(w, bits, pad)
+    n = int(w.offsets[-1])
+    assert np.array_equal(bits[:n], to_host_bits(ref)[:n])
+    # the workers planned for XCD 7 (w mod 8 == 7) run nothing, and so does the XCD that runs
+    # them (dispatch may rotate the whole grid by r XCDs)
+    rot = _rotation(rec)
     assert rec["rows"][rec["wg"] % 8 == 7].sum() == 0
-    assert rec["rows"][rec["xcc_id"] == (7 + rot.pop()) % 8].sum() == 0
+    assert rec["rows"][rec["xcc_id"] == (7 + rot) % 8].sum() == 0
     assert rec["rows"].sum() == int(w.rows.sum())
     assert st["xcd_bytes"][7] == 0
+
+
+def test_weighted_xcd_plan_skewed_weights_uniform_batch():
+    """64 slices of 512 x 512 fp32 with skewed weights [4, 1, 1, 1, 1, 1, 1, 0.5]: XCD x is given
+    a share of the rows in proportion to its weight (every XCD has the same workgroups; whole
+    rows, so within two rows of the exact share), the rows each XCD's waves report match the
+    plan's per-XCD bytes, and the output matches the fp64
+    oracle element by element with the sentinel intact past the extent."""
+    w = workloads.generate("c2", batch=64)
+    weights = [4, 1, 1, 1, 1, 1, 1, 0.5]
+    pad = 128
+    bits, st, rec = _run_weighted(w, weights, pad)
+    _check_weighted_against_oracle(w, bits, pad)
+    row_bytes = 512 * 4 * 2
+    total = int(st["algorithmic_bytes"])
+    xb = np.array(st["xcd_bytes"][:8], np.int64)
+    assert int(xb.sum()) == total
+    share = np.array(weights) / sum(weights) * total
+    assert np.all(np.abs(xb - share) <= 2 * row_bytes), (xb.tolist(), share.tolist())
+    rot = _rotation(rec)
+    for x in range(8):
+        rows_x = int(rec["rows"][rec["xcc_id"] == (x + rot) % 8].sum())
+        assert rows_x * row_bytes == int(xb[x]), (x, rows_x)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

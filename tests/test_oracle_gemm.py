@@ -106,3 +106,53 @@ def test_bad_arguments():
         gemm.batched_gemm(a, a, 2, 3, 4, 4, "nt")
     with pytest.raises(TypeError):
         gemm.batched_gemm(np.zeros(12, np.float32), a, 1, 3, 4, 4, "nt")
+
+
+# bf16 bit patterns of the small integers below, written out by hand (sign, 8-bit exponent with
+# bias 127, 7-bit mantissa): an independent check of the decode as well.
+_BF16_HAND = {0: 0x0000, 1: 0x3F80, -1: 0xBF80, 2: 0x4000, -2: 0xC000, 3: 0x4040,
+              -4: 0xC080, 5: 0x40A0, 6: 0x40C0, 0.5: 0x3F00, 7: 0x40E0, 0.25: 0x3E80,
+              -3: 0xC040, 4: 0x4080}
+
+
+def _hand_bits(vals):
+    return np.array([_BF16_HAND[v] for v in vals], np.uint16)
+
+
+@pytest.mark.parametrize("layout", ["nt", "nn"])
+def test_abs_product_sums_hand_values(layout):
+    """sum_k |a_ik| |b_kj| written out by hand on mixed-sign integers, two batch indices.
+
+    Batch 0: A = [[1, -2, 3], [-1, 0, 2]], B (one key per row, NT) = [[-4, 5, 6], [2, 1, 0]]:
+      S[0][0] = 1*4 + 2*5 + 3*6 = 32     (the signed sum is -4 - 10 + 18 = 4)
+      S[0][1] = 1*2 + 2*1 + 3*0 = 4      (signed: 2 - 2 + 0 = 0)
+      S[1][0] = 1*4 + 0*5 + 2*6 = 16
+      S[1][1] = 1*2 + 0*1 + 2*0 = 2      (signed: -2)
+    Batch 1: A = [[0.5, 0, -4], [7, 1, -1]], B = [[2, -3, 0.25], [-1, 4, 1]]:
+      S[0][0] = 0.5*2 + 0*3 + 4*0.25 = 2
+      S[0][1] = 0.5*1 + 0*4 + 4*1 = 4.5
+      S[1][0] = 7*2 + 1*3 + 1*0.25 = 17.25
+      S[1][1] = 7*1 + 1*4 + 1*1 = 12
+    A product of row sums (sum|a| * sum|b|: 6 * 15 = 90 at [0][0]), a missing absolute value,
+    a factor of k or 2, or batch 0's B reused for batch 1 each changes some entry."""
+    a = [1, -2, 3, -1, 0, 2, 0.5, 0, -4, 7, 1, -1]
+    b_nt = [[[-4, 5, 6], [2, 1, 0]], [[2, -3, 0.25], [-1, 4, 1]]]
+    if layout == "nt":
+        b = [v for batch in b_nt for row in batch for v in row]
+    else:  # NN stores B as k x n: the transpose of the NT rows above
+        b = [batch[j][q] for batch in b_nt for q in range(3) for j in range(2)]
+    s = gemm.abs_product_sums(_hand_bits(a), _hand_bits(b), 2, 2, 2, 3, layout)
+    assert s.tolist() == [32.0, 4.0, 16.0, 2.0, 2.0, 4.5, 17.25, 12.0]
+    # the decode of the hand-written patterns, through the product itself
+    c = gemm.batched_gemm(_hand_bits(a), _hand_bits(b), 2, 2, 2, 3, layout)
+    assert c.tolist() == [4.0, 0.0, 16.0, -2.0, 0.0, -4.5, 10.75, -4.0]
+
+
+def test_abs_product_sums_one_row_hand_values():
+    """m = n = 1, k = 4 over two batch indices: sum|a||b| = 3+3+2+2 = 10 and
+    0.5*2 + 0*7 + 4*0.25 + 1*3 = 5 (batch 0's B would give 6.5)."""
+    a = [1, -1, 2, -2, 0.5, 0, -4, 1]
+    b = [3, 3, -1, 1, 2, 7, 0.25, -3]
+    for layout in ("nt", "nn"):  # with n = 1 both layouts store B the same way
+        s = gemm.abs_product_sums(_hand_bits(a), _hand_bits(b), 2, 1, 1, 4, layout)
+        assert s.tolist() == [10.0, 5.0]
