@@ -223,6 +223,26 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets,
                        const int32_t* rows, const int32_t* cols, int64_t batch,
                        bsm_dtype dtype, bsm_schedule schedule, void* stream);
 
+/* Size of the static device buffer of bsm_softmax_noalloc (per device). */
+#define BSM_NOALLOC_SCRATCH_BYTES (8 * 1024 * 1024)
+
+/* bsm_softmax for callers that cannot allocate device memory (hipMalloc is not allowed where
+ * they run: tight serving loops, harnesses that forbid it).  Same arguments, checks and result
+ * as bsm_softmax, but nothing is allocated on the device or pinned on the host and no plan is
+ * cached: every call builds its plan on the host and copies its work table into a static
+ * device buffer of BSM_NOALLOC_SCRATCH_BYTES bytes that the library holds on each device until
+ * the process ends.  A plan whose table is larger (the call's message gives its size) returns
+ * BSM_ERR_INVALID_ARG; BALANCED tables of the 384-slice workloads take 64 KiB (512 x 512
+ * slices) to 3.4 MiB (ragged 64..1024-wide slices).  The copy is stream-ordered on `stream`
+ * and the call returns once it has reached the device (it waits for the work queued before it
+ * on `stream`); the kernel then runs asynchronously.  Every call on a device shares its
+ * buffer: calls on one stream run in order, but calls that overlap on one device through
+ * different streams or threads race (a later call may overwrite the table an earlier launch
+ * is still reading).  Under stream capture it returns BSM_ERR_UNSUPPORTED. */
+bsm_status bsm_softmax_noalloc(const void* in, void* out, const int64_t* slice_offsets,
+                               const int32_t* rows, const int32_t* cols, int64_t batch,
+                               bsm_dtype dtype, bsm_schedule schedule, void* stream);
+
 /* Build a reusable plan: the work table of the HW batch scheduler of Section 5, built once
  * up front and reused for every execution.  The table is uploaded to the device before this
  * returns (synchronously).

@@ -6,10 +6,10 @@ this package is its ctypes binding. Build with `python -m paper_2002_07062_amd.b
 
 from .bsm import (  # noqa: F401
     BSM_BF16, BSM_ERR_ALIAS, BSM_ERR_HIP, BSM_ERR_INVALID_ARG, BSM_ERR_OOM, BSM_ERR_UNSUPPORTED,
-    BSM_F32, BSM_FLAG_CONTIGUOUS_BANKS, BSM_FLAG_TEMPORAL, BSM_OK, BSM_SCHED_BALANCED, BSM_SCHED_RR, BSM_SCHED_XCD, DTYPES, ITEM_DTYPE,
+    BSM_F32, BSM_FLAG_CONTIGUOUS_BANKS, BSM_NOALLOC_SCRATCH_BYTES, BSM_FLAG_TEMPORAL, BSM_OK, BSM_SCHED_BALANCED, BSM_SCHED_RR, BSM_SCHED_XCD, DTYPES, ITEM_DTYPE,
     LIB_PATH, SCHEDULES, TRACE_DTYPE, BsmError, Plan, bsm_abi_version, bsm_cache_clear, bsm_copy,
     bsm_default_topology, bsm_device_info, bsm_last_error, bsm_plan_create, bsm_plan_describe,
     bsm_plan_destroy, bsm_plan_execute, bsm_plan_execute_backward, bsm_plan_export, bsm_softmax,
-    bsm_softmax_backward, bsm_status_string, BSM_GEMM_NN, BSM_GEMM_NT, GEMM_LAYOUTS, bsm_gemm,
+    bsm_softmax_backward, bsm_softmax_noalloc, bsm_status_string, BSM_GEMM_NN, BSM_GEMM_NT, GEMM_LAYOUTS, bsm_gemm,
     bsm_gemm_execute, bsm_gemm_plan_create,
     bsm_topology, load)

@@ -24,6 +24,7 @@ BSM_OK, BSM_ERR_INVALID_ARG, BSM_ERR_UNSUPPORTED, BSM_ERR_ALIAS, BSM_ERR_OOM, BS
 BSM_F32, BSM_BF16 = 0, 1
 BSM_SCHED_RR, BSM_SCHED_BALANCED, BSM_SCHED_XCD = 0, 1, 2
 BSM_MAX_XCD = 16
+BSM_NOALLOC_SCRATCH_BYTES = 8 * 1024 * 1024  # static buffer of bsm_softmax_noalloc
 BSM_FLAG_TEMPORAL = 1
 BSM_FLAG_CONTIGUOUS_BANKS = 2
 
@@ -111,6 +112,8 @@ def load() -> ctypes.CDLL:
     sig = {
         "bsm_softmax": ([vp, vp, P(i64), P(i32), P(i32), i64, ctypes.c_int, ctypes.c_int, vp],
                         ctypes.c_int),
+        "bsm_softmax_noalloc": ([vp, vp, P(i64), P(i32), P(i32), i64, ctypes.c_int, ctypes.c_int,
+                                 vp], ctypes.c_int),
         "bsm_plan_create": ([P(vp), P(i64), P(i32), P(i32), i64, ctypes.c_int, ctypes.c_int,
                              P(ctypes.c_int8), P(bsm_topology), ctypes.c_int], ctypes.c_int),
         "bsm_plan_create_weighted": ([P(vp), P(i64), P(i32), P(i32), i64, ctypes.c_int,
@@ -242,6 +245,22 @@ def bsm_softmax(x, out, rows, cols, slice_offsets=None, batch=None, schedule="ba
     with torch.cuda.device(x.device):
         _check(lib.bsm_softmax(_ptr(x), _ptr(out), op, rp, cp, n, _dtype_code(x.dtype),
                                _schedule_code(schedule), _stream_of(x, stream)))
+    return out
+
+
+def bsm_softmax_noalloc(x, out, rows, cols, slice_offsets=None, batch=None, schedule="balanced",
+                        stream=None):
+    """bsm_softmax with the work table in the library's static device buffer (no device or
+    pinned allocation; see bsm.h). Returns out."""
+    lib = load()
+    if out.dtype != x.dtype:
+        raise TypeError("x and out must share a dtype")
+    keep = _geometry(rows, cols, slice_offsets, batch)
+    o, op, r, rp, c, cp, n = keep
+    _check_sizes(_extent(o, r, c, n), x, out)
+    with torch.cuda.device(x.device):
+        _check(lib.bsm_softmax_noalloc(_ptr(x), _ptr(out), op, rp, cp, n, _dtype_code(x.dtype),
+                                       _schedule_code(schedule), _stream_of(x, stream)))
     return out
 
 

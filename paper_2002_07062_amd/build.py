@@ -44,7 +44,7 @@ def build(verbose: bool = False) -> str:
     hipcc = _hipcc()
     sources = ["bsm_kernels.hip", "bsm_kernels_f32.hip", "bsm_kernels_f32_shifted.hip",
                "bsm_kernels_bf16.hip", "bsm_kernels_bf16_shifted.hip", "bsm_gemm.hip",
-               "bsm_api.cpp", "bsm_plan.cpp"]
+               "bsm_noalloc.hip", "bsm_api.cpp", "bsm_plan.cpp"]
     with tempfile.TemporaryDirectory(prefix="bsm_build_") as tmp:
         def compile_one(src: str) -> str:
             obj = os.path.join(tmp, src.replace(".", "_") + ".o")

@@ -962,11 +962,12 @@ bsm_status run_cached(const KeyView& kv, hipStream_t stream, Build build, Launch
     return st;
 }
 
-// One-shot call: the arguments are checked before any HIP call (allocation-free in the
-// common case of slices in ascending order), then a cached plan for the geometry runs.
-bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
-                    const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
-                    int64_t batch, bsm_dtype dtype, bsm_schedule schedule, void* stream) {
+// Argument checks of the one-shot calls, before any HIP call (allocation-free in the common
+// case of slices in ascending order).  *extent = 0: nothing to do.
+bsm_status check_one_shot(bool backward, const void* a, const void* b, const void* out,
+                          const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
+                          int64_t batch, bsm_dtype dtype, bsm_schedule schedule, int64_t* extent_out) {
+    *extent_out = 0;
     if (!valid_dtype(dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(dtype));
     if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
     int64_t extent = 0;
@@ -986,6 +987,18 @@ bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
     const int64_t extent_bytes = extent * elem_bytes_of(dtype);
     if (partial_overlap(a, out, extent_bytes) || (backward && partial_overlap(b, out, extent_bytes)))
         return fail(BSM_ERR_ALIAS, "an input and the output overlap without being equal");
+    *extent_out = extent;
+    return BSM_OK;
+}
+
+// One-shot call: checked arguments, then a cached plan for the geometry runs.
+bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
+                    const int64_t* slice_offsets, const int32_t* rows, const int32_t* cols,
+                    int64_t batch, bsm_dtype dtype, bsm_schedule schedule, void* stream) {
+    int64_t extent = 0;
+    bsm_status st = check_one_shot(backward, a, b, out, slice_offsets, rows, cols, batch, dtype,
+                                   schedule, &extent);
+    if (st != BSM_OK || extent == 0) return st;
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -1006,6 +1019,53 @@ bsm_status one_shot(bool backward, const void* a, const void* b, void* out,
                                nullptr, nullptr, device, 0, false, false);
         },
         [&](bsm_plan p) { return execute_plan(p, backward, a, b, out, stream, nullptr); });
+}
+
+// bsm_softmax with the work table in the library's static device buffer: the plan is built on
+// the host for this call only and its table copied into the buffer on `stream`; nothing is
+// allocated on the device or pinned.
+bsm_status softmax_noalloc(const void* in, void* out, const int64_t* slice_offsets,
+                           const int32_t* rows, const int32_t* cols, int64_t batch,
+                           bsm_dtype dtype, bsm_schedule schedule, void* stream) {
+    int64_t extent = 0;
+    bsm_status st = check_one_shot(false, in, nullptr, out, slice_offsets, rows, cols, batch,
+                                   dtype, schedule, &extent);
+    if (st != BSM_OK || extent == 0) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (is_capturing(s))
+        return fail(BSM_ERR_UNSUPPORTED, "bsm_softmax_noalloc under stream capture (its table "
+                                         "copy waits for the stream)");
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    bsm_plan raw = nullptr;
+    st = create_plan(&raw, slice_offsets, rows, cols, batch, dtype, schedule, nullptr, nullptr,
+                     nullptr, device, 0, false, false);
+    if (st != BSM_OK) return st;
+    std::unique_ptr<bsm_plan_s> p(raw);  // host table only
+    const size_t need = table_bytes(p->table);
+    if (need > static_cast<size_t>(BSM_NOALLOC_SCRATCH_BYTES))
+        return fail(BSM_ERR_INVALID_ARG,
+                    "work table of %zu bytes (%lld items) exceeds the %d bytes of the "
+                    "bsm_softmax_noalloc buffer",
+                    need, static_cast<long long>(p->table.items.size()), BSM_NOALLOC_SCRATCH_BYTES);
+    void* scratch_ptr = nullptr;
+    e = bsm::noalloc_scratch(device, &scratch_ptr);
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the static buffer");
+    char* base = static_cast<char*>(scratch_ptr);
+    const size_t items_at = table_items_at(p->table);
+    // pageable sources: the copies complete before they return, in stream order on `s`
+    e = hipMemcpyAsync(base, p->table.worker_ptr.data(),
+                       p->table.worker_ptr.size() * sizeof(int32_t), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && !p->table.items.empty())
+        e = hipMemcpyAsync(base + items_at, p->table.items.data(),
+                           p->table.items.size() * sizeof(bsm_item), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host table is freed on return
+    if (e != hipSuccess) return hip_fail(e, "copying the work table to the static buffer");
+    p->pooled = true;  // the buffer is not the plan's
+    p->d_worker_ptr = reinterpret_cast<const int32_t*>(base);
+    p->d_items = reinterpret_cast<const bsm_item*>(base + items_at);
+    return execute_plan(p.get(), false, in, nullptr, out, stream, nullptr);
 }
 
 }  // namespace
@@ -1066,6 +1126,12 @@ bsm_status bsm_softmax(const void* in, void* out, const int64_t* slice_offsets, 
                        void* stream) {
     return one_shot(false, in, nullptr, out, slice_offsets, rows, cols, batch, dtype, schedule,
                     stream);
+}
+
+bsm_status bsm_softmax_noalloc(const void* in, void* out, const int64_t* slice_offsets,
+                               const int32_t* rows, const int32_t* cols, int64_t batch,
+                               bsm_dtype dtype, bsm_schedule schedule, void* stream) {
+    return softmax_noalloc(in, out, slice_offsets, rows, cols, batch, dtype, schedule, stream);
 }
 
 bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,

@@ -64,4 +64,9 @@ hipError_t resident_wgs_per_cu(bsm_dtype dtype, int kernel_class, bool shifted, 
 
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int n_cu, hipStream_t stream);
 
+// Device address of `device`'s copy of the static scratch buffer of bsm_softmax_noalloc
+// (BSM_NOALLOC_SCRATCH_BYTES bytes, 256-byte aligned), looked up once per device with
+// hipGetSymbolAddress; `device` must be current.
+hipError_t noalloc_scratch(int device, void** ptr);
+
 }  // namespace bsm

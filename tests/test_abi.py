@@ -242,3 +242,41 @@ def test_one_shot_argument_check_agrees_with_plan_validation():
             assert st_one != bsm.BSM_ERR_INVALID_ARG, (t, rows, cols, offs, bsm.bsm_last_error())
             seen["ok"] += 1
     assert seen["ok"] > 50 and seen["bad"] > 50, seen
+
+
+def test_noalloc_buffer_size_matches_the_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define BSM_NOALLOC_SCRATCH_BYTES \((\d+) \* (\d+) \* (\d+)\)", text)
+    assert m, "BSM_NOALLOC_SCRATCH_BYTES not found"
+    assert int(m.group(1)) * int(m.group(2)) * int(m.group(3)) == bsm.BSM_NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_checks_arguments_before_any_gpu_call():
+    lib = bsm.load()
+    r, c, o, rp, cp, op = _c_arrays([4, 4], [64, 64], [0, 256])
+    assert lib.bsm_softmax_noalloc(None, None, None, rp, cp, 0, 0, 0, None) == bsm.BSM_OK
+    assert lib.bsm_softmax_noalloc(None, None, op, rp, cp, 2, 0, 0, None) == bsm.BSM_ERR_INVALID_ARG
+    assert lib.bsm_softmax_noalloc(ctypes.c_void_p(1 << 20), ctypes.c_void_p((1 << 20) + 64), op,
+                                   rp, cp, 2, 0, 0, None) == bsm.BSM_ERR_ALIAS
+    r2, c2, o2, rp2, cp2, op2 = _c_arrays([4, 4], [64, 64], [0, 100])
+    assert lib.bsm_softmax_noalloc(ctypes.c_void_p(16), ctypes.c_void_p(16), op2, rp2, cp2, 2, 0,
+                                   0, None) == bsm.BSM_ERR_INVALID_ARG
+
+
+def test_largest_workload_tables_fit_the_noalloc_buffer():
+    """The BALANCED and XCD tables of the 384-slice workloads (host-only plans on the MI355X
+    topology) fit the static buffer of bsm_softmax_noalloc."""
+    import workloads
+
+    topo = dict(n_cu=256, n_xcd=8)
+    for cfg in ("c2", "c3", "c5"):
+        w = workloads.generate(cfg, values=False)
+        for sch in ("balanced", "xcd", "rr"):
+            p = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                                    schedule=sch, topology=dict(topo, wg_threads=256,
+                                                                wg_per_cu=2 if w.dtype == "f32" else 4),
+                                    device=-1)
+            d = bsm.bsm_plan_describe(p)
+            p.destroy()
+            need = ((d["n_workers"] + 1) * 4 + 255) // 256 * 256 + max(d["n_items"], 1) * 32
+            assert need <= bsm.BSM_NOALLOC_SCRATCH_BYTES, (cfg, sch, need)

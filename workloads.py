@@ -133,9 +133,11 @@ def packed_offsets(rows: np.ndarray, cols: np.ndarray) -> np.ndarray:
     return off
 
 
-def generate(name: str, seed: int | None = None, batch: int | None = None) -> Workload:
+def generate(name: str, seed: int | None = None, batch: int | None = None,
+             values: bool = True) -> Workload:
     """Draw one workload. `batch` (<= the spec's) keeps only the first slices' geometry, with
-    the same draws for them, for tests that need a small but faithful sample."""
+    the same draws for them, for tests that need a small but faithful sample. values=False
+    draws the geometry only (x is empty)."""
     sp = spec(name)
     rng = np.random.default_rng(sp.seed if seed is None else seed)
     B = sp.batch
@@ -158,6 +160,9 @@ def generate(name: str, seed: int | None = None, batch: int | None = None) -> Wo
             mask_len = mask_len[:batch]
     offsets = packed_offsets(rows, cols)
     total = int(offsets[-1])
+    if not values:
+        return Workload(sp.name, sp.dtype, np.zeros(0, np.float32), offsets, rows, cols,
+                        uniform=sp.ragged is None, mask_len=mask_len)
     x = rng.standard_normal(total, dtype=np.float32)
     x *= np.float32(sp.sigma)
     if sp.dtype == BF16:
