@@ -313,15 +313,21 @@ def trace_stats(w, schedule):
     busy = (rec["t_end"] - rec["t_start"]).astype(np.float64) / hz * 1e6
     t0, t1 = int(rec["t_start"].min()), int(rec["t_end"].max())
     span = (t1 - t0) / hz * 1e6
-    per_xcd = {}
+    per_xcd, idle_xcd, start_xcd = {}, {}, {}
     for x_id in np.unique(rec["xcc_id"]):
         m = rec["xcc_id"] == x_id
         per_xcd[int(x_id)] = round(float((rec["t_end"][m].max() - t0) / hz * 1e6), 2)
+        start_xcd[int(x_id)] = round(float((rec["t_start"][m].min() - t0) / hz * 1e6), 2)
+        # wave-time of this XCD's waves left idle before the kernel's last wave ends
+        idle_xcd[int(x_id)] = round(1.0 - float(busy[m].sum()) / (int(m.sum()) * span), 4) if span > 0 else 0.0
     working = rec["rows"] > 0
+    n_xcd = max(1, int(st["n_xcd"]))
+    rot = sorted(set(((rec["xcc_id"].astype(np.int64) - rec["wg"].astype(np.int64)) % n_xcd).tolist()))
     return {"makespan_us": round(span, 2), "mean_wave_busy_us": round(float(busy.mean()), 2),
             "idle_frac": round(1.0 - float(busy.sum()) / (len(busy) * span), 4) if span > 0 else 0.0,
             "waves_with_work": int(working.sum()), "waves": int(len(rec)),
-            "xcd_finish_us": per_xcd}
+            "xcd_finish_us": per_xcd, "xcd_first_start_us": start_xcd, "xcd_idle_frac": idle_xcd,
+            "xcc_minus_wg_mod_n_xcd": rot}
 
 
 def producer_consumer(iters=20):
@@ -469,23 +475,228 @@ def l2_locality(nslices=16, iters=30):
     return res
 
 
-def cpu_baseline(w):
+def time_hip_memcpy(xs, outs, nbytes, steps, warmup):
+    """hipMemcpyAsync device-to-device of `nbytes` (the runtime's own copy engine path), same
+    rotation and timing as time_copy: the vendor copy ceiling beside the library's copy kernel."""
+    import ctypes
+
+    import torch
+
+    hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch has loaded (same SONAME)
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
+    dtod = 3  # hipMemcpyDeviceToDevice
+    stream = torch.cuda.current_stream().cuda_stream
+    n = len(xs)
+
+    def cp(i):
+        rc = hip.hipMemcpyAsync(outs[i % n].data_ptr(), xs[i % n].data_ptr(), nbytes, dtod, stream)
+        if rc != 0:
+            raise RuntimeError(f"hipMemcpyAsync failed ({rc})")
+
+    for i in range(warmup):
+        cp(i)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        cp(i)
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def c3_balanced_bits(w):
+    """One BALANCED launch on the bf16 workload `w`; returns the output's raw bf16 bits (host)."""
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+
+    x = _to_device(w)
+    out = torch.zeros_like(x)
+    plan = bsm.bsm_plan_create(w.rows, w.cols, w.offsets[: w.batch], dtype=w.dtype,
+                               schedule="balanced", device=0)
+    bsm.bsm_plan_execute(plan, x, out)
+    torch.cuda.synchronize()
+    plan.destroy()
+    bits = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    del x, out
+    torch.cuda.empty_cache()
+    return bits
+
+
+def launch_bound_c1(steps=200, warmup=20):
+    """C1 (8 slices of 64 x 64 fp32, 256 KiB): launch-bound, so the figure is microseconds per
+    call. Per schedule: a plan's back-to-back executions (event-timed region / steps) and the
+    host time of plan creation; and the one-shot call on a warm cache, called through the C ABI
+    with its arguments marshalled once, and through the Python binding: host microseconds per
+    call (argument checks, cache lookup, launch) and the event-timed region per call."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    import paper_2002_07062_amd as bsm
+    import workloads
+
+    w = workloads.generate("c1")
+    res = {"workload": w.name, "algorithmic_bytes": w.algorithmic_bytes}
+    for sch in ("rr", "balanced", "xcd"):
+        r, _ = run_workload("c1", sch, steps, warmup, rotate=2, w=w)
+        res[sch] = {"us_per_call": round(r["ms_per_step"] * 1e3, 3),
+                    "plan_build_ms": round(r["plan_build_ms"], 3), "n_items": r["n_items"]}
+    x = _to_device(w)
+    out = torch.empty_like(x)
+    R, C = int(w.rows[0]), int(w.cols[0])
+    lib = bsm.load()
+    rows = np.array([R], np.int32)
+    cols = np.array([C], np.int32)
+    rp = rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    cp = cols.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    stream = torch.cuda.current_stream().cuda_stream
+    xp, op = x.data_ptr(), out.data_ptr()
+
+    def c_abi():
+        rc = lib.bsm_softmax(xp, op, None, rp, cp, w.batch, bsm.BSM_F32, bsm.BSM_SCHED_BALANCED,
+                             stream)
+        if rc != bsm.BSM_OK:
+            raise RuntimeError(bsm.bsm_last_error())
+
+    def binding():
+        bsm.bsm_softmax(x, out, R, C, batch=w.batch)
+
+    for label, fn in (("one_shot_cached_c_abi", c_abi), ("one_shot_cached_python", binding)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        h0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        host = (time.perf_counter() - h0) / steps
+        t1.record()
+        torch.cuda.synchronize()
+        res[label] = {"host_us_per_call": round(host * 1e6, 2),
+                      "us_per_call": round(t0.elapsed_time(t1) / steps * 1e3, 3)}
+    return res
+
+
+def vendor_bmm(name, steps, warmup):
+    """The same batched product through torch.bmm (hipBLASLt), bf16 operands and output,
+    rotated like run_gemm; the scores product gets K already transposed and contiguous (bf16
+    bmm of a transposed view is avoided). Times the product only."""
+    import numpy as np
+    import torch
+
+    batch, m, n, k, layout = GEMM_SHAPES[name]
+    nbytes = batch * (2 * (m * k + n * k) + 2 * m * n)
+    n_sets = _rotation(nbytes)
+    rng = np.random.default_rng(5)
+    a0 = torch.from_numpy(rng.standard_normal(batch * m * k, dtype=np.float32)).to(torch.bfloat16).cuda()
+    b0 = torch.from_numpy(rng.standard_normal(batch * n * k, dtype=np.float32)).to(torch.bfloat16).cuda()
+    A = [a0.view(batch, m, k)] + [a0.clone().view(batch, m, k) for _ in range(n_sets - 1)]
+    if layout == "nt":  # B stored n x k per batch: hand bmm its transpose as a k x n copy
+        B = [b0.view(batch, n, k).transpose(1, 2).contiguous() for _ in range(n_sets)]
+    else:
+        B = [b0.view(batch, k, n)] + [b0.clone().view(batch, k, n) for _ in range(n_sets - 1)]
+    Cs = [torch.empty(batch, m, n, dtype=torch.bfloat16, device="cuda") for _ in range(n_sets)]
+    for i in range(warmup):
+        torch.bmm(A[i % n_sets], B[i % n_sets], out=Cs[i % n_sets])
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        torch.bmm(A[i % n_sets], B[i % n_sets], out=Cs[i % n_sets])
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    del A, B, Cs, a0, b0
+    torch.cuda.empty_cache()
+    return {"us": round(ms * 1e3, 2), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "algorithmic_bytes": nbytes, "library": "torch.bmm (hipBLASLt)"}
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _bf16_rne_bits(v):
+    """Round-to-nearest-even bf16 bit patterns of non-negative fp64 values (exact: the two bf16
+    neighbours are compared in fp64; ties go to the even pattern)."""
+    import numpy as np
+
+    f = v.astype(np.float32)  # within 2^-24 of v: the bf16 neighbours of v are those of f
+    lo = (f.view(np.uint32) >> 16).astype(np.uint32)
+    hi = lo + 1
+    lo_v = (lo << 16).view(np.float32).astype(np.float64)
+    hi_v = (hi << 16).view(np.float32).astype(np.float64)
+    d_lo, d_hi = v - lo_v, hi_v - v
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (lo % 2 == 1))
+    return np.where(pick_hi, hi, lo).astype(np.uint16)
+
+
+def cpu_baseline(w, bf16_check=None):
+    """The fp64 oracle timed on this host: the whole workload at 1 thread and on all the
+    threads this job may use (its affinity, capped at the 16 host threads a one-GPU job is
+    given), repeated until 3 s have passed. bf16_check = (workload, GPU output bits): the oracle
+    also runs on that bf16 workload (timed the same way, once), and the GPU outputs that are not
+    the round-to-nearest-even bf16 of the fp64 value are counted."""
+    import numpy as np
+
     import oracle
 
-    threads = min(16, len(os.sched_getaffinity(0)))
-    out = None
-    reps = 0
-    t0 = time.perf_counter()
-    # the whole workload, repeated until at least 3 s have passed (at least three times)
-    while reps < 3 or time.perf_counter() - t0 < 3.0:
-        out = oracle.softmax(w.x, w.dtype, w.offsets[: w.batch], w.rows, w.cols, nthreads=threads,
-                             out=out)
-        reps += 1
-    dt = (time.perf_counter() - t0) / reps
-    return {"value": round(w.algorithmic_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt * reps, 3),
-            "sample": f"all {w.batch} slices of {w.name}, {reps} times (fp64 reference, {threads} "
-                      "threads, bytes counted as the fp32 read-once + write-once of the GPU path)"}
+    avail = len(os.sched_getaffinity(0))
+    share = min(16, avail)
+
+    def timed(threads, min_s=3.0, work=w):
+        out, reps = None, 0
+        t0 = time.perf_counter()
+        while reps < 1 or time.perf_counter() - t0 < min_s:
+            out = oracle.softmax(work.x, work.dtype, work.offsets[: work.batch], work.rows,
+                                 work.cols, nthreads=threads, out=out)
+            reps += 1
+        dt = (time.perf_counter() - t0) / reps
+        return out, dt, reps
+
+    _, dt, reps = timed(share)
+    _, dt1, reps1 = timed(1)
+    res = {"value": round(w.algorithmic_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": share,
+           "kind": "oracle", "seconds": round(dt * reps, 3),
+           "sample": f"all {w.batch} slices of {w.name}, {reps} times (fp64 reference, {share} "
+                     "threads, bytes counted as the fp32 read-once + write-once of the GPU path)",
+           "single_thread": {"value": round(w.algorithmic_bytes / dt1 / 1e9, 3), "unit": "GB/s",
+                             "cores": 1, "seconds": round(dt1 * reps1, 3),
+                             "sample": f"all {w.batch} slices of {w.name}, {reps1} times"},
+           "host_threads_in_affinity": avail, "cpu_model": _cpu_model()}
+    if bf16_check is not None:
+        wb, bits = bf16_check
+        ref, dtb, _ = timed(share, 0.0, wb)
+        live = ~np.isnan(ref)
+        covered = np.zeros(ref.shape[0], bool)
+        for o, R, C in zip(wb.offsets[: wb.batch], wb.rows, wb.cols):
+            covered[int(o):int(o) + int(R) * int(C)] = True
+        sel = live & covered
+        non_rne = int(np.count_nonzero(bits[sel] != _bf16_rne_bits(ref[sel])))
+        res["bf16_rounding"] = {
+            "workload": wb.name, "outputs": int(sel.sum()), "non_rne": non_rne,
+            "non_rne_frac": non_rne / max(1, int(sel.sum())),
+            "oracle_seconds": round(dtb, 3),
+            "note": "GPU bf16 outputs (BALANCED) that differ from the round-to-nearest-even "
+                    "bf16 of the fp64 oracle value"}
+    return res
 
 
 def main() -> int:
@@ -578,9 +789,11 @@ def main() -> int:
     outs = [torch.empty_like(x0) for _ in range(n_pairs)]
     half = w.algorithmic_bytes // 2
     copy_ms = time_copy(xs, outs, half, args.steps, args.warmup)
+    memcpy_ms = time_hip_memcpy(xs, outs, half, args.steps, args.warmup)
     del xs, outs, x0
     torch.cuda.empty_cache()
     copy_gbs = w.algorithmic_bytes / (copy_ms * 1e-3) / 1e9
+    memcpy_gbs = w.algorithmic_bytes / (memcpy_ms * 1e-3) / 1e9
 
     extra = {}
     if not args.no_extra:
@@ -588,7 +801,7 @@ def main() -> int:
             if sch == args.schedule:
                 continue
             r, _ = run_workload(args.workload, sch, args.steps, args.warmup, w=w)
-            extra[f"{args.workload}_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_worker_cost")}
+            extra[f"{args.workload}_{sch}"] = {k: r[k] for k in ("gbs", "launch_ms_avg", "ms_per_step", "max_over_mean_worker_cost", "plan_build_ms")}
         for sch in ("rr", "balanced", "xcd"):
             if sch != args.schedule:
                 extra[f"{args.workload}_{sch}"]["trace"] = trace_stats(w, sch)
@@ -597,10 +810,13 @@ def main() -> int:
             for sch in ("rr", "balanced", "xcd"):
                 r, wk = run_workload(cfg, sch, args.steps, args.warmup, w=wk)
                 extra[f"{cfg}_{sch}"] = {k: r[k] for k in ("gbs", "ms_per_step", "max_over_mean_worker_cost",
-                                                        "moved_bytes", "n_items")}
-                if cfg == "c5":
+                                                        "moved_bytes", "n_items", "plan_build_ms")}
+                if cfg in ("c4", "c5"):
                     extra[f"{cfg}_{sch}"]["trace"] = trace_stats(wk, sch)
+                if cfg == "c3" and sch == "balanced":
+                    c3_bits = c3_balanced_bits(wk)
             del wk
+        extra["c1"] = launch_bound_c1()
         # one GPU's share of C2 under 8-way head sharding: 48 slices, where a slice per
         # workgroup can occupy at most 48 of the 512 workgroups
         wk = workloads.generate("c2", batch=48)
@@ -621,6 +837,7 @@ def main() -> int:
                                             for k, v in r.items()} for sch, r in res.items()}
             extra[f"gemm_{gname}"]["balanced_over_rr"] = round(res["rr"]["ms_per_step"] /
                                                                res["balanced"]["ms_per_step"], 3)
+            extra[f"gemm_{gname}"]["vendor"] = vendor_bmm(gname, args.steps, args.warmup)
         extra["producer_consumer"] = producer_consumer()
         extra["attention_pipeline"] = attention_pipeline()
         extra["l2_locality_16MB_us"] = l2_locality()
@@ -639,7 +856,12 @@ def main() -> int:
         extra["odd_backward_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step")}
 
     head_trace = None if args.no_extra else trace_stats(w, args.schedule)
-    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
+    cpu = None
+    if not args.no_cpu_baseline:
+        check = None
+        if not args.no_extra:
+            check = (workloads.generate("c3"), c3_bits)
+        cpu = cpu_baseline(w, check)
     achieved = head["launch_gbs"]
     prof, current = _profiled(head["workload"], args.schedule)
     line = {
@@ -673,10 +895,18 @@ def main() -> int:
                      "launch_us_median_single": round(head["launch_ms_median"] * 1e3, 2),
                      "launch_us_p10_single": round(head["launch_ms_p10"] * 1e3, 2),
                      "launch_us_p90_single": round(head["launch_ms_p90"] * 1e3, 2),
-                     "bytes_per_launch": head["algorithmic_bytes"]},
+                     "bytes_per_launch": head["algorithmic_bytes"],
+                     "profile": (f"profiles/bsm_softmax_kernel.{head['workload']}.{args.schedule}.json: "
+                                 "rocprofv3 summary committed with the kernel source it was taken "
+                                 "on (same sha256 as now), on another MI355X of the same kind"
+                                 if (prof and current) else None)},
         "trace": head_trace,
         "copy_ceiling": {"gbs": round(copy_gbs, 2), "us": round(copy_ms * 1e3, 2),
-                         "softmax_pct_of_copy": round(100.0 * head["gbs"] / copy_gbs, 2)},
+                         "softmax_pct_of_copy": round(100.0 * head["gbs"] / copy_gbs, 2),
+                         "hipMemcpyAsync_dtod_gbs": round(memcpy_gbs, 2),
+                         "hipMemcpyAsync_dtod_us": round(memcpy_ms * 1e3, 2),
+                         "softmax_pct_of_hipMemcpyAsync": round(100.0 * head["gbs"] / memcpy_gbs, 2)},
+        "plan_build_ms": round(head["plan_build_ms"], 3),
         "cpu_baseline": cpu,
         "device": {"arch": info["arch"], "n_cu": info["n_cu"], "n_xcd": info["n_xcd"]},
         "extra": extra,

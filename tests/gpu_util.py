@@ -82,6 +82,27 @@ def compare(y_bits: np.ndarray, y_ref: np.ndarray, dtype: str, mask: np.ndarray 
     return (float(err.max()) if err.size else 0.0), int(y.size)
 
 
+def bf16_rne_bits(v: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even bf16 bit patterns of non-negative fp64 values: the two bf16
+    neighbours of v (those of its nearest fp32, which lies within half an fp32 ulp of v, never
+    across a bf16 value) compared in fp64, ties to the even pattern."""
+    f = v.astype(np.float32)
+    lo = (f.view(np.uint32) >> 16).astype(np.uint32)
+    hi = lo + 1
+    lo_v = (lo << 16).view(np.float32).astype(np.float64)
+    hi_v = (hi << 16).view(np.float32).astype(np.float64)
+    d_lo, d_hi = v - lo_v, hi_v - v
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (lo % 2 == 1))
+    return np.where(pick_hi, hi, lo).astype(np.uint16)
+
+
+def count_non_rne(y_bits: np.ndarray, y_ref: np.ndarray) -> tuple[int, int]:
+    """bf16 outputs that are not the round-to-nearest-even of the fp64 reference (NaN rows
+    excluded): (count, outputs compared)."""
+    live = ~np.isnan(y_ref)
+    return int(np.count_nonzero(y_bits[live] != bf16_rne_bits(y_ref[live]))), int(live.sum())
+
+
 def run_plan(w, schedule="xcd", x=None, out=None, topology=None, trace=None, home_xcd=None):
     """Run the workload through bsm_plan_create/execute; returns (out tensor, plan stats)."""
     offsets = w.offsets[: w.batch]

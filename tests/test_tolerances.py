@@ -52,3 +52,20 @@ def test_backward_tolerance_bf16_inputs_decode():
     one = backward_tolerance(np.array([1], np.float32), np.array([-3], np.float32), "f32",
                              [0], [1], [1])
     assert one.tolist() == [30 * U]
+
+
+def test_bf16_rne_bits_hand_values():
+    """Round-to-nearest-even to bf16 on hand-chosen values: exact bf16 values stay; 1 + 2^-8
+    (the midpoint between 1 and 1 + 2^-7) goes to the even 1.0 = 0x3F80; 1 + 3 * 2^-8 (the
+    midpoint between 1 + 2^-7 and 1 + 2^-6) goes to the even 1 + 2^-6 = 0x3F82; just above a
+    midpoint rounds up, just below rounds down; 0 gives +0; 1/3 = 0x3EAB (0.333984375 is
+    nearer than 0.33203125)."""
+    from gpu_util import bf16_rne_bits, count_non_rne
+
+    v = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -8 + 2 ** -30, 1 + 2 ** -8 - 2 ** -30,
+                  0.0, 1 / 3, 0.5, 2 ** -20])
+    want = [0x3F80, 0x3F80, 0x3F82, 0x3F81, 0x3F80, 0x0000, 0x3EAB, 0x3F00, 0x3580]
+    assert bf16_rne_bits(v).tolist() == want
+    bits = np.array(want, np.uint16)
+    bits[2] = 0x3F81  # one output rounded the other way
+    assert count_non_rne(bits, v) == (1, len(v))
