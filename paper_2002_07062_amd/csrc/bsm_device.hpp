@@ -83,17 +83,20 @@ __device__ __forceinline__ float group_reduce(float v) {
     return v;
 }
 
-// In-lane pairwise reduction of K values (K a power of two).
+// In-lane pairwise reduction of K values: neighbours combine in pairs, an odd last value is
+// carried to the next level, until one is left (a fixed tree for each K).
 template <int K, class Op>
 __device__ __forceinline__ float lane_reduce(const float* x) {
-    static_assert(K > 0 && (K & (K - 1)) == 0, "lane_reduce needs a power of two");
+    static_assert(K > 0, "lane_reduce needs a value");
     if constexpr (K == 1) {
         return x[0];
     } else {
-        float t[K / 2];
+        constexpr int H = (K + 1) / 2;
+        float t[H];
 #pragma unroll
         for (int i = 0; i < K / 2; ++i) t[i] = Op::f(x[2 * i], x[2 * i + 1]);
-        return lane_reduce<K / 2, Op>(t);
+        if constexpr (K % 2 == 1) t[H - 1] = x[K - 1];
+        return lane_reduce<H, Op>(t);
     }
 }
 
@@ -297,26 +300,33 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
 // base + k * stride.  Within a range the worker's rows are wave*RPW + sub + j*step, j = 0, 1,
 // ... (RPW = 64/G rows per wave, step = rows covered by all the worker's waves at once); loop
 // trip counts depend on the wave only, so lanes never diverge across iterations.
-template <class E, int G, int V, bool VEC, bool SHIFT>
+template <class E, int G, int V, int U, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t run_item(const typename E::T* in, typename E::T* out,
                                              int64_t base, int cols, int nrows, int reps,
                                              int64_t stride, int wave, int nwaves, int lane64) {
     constexpr int RPW = 64 / G;
-    // Rows in flight per group: kVecsInFlight 16-byte loads per lane for aligned rows; one row
-    // for the element-wise path, whose per-element addresses cost registers.
-    constexpr int U = bsm::rows_per_group_in_flight(V, VEC);
     const int sub = lane64 / G;
     const int lane = lane64 % G;
     const int step = nwaves * RPW;
     uint32_t done = 0;
     for (int k = 0; k < reps; ++k) {
         const int64_t b = base + k * stride;
-        for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
+        int r0 = wave * RPW;
+        // U rows per group while the last of them still has a row; the rest one at a time, so a
+        // short remainder does not pay for U rows
+        for (; r0 + (U - 1) * step < nrows; r0 += U * step) {
             rows_u<E, G, V, U, VEC, SHIFT>(in, out, b, cols, nrows, r0 + sub, step, lane);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int left = nrows - (r0 + u * step);
-                done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+                done += left < RPW ? left : RPW;
+            }
+        }
+        if constexpr (U > 1) {
+            for (; r0 < nrows; r0 += step) {
+                rows_u<E, G, V, 1, VEC, SHIFT>(in, out, b, cols, nrows, r0 + sub, step, lane);
+                const int left = nrows - r0;
+                done += left < RPW ? left : RPW;
             }
         }
     }
@@ -746,23 +756,39 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
                                                   int64_t stride, int wave, int nwaves,
                                                   int lane64, float* lds, int cap, bool team) {
     const int nvec = VEC ? span_vecs<E, SHIFT>(cols) : (cols + E::kEPV - 1) / E::kEPV;
-#define BSM_RUN(G, V) run_item<E, G, V, VEC, SHIFT>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
-    if (nvec <= 16) return BSM_RUN(16, 1);
-    if (nvec <= 32) return BSM_RUN(32, 1);
-    // Larger register tiles only for 16-byte vectors; longer element-wise rows take the one-wave
-    // path.  Rows of 33..64 vectors: 32 lanes x 2 vectors rather than 64 x 1 (a shorter
-    // butterfly and half the per-row work per value: +7% on 384 x 512 x 512 bf16); the host
-    // gives such rows kernel class 1, so the tile depends on the row length only.
-    if constexpr (VEC && KCLASS >= 1) {
-        if (nvec <= 64) return BSM_RUN(32, 2);
-        if (nvec <= 128) return BSM_RUN(64, 2);
-    }
-    if (nvec <= 64) return BSM_RUN(64, 1);
-    if constexpr (VEC && KCLASS >= 2) {
-        if (nvec <= 256) return BSM_RUN(64, 4);
-    }
-    if constexpr (VEC && KCLASS >= 3) {
-        if (nvec <= 512) return BSM_RUN(64, 8);
+#define BSM_RUN(G, V, U) run_item<E, G, V, U, VEC, SHIFT>(in, out, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    if constexpr (VEC) {
+        // the tile of bsm::tile_for: one wave-uniform branch per (G, V, U) the class can pick
+        constexpr bool F = E::kBytes == 4;
+        const bsm::Tile t = bsm::tile_for(nvec, KCLASS < 3 ? KCLASS : 3, E::kBytes);
+#define BSM_TILE(g, v, u) if (t.G == g && t.V == v && t.U == u) return BSM_RUN(g, v, u)
+        BSM_TILE(16, 1, 4);
+        if constexpr (F) BSM_TILE(32, 1, 8);
+        BSM_TILE(32, 1, 4);
+        if constexpr (KCLASS >= 1) {
+            if constexpr (F) {
+                BSM_TILE(32, 2, 4);
+                BSM_TILE(16, 5, 1);
+                BSM_TILE(64, 2, 3);
+            }
+            BSM_TILE(32, 2, 2);
+            BSM_TILE(64, 2, 2);
+        }
+        if constexpr (KCLASS >= 2) {
+            if constexpr (F) BSM_TILE(32, 5, 1);
+            BSM_TILE(64, 4, 1);
+        }
+        if constexpr (KCLASS >= 3) {
+            if constexpr (F) BSM_TILE(64, 5, 1);
+            BSM_TILE(64, 8, 1);
+        }
+#undef BSM_TILE
+    } else {
+        // element-wise rows (buffers not 16-byte aligned), one row per group in flight: the
+        // per-element addresses cost registers; longer rows take the one-wave path
+        if (nvec <= 16) return BSM_RUN(16, 1, 1);
+        if (nvec <= 32) return BSM_RUN(32, 1, 1);
+        if (nvec <= 64) return BSM_RUN(64, 1, 1);
     }
 #undef BSM_RUN
     if constexpr (VEC && KCLASS >= 4) {

@@ -10,22 +10,48 @@ constexpr int kWave = 64;
 constexpr int kVecBytes = 16;   // one 128-bit access
 constexpr int kVecsInFlight = 4;  // 16-byte loads per lane a wave keeps in flight (any dtype)
 
-// Lanes per row G and 16-byte vectors per lane V for a row of `nvec` vectors.  Rows beyond
-// 64 * max_v vectors take the two-pass path (G = 64, V = 0).
+// Register tile of an aligned row of `nvec` 16-byte vectors in a kernel of class `kclass`: G
+// lanes per row (a group), V vectors per lane, U rows per group in flight.  V = 0: beyond the
+// register tiles of the class.
+//
+// Measured on MI355X (uniform batches of ~200 MB): a tile streams at the copy rate when it is
+// full; a partly filled one loses in proportion to the bytes its lanes keep in flight.  fp32
+// rows (8 waves per CU) therefore take tiles that keep about 4-5 KiB per wave in flight: more
+// rows per group for half-filled 32-lane tiles, 5 vectors per lane where a 5-vector tile fits
+// the row better than a power of two.  bf16 rows run 16 waves per CU with twice the arithmetic
+// per byte: larger tiles raise their registers past that occupancy, and they keep the
+// power-of-two tiles with four 16-byte loads per lane in flight.  Rows of 33..64 vectors take
+// 32 lanes x 2 vectors rather than 64 x 1 (a shorter butterfly and half the per-row work per
+// value: +7% on 384 x 512 x 512 bf16).
 struct Tile {
     int G;
     int V;
+    int U;
 };
 
-constexpr Tile tile_for(int64_t nvec, int max_v) {
-    if (nvec <= 16) return Tile{16, 1};
-    if (nvec <= 32) return Tile{32, 1};
-    if (max_v >= 2 && nvec <= 64) return Tile{32, 2};  // (kernel class >= 1 for such rows)
-    if (nvec <= 64) return Tile{64, 1};
-    if (max_v >= 2 && nvec <= 128) return Tile{64, 2};
-    if (max_v >= 4 && nvec <= 256) return Tile{64, 4};
-    if (max_v >= 8 && nvec <= 512) return Tile{64, 8};
-    return Tile{64, 0};
+constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes) {
+    if (nvec <= 16) return Tile{16, 1, 4};
+    if (elem_bytes == 4 && nvec <= 24) return Tile{32, 1, 8};
+    if (nvec <= 32) return Tile{32, 1, 4};
+    if (kclass >= 1) {
+        if (elem_bytes == 4) {
+            if (nvec <= 40) return Tile{32, 2, 4};
+            if (nvec <= 64) return Tile{32, 2, 2};
+            if (nvec <= 80) return Tile{16, 5, 1};
+            if (nvec <= 96) return Tile{64, 2, 3};
+        }
+        if (nvec <= 64) return Tile{32, 2, 2};
+        if (nvec <= 128) return Tile{64, 2, 2};
+    }
+    if (kclass >= 2) {
+        if (elem_bytes == 4 && nvec <= 160) return Tile{32, 5, 1};
+        if (nvec <= 256) return Tile{64, 4, 1};
+    }
+    if (kclass >= 3) {
+        if (elem_bytes == 4 && nvec <= 320) return Tile{64, 5, 1};
+        if (nvec <= 512) return Tile{64, 8, 1};
+    }
+    return Tile{64, 0, 1};
 }
 
 // Rows beyond the register tile are held in the registers of a whole workgroup: kTeamThreads
@@ -41,27 +67,17 @@ constexpr int team_threads(int kernel_class) {
     return kernel_class >= kLongestClass ? 2 * kTeamThreads : kTeamThreads;
 }
 
-// Rows per group a wave keeps in flight: enough rows that each lane has kVecsInFlight 16-byte
-// loads outstanding (one row for the element-wise and two-pass paths).
+// Rows per group for kVecsInFlight 16-byte loads per lane (one row for the element-wise path);
+// the backward pass, which reads two inputs, keeps half as many rows in flight.
 constexpr int rows_per_group_in_flight(int V, bool vec_path) {
     return (!vec_path || V == 0 || V >= kVecsInFlight) ? 1 : kVecsInFlight / V;
-}
-
-// Rows a wave keeps in flight per step: that many rows per group of G lanes, 64/G groups.
-constexpr int rows_in_flight(int G, int V, bool vec_path) {
-    return (kWave / G) * rows_per_group_in_flight(V, vec_path);
-}
-
-// Largest register tile (vectors per lane) a kernel class carries.
-constexpr int max_v_of_class(int kernel_class) {
-    return kernel_class <= 0 ? 1 : kernel_class == 1 ? 2 : kernel_class == 2 ? 4 : 8;
 }
 
 // Rows one wave finishes per step for a row of `cols` elements (aligned rows).
 constexpr int wave_step_rows(int64_t cols, int elem_bytes, int kernel_class) {
     const int64_t nvec = (cols * elem_bytes + kVecBytes - 1) / kVecBytes;
-    const Tile t = tile_for(nvec, max_v_of_class(kernel_class));
-    return rows_in_flight(t.G, t.V, true);
+    const Tile t = tile_for(nvec, kernel_class, elem_bytes);
+    return t.V == 0 ? 1 : (kWave / t.G) * t.U;
 }
 
 }  // namespace bsm
