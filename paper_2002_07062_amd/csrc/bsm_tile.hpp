@@ -51,6 +51,14 @@ constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes) {
         if (elem_bytes == 4 && nvec <= 320) return Tile{64, 5, 1};
         if (nvec <= 512) return Tile{64, 8, 1};
     }
+    if (kclass >= 4) {
+        // long-row plans (workgroup workers, 8 waves per CU): rows of up to 768 vectors are
+        // still held by one wave each, the workgroup's waves taking turns at the item's rows
+        // (a 16-vector tile measured 3.5% slower than the workgroup-held row at 1024 fp32
+        // vectors, and does not fit 256 registers in bf16)
+        if (nvec <= 640) return Tile{64, 10, 1};
+        if (nvec <= 768) return Tile{64, 12, 1};
+    }
     return Tile{64, 0, 1};
 }
 
@@ -73,11 +81,15 @@ constexpr int rows_per_group_in_flight(int V, bool vec_path) {
     return (!vec_path || V == 0 || V >= kVecsInFlight) ? 1 : kVecsInFlight / V;
 }
 
-// Rows one wave finishes per step for a row of `cols` elements (aligned rows).
+// Rows one worker finishes per step for a row of `cols` elements (aligned rows): one wave's
+// tile step, times the waves of the workgroup that is the worker in long-row plans (kernel
+// class >= 4); one row for a row the workgroup holds.
 constexpr int wave_step_rows(int64_t cols, int elem_bytes, int kernel_class) {
     const int64_t nvec = (cols * elem_bytes + kVecBytes - 1) / kVecBytes;
     const Tile t = tile_for(nvec, kernel_class, elem_bytes);
-    return t.V == 0 ? 1 : (kWave / t.G) * t.U;
+    if (t.V == 0) return 1;
+    const int rows = (kWave / t.G) * t.U;
+    return kernel_class >= 4 ? rows * (team_threads(kernel_class) / kWave) : rows;
 }
 
 }  // namespace bsm
