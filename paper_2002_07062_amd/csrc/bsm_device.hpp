@@ -33,6 +33,11 @@
 #include "bsm.h"
 #include "bsm_tile.hpp"
 
+// No multiply-add contraction anywhere in this code: the same row may run through different
+// instances (a tile's U-row and one-row forms), and a fused a*b+c in one of them would round
+// differently from the other, so a row's bits would depend on the schedule.
+#pragma clang fp contract(off)
+
 namespace bsm_dev {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -914,26 +919,33 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
     }
 }
 
-template <class E, int G, int V, bool VEC, bool SHIFT>
+template <class E, int G, int V, int U, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t run_item_bwd(const typename E::T* y, const typename E::T* dy,
                                                  typename E::T* dx, int64_t base, int cols,
                                                  int nrows, int reps, int64_t stride, int wave,
                                                  int nwaves, int lane64) {
     constexpr int RPW = 64 / G;
-    constexpr int UF = bsm::rows_per_group_in_flight(V, VEC);
-    constexpr int U = UF >= 2 ? UF / 2 : 1;
     const int sub = lane64 / G;
     const int lane = lane64 % G;
     const int step = nwaves * RPW;
     uint32_t done = 0;
     for (int k = 0; k < reps; ++k) {
         const int64_t b = base + k * stride;
-        for (int r0 = wave * RPW; r0 < nrows; r0 += U * step) {
+        int r0 = wave * RPW;
+        // as run_item: U rows per group while the last of them has a row, then one at a time
+        for (; r0 + (U - 1) * step < nrows; r0 += U * step) {
             rows_u_bwd<E, G, V, U, VEC, SHIFT>(y, dy, dx, b, cols, nrows, r0 + sub, step, lane);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int left = nrows - (r0 + u * step);
-                done += left <= 0 ? 0 : (left < RPW ? left : RPW);
+                done += left < RPW ? left : RPW;
+            }
+        }
+        if constexpr (U > 1) {
+            for (; r0 < nrows; r0 += step) {
+                rows_u_bwd<E, G, V, 1, VEC, SHIFT>(y, dy, dx, b, cols, nrows, r0 + sub, step, lane);
+                const int left = nrows - r0;
+                done += left < RPW ? left : RPW;
             }
         }
     }
@@ -1205,17 +1217,32 @@ __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
             return team_item_bwd<E, KCLASS, SHIFT>(y, dy, dx, base, cols, nrows, reps, stride,
                                                    wave, nwaves, lane64);
     }
-#define BSM_RUN_BWD(G, V) run_item_bwd<E, G, V, VEC, SHIFT>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
-    // (Rows of 33..64 vectors keep 64 lanes x 1 vector here: with two input streams the
-    // forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x 512 bf16.)
-    if (nvec <= 16) return BSM_RUN_BWD(16, 1);
-    if (nvec <= 32) return BSM_RUN_BWD(32, 1);
-    if (nvec <= 64) return BSM_RUN_BWD(64, 1);
-    if constexpr (VEC && KCLASS >= 1) {
-        if (nvec <= 128) return BSM_RUN_BWD(64, 2);
-    }
-    if constexpr (VEC && KCLASS >= 2) {
-        if (nvec <= 256) return BSM_RUN_BWD(64, 4);
+#define BSM_RUN_BWD(G, V, U) run_item_bwd<E, G, V, U, VEC, SHIFT>(y, dy, dx, base, cols, nrows, reps, stride, wave, nwaves, lane64)
+    if constexpr (VEC) {
+        // the tile of bsm::tile_for_bwd (rows of 33..64 vectors keep 64 lanes x 1 vector: with
+        // two input streams the forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x
+        // 512 bf16)
+        constexpr bool F = E::kBytes == 4;
+        const bsm::Tile t = bsm::tile_for_bwd(nvec, KCLASS < 3 ? KCLASS : 3, E::kBytes);
+#define BSM_TILE(g, v, u) if (t.G == g && t.V == v && t.U == u) return BSM_RUN_BWD(g, v, u)
+        BSM_TILE(16, 1, 2);
+        if constexpr (F) BSM_TILE(32, 1, 4);
+        BSM_TILE(32, 1, 2);
+        if constexpr (KCLASS >= 1) {
+            if constexpr (F) {
+                BSM_TILE(64, 1, 4);
+                BSM_TILE(64, 2, 2);
+            }
+            BSM_TILE(64, 1, 2);
+            BSM_TILE(64, 2, 1);
+        }
+        if constexpr (KCLASS >= 2) BSM_TILE(64, 4, 1);
+        if constexpr (F && KCLASS >= 3) BSM_TILE(64, 8, 1);
+#undef BSM_TILE
+    } else {
+        if (nvec <= 16) return BSM_RUN_BWD(16, 1, 1);
+        if (nvec <= 32) return BSM_RUN_BWD(32, 1, 1);
+        if (nvec <= 64) return BSM_RUN_BWD(64, 1, 1);
     }
 #undef BSM_RUN_BWD
     if constexpr (!VEC || KCLASS >= 3) {

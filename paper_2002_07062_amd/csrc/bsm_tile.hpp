@@ -8,7 +8,6 @@ namespace bsm {
 
 constexpr int kWave = 64;
 constexpr int kVecBytes = 16;   // one 128-bit access
-constexpr int kVecsInFlight = 4;  // 16-byte loads per lane a wave keeps in flight (any dtype)
 
 // Register tile of an aligned row of `nvec` 16-byte vectors in a kernel of class `kclass`: G
 // lanes per row (a group), V vectors per lane, U rows per group in flight.  V = 0: beyond the
@@ -62,6 +61,28 @@ constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes) {
     return Tile{64, 0, 1};
 }
 
+// Register tile of the backward pass (two input streams, y and dy) for an aligned row of
+// `nvec` vectors; V = 0: the one-wave or workgroup paths.  bf16 rows keep half the forward
+// pass's rows in flight.  fp32 rows, like the forward pass, keep about 4-5 KiB of both streams
+// per wave in flight where a power-of-two tile is partly empty, and rows of 257-512 vectors
+// keep a 64 x 8 register tile (the one-wave path, staging y and dy in LDS, ran them at
+// 3.7 TB/s).
+constexpr Tile tile_for_bwd(int64_t nvec, int kclass, int elem_bytes) {
+    const bool f = elem_bytes == 4;
+    if (nvec <= 16) return Tile{16, 1, 2};
+    if (f && nvec <= 24) return Tile{32, 1, 4};
+    if (nvec <= 32) return Tile{32, 1, 2};
+    if (kclass >= 1) {
+        if (f && nvec <= 40) return Tile{64, 1, 4};
+        if (nvec <= 64) return Tile{64, 1, 2};
+        if (f && nvec <= 80) return Tile{64, 2, 2};
+        if (nvec <= 128) return Tile{64, 2, 1};
+    }
+    if (kclass >= 2 && nvec <= 256) return Tile{64, 4, 1};
+    if (f && kclass >= 3 && nvec <= 512) return Tile{64, 8, 1};
+    return Tile{64, 0, 1};
+}
+
 // Rows beyond the register tile are held in the registers of a whole workgroup: kTeamThreads
 // threads with up to kTeamValues values per lane in kernel class 4 (rows of up to
 // kTeamThreads * kTeamValues elements), twice that in class 5, whose instances need twice the
@@ -73,12 +94,6 @@ constexpr int kLongestClass = 6;
 // Threads of the workgroup that holds a row, by kernel class (>= 4).
 constexpr int team_threads(int kernel_class) {
     return kernel_class >= kLongestClass ? 2 * kTeamThreads : kTeamThreads;
-}
-
-// Rows per group for kVecsInFlight 16-byte loads per lane (one row for the element-wise path);
-// the backward pass, which reads two inputs, keeps half as many rows in flight.
-constexpr int rows_per_group_in_flight(int V, bool vec_path) {
-    return (!vec_path || V == 0 || V >= kVecsInFlight) ? 1 : kVecsInFlight / V;
 }
 
 // Rows one worker finishes per step for a row of `cols` elements (aligned rows): one wave's
