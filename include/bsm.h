@@ -111,8 +111,9 @@ typedef struct bsm_topology {
 /* Virtual banks of the XCD schedule (Section 4.1's memory banks; MI355X in NPS1 interleaves HBM
  * over all stacks, so a bank is a planning construct).  By default the span of the non-empty
  * slices is cut into chunks dealt to the n_xcd banks in turn: a chunk is the mean slice extent
- * times the smallest factor that makes it at least 256 KiB, so uniform slices of 256 KiB or more
- * are homed on XCD s mod n_xcd.  The XCDs then stream neighbouring memory at any moment.  When the
+ * times the smallest factor that makes it at least 1 MiB (about one round of an XCD's workers),
+ * so uniform slices of 1 MiB or more are homed on XCD s mod n_xcd.  Each XCD then streams a
+ * contiguous chunk while the others stream the neighbouring ones.  When the
  * span holds no more than n_xcd chunks, or with BSM_FLAG_CONTIGUOUS_BANKS, the banks are n_xcd
  * equal contiguous ranges (the layout of Section 4.1's batch-to-bank table).  Homes change only
  * who computes a row: the output bits are the same. */

@@ -119,7 +119,7 @@ def bank_bounds(lo: int, hi: int, n_banks: int):
 
 
 def interleave_chunk(offsets, rows, cols, n_banks: int, elem_bytes: int,
-                     min_chunk_bytes: int = 256 * 1024) -> int:
+                     min_chunk_bytes: int = 1024 * 1024) -> int:
     """Chunk (elements) of the interleaved virtual banks: the span [lo, hi) of the non-empty
     slices divided by their number (floor, at least 1) is the mean slice extent m; the chunk is
     the smallest multiple of m holding at least min_chunk_bytes. Returns 0 (contiguous banks)
@@ -139,7 +139,7 @@ def interleave_chunk(offsets, rows, cols, n_banks: int, elem_bytes: int,
 
 
 def bank_table(offsets, rows, cols, n_banks: int, layout: str = "contiguous",
-               elem_bytes: int = 4):
+               elem_bytes: int = 4, min_chunk_bytes: int = 1024 * 1024):
     """Batch-to-bank table by counting, element by element, which bank holds each element.
 
     The banks partition the elements spanned by the non-empty slices, [lo, hi). layout
@@ -162,7 +162,7 @@ def bank_table(offsets, rows, cols, n_banks: int, layout: str = "contiguous",
     hi = max(int(offsets[s]) + sizes[s] for s in live)
     chunk = 0
     if layout == "interleaved":
-        chunk = interleave_chunk(offsets, rows, cols, n_banks, elem_bytes)
+        chunk = interleave_chunk(offsets, rows, cols, n_banks, elem_bytes, min_chunk_bytes)
     elif layout != "contiguous":
         raise ValueError(layout)
     bound = bank_bounds(lo, hi, n_banks)

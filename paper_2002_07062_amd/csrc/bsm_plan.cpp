@@ -378,6 +378,14 @@ std::vector<std::vector<Span>> xcd_streams(const Geometry& g, const Topology& t,
             for (const Span& s : recv[x]) push_span(&stream[x], s);
         tab->stats.moved_cost = moved_cost;
         tab->stats.moved_bytes = moved_bytes;
+        // Each XCD takes its rows in memory order, received ones included, so that the eight
+        // XCDs sweep the tensor together instead of ending on rows scattered over it.
+        for (int x = 0; x < n; ++x) {
+            std::vector<Span> v = std::move(stream[x]);
+            std::sort(v.begin(), v.end(), [](const Span& a, const Span& b) { return a.off < b.off; });
+            stream[x].clear();
+            for (const Span& sp : v) push_span(&stream[x], sp);
+        }
     }
     return stream;
 }

@@ -53,9 +53,11 @@ struct Table {
 
 // Smallest chunk of the interleaved virtual banks of the XCD schedule.  Measured on MI355X: with
 // chunks of at least this size (and at least one mean slice) the eight XCDs stream neighbouring
-// memory at any moment and the XCD schedule runs as fast as BALANCED on cold data, where eight
-// contiguous banks, one window per XCD ~1/8 of the batch apart, cost 4-13%.
-constexpr int64_t kBankChunkBytes = 256 * 1024;
+// memory at any moment, each XCD about one round of its workers (256 waves x 4 KiB of input)
+// inside one chunk, and the XCD schedule runs within 1.5% of BALANCED on cold uniform data;
+// eight contiguous banks, one window per XCD ~1/8 of the batch apart, cost 4-13%, and 256 KiB
+// chunks (one XCD round spread over eight chunks) 3-12% on 16384 x 128 x 128 fp32.
+constexpr int64_t kBankChunkBytes = 1024 * 1024;
 
 // Chunk, in elements, of the interleaved virtual banks for `g` over n banks: the mean extent of a
 // non-empty slice times the smallest factor that makes it at least kBankChunkBytes.  0 means n

@@ -458,7 +458,7 @@ def test_temporal_cache_policy_gives_the_same_bits(cfg):
 def test_bank_layouts_give_the_same_bits(cfg, batch):
     """Interleaved (default) and contiguous virtual banks home the slices on different XCDs;
     the outputs are identical to each other and to BALANCED, and the default homes of a uniform
-    batch follow the interleaving (C2: slice s on XCD s mod 8; C4: groups of four)."""
+    batch follow the interleaving (C2: slice s on XCD s mod 8; C4: groups of sixteen)."""
     w = workloads.generate(cfg, batch=batch)
     print(f"[{cfg}] batch {batch}", flush=True)
     x = to_device(w.x, w.dtype)
@@ -475,7 +475,7 @@ def test_bank_layouts_give_the_same_bits(cfg, batch):
         _, _, home, _ = bsm.bsm_plan_export(plan)
         plan.destroy()
         s = np.arange(w.batch)
-        group = 1 if cfg == "c2" else 4
+        group = 1 if cfg == "c2" else 16
         assert home.tolist() == ((s // group) % st_a["n_xcd"]).tolist()
 
 

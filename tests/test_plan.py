@@ -179,11 +179,12 @@ def test_homes_match_bruteforce_bank_table(layout, name, n_xcd):
     assert d["bank_home"] == t["L"].tolist()
 
 
-@pytest.mark.parametrize("name,group", [("c2", 1), ("c3", 1), ("c4", 4)])
+@pytest.mark.parametrize("name,group", [("c2", 1), ("c3", 2), ("c4", 16)])
 def test_default_banks_deal_uniform_slices_to_xcds_in_turn(name, group):
-    """Interleaved banks on uniform batches: slices of 256 KiB or more (C2's 1 MiB fp32, C3's
-    512 KiB bf16) are homed on XCD s mod 8 with no overlap, and 64 KiB slices (C4) in groups of
-    four (a 256 KiB chunk); the contiguous layout homes slice s on bank floor(8 s / B)."""
+    """Interleaved banks on uniform batches: slices of 1 MiB or more (C2's fp32) are homed on
+    XCD s mod 8 with no overlap, C3's 512 KiB bf16 slices in pairs and C4's 64 KiB slices in
+    groups of sixteen (a 1 MiB chunk); the contiguous layout homes slice s on bank
+    floor(8 s / B)."""
     w = WL[name]
     d, _, _, home, ov = _plan(w, "xcd", MI355X)
     s = np.arange(w.batch)

@@ -68,14 +68,16 @@ def test_bank_table_tie_goes_to_lowest_bank():
 
 
 def test_interleaved_banks_by_hand():
-    """Four contiguous slices of 65536, 65536, 98304 and 32768 fp32 elements over two banks:
-    span 262144, mean extent 65536 = 256 KiB, so the chunk is one mean slice and the chunks
-    [0, 65536) [65536, 131072) [131072, 196608) [196608, 262144) go to banks 0, 1, 0, 1.
-    Slice 2 holds 65536 elements on bank 0 and 32768 on bank 1 (OVERLAP, home 0)."""
+    """Four contiguous slices of 65536, 65536, 98304 and 32768 fp32 elements over two banks with
+    a 256 KiB smallest chunk: span 262144, mean extent 65536 = 256 KiB, so the chunk is one mean
+    slice and the chunks [0, 65536) [65536, 131072) [131072, 196608) [196608, 262144) go to
+    banks 0, 1, 0, 1. Slice 2 holds 65536 elements on bank 0 and 32768 on bank 1 (OVERLAP,
+    home 0)."""
     sizes = [65536, 65536, 98304, 32768]
     off = np.concatenate([[0], np.cumsum(sizes)[:-1]])
-    assert pc.interleave_chunk(off, [1] * 4, sizes, 2, 4) == 65536
-    t = pc.bank_table(off, [1] * 4, sizes, 2, layout="interleaved", elem_bytes=4)
+    assert pc.interleave_chunk(off, [1] * 4, sizes, 2, 4, min_chunk_bytes=256 * 1024) == 65536
+    t = pc.bank_table(off, [1] * 4, sizes, 2, layout="interleaved", elem_bytes=4,
+                      min_chunk_bytes=256 * 1024)
     assert t["counts"].tolist() == [[65536, 0], [0, 65536], [65536, 32768], [0, 32768]]
     assert t["home"].tolist() == [0, 1, 0, 1]
     assert t["overlap"].tolist() == [0, 0, 1, 0]
@@ -83,17 +85,19 @@ def test_interleaved_banks_by_hand():
 
 
 def test_interleave_chunk_rules():
-    # 1 MiB fp32 slices: the chunk is one slice; 64 KiB slices: four; bf16 halves the bytes
+    # 1 MiB fp32 slices: the chunk is one slice; 64 KiB slices: sixteen; bf16 halves the bytes
     assert pc.interleave_chunk([0], [512] * 1, [512], 8, 4) == 0  # one slice: contiguous
     off = np.arange(16) * 262144
     assert pc.interleave_chunk(off, [512] * 16, [512] * 16, 8, 4) == 262144
-    off = np.arange(64) * 16384
-    assert pc.interleave_chunk(off, [128] * 64, [128] * 64, 8, 4) == 4 * 16384
-    # bf16: eight 32 KiB slices per chunk, and 8 such chunks need more than 64 slices
-    assert pc.interleave_chunk(off, [128] * 64, [128] * 64, 8, 2) == 0
-    off = np.arange(128) * 16384
-    assert pc.interleave_chunk(off, [128] * 128, [128] * 128, 8, 2) == 8 * 16384
-    # 8 slices of 64x64 fp32 (C1): 8 chunks of 256 KiB exceed the 128 KiB span -> contiguous
+    off = np.arange(256) * 16384
+    assert pc.interleave_chunk(off, [128] * 256, [128] * 256, 8, 4) == 16 * 16384
+    # 64 such slices make 4 chunks, fewer than the 8 banks: contiguous
+    assert pc.interleave_chunk(off[:64], [128] * 64, [128] * 64, 8, 4) == 0
+    # bf16: 32 slices of 32 KiB per chunk, and more than 8 such chunks need more than 256
+    assert pc.interleave_chunk(off, [128] * 256, [128] * 256, 8, 2) == 0
+    off2 = np.arange(512) * 16384
+    assert pc.interleave_chunk(off2, [128] * 512, [128] * 512, 8, 2) == 32 * 16384
+    # 8 slices of 64x64 fp32 (C1): 8 chunks of 1 MiB exceed the 128 KiB span -> contiguous
     off = np.arange(8) * 4096
     assert pc.interleave_chunk(off, [64] * 8, [64] * 8, 8, 4) == 0
     t = pc.bank_table(off, [64] * 8, [64] * 8, 8, layout="interleaved")
