@@ -844,11 +844,19 @@ def main() -> int:
         # rows longer than the register tile, held in the registers of a workgroup (256 threads:
         # up to 8192 elements in kernel class 4, 16384 in class 5; 512 threads: up to 32768 in
         # class 6) and read once, forward and backward
-        for name in ("long4k", "long", "long16k", "long32k"):
+        for name in ("long4k", "long", "long16k", "long32k", "long4104bf16", "long8200bf16"):
             r, _ = run_workload(name, "balanced", args.steps, args.warmup)
             extra[f"{name}_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}
             r = run_backward(name, "balanced", args.steps, args.warmup)
             extra[f"{name}_backward_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step")}
+        # uniform fp32 batches at one row width each: full and partly filled register tiles
+        extra["widths_f32"] = {}
+        for c in (64, 72, 96, 136, 264, 520):
+            r, _ = run_workload(f"w{c}", "balanced", args.steps, args.warmup)
+            rb = run_backward(f"w{c}", "balanced", args.steps, args.warmup)
+            extra["widths_f32"][str(c)] = {"gbs": round(r["gbs"], 1),
+                                           "backward_gbs": round(rb["gbs"], 1),
+                                           "ms_per_step": r["ms_per_step"]}
         # rows that do not start or end on a 16-byte vector (1001 fp32): shifted vectors
         r, _ = run_workload("odd", "balanced", args.steps, args.warmup)
         extra["odd_balanced"] = {k: r[k] for k in ("gbs", "ms_per_step", "kernel_class")}

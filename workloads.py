@@ -74,14 +74,31 @@ SPECS = {
     "long_32x64x16384_f32": Spec(
         "long_32x64x16384_f32", 32, 64, 16384, F32, 3.0, 8,
         doc="32 slices x 64x16384 fp32, N(0,9): the longest register-held rows (class 5, 16 vectors per lane)"),
+    # bf16 rows just past the one-wave register tile: 513 and 1025 16-byte vectors
+    "long_128x96x4104_bf16": Spec(
+        "long_128x96x4104_bf16", 128, 96, 4104, BF16, 3.0, 11,
+        doc="128 slices x 96x4104 bf16, N(0,9): 513 vectors per row, one past the 512 of the "
+            "largest short-row tile"),
+    "long_64x96x8200_bf16": Spec(
+        "long_64x96x8200_bf16", 64, 96, 8200, BF16, 3.0, 12,
+        doc="64 slices x 96x8200 bf16, N(0,9): 1025 vectors per row, held by a workgroup"),
 }
+# Uniform fp32 batches of ~200 MB input at one row width each: full and partly filled register
+# tiles (the widths of the ragged workload run from 64 to 1024).
+for _c in (64, 72, 96, 136, 264, 520):
+    _r = round(50e6 / (64 * _c))
+    _n = f"width_64x{_r}x{_c}_f32"
+    SPECS[_n] = Spec(_n, 64, _r, _c, F32, 3.0, 100 + _c,
+                     doc=f"64 slices x {_r}x{_c} fp32, N(0,9): rows of {_c // 4} 16-byte vectors")
 
 # Short aliases used by the bench and the tests.
 ALIASES = {"c1": "c1_8x64x64_f32", "c2": "c2_384x512x512_f32",
            "c3": "c3_384x512x512_bf16_mask", "c4": "c4_16384x128x128_f32",
            "c5": "c5_384_ragged_f32", "long": "long_64x64x8192_f32",
            "long4k": "long_128x64x4096_f32", "long16k": "long_32x64x16384_f32",
-           "odd": "odd_64x768x1001_f32", "long32k": "long_16x64x32768_f32"}
+           "odd": "odd_64x768x1001_f32", "long32k": "long_16x64x32768_f32",
+           "long4104bf16": "long_128x96x4104_bf16", "long8200bf16": "long_64x96x8200_bf16"}
+ALIASES.update({f"w{s.cols}": n for n, s in SPECS.items() if n.startswith("width_")})
 
 
 @dataclasses.dataclass
