@@ -318,7 +318,12 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     const int nk = (s.k + kChunkK - 1) / kChunkK;  // k > 0 here
     const int nj = (s.n + kBlockN - 1) / kBlockN;
     const int nsteps = nk * nj;
+    // Accumulators are zero at every column block's start: set here and again after each
+    // block's output (AREG, one step per block: the block's first MFMA takes a zero addend
+    // instead), not selected at every step.
     f32x16 acc[kBlockTiles];
+#pragma unroll
+    for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
     Pieces<!AREG> p[kDepth];
     u16x8 a_reg[AREG ? kChunkK / kTileK : 1];
     if constexpr (AREG) {  // A once, through the wave's LDS into its MFMA layout
@@ -331,38 +336,56 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
             a_reg[q] = *reinterpret_cast<const u16x8*>(la + li * kLdk + q * kTileK + 8 * h);
         wave_lds_sync();
     }
-    auto load = [&](int st, Pieces<!AREG>& pp) {
-        const int js = st / nk, ks = st - js * nk;
-        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, js * kBlockN, ks * kChunkK, wave, lane,
+    // The steps' (column block, reduction slice) pairs are counted up as the steps go, not
+    // divided out of the step index: on this path every scalar instruction counts, twelve
+    // waves per CU share the scalar unit.  The load stream runs kDepth steps ahead and stays
+    // on the last step once it gets there (its loads are then issued again, unused).
+    int ld_st = 0, ld_j = 0, ld_k = 0;
+    auto load = [&](Pieces<!AREG>& pp) {
+        load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, ld_j * kBlockN, ld_k * kChunkK, wave, lane,
                                       !TEMPORAL && nj == 1, pp);  // A read once when one column block
+        if (ld_st + 1 < nsteps) {
+            ++ld_st;
+            if (++ld_k == nk) { ld_k = 0; ++ld_j; }
+        }
     };
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) load(d < nsteps ? d : nsteps - 1, p[d]);
+    for (int d = 0; d < kDepth; ++d) load(p[d]);
     static_assert(kDepth == 2, "the step loop below is written for two buffers");
+    // Wave priority 3 .. 0 by the workgroup's own progress: step st of this round has done
+    // done_rows * nsteps + round_rows_n * st of total_rows * nsteps row-steps, and the
+    // priority is 3 - floor(4 done / total) (at least 0).  The steps where the quotient
+    // reaches 1, 2 and 3 are worked out once per round (measured: -2.5% time on the context
+    // product; the one-step scores product gains nothing and skips it).
+    int prio_step[3] = {0, 0, 0};
+    if constexpr (!AREG) {
+        const int64_t tot = static_cast<int64_t>(total_rows > 0 ? total_rows : 1) * nsteps;
+        const int64_t done4 = 4 * static_cast<int64_t>(done_rows) * nsteps;
+        const int64_t per4 = 4 * static_cast<int64_t>(round_rows_n > 0 ? round_rows_n : 1);
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const int64_t need = (q + 1) * tot - done4;  // 4 * row-steps still short of q + 1
+            const int64_t t = need <= 0 ? 0 : (need + per4 - 1) / per4;
+            prio_step[q] = t < nsteps ? static_cast<int>(t) : nsteps;
+        }
+    }
+    int cur_j = 0, cur_k = 0;
     // One step: st's operands (in pp, loaded kDepth steps ago) go to LDS buffer lb, then
     // step st + kDepth's loads are issued into pp, then st's arithmetic and, at a column
     // block's end, its output.
     auto step = [&](int st, Pieces<!AREG>& pp, uint16_t* lb) {
-        if constexpr (!AREG) {  // priority 3 .. 0 by the workgroup's own progress (rows done,
-                                // steps of this round); measured: -2.5% time on the context
-                                // product, no gain on the one-step scores product
-            const int64_t prog = static_cast<int64_t>(done_rows) * nsteps + static_cast<int64_t>(round_rows_n) * st;
-            const int64_t tot = static_cast<int64_t>(total_rows) * nsteps;
-            set_prio(3 - static_cast<int>((4 * prog) / (tot > 0 ? tot : 1)));
-        }
-        const int jb = st / nk, kb = st - jb * nk;
+        if constexpr (!AREG)
+            set_prio(3 - (st >= prio_step[0]) - (st >= prio_step[1]) - (st >= prio_step[2]));
+        const int jb = cur_j, kb = cur_k;
+        if (++cur_k == nk) { cur_k = 0; ++cur_j; }
         const int j0 = jb * kBlockN;
-        if (kb == 0) {
-#pragma unroll
-            for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
-        }
         // lb (buffer st % 2) was last read at step st - 2; every wave finished that step
         // before the barrier of step st - 1, so one barrier per step orders both uses.
         write_step<LAYOUT, VEC, !AREG>(pp, s, rows, j0, kb * kChunkK, wave, lane, la, lb);
         __syncthreads();
         // issued on every step (past the last step: the last step's operands again, cache
         // hits, unused), so that every path has the same loads in flight
-        load(st + kDepth < nsteps ? st + kDepth : nsteps - 1, pp);
+        load(pp);
         if (rows > 0) {  // wave-uniform
 #pragma unroll
             for (int kk = 0; kk < kChunkK; kk += kTileK) {
@@ -377,7 +400,8 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
                             bf16x8, *reinterpret_cast<const u16x8*>(lb + (t * kTileN + li) * kLdk + kk + 8 * h));
                     else
                         bv = nn_row_operand(lb, t, kk, lane);
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[t], 0, 0, 0);
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        bv, av, (AREG && kk == 0) ? f32x16{} : acc[t], 0, 0, 0);
                 }
             }
         }
@@ -412,6 +436,10 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
             store_block_f32<VEC, TEMPORAL>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
         }
         wave_lds_sync();  // the next step rewrites the region
+        if constexpr (!AREG) {
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
+        }
     };
     // Two steps per iteration and the odd one after the loop, so that every path around the
     // loop issues the same loads (a step waits for its own loads only, not for the next
