@@ -11,7 +11,7 @@ namespace {
 
 using bsm_mm::Shape;
 
-template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL>
+template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
 hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const int32_t* worker_ptr,
                     const bsm_item* items, int n_wg, void* trace, hipStream_t stream) {
     const uint16_t* a_a = static_cast<const uint16_t*>(a);
@@ -21,7 +21,7 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &a_trace};
     const size_t lds = static_cast<size_t>(bsm_mm::wg_lds_bytes(BF16OUT));
-    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC, TEMPORAL>),
+    return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC, TEMPORAL, AREG>),
                            dim3(n_wg), dim3(bsm_mm::kGemmThreads), args, lds, stream);
 }
 
@@ -52,14 +52,17 @@ hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, 
                            reinterpret_cast<uintptr_t>(c);
     const bool vec = (ptrs & 15) == 0 && k % 8 == 0 &&
                      n % ((layout == bsm_mm::kNN || bf16_out) ? 8 : 4) == 0;
-#define BSM_G(M, O, V, T) launch_g<M, O, V, T>(a, b, c, s, d_worker_ptr, d_items, n_wg, trace, stream)
-#define BSM_G1(M, T) (bf16_out ? (vec ? BSM_G(M, true, true, T) : BSM_G(M, true, false, T)) \
-                               : (vec ? BSM_G(M, false, true, T) : BSM_G(M, false, false, T)))
+    const bool areg = bsm_mm::use_areg(vec, n, k);
+#define BSM_G(M, O, V, T, R) launch_g<M, O, V, T, R>(a, b, c, s, d_worker_ptr, d_items, n_wg, trace, stream)
+#define BSM_GV(M, O, T) (!vec ? BSM_G(M, O, false, T, false) \
+                              : (areg ? BSM_G(M, O, true, T, true) : BSM_G(M, O, true, T, false)))
+#define BSM_G1(M, T) (bf16_out ? BSM_GV(M, true, T) : BSM_GV(M, false, T))
 #define BSM_G2(M) (temporal ? BSM_G1(M, true) : BSM_G1(M, false))
     if (layout == bsm_mm::kNN) return BSM_G2(bsm_mm::kModeNn);
     return BSM_G2(bsm_mm::kModeNt);
 #undef BSM_G2
 #undef BSM_G1
+#undef BSM_GV
 #undef BSM_G
 }
 

@@ -474,7 +474,7 @@ constexpr int kWavesPerSimd = 3;
 // Worker loop: workgroup w runs its items; an item's rows are taken up to 128 at a time (cut
 // where a batch ends), 32 per wave.  Every bound of these loops is the same for the four
 // waves, so they meet the same barriers.
-template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL>
+template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
                                             const Shape& s, const int32_t* __restrict__ worker_ptr,
                                             const bsm_item* __restrict__ items,
@@ -486,7 +486,6 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
     uint16_t* const lw = lds_base + wave * (wave_lds_bytes(BF16OUT) / 2);
     uint16_t* const lbs = lds_base + kWaves * (wave_lds_bytes(BF16OUT) / 2);
-    const bool areg = VEC && s.k <= kChunkK && s.n > kBlockN;  // (registers: 16-byte form only)
     uint32_t done = 0;
     const int i_begin = worker_ptr[w];
     const int i_end = worker_ptr[w + 1];
@@ -511,12 +510,9 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
                 if (s.k == 0)
                     zero_rows<BF16OUT>(c, s, bidx, i + wave * kTileM, mine, lane);
-                else if (areg)
-                    round_rows<kLayout, BF16OUT, VEC, true, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
-                                                            wave, lane, lw, lbs, wg_done, seg, total_rows);
                 else
-                    round_rows<kLayout, BF16OUT, VEC, false, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
-                                                             wave, lane, lw, lbs, wg_done, seg, total_rows);
+                    round_rows<kLayout, BF16OUT, VEC, AREG, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                                                            wave, lane, lw, lbs, wg_done, seg, total_rows);
                 wg_done += seg;
                 done += static_cast<uint32_t>(mine);
                 g += seg;
@@ -544,13 +540,16 @@ constexpr int kGemmThreads = 64 * kWaves;
 // registers do not fit three.
 // TEMPORAL: ordinary stores of C and loads of A (a consumer finds C in the Infinity Cache)
 // instead of nontemporal ones; a compile-time choice, so the default instance carries no
-// branch for it.
-template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL>
+// branch for it.  AREG (A's operands held in registers, k <= 64 < n, 16-byte form only): a
+// separate instance too, so that neither form's registers are allocated for the other's.
+constexpr bool use_areg(bool vec, int n, int k) { return vec && k <= kChunkK && n > kBlockN; }
+template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
 __global__ void __launch_bounds__(kGemmThreads, VEC ? kWavesPerSimd : 2)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 bsm_trace_rec* __restrict__ trace) {
-    gemm_worker<MODE, BF16OUT, VEC, TEMPORAL>(a, b, c, s, worker_ptr, items, trace, bsm_gemm_lds);
+    static_assert(VEC || !AREG, "registers hold A in the 16-byte form only");
+    gemm_worker<MODE, BF16OUT, VEC, TEMPORAL, AREG>(a, b, c, s, worker_ptr, items, trace, bsm_gemm_lds);
 }
 
 }  // namespace bsm_mm
