@@ -725,14 +725,20 @@ __device__ __forceinline__ uint32_t team_item(const typename E::T* in, typename 
     } else if (E::kBytes == 2 && kMaxL >= 6 && per_lane <= 6) {
         // bf16 rows of 5 or 6 vectors per lane (e.g. 8200 elements): two rows in flight, as for
         // the shortest rows (8200 bf16: 4.05 -> 4.3 TB/s against one row of 8 vectors per lane,
-        // 5 of them used; fp32 rows lost 1.5-4% this way and keep one row of 8)
+        // 5 of them used; fp32 rows lost 1.5-4% this way and keep one row of 8), in a tile of
+        // exactly 5 slots where 5 suffice (8200 bf16: 4.76 -> 4.97 TB/s against 6; the
+        // backward pass lost 5% with a 5-slot tile and keeps its 8)
         RowWalk<2> w(base, cols, nrows, reps, stride);
         while (w.more()) {
             int64_t off[2];
             bool act[2];
             w.next(off, act);
-            team_rows<E, (kMaxL >= 6 ? 6 : 4), 2, SHIFT>(in, out, off, act, cols, t, nt, wave,
-                                                         nwaves, lane);
+            if (per_lane <= 5)
+                team_rows<E, (kMaxL >= 6 ? 5 : 4), 2, SHIFT>(in, out, off, act, cols, t, nt, wave,
+                                                             nwaves, lane);
+            else
+                team_rows<E, (kMaxL >= 6 ? 6 : 4), 2, SHIFT>(in, out, off, act, cols, t, nt, wave,
+                                                             nwaves, lane);
         }
     } else if (per_lane <= kMaxL) {
         RowWalk<1> w(base, cols, nrows, reps, stride);
