@@ -105,6 +105,24 @@ __device__ __forceinline__ float lane_reduce(const float* x) {
     }
 }
 
+// In-lane sum of a[k] g[k] by the same pairwise tree, its first level fused: a[2i] g[2i] +
+// a[2i+1] g[2i+1] as one fma over one product, so that no product is held in a register of its
+// own (with K products formed first, a backward row held by a lane needs 3K values at once).
+template <int K>
+__device__ __forceinline__ float lane_dot(const float* a, const float* g) {
+    static_assert(K > 0, "lane_dot needs a value");
+    if constexpr (K == 1) {
+        return a[0] * g[0];
+    } else {
+        constexpr int H = (K + 1) / 2;
+        float t[H];
+#pragma unroll
+        for (int i = 0; i < K / 2; ++i) t[i] = __builtin_fmaf(a[2 * i], g[2 * i], a[2 * i + 1] * g[2 * i + 1]);
+        if constexpr (K % 2 == 1) t[H - 1] = a[K - 1] * g[K - 1];
+        return lane_reduce<H, OpAdd>(t);
+    }
+}
+
 // 16-byte accesses, nontemporal (streaming) or ordinary (cache-resident) by NT.
 template <bool NT, class V>
 __device__ __forceinline__ V load16(const V* p) {
@@ -900,10 +918,7 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        float p[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) p[k] = a[u][k] * g[u][k];
-        const float d = group_reduce<G, OpAdd>(lane_reduce<K, OpAdd>(p));
+        const float d = group_reduce<G, OpAdd>(lane_dot<K>(a[u], g[u]));
 #pragma unroll
         for (int k = 0; k < K; ++k) a[u][k] = a[u][k] * (g[u][k] - d);
         const int r = r0 + u * step;
@@ -1024,10 +1039,7 @@ __device__ __forceinline__ void team_rows_bwd(const typename E::T* y, const type
         const RowVecs<E, SHIFT> rv(off[u], cols);
         team_unpack<E, L, SHIFT>(rv, t, nt, ra[u], a[u], 0.0f);
         team_unpack<E, L, SHIFT>(rv, t, nt, rg[u], g[u], 0.0f);
-        float p[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) p[k] = a[u][k] * g[u][k];
-        d[u] = group_reduce<64, OpAdd>(lane_reduce<K, OpAdd>(p));
+        d[u] = group_reduce<64, OpAdd>(lane_dot<K>(a[u], g[u]));
     }
     team_combine<OpAdd, U>(d, which, wave, nwaves, lane);
 #pragma unroll
