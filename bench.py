@@ -206,6 +206,8 @@ def run_backward(name, schedule, steps, warmup, w=None):
 GEMM_SHAPES = {  # Section 6's two batch products of BERT attention (batch, m, n, k, layout)
     "scores_384x512x512x64": (384, 512, 512, 64, "nt"),
     "context_384x512x64x512": (384, 512, 64, 512, "nn"),
+    # the score product with the row softmax in the same kernel (P = softmax(Q K^T / 8))
+    "scores_softmax_384x512x512x64": (384, 512, 512, 64, "nt_softmax"),
 }
 
 
@@ -374,8 +376,10 @@ def attention_pipeline(steps=30, warmup=5, batch=384, seq=512, d=64):
     over enough sets to stay out of the Infinity Cache. Compares the default streaming
     (nontemporal) accesses with BSM_FLAG_TEMPORAL on all three plans, so that the 201 MB score
     tensor written by the first product can be served from the 256 MB Infinity Cache to the
-    softmax and then to the second product. Returns microseconds per pipeline and per stage
-    (each stage alone, same buffers) and algorithmic bytes."""
+    softmax and then to the second product. The "fused" variant computes P = softmax(Q K^T /
+    sqrt(d)) in one kernel (the score product's "nt_softmax" layout: S never stored), then the
+    context product. Returns microseconds per pipeline and per stage (each stage alone, same
+    buffers) and algorithmic bytes."""
     import torch
 
     import paper_2002_07062_amd as bsm
@@ -430,6 +434,24 @@ def attention_pipeline(steps=30, warmup=5, batch=384, seq=512, d=64):
                       "softmax_us": timed(soft), "context_us": timed(context)}
         for p in (p_s, p_c, p_m):
             p.destroy()
+    p_f = bsm.bsm_gemm_plan_create(batch, seq, seq, d, "nt_softmax", "bf16", "balanced", device=0)
+    p_c = bsm.bsm_gemm_plan_create(batch, seq, d, seq, "nn", "bf16", "balanced", device=0)
+
+    def probs(i):
+        bsm.bsm_gemm_execute(p_f, Q[i], K[i], S, scale)
+
+    def context_f(i):
+        bsm.bsm_gemm_execute(p_c, S, V[i], O[i])
+
+    def pipe_f(i):
+        probs(i)
+        context_f(i)
+
+    res["fused"] = {"pipeline_us": timed(pipe_f), "scores_softmax_us": timed(probs),
+                    "context_us": timed(context_f)}
+    res["algorithmic_bytes"]["scores_softmax"] = res["algorithmic_bytes"]["scores"]
+    for p in (p_f, p_c):
+        p.destroy()
     del Q, K, V, O, S
     torch.cuda.empty_cache()
     return res
@@ -589,7 +611,8 @@ def launch_bound_c1(steps=200, warmup=20):
 def vendor_bmm(name, steps, warmup):
     """The same batched product through torch.bmm (hipBLASLt), bf16 operands and output,
     rotated like run_gemm; the scores product gets K already transposed and contiguous (bf16
-    bmm of a transposed view is avoided). Times the product only."""
+    bmm of a transposed view is avoided). Times the product only; for the "nt_softmax" shape,
+    the product followed by torch.softmax over each score row (the unfused library route)."""
     import numpy as np
     import torch
 
@@ -600,26 +623,32 @@ def vendor_bmm(name, steps, warmup):
     a0 = torch.from_numpy(rng.standard_normal(batch * m * k, dtype=np.float32)).to(torch.bfloat16).cuda()
     b0 = torch.from_numpy(rng.standard_normal(batch * n * k, dtype=np.float32)).to(torch.bfloat16).cuda()
     A = [a0.view(batch, m, k)] + [a0.clone().view(batch, m, k) for _ in range(n_sets - 1)]
-    if layout == "nt":  # B stored n x k per batch: hand bmm its transpose as a k x n copy
+    if layout in ("nt", "nt_softmax"):  # B stored n x k per batch: hand bmm a k x n copy
         B = [b0.view(batch, n, k).transpose(1, 2).contiguous() for _ in range(n_sets)]
     else:
         B = [b0.view(batch, k, n)] + [b0.clone().view(batch, k, n) for _ in range(n_sets - 1)]
     Cs = [torch.empty(batch, m, n, dtype=torch.bfloat16, device="cuda") for _ in range(n_sets)]
+    def run(i):
+        torch.bmm(A[i], B[i], out=Cs[i])
+        if layout == "nt_softmax":
+            torch.softmax(Cs[i], dim=-1)
+
     for i in range(warmup):
-        torch.bmm(A[i % n_sets], B[i % n_sets], out=Cs[i % n_sets])
+        run(i % n_sets)
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
     for i in range(steps):
-        torch.bmm(A[i % n_sets], B[i % n_sets], out=Cs[i % n_sets])
+        run(i % n_sets)
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
     del A, B, Cs, a0, b0
     torch.cuda.empty_cache()
     return {"us": round(ms * 1e3, 2), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-            "algorithmic_bytes": nbytes, "library": "torch.bmm (hipBLASLt)"}
+            "algorithmic_bytes": nbytes,
+            "library": "torch.bmm (hipBLASLt)" + (" + torch.softmax" if layout == "nt_softmax" else "")}
 
 
 def _cpu_model() -> str:

@@ -306,7 +306,16 @@ bsm_status bsm_softmax_backward(const void* y, const void* dy, void* dx,
  * All operands row-major, batch after batch (A_b at b*m*k, B_b at b*n*k, C_b at b*m*n
  * elements).  A and B are bf16; C is fp32 or bf16 (round to nearest even); accumulation in
  * fp32 on the matrix cores. */
-typedef enum { BSM_GEMM_NT = 0, BSM_GEMM_NN = 1, BSM_GEMM_LAYOUT_MAX_ENUM = 0x7FFFFFFF } bsm_gemm_layout;
+typedef enum {
+    BSM_GEMM_NT = 0,
+    BSM_GEMM_NN = 1,
+    /* C_b = row softmax of alpha * A_b * B_b^T (A_b m x k, B_b n x k): Section 6's score
+     * product followed by Section 2's softmax of every score row (each row of C_b sums to 1
+     * over its n columns), in one kernel: the scores are never stored.  k == 0 gives rows
+     * of 1/n. */
+    BSM_GEMM_NT_SOFTMAX = 2,
+    BSM_GEMM_LAYOUT_MAX_ENUM = 0x7FFFFFFF
+} bsm_gemm_layout;
 
 /* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
  * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 3).  A plan

@@ -9,8 +9,12 @@ What it computes, for every batch index b (each operand stored row-major, batch 
     layout "nt":  C_b = alpha * A_b @ B_b^T     A_b: m x k,  B_b: n x k,  C_b: m x n
     layout "nn":  C_b = alpha * A_b @ B_b       A_b: m x k,  B_b: k x n,  C_b: m x n
 
+    layout "nt_softmax": C_b = row softmax of (alpha * A_b @ B_b^T)
+
 "nt" is the score product Q K^T of attention (keys stored one per row); "nn" is the context
-product P V. Operands are bf16 bit patterns (or fp32 / fp64 values), converted to fp64
+product P V; "nt_softmax" is the score product followed by Section 2's softmax of every score
+row (scores_softmax below: this module's product, then the softmax oracle of oracle/softmax.py
+over the batch * m rows of n values). Operands are bf16 bit patterns (or fp32 / fp64 values), converted to fp64
 exactly; the product of each batch is numpy's fp64 matrix product (a library primitive),
 then scaled by alpha in fp64.
 """
@@ -64,3 +68,17 @@ def abs_product_sums(a: np.ndarray, b: np.ndarray, batch: int, m: int, n: int, k
     A = np.abs(_to_f64(np.ascontiguousarray(a).reshape(-1), dtype))
     B = np.abs(_to_f64(np.ascontiguousarray(b).reshape(-1), dtype))
     return batched_gemm(A, B, batch, m, n, k, layout, 1.0, "f64")
+
+
+def scores_softmax(a: np.ndarray, b: np.ndarray, batch: int, m: int, n: int, k: int,
+                   alpha: float = 1.0, dtype: str = "bf16") -> np.ndarray:
+    """fp64 P (batch * m * n): the row softmax of the "nt" product alpha * A_b @ B_b^T, each of
+    the batch * m rows normalised over its n values (Section 6's score product, then Section
+    2's softmax). Composed from batched_gemm and the fp64 softmax oracle; k == 0 gives 1/n."""
+    from .softmax import softmax as softmax_oracle
+
+    C = batched_gemm(a, b, batch, m, n, k, "nt", alpha, dtype)
+    if batch == 0 or m == 0 or n == 0:
+        return C
+    offsets = np.arange(batch, dtype=np.int64) * (m * n)
+    return softmax_oracle(C, "f64", offsets, np.full(batch, m, np.int32), np.full(batch, n, np.int32))

@@ -10,6 +10,7 @@ from .bsm import (  # noqa: F401
     LIB_PATH, SCHEDULES, TRACE_DTYPE, BsmError, Plan, bsm_abi_version, bsm_cache_clear, bsm_copy,
     bsm_default_topology, bsm_device_info, bsm_last_error, bsm_plan_create, bsm_plan_describe,
     bsm_plan_destroy, bsm_plan_execute, bsm_plan_execute_backward, bsm_plan_export, bsm_softmax,
-    bsm_softmax_backward, bsm_softmax_noalloc, bsm_status_string, BSM_GEMM_NN, BSM_GEMM_NT, GEMM_LAYOUTS, bsm_gemm,
+    bsm_softmax_backward, bsm_softmax_noalloc, bsm_status_string, BSM_GEMM_NN, BSM_GEMM_NT, BSM_GEMM_NT_SOFTMAX,
+    GEMM_LAYOUTS, bsm_gemm,
     bsm_gemm_execute, bsm_gemm_plan_create,
     bsm_topology, load)

@@ -29,8 +29,9 @@ BSM_FLAG_TEMPORAL = 1
 BSM_FLAG_CONTIGUOUS_BANKS = 2
 
 SCHEDULES = {"rr": BSM_SCHED_RR, "balanced": BSM_SCHED_BALANCED, "xcd": BSM_SCHED_XCD}
-BSM_GEMM_NT, BSM_GEMM_NN = 0, 1
-GEMM_LAYOUTS = {"nt": BSM_GEMM_NT, "nn": BSM_GEMM_NN}
+BSM_GEMM_NT, BSM_GEMM_NN, BSM_GEMM_NT_SOFTMAX = 0, 1, 2
+# "nt_softmax": C = row softmax of alpha A B^T (the score product and the softmax in one kernel)
+GEMM_LAYOUTS = {"nt": BSM_GEMM_NT, "nn": BSM_GEMM_NN, "nt_softmax": BSM_GEMM_NT_SOFTMAX}
 DTYPES = {"f32": BSM_F32, "bf16": BSM_BF16}
 
 
@@ -466,7 +467,8 @@ def _check_gemm_tensors(batch, m, n, k, a, b, c, c_dtype) -> None:
 
 def bsm_gemm_plan_create(batch, m, n, k, layout="nt", out_dtype="f32", schedule="balanced",
                          home_xcd=None, topology=None, device=0) -> Plan:
-    """Plan of the batched product C_b = alpha A_b B_b^T ("nt") or alpha A_b B_b ("nn")."""
+    """Plan of the batched product C_b = alpha A_b B_b^T ("nt"), alpha A_b B_b ("nn"), or the
+    row softmax of alpha A_b B_b^T ("nt_softmax")."""
     lib = load()
     h, hp = _arr(home_xcd, np.int8)
     topo = None

@@ -33,7 +33,8 @@ struct bsm_plan_s {
     int kernel_class = 0;
     bool shifted = false;  // some slice's rows do not start and end on 16-byte vectors
     // A matrix-product plan (bsm_gemm_plan_create) instead of a softmax plan: the slices are
-    // the outputs C_b (gemm_m x gemm_n), A_b is gemm_m x gemm_k, layout 0 = NT, 1 = NN.
+    // the outputs C_b (gemm_m x gemm_n), A_b is gemm_m x gemm_k, layout 0 = NT, 1 = NN,
+    // 2 = NT with the row softmax of the products.
     bool gemm = false;
     int gemm_m = 0, gemm_n = 0, gemm_k = 0, gemm_layout = 0;
     int64_t gemm_batch = 0;
@@ -452,7 +453,8 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
                             bool upload = true) {
     if (!out_plan) return fail(BSM_ERR_INVALID_ARG, "out_plan is NULL");
     *out_plan = nullptr;
-    if (layout != 0 && layout != 1) return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", layout);
+    if (layout != BSM_GEMM_NT && layout != BSM_GEMM_NN && layout != BSM_GEMM_NT_SOFTMAX)
+        return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", layout);
     if (batch < 0 || m < 0 || n < 0 || k < 0)
         return fail(BSM_ERR_INVALID_ARG, "negative size (batch %lld, m %d, n %d, k %d)",
                     static_cast<long long>(batch), m, n, k);
@@ -1152,7 +1154,7 @@ bsm_status bsm_gemm(const void* a, const void* b, void* c, int64_t batch, int32_
                     bsm_schedule schedule, void* stream) {
     if (!valid_dtype(out_dtype)) return fail(BSM_ERR_INVALID_ARG, "unknown dtype %d", static_cast<int>(out_dtype));
     if (!valid_schedule(schedule)) return fail(BSM_ERR_INVALID_ARG, "unknown schedule %d", static_cast<int>(schedule));
-    if (layout != BSM_GEMM_NT && layout != BSM_GEMM_NN)
+    if (layout != BSM_GEMM_NT && layout != BSM_GEMM_NN && layout != BSM_GEMM_NT_SOFTMAX)
         return fail(BSM_ERR_INVALID_ARG, "unknown layout %d", static_cast<int>(layout));
     if (batch < 0 || m < 0 || n < 0 || k < 0) return fail(BSM_ERR_INVALID_ARG, "negative size");
     if (batch == 0 || m == 0 || n == 0) return BSM_OK;

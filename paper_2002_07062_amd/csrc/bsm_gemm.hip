@@ -59,6 +59,7 @@ hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, 
 #define BSM_G1(M, T) (bf16_out ? BSM_GV(M, true, T) : BSM_GV(M, false, T))
 #define BSM_G2(M) (temporal ? BSM_G1(M, true) : BSM_G1(M, false))
     if (layout == bsm_mm::kNN) return BSM_G2(bsm_mm::kModeNn);
+    if (layout == bsm_mm::kModeNtSoftmax) return BSM_G2(bsm_mm::kModeNtSoftmax);
     return BSM_G2(bsm_mm::kModeNt);
 #undef BSM_G2
 #undef BSM_G1

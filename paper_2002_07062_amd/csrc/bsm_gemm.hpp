@@ -6,6 +6,9 @@
 //   layout NT:  C_b = alpha A_b B_b^T   (A_b: m x k, B_b: n x k; e.g. Q K^T)
 //   layout NN:  C_b = alpha A_b B_b     (A_b: m x k, B_b: k x n; e.g. P V)
 //
+//   NT + softmax: C_b = row softmax of alpha A_b B_b^T  (the score product with Section 2's
+//                 softmax of each score row in the same kernel; S is never stored)
+//
 // bf16 operands, fp32 accumulation on the matrix cores (v_mfma_f32_32x32x16_bf16), fp32 or
 // bf16 (round to nearest even) output.  A workgroup of four waves takes up to 128 rows of one
 // batch index at a time, 32 per wave, and walks the output in blocks of 64 columns (two
@@ -21,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "bsm.h"
 
@@ -305,7 +309,27 @@ __device__ __forceinline__ void set_prio(int p) {
     else __builtin_amdgcn_s_setprio(0);
 }
 
-template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG, bool TEMPORAL>
+constexpr float kLog2eF = 1.44269504088896340736f;
+constexpr float kNegInfF = -__builtin_huge_valf();
+
+// The value of lane l and of lane l ^ 32 (the other half of an output row's 32x32 tile
+// lanes) combined by op (commutative: both lanes end with identical bits).  The partner's value
+// comes through ds_bpermute: with v_permlane32_swap on two copies of one value, the compiler
+// used one of the two results twice.
+template <class F>
+__device__ __forceinline__ float half_pair(float v, int lane, F op) {
+    const float o = __builtin_bit_cast(
+        float, __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __builtin_bit_cast(int, v)));
+    return op(v, o);
+}
+
+// SOFTMAX (NT only): each row's column blocks are walked twice.  The first pass keeps the
+// row's running maximum M of the logits (in base-2 units, y = alpha s log2 e) and the sum of
+// 2^(y - M) over the columns seen so far, rescaled whenever M rises (each lane sums its own
+// columns; the two lanes of a row exchange their maxima per block and add their sums at the
+// end).  The second pass recomputes the products and writes 2^(y - M) / sum.  Recomputing costs
+// matrix-core time, which these products have to spare; storing S would cost its bytes twice.
+template <int LAYOUT, bool BF16OUT, bool VEC, bool AREG, bool TEMPORAL, bool SOFTMAX = false>
 __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b, void* c,
                                            const Shape& s, int64_t bidx, int i0, int rows,
                                            int wave, int lane, uint16_t* lw, uint16_t* lbs,
@@ -318,6 +342,7 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     const int nk = (s.k + kChunkK - 1) / kChunkK;  // k > 0 here
     const int nj = (s.n + kBlockN - 1) / kBlockN;
     const int nsteps = nk * nj;
+    const int nall = (SOFTMAX ? 2 : 1) * nsteps;  // both passes' steps, in one stream
     // Accumulators are zero at every column block's start: set here and again after each
     // block's output (AREG, one step per block: the block's first MFMA takes a zero addend
     // instead), not selected at every step.
@@ -344,9 +369,12 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     auto load = [&](Pieces<!AREG>& pp) {
         load_step<LAYOUT, VEC, !AREG>(a_blk, b_blk, s, rows, ld_j * kBlockN, ld_k * kChunkK, wave, lane,
                                       !TEMPORAL && nj == 1, pp);  // A read once when one column block
-        if (ld_st + 1 < nsteps) {
+        if (ld_st + 1 < nall) {
             ++ld_st;
-            if (++ld_k == nk) { ld_k = 0; ++ld_j; }
+            if (++ld_k == nk) {
+                ld_k = 0;
+                if (++ld_j == nj) ld_j = 0;  // the second pass starts again at block 0
+            }
         }
     };
 #pragma unroll
@@ -359,25 +387,32 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     // product; the one-step scores product gains nothing and skips it).
     int prio_step[3] = {0, 0, 0};
     if constexpr (!AREG) {
-        const int64_t tot = static_cast<int64_t>(total_rows > 0 ? total_rows : 1) * nsteps;
-        const int64_t done4 = 4 * static_cast<int64_t>(done_rows) * nsteps;
+        const int64_t tot = static_cast<int64_t>(total_rows > 0 ? total_rows : 1) * nall;
+        const int64_t done4 = 4 * static_cast<int64_t>(done_rows) * nall;
         const int64_t per4 = 4 * static_cast<int64_t>(round_rows_n > 0 ? round_rows_n : 1);
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
             const int64_t need = (q + 1) * tot - done4;  // 4 * row-steps still short of q + 1
             const int64_t t = need <= 0 ? 0 : (need + per4 - 1) / per4;
-            prio_step[q] = t < nsteps ? static_cast<int>(t) : nsteps;
+            prio_step[q] = t < nall ? static_cast<int>(t) : nall;
         }
     }
     int cur_j = 0, cur_k = 0;
+    float sm_max = kNegInfF, sm_sum = 0.0f, sm_inv = 0.0f;  // SOFTMAX: this lane's row
     // One step: st's operands (in pp, loaded kDepth steps ago) go to LDS buffer lb, then
     // step st + kDepth's loads are issued into pp, then st's arithmetic and, at a column
     // block's end, its output.
-    auto step = [&](int st, Pieces<!AREG>& pp, uint16_t* lb) {
+    // PASS (a compile-time tag): 0 without SOFTMAX, else 1 (row statistics) or 2 (output), so
+    // that each pass's step is compiled on its own.
+    auto step = [&](auto pass, int st, Pieces<!AREG>& pp, uint16_t* lb) {
+        constexpr int PASS = decltype(pass)::value;
         if constexpr (!AREG)
             set_prio(3 - (st >= prio_step[0]) - (st >= prio_step[1]) - (st >= prio_step[2]));
         const int jb = cur_j, kb = cur_k;
-        if (++cur_k == nk) { cur_k = 0; ++cur_j; }
+        if (++cur_k == nk) {
+            cur_k = 0;
+            if (++cur_j == nj) cur_j = 0;
+        }
         const int j0 = jb * kBlockN;
         // lb (buffer st % 2) was last read at step st - 2; every wave finished that step
         // before the barrier of step st - 1, so one barrier per step orders both uses.
@@ -410,6 +445,81 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
         // column block done: tile t, lane (li, h) holds output row li, columns
         // j0 + 32 t + 8 g + 4 h + 0..3
         const int jn = s.n - j0 < kBlockN ? s.n - j0 : kBlockN;
+        float scale = s.alpha;
+        if constexpr (SOFTMAX) {
+            // Logits in base-2 units, y = acc * c with c = alpha log2 e, never formed on their
+            // own: the row maximum of y is c times the maximum (c < 0: minimum) of acc, and each
+            // 2^(y - M) takes one fma and one v_exp_f32.  Columns past n (a partial last block)
+            // count as -inf.
+            const float c2 = s.alpha * kLog2eF;
+            const bool full = jn == kBlockN;  // wave-uniform: only a partial last block masks
+            auto col_ok = [&](int t, int i) { return t * kTileN + 8 * (i / 4) + 4 * h + (i % 4) < jn; };
+            if constexpr (PASS == 1) {  // first pass: fold this block into the row's maximum and sum
+                // the block's largest y is c times its largest (c < 0: smallest) product; the four
+                // loops leave acc untouched, so no branch needs copies of it
+                auto extreme = [&](auto pick, float none) {
+                    float e = none;
+                    if (full) {
+#pragma unroll
+                        for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) e = pick(e, acc[t][i]);
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) e = pick(e, col_ok(t, i) ? acc[t][i] : none);
+                    }
+                    return e;
+                };
+                float bm = c2 >= 0.0f
+                               ? extreme([](float u, float v) { return __builtin_elementwise_maximum(u, v); }, kNegInfF)
+                               : extreme([](float u, float v) { return __builtin_elementwise_minimum(u, v); }, -kNegInfF);
+                bm = c2 == 0.0f ? 0.0f : c2 * bm;  // the block's largest y (alpha = 0: all y are 0)
+                bm = half_pair(bm, lane, [](float u, float v) { return __builtin_elementwise_maximum(u, v); });
+                const float mx = __builtin_elementwise_maximum(sm_max, bm);
+                const float ms = mx == kNegInfF ? 0.0f : mx;
+#pragma unroll
+                for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) acc[t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[t][i], c2, -ms));
+                if (!full) {  // columns past n add nothing
+#pragma unroll
+                    for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            if (!col_ok(t, i)) acc[t][i] = 0.0f;
+                }
+                // pairwise sum of the lane's 32 values: within each tile 16 -> 1, then the tiles
+#pragma unroll
+                for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                    for (int w = 8; w >= 1; w /= 2)
+#pragma unroll
+                        for (int i = 0; i < w; ++i) acc[t][i] = acc[t][2 * i] + acc[t][2 * i + 1];
+                static_assert(kBlockTiles == 2, "two tiles per block");
+                const float bs = acc[0][0] + acc[1][0];
+                sm_sum = sm_sum * __builtin_amdgcn_exp2f(sm_max - ms) + bs;
+                sm_max = mx;
+                if (jb + 1 == nj) {  // the row's last block: both lanes' sums, and 1 / sum
+                    const float tot = half_pair(sm_sum, lane, [](float u, float v) { return u + v; });
+                    sm_inv = tot == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(tot);
+                }
+                if constexpr (!AREG) {
+#pragma unroll
+                    for (int t = 0; t < kBlockTiles; ++t) acc[t] = f32x16{};
+                }
+                return;
+            }
+            // second pass: the block's probabilities, then the ordinary output path
+            const float ms = sm_max == kNegInfF ? 0.0f : sm_max;
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    acc[t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[t][i], c2, -ms)) * sm_inv;
+            scale = 1.0f;
+        }
         if constexpr (BF16OUT) {  // rounded to bf16 (nearest even) on the way into LDS
             uint16_t* const lh = lw;
 #pragma unroll
@@ -417,8 +527,8 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     *reinterpret_cast<u32x2*>(lh + li * kLdh + t * kTileN + 8 * g + 4 * h) =
-                        u32x2{pack_bf16(s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1]),
-                              pack_bf16(s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3])};
+                        u32x2{pack_bf16(scale * acc[t][4 * g], scale * acc[t][4 * g + 1]),
+                              pack_bf16(scale * acc[t][4 * g + 2], scale * acc[t][4 * g + 3])};
             }
             wave_lds_sync();
             store_block_bf16<VEC, TEMPORAL>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lh);
@@ -429,8 +539,8 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     *reinterpret_cast<f32x4*>(lc + li * kLdc + t * kTileN + 8 * g + 4 * h) =
-                        f32x4{s.alpha * acc[t][4 * g], s.alpha * acc[t][4 * g + 1],
-                              s.alpha * acc[t][4 * g + 2], s.alpha * acc[t][4 * g + 3]};
+                        f32x4{scale * acc[t][4 * g], scale * acc[t][4 * g + 1],
+                              scale * acc[t][4 * g + 2], scale * acc[t][4 * g + 3]};
             }
             wave_lds_sync();
             store_block_f32<VEC, TEMPORAL>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
@@ -444,31 +554,54 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     // Two steps per iteration and the odd one after the loop, so that every path around the
     // loop issues the same loads (a step waits for its own loads only, not for the next
     // step's, which the wait-count insertion would otherwise have to assume).
+    // With SOFTMAX the second pass continues the same buffer order: it starts on buffer 1
+    // when the first pass has an odd number of steps.
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    using P2 = std::integral_constant<int, 2>;
     int st = 0;
-    for (; st + 1 < nsteps; st += 2) {
-        step(st, p[0], lbs);
-        step(st + 1, p[1], lbs + kBBufElems);
+    auto run = [&](auto pass, int end, bool odd_start) {
+        if (!odd_start) {
+            for (; st + 1 < end; st += 2) {
+                step(pass, st, p[0], lbs);
+                step(pass, st + 1, p[1], lbs + kBBufElems);
+            }
+            if (st < end) step(pass, st++, p[0], lbs);
+        } else {
+            for (; st + 1 < end; st += 2) {
+                step(pass, st, p[1], lbs + kBBufElems);
+                step(pass, st + 1, p[0], lbs);
+            }
+            if (st < end) step(pass, st++, p[1], lbs + kBBufElems);
+        }
+    };
+    if constexpr (!SOFTMAX) {
+        run(P0{}, nall, false);
+    } else {
+        run(P1{}, nsteps, false);
+        run(P2{}, nall, (nsteps & 1) != 0);
     }
-    if (st < nsteps) step(st, p[0], lbs);
 }
 
-// An empty reduction (k == 0): the wave's output rows are zeros.
-template <bool BF16OUT>
+// An empty reduction (k == 0): the wave's output rows are zeros, or with SOFTMAX the
+// softmax of a row of zero logits, 1/n (as the two passes compute it: 2^0 times 1 / n).
+template <bool BF16OUT, bool SOFTMAX>
 __device__ __forceinline__ void zero_rows(void* c, const Shape& s, int64_t bidx, int i0, int rows,
                                           int lane) {
+    const float v = SOFTMAX ? __builtin_amdgcn_rcpf(static_cast<float>(s.n)) : 0.0f;
     for (int r = 0; r < rows; ++r) {
         const int64_t off = bidx * s.c_batch + static_cast<int64_t>(i0 + r) * s.n;
         for (int j = lane; j < s.n; j += 64) {
             if constexpr (BF16OUT)
-                static_cast<uint16_t*>(c)[off + j] = 0;
+                static_cast<uint16_t*>(c)[off + j] = static_cast<uint16_t>(pack_bf16(v, 0.0f) & 0xFFFFu);
             else
-                static_cast<float*>(c)[off + j] = 0.0f;
+                static_cast<float*>(c)[off + j] = v;
         }
     }
 }
 
-// Kernel modes (one compiled instance each): NT and NN.
-enum { kModeNt = 0, kModeNn = 1 };
+// Kernel modes (one compiled instance each): NT, NN and NT with the row softmax.
+enum { kModeNt = 0, kModeNn = 1, kModeNtSoftmax = 2 };
 constexpr int kWavesPerSimd = 3;
 
 // Worker loop: workgroup w runs its items; an item's rows are taken up to 128 at a time (cut
@@ -480,6 +613,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                                             const bsm_item* __restrict__ items,
                                             bsm_trace_rec* __restrict__ trace, uint16_t* lds_base) {
     constexpr int kLayout = MODE == kModeNn ? kNN : kNT;
+    constexpr bool kSoftmax = MODE == kModeNtSoftmax;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int lane = static_cast<int>(threadIdx.x) & 63;
@@ -509,9 +643,9 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 int mine = seg - wave * kTileM;
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
                 if (s.k == 0)
-                    zero_rows<BF16OUT>(c, s, bidx, i + wave * kTileM, mine, lane);
+                    zero_rows<BF16OUT, kSoftmax>(c, s, bidx, i + wave * kTileM, mine, lane);
                 else
-                    round_rows<kLayout, BF16OUT, VEC, AREG, TEMPORAL>(a, b, c, s, bidx, i + wave * kTileM, mine,
+                    round_rows<kLayout, BF16OUT, VEC, AREG, TEMPORAL, kSoftmax>(a, b, c, s, bidx, i + wave * kTileM, mine,
                                                             wave, lane, lw, lbs, wg_done, seg, total_rows);
                 wg_done += seg;
                 done += static_cast<uint32_t>(mine);

@@ -156,3 +156,31 @@ def test_abs_product_sums_one_row_hand_values():
     for layout in ("nt", "nn"):  # with n = 1 both layouts store B the same way
         s = gemm.abs_product_sums(_hand_bits(a), _hand_bits(b), 2, 1, 1, 4, layout)
         assert s.tolist() == [10.0, 5.0]
+
+
+def test_scores_softmax_hand_values():
+    """Row softmax of alpha A B^T by hand: A = [[1, 0], [0, 2]] (m = 2, k = 2), B = I (n = 2),
+    alpha = ln 3: scores [[ln 3, 0], [0, 2 ln 3]], so the rows are [e^ln3, 1] / (3 + 1) =
+    [3/4, 1/4] and [1, 9] / 10 = [1/10, 9/10]."""
+    a = _hand_bits([1, 0, 0, 2])
+    b = _hand_bits([1, 0, 0, 1])
+    p = gemm.scores_softmax(a, b, 1, 2, 2, 2, alpha=float(np.log(3.0)))
+    assert np.allclose(p, [0.75, 0.25, 0.1, 0.9], rtol=0, atol=1e-15)
+
+
+def test_scores_softmax_rows_and_degenerate_cases():
+    rng = np.random.default_rng(66)
+    batch, m, n, k = 3, 5, 7, 16
+    a = _bf16(rng.standard_normal(batch * m * k))
+    b = _bf16(rng.standard_normal(batch * n * k))
+    p = gemm.scores_softmax(a, b, batch, m, n, k, alpha=0.25).reshape(batch * m, n)
+    assert np.all(p > 0) and np.allclose(p.sum(axis=1), 1.0, rtol=0, atol=1e-14)
+    # a larger score gives a larger probability (the order of each row is kept)
+    s = gemm.batched_gemm(a, b, batch, m, n, k, "nt", 0.25).reshape(batch * m, n)
+    assert np.array_equal(np.argsort(s, axis=1, kind="stable"), np.argsort(p, axis=1, kind="stable"))
+    # alpha = 0 and k = 0: every score is 0, every probability 1/n
+    assert np.allclose(gemm.scores_softmax(a, b, batch, m, n, k, alpha=0.0), 1.0 / n, rtol=0, atol=1e-15)
+    z = np.zeros(0, np.uint16)
+    assert np.allclose(gemm.scores_softmax(z, z, batch, m, n, 0), 1.0 / n, rtol=0, atol=1e-15)
+    # n = 1: the single probability is 1
+    assert np.allclose(gemm.scores_softmax(a, b[: batch * k], batch, m, 1, k), 1.0, rtol=0, atol=0)

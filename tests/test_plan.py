@@ -404,10 +404,12 @@ def test_gemm_plans_cover_every_output_row_in_128_row_blocks(schedule, shape):
 
 
 def test_gemm_plan_rejects_bad_arguments():
-    for args in [(-1, 4, 4, 4, 0), (1, -4, 4, 4, 0), (1, 4, 4, 4, 2)]:
+    for args in [(-1, 4, 4, 4, 0), (1, -4, 4, 4, 0), (1, 4, 4, 4, 3)]:
         with pytest.raises(bsm.BsmError) as e:
             bsm.bsm_gemm_plan_create(*args[:4], layout=args[4], topology=MI355X, device=-1)
         assert e.value.status == bsm.BSM_ERR_INVALID_ARG
+    # layout 2 is the score product with the row softmax
+    bsm.bsm_gemm_plan_create(1, 4, 4, 4, layout=2, topology=MI355X, device=-1).destroy()
     # a matrix-product plan does not run as a softmax, nor a softmax plan as a product
     lib = bsm.load()
     import ctypes
