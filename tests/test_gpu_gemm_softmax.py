@@ -115,6 +115,20 @@ def test_scores_softmax_large_logits_and_k0():
     assert np.allclose(got0, 1.0 / n, rtol=2.0 ** -20, atol=0)
 
 
+@pytest.mark.parametrize("k", [64, 72])
+def test_scores_softmax_negative_and_zero_alpha(k):
+    """alpha < 0: the largest logit comes from the smallest product; alpha = 0: every logit is 0
+    and each row is 1/n. Both operand forms (A in registers for k <= 64, through LDS above) and
+    a partial last column block (n = 200)."""
+    batch, m, n = 2, 80, 200
+    a, b = _operands(batch, m, n, k, seed=93 + k)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    for alpha in (-0.5, 0.0):
+        got = _run(batch, m, n, k, "f32", "balanced", a_d, b_d, alpha)
+        _check(got, a, b, batch, m, n, k, alpha, "f32")
+    assert np.allclose(bits_to_f64(got), 1.0 / n, rtol=2.0 ** -20, atol=0)
+
+
 def test_scores_softmax_one_shot():
     batch, m, n, k = 3, 128, 192, 64
     a, b = _operands(batch, m, n, k, seed=92)
