@@ -72,8 +72,8 @@ def _run(batch, m, n, k, out, schedule, a_d, b_d, alpha):
 
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", [(3, 200, 136, 64), (2, 130, 520, 72), (4, 64, 64, 16),
-                                   (1, 257, 1000, 128), (2, 33, 9, 8)],
-                         ids=["tails", "k72", "small", "wide", "narrow"])
+                                   (1, 257, 1000, 128), (2, 33, 9, 8), (2, 70, 203, 20)],
+                         ids=["tails", "k72", "small", "wide", "narrow", "elementwise"])
 def test_scores_softmax_tails_all_schedules(shape, out):
     batch, m, n, k = shape
     print(f"[nt_softmax {shape} {out}]", flush=True)
@@ -127,6 +127,24 @@ def test_scores_softmax_negative_and_zero_alpha(k):
         got = _run(batch, m, n, k, "f32", "balanced", a_d, b_d, alpha)
         _check(got, a, b, batch, m, n, k, alpha, "f32")
     assert np.allclose(bits_to_f64(got), 1.0 / n, rtol=2.0 ** -20, atol=0)
+
+
+def test_scores_softmax_temporal_flag_gives_the_same_bits():
+    """BSM_FLAG_TEMPORAL only changes the cache hints of P's stores and Q's loads."""
+    batch, m, n, k = 16, 256, 512, 64
+    a, b = _operands(batch, m, n, k, seed=95)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    outs = []
+    for flags in (0, bsm.BSM_FLAG_TEMPORAL):
+        p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt_softmax", "bf16", "balanced",
+                                     topology={"flags": flags}, device=0)
+        c = torch.empty(batch * m * n, dtype=torch.bfloat16, device="cuda")
+        bsm.bsm_gemm_execute(p, a_d, b_d, c, 0.125)
+        torch.cuda.synchronize()
+        p.destroy()
+        outs.append(to_host_bits(c))
+    _check(outs[0], a, b, batch, m, n, k, 0.125, "bf16")
+    assert np.array_equal(outs[0], outs[1])
 
 
 def test_scores_softmax_one_shot():
