@@ -96,13 +96,27 @@ constexpr int team_threads(int kernel_class) {
     return kernel_class >= kLongestClass ? 2 * kTeamThreads : kTeamThreads;
 }
 
+// Rows a workgroup holds at a time (kernel class >= 4) when a row takes `per_lane` vectors per
+// lane: two for the shortest rows (at most 3 vectors per lane) and for bf16 rows of 5 or 6
+// vectors per lane in classes 5 and 6, one otherwise (the kernel's team_item makes the same
+// choice).
+constexpr int team_rows_in_flight(int per_lane, int kernel_class, int elem_bytes) {
+    const int max_l = (kernel_class >= 5 ? 2 : 1) * kTeamValues * elem_bytes / kVecBytes;
+    return (per_lane <= 3 || (elem_bytes == 2 && max_l >= 6 && per_lane <= 6)) ? 2 : 1;
+}
+
 // Rows one worker finishes per step for a row of `cols` elements (aligned rows): one wave's
 // tile step, times the waves of the workgroup that is the worker in long-row plans (kernel
-// class >= 4); one row for a row the workgroup holds.
+// class >= 4); for a row the workgroup holds, the rows it holds at a time, so that a piece of
+// a balanced table does not leave half of a row pair empty.
 constexpr int wave_step_rows(int64_t cols, int elem_bytes, int kernel_class) {
     const int64_t nvec = (cols * elem_bytes + kVecBytes - 1) / kVecBytes;
     const Tile t = tile_for(nvec, kernel_class, elem_bytes);
-    if (t.V == 0) return 1;
+    if (t.V == 0) {
+        if (kernel_class < 4) return 1;
+        const int nt = team_threads(kernel_class);
+        return team_rows_in_flight(static_cast<int>((nvec + nt - 1) / nt), kernel_class, elem_bytes);
+    }
     const int rows = (kWave / t.G) * t.U;
     return kernel_class >= 4 ? rows * (team_threads(kernel_class) / kWave) : rows;
 }
