@@ -147,6 +147,27 @@ def test_scores_softmax_temporal_flag_gives_the_same_bits():
     assert np.array_equal(outs[0], outs[1])
 
 
+@pytest.mark.parametrize("rising", [True, False])
+def test_scores_softmax_running_maximum_moves_every_block(rising):
+    """Scores that rise (or fall) along each row: with rising scores the running maximum moves
+    up in every 64-column block, so the sum kept so far is rescaled 32 times, down to nothing
+    for the first blocks; with falling ones it is set by the first block and every later block
+    adds terms far below it. Row i's scores are (i + 1) / 8 * j / 64 (+ noise), up to ~256."""
+    batch, m, n, k = 2, 64, 2048, 16
+    rng = np.random.default_rng(96)
+    q = np.zeros((batch, m, k), np.float32)
+    q[:, :, 0] = (np.arange(m, dtype=np.float32) + 1.0) / 8.0
+    q[:, :, 1:] = 0.05 * rng.standard_normal((batch, m, k - 1), dtype=np.float32)
+    key = np.zeros((batch, n, k), np.float32)
+    ramp = np.arange(n, dtype=np.float32) / 64.0
+    key[:, :, 0] = ramp if rising else ramp[::-1]
+    key[:, :, 1:] = rng.standard_normal((batch, n, k - 1), dtype=np.float32)
+    a = workloads._to_bf16_bits(q.reshape(-1))
+    b = workloads._to_bf16_bits(key.reshape(-1))
+    got = _run(batch, m, n, k, "f32", "balanced", _dev_bf16(a), _dev_bf16(b), 1.0)
+    _check(got, a, b, batch, m, n, k, 1.0, "f32")
+
+
 def test_scores_softmax_one_shot():
     batch, m, n, k = 3, 128, 192, 64
     a, b = _operands(batch, m, n, k, seed=92)
