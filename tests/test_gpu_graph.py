@@ -1,6 +1,6 @@
 """Plans executed inside a captured HIP graph (torch.cuda.CUDAGraph). A plan's work table is
 uploaded when the plan is built and an execution is one kernel launch (no memset, copy or
-synchronisation), so forward, backward and product executions can be captured. Each replay is
+synchronisation), so forward, backward, product and product-with-softmax executions can be captured. Each replay is
 checked bit for bit against eager executions on the same inputs, with eager work (new inputs)
 between replays."""
 
@@ -31,6 +31,7 @@ def test_captured_graph_replays_match_eager(dtype):
                                schedule="balanced", device=0)
     batch, m, nn, k = 6, 256, 256, 64
     gplan = bsm.bsm_gemm_plan_create(batch, m, nn, k, "nt", "bf16", "balanced", device=0)
+    splan = bsm.bsm_gemm_plan_create(batch, m, nn, k, "nt_softmax", "f32", "balanced", device=0)
     x = to_device(w.x, dtype)
     tdt = x.dtype
     out, dx = torch.zeros_like(x), torch.zeros_like(x)
@@ -38,6 +39,7 @@ def test_captured_graph_replays_match_eager(dtype):
     a = torch.randn(batch * m * k, device="cuda").to(torch.bfloat16)
     b = torch.randn(batch * nn * k, device="cuda").to(torch.bfloat16)
     c = torch.zeros(batch * m * nn, device="cuda", dtype=torch.bfloat16)
+    p = torch.zeros(batch * m * nn, device="cuda", dtype=torch.float32)
 
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
@@ -45,6 +47,7 @@ def test_captured_graph_replays_match_eager(dtype):
         bsm.bsm_plan_execute(plan, x, out)
         bsm.bsm_plan_execute_backward(plan, out, dy, dx)
         bsm.bsm_gemm_execute(gplan, a, b, c, alpha=0.125)
+        bsm.bsm_gemm_execute(splan, a, b, p, alpha=0.125)
     torch.cuda.current_stream().wait_stream(stream)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
@@ -52,6 +55,7 @@ def test_captured_graph_replays_match_eager(dtype):
         bsm.bsm_plan_execute(plan, x, out)
         bsm.bsm_plan_execute_backward(plan, out, dy, dx)
         bsm.bsm_gemm_execute(gplan, a, b, c, alpha=0.125)
+        bsm.bsm_gemm_execute(splan, a, b, p, alpha=0.125)
 
     rng = np.random.default_rng(52)
     for rep in range(4):
@@ -65,14 +69,17 @@ def test_captured_graph_replays_match_eager(dtype):
         graph.replay()
         torch.cuda.synchronize()
         ref_out, ref_dx = torch.zeros_like(x), torch.zeros_like(x)
-        ref_c = torch.zeros_like(c)
+        ref_c, ref_p = torch.zeros_like(c), torch.zeros_like(p)
         bsm.bsm_plan_execute(plan, x, ref_out)
         bsm.bsm_plan_execute_backward(plan, ref_out, dy, ref_dx)
         bsm.bsm_gemm_execute(gplan, a, b, ref_c, alpha=0.125)
+        bsm.bsm_gemm_execute(splan, a, b, ref_p, alpha=0.125)
         torch.cuda.synchronize()
         assert torch.equal(_bits(out)[mask], _bits(ref_out)[mask]), rep
         assert torch.equal(_bits(dx)[mask], _bits(ref_dx)[mask]), rep
         assert torch.equal(_bits(c), _bits(ref_c)), rep
+        assert torch.equal(_bits(p), _bits(ref_p)), rep
     del graph
     plan.destroy()
     gplan.destroy()
+    splan.destroy()
