@@ -319,6 +319,108 @@ __device__ __forceinline__ void rows_u(const typename E::T* in, typename E::T* o
     }
 }
 
+// The reductions of U rows held by lanes gb .. gb + n - 1 each (n <= 32, any n; i = lane - gb):
+// a tree to the row's first lane (lane i < d takes lane i + d while i + d < n, d = 16, 8, 4, 2,
+// 1), then one ds_bpermute from it, so every lane of a row ends with the same bits.  Each step
+// is taken for all U rows before the next, so that their LDS round trips overlap.
+template <class Op, int U>
+__device__ __forceinline__ void seg_reduce(float (&a)[U], int i, int n, int gb) {
+#pragma unroll
+    for (int d = 16; d >= 1; d /= 2) {
+        float o[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            o[u] = __builtin_bit_cast(
+                float, __builtin_amdgcn_ds_bpermute((gb + i + d) << 2, __builtin_bit_cast(int, a[u])));
+        const bool take = i < d && i + d < n;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (take) a[u] = Op::f(a[u], o[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        a[u] = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(gb << 2, __builtin_bit_cast(int, a[u])));
+}
+
+// Packed tile (tile_for's G = n, not a power of two): aligned rows of n vectors, 64 / n rows side
+// by side in a wave, row g on lanes [g n, g n + n), one vector per lane, U rows per group in
+// flight.  A load instruction then moves 64 / n consecutive rows with almost every lane busy,
+// where a power-of-two group would leave up to half of its lanes idle.
+template <class E, int U>
+__device__ __forceinline__ void rows_packed(const typename E::T* in, typename E::T* out,
+                                            int64_t base, int n, int nrows, int r0, int step,
+                                            int i, int gb, bool on) {
+    constexpr int EPV = E::kEPV;
+    const int cols = n * EPV;
+    float x[U][EPV];
+    typename E::R raw[U];
+    bool act[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = r0 + u * step;
+        act[u] = on && r < nrows;
+        raw[u] = act[u] ? E::load_raw(in + base + static_cast<int64_t>(r) * cols + i * EPV)
+                        : E::raw_fill(kNegInf);
+    }
+    float m[U], s[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        E::unpack(raw[u], x[u]);
+        m[u] = lane_reduce<EPV, OpMax>(x[u]);
+    }
+    seg_reduce<OpMax, U>(m, i, n, gb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float ms = (m[u] == kNegInf) ? 0.0f : m[u];
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) x[u][k] = __builtin_amdgcn_exp2f((x[u][k] - ms) * kLog2e);
+        s[u] = lane_reduce<EPV, OpAdd>(x[u]);
+    }
+    seg_reduce<OpAdd, U>(s, i, n, gb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float inv = (s[u] == 0.0f) ? 0.0f : __builtin_amdgcn_rcpf(s[u]);
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) x[u][k] *= inv;
+        if (act[u])
+            E::store_vec(out + base + static_cast<int64_t>(r0 + u * step) * cols + i * EPV, x[u]);
+    }
+}
+
+// One item in packed tiles, walked like run_item with 64 / n rows per wave.
+template <class E, int U>
+__device__ __forceinline__ uint32_t run_item_packed(const typename E::T* in, typename E::T* out,
+                                                    int64_t base, int cols, int nrows, int reps,
+                                                    int64_t stride, int wave, int nwaves,
+                                                    int lane64) {
+    const int n = cols / E::kEPV;
+    const int rpw = 64 / n;
+    const int sub = lane64 / n;
+    const int i = lane64 - sub * n;
+    const bool on = sub < rpw;
+    const int gb = sub * n;
+    const int step = nwaves * rpw;
+    uint32_t done = 0;
+    for (int k = 0; k < reps; ++k) {
+        const int64_t b = base + k * stride;
+        int r0 = wave * rpw;
+        for (; r0 + (U - 1) * step < nrows; r0 += U * step) {
+            rows_packed<E, U>(in, out, b, n, nrows, r0 + sub, step, i, gb, on);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int left = nrows - (r0 + u * step);
+                done += left < rpw ? left : rpw;
+            }
+        }
+        for (; r0 < nrows; r0 += step) {
+            rows_packed<E, 1>(in, out, b, n, nrows, r0 + sub, step, i, gb, on);
+            const int left = nrows - r0;
+            done += left < rpw ? left : rpw;
+        }
+    }
+    return done;
+}
+
 // One item with G lanes per row: `reps` ranges of `nrows` rows, range k starting at element
 // base + k * stride.  Within a range the worker's rows are wave*RPW + sub + j*step, j = 0, 1,
 // ... (RPW = 64/G rows per wave, step = rows covered by all the worker's waves at once); loop
@@ -801,7 +903,12 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
     if constexpr (VEC) {
         // the tile of bsm::tile_for: one wave-uniform branch per (G, V, U) the class can pick
         constexpr bool F = E::kBytes == 4;
-        const bsm::Tile t = bsm::tile_for(nvec, KCLASS < 4 ? KCLASS : 4, E::kBytes);
+        const bsm::Tile t = bsm::tile_for(nvec, KCLASS < 4 ? KCLASS : 4, E::kBytes, !SHIFT);
+        if constexpr (F && !SHIFT && KCLASS == 0) {
+            if (t.V == 1 && (t.G & (t.G - 1)) != 0)  // packed tile
+                return run_item_packed<E, 4>(in, out, base, cols, nrows, reps, stride, wave,
+                                             nwaves, lane64);
+        }
 #define BSM_TILE(g, v, u) if (t.G == g && t.V == v && t.U == u) return BSM_RUN(g, v, u)
         BSM_TILE(16, 1, 4);
         if constexpr (F) BSM_TILE(32, 1, 8);

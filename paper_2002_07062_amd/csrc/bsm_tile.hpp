@@ -10,8 +10,8 @@ constexpr int kWave = 64;
 constexpr int kVecBytes = 16;   // one 128-bit access
 
 // Register tile of an aligned row of `nvec` 16-byte vectors in a kernel of class `kclass`: G
-// lanes per row (a group), V vectors per lane, U rows per group in flight.  V = 0: beyond the
-// register tiles of the class.
+// lanes per row (a group), V vectors per lane, U rows per group in flight, 64 / G groups per
+// wave.  V = 0: beyond the register tiles of the class.
 //
 // Measured on MI355X (uniform batches of ~200 MB): a tile streams at the copy rate when it is
 // full; a partly filled one loses in proportion to the bytes its lanes keep in flight.  fp32
@@ -28,7 +28,17 @@ struct Tile {
     int U;
 };
 
-constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes) {
+constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes, bool packed = true) {
+    // fp32 rows of 9-10 and 17-21 vectors in plans of kernel class 0: packed groups of exactly
+    // nvec lanes, 64 / nvec rows side by side per wave (G = nvec, not a power of two, marks the
+    // packed tile), where a power-of-two group leaves 34-47% of its lanes idle.  Measured
+    // against the tiles they replace (uniform ~200 MB batches, alternating runs on one box, GB/s):
+    // 36 fp32 4590 -> 5250, 40 4980 -> 5320, 68 4670 -> 4960, 72 5030 -> 5060, 84 5000 -> 5260;
+    // 44 and 48 (5 groups of 11 or 12) lost 2-3%, and so did the ragged batch (-1.5%) with the
+    // packed code in its class-2 instance even where no row took it, so higher classes keep
+    // the power-of-two tiles.  Only rows that start and end on 16-byte vectors (`packed`).
+    if (packed && kclass == 0 && elem_bytes == 4 && ((nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))
+        return Tile{static_cast<int>(nvec), 1, 4};
     if (nvec <= 16) return Tile{16, 1, 4};
     if (elem_bytes == 4 && nvec <= 24) return Tile{32, 1, 8};
     if (nvec <= 32) return Tile{32, 1, 4};

@@ -107,6 +107,24 @@ def test_partial_tile_widths_all_schedules(dtype):
     assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
 
 
+def test_packed_tile_widths_all_schedules():
+    """fp32 rows of 9-10 and 17-21 vectors in a plan of kernel class 0 (every width <= 256):
+    packed groups of exactly that many lanes, 64 / n rows side by side per wave, with row counts
+    that leave partly filled waves and steps; a 64-wide slice (power-of-two tile) in the same
+    plan. Every schedule matches the oracle and all three give the same bits."""
+    cols = [36, 40, 68, 72, 76, 80, 84, 64, 37, 70]
+    rng = np.random.default_rng(23)
+    rows = [int(r) for r in rng.integers(1, 120, size=len(cols))]
+    w = workloads.custom(rows, cols, dtype="f32", sigma=3.0, seed=24, gap=4)
+    results = []
+    for schedule in SCHEDULES:
+        print(f"[packed tile {schedule}] cols {cols} rows {rows}", flush=True)
+        bits, st = _check_ragged(w, schedule)
+        assert st["kernel_class"] == 0
+        results.append(bits)
+    assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_partial_tile_special_values_stay_in_their_row(dtype):
     """Rows handled side by side in one wave step: a NaN, +inf or fully masked row changes only
