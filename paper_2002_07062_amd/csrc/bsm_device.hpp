@@ -904,7 +904,7 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
         // the tile of bsm::tile_for: one wave-uniform branch per (G, V, U) the class can pick
         constexpr bool F = E::kBytes == 4;
         const bsm::Tile t = bsm::tile_for(nvec, KCLASS < 4 ? KCLASS : 4, E::kBytes, !SHIFT);
-        if constexpr (F && !SHIFT && KCLASS == 0) {
+        if constexpr (!SHIFT && KCLASS == 0) {
             if (t.V == 1 && (t.G & (t.G - 1)) != 0)  // packed tile
                 return run_item_packed<E, 4>(in, out, base, cols, nrows, reps, stride, wave,
                                              nwaves, lane64);

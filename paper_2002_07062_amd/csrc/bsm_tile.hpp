@@ -29,15 +29,16 @@ struct Tile {
 };
 
 constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes, bool packed = true) {
-    // fp32 rows of 9-10 and 17-21 vectors in plans of kernel class 0: packed groups of exactly
-    // nvec lanes, 64 / nvec rows side by side per wave (G = nvec, not a power of two, marks the
+    // Rows of 9-10 and 17-21 vectors in plans of kernel class 0: packed groups of exactly nvec
+    // lanes, 64 / nvec rows side by side per wave (G = nvec, not a power of two, marks the
     // packed tile), where a power-of-two group leaves 34-47% of its lanes idle.  Measured
     // against the tiles they replace (uniform ~200 MB batches, alternating runs on one box, GB/s):
-    // 36 fp32 4590 -> 5250, 40 4980 -> 5320, 68 4670 -> 4960, 72 5030 -> 5060, 84 5000 -> 5260;
-    // 44 and 48 (5 groups of 11 or 12) lost 2-3%, and so did the ragged batch (-1.5%) with the
-    // packed code in its class-2 instance even where no row took it, so higher classes keep
-    // the power-of-two tiles.  Only rows that start and end on 16-byte vectors (`packed`).
-    if (packed && kclass == 0 && elem_bytes == 4 && ((nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))
+    // fp32 36 4590 -> 5250, 40 4980 -> 5320, 68 4670 -> 4960, 72 5030 -> 5060, 84 5000 -> 5260;
+    // bf16 72 4610 -> 5080, 80 equal, 136 4270 -> 4650, 144 4480 -> 4860, 168 4660 -> 5080.
+    // 44 and 48 fp32 (5 groups of 11 or 12) lost 2-3%, and so did the ragged batch (-1.5%)
+    // with the packed code in its class-2 instance even where no row took it, so higher classes
+    // keep the power-of-two tiles.  Only rows that start and end on 16-byte vectors (`packed`).
+    if (packed && kclass == 0 && ((nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))
         return Tile{static_cast<int>(nvec), 1, 4};
     if (nvec <= 16) return Tile{16, 1, 4};
     if (elem_bytes == 4 && nvec <= 24) return Tile{32, 1, 8};

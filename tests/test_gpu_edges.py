@@ -107,18 +107,23 @@ def test_partial_tile_widths_all_schedules(dtype):
     assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
 
 
-def test_packed_tile_widths_all_schedules():
-    """fp32 rows of 9-10 and 17-21 vectors in a plan of kernel class 0 (every width <= 256):
+PACKED_COLS = {"f32": [36, 40, 68, 72, 76, 80, 84, 64, 37, 70],
+               "bf16": [72, 80, 136, 144, 152, 160, 168, 128, 73, 140]}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_packed_tile_widths_all_schedules(dtype):
+    """Rows of 9-10 and 17-21 vectors in a plan of kernel class 0 (every row <= 64 vectors):
     packed groups of exactly that many lanes, 64 / n rows side by side per wave, with row counts
-    that leave partly filled waves and steps; a 64-wide slice (power-of-two tile) in the same
-    plan. Every schedule matches the oracle and all three give the same bits."""
-    cols = [36, 40, 68, 72, 76, 80, 84, 64, 37, 70]
+    that leave partly filled waves and steps; a power-of-two slice and two unaligned ones in the
+    same plan. Every schedule matches the oracle and all three give the same bits."""
+    cols = PACKED_COLS[dtype]
     rng = np.random.default_rng(23)
     rows = [int(r) for r in rng.integers(1, 120, size=len(cols))]
-    w = workloads.custom(rows, cols, dtype="f32", sigma=3.0, seed=24, gap=4)
+    w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=24, gap=4 if dtype == "f32" else 8)
     results = []
     for schedule in SCHEDULES:
-        print(f"[packed tile {schedule}] cols {cols} rows {rows}", flush=True)
+        print(f"[packed tile {dtype} {schedule}] cols {cols} rows {rows}", flush=True)
         bits, st = _check_ragged(w, schedule)
         assert st["kernel_class"] == 0
         results.append(bits)
