@@ -72,11 +72,12 @@ struct OpAdd {
 // Reduction over aligned groups of G lanes; all lanes of a group end with identical bits.
 template <int G, class Op>
 __device__ __forceinline__ float group_reduce(float v) {
-    static_assert(G == 16 || G == 32 || G == 64, "group size");
+    static_assert(G == 8 || G == 16 || G == 32 || G == 64, "group size");
     v = Op::f(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]: partner lane ^ 1
     v = Op::f(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]: partner lane ^ 2
     v = Op::f(v, dpp<0x141>(v));  // row_half_mirror: partner in the other quad of 8
-    v = Op::f(v, dpp<0x140>(v));  // row_mirror: partner in the other half of the 16-lane row
+    if constexpr (G >= 16)
+        v = Op::f(v, dpp<0x140>(v));  // row_mirror: partner in the other half of the 16-lane row
     if constexpr (G >= 32) {      // rows 2k and 2k+1 meet
         auto p = __builtin_amdgcn_permlane16_swap(f_bits(v), f_bits(v), false, false);
         v = Op::f(bits_f(p[0]), bits_f(p[1]));
@@ -910,6 +911,7 @@ __device__ __forceinline__ uint32_t dispatch_item(const typename E::T* in, typen
                                              nwaves, lane64);
         }
 #define BSM_TILE(g, v, u) if (t.G == g && t.V == v && t.U == u) return BSM_RUN(g, v, u)
+        if constexpr (KCLASS == 0) BSM_TILE(8, 1, 4);
         BSM_TILE(16, 1, 4);
         if constexpr (F) BSM_TILE(32, 1, 8);
         BSM_TILE(32, 1, 4);

@@ -29,17 +29,20 @@ struct Tile {
 };
 
 constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes, bool packed = true) {
-    // Rows of 9-10 and 17-21 vectors in plans of kernel class 0: packed groups of exactly nvec
-    // lanes, 64 / nvec rows side by side per wave (G = nvec, not a power of two, marks the
-    // packed tile), where a power-of-two group leaves 34-47% of its lanes idle.  Measured
-    // against the tiles they replace (uniform ~200 MB batches, alternating runs on one box, GB/s):
-    // fp32 36 4590 -> 5250, 40 4980 -> 5320, 68 4670 -> 4960, 72 5030 -> 5060, 84 5000 -> 5260;
-    // bf16 72 4610 -> 5080, 80 equal, 136 4270 -> 4650, 144 4480 -> 4860, 168 4660 -> 5080.
-    // 44 and 48 fp32 (5 groups of 11 or 12) lost 2-3%, and so did the ragged batch (-1.5%)
-    // with the packed code in its class-2 instance even where no row took it, so higher classes
-    // keep the power-of-two tiles.  Only rows that start and end on 16-byte vectors (`packed`).
-    if (packed && kclass == 0 && ((nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))
+    // Rows of 5-7, 9-10 and 17-21 vectors in plans of kernel class 0: packed groups of exactly
+    // nvec lanes, 64 / nvec rows side by side per wave (G = nvec, not a power of two, marks the
+    // packed tile), where a power-of-two group leaves 34-69% of its lanes idle; rows of 8
+    // vectors take eight 8-lane groups.  Measured against the tiles they replace (uniform
+    // ~200 MB batches, alternating runs on one box, GB/s): fp32 20 2940 -> 5270, 24 3540 ->
+    // 5310, 28 3910 -> 5240, 32 4210 -> 5710, 36 4590 -> 5250, 40 4980 -> 5320, 68 4670 ->
+    // 4960, 72 5030 -> 5060, 84 5000 -> 5260; bf16 64 4500 -> 5180, 72 4610 -> 5080, 80 equal,
+    // 136 4270 -> 4650, 144 4480 -> 4860, 168 4660 -> 5080.  44 and 48 fp32 (5 groups of 11 or
+    // 12) lost 2-3%, and so did the ragged batch (-1.5%) with the packed code in its class-2
+    // instance even where no row took it, so higher classes keep the power-of-two tiles.  Only
+    // rows that start and end on 16-byte vectors (`packed`).
+    if (packed && kclass == 0 && ((nvec >= 5 && nvec <= 7) || (nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))
         return Tile{static_cast<int>(nvec), 1, 4};
+    if (kclass == 0 && nvec == 8) return Tile{8, 1, 4};
     if (nvec <= 16) return Tile{16, 1, 4};
     if (elem_bytes == 4 && nvec <= 24) return Tile{32, 1, 8};
     if (nvec <= 32) return Tile{32, 1, 4};

@@ -107,14 +107,15 @@ def test_partial_tile_widths_all_schedules(dtype):
     assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
 
 
-PACKED_COLS = {"f32": [36, 40, 68, 72, 76, 80, 84, 64, 37, 70],
-               "bf16": [72, 80, 136, 144, 152, 160, 168, 128, 73, 140]}
+PACKED_COLS = {"f32": [20, 24, 28, 32, 36, 40, 68, 72, 76, 80, 84, 64, 37, 70],
+               "bf16": [40, 48, 56, 64, 72, 80, 136, 144, 152, 160, 168, 128, 73, 140]}
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_packed_tile_widths_all_schedules(dtype):
-    """Rows of 9-10 and 17-21 vectors in a plan of kernel class 0 (every row <= 64 vectors):
-    packed groups of exactly that many lanes, 64 / n rows side by side per wave, with row counts
+    """Rows of 5-7, 9-10 and 17-21 vectors in a plan of kernel class 0 (every row <= 64
+    vectors): packed groups of exactly that many lanes, 64 / n rows side by side per wave, and
+    rows of 8 vectors in eight 8-lane groups, with row counts
     that leave partly filled waves and steps; a power-of-two slice and two unaligned ones in the
     same plan. Every schedule matches the oracle and all three give the same bits."""
     cols = PACKED_COLS[dtype]
