@@ -1049,6 +1049,76 @@ __device__ __forceinline__ void rows_u_bwd(const typename E::T* y, const typenam
     }
 }
 
+// The backward pass in packed tiles (rows of n vectors, n not a power of two, row j of a wave
+// on lanes [j n, j n + n)): d = sum(dy * y) by the same tree as the forward pass's reductions,
+// then dx = y (dy - d).
+template <class E, int U>
+__device__ __forceinline__ void rows_packed_bwd(const typename E::T* y, const typename E::T* dy,
+                                                typename E::T* dx, int64_t base, int n, int nrows,
+                                                int r0, int step, int i, int gb, bool on) {
+    constexpr int EPV = E::kEPV;
+    const int cols = n * EPV;
+    float a[U][EPV], g[U][EPV];
+    typename E::R ra[U], rg[U];
+    bool act[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t o = base + static_cast<int64_t>(r0 + u * step) * cols + i * EPV;
+        act[u] = on && r0 + u * step < nrows;
+        ra[u] = act[u] ? E::load_raw(y + o) : E::raw_fill(0.0f);
+        rg[u] = act[u] ? E::load_raw(dy + o) : E::raw_fill(0.0f);
+    }
+    float d[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        E::unpack(ra[u], a[u]);
+        E::unpack(rg[u], g[u]);
+        d[u] = lane_dot<EPV>(a[u], g[u]);
+    }
+    seg_reduce<OpAdd, U>(d, i, n, gb);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int k = 0; k < EPV; ++k) a[u][k] = a[u][k] * (g[u][k] - d[u]);
+        if (act[u])
+            E::store_vec(dx + base + static_cast<int64_t>(r0 + u * step) * cols + i * EPV, a[u]);
+    }
+}
+
+template <class E, int U>
+__device__ __forceinline__ uint32_t run_item_packed_bwd(const typename E::T* y,
+                                                        const typename E::T* dy,
+                                                        typename E::T* dx, int64_t base, int cols,
+                                                        int nrows, int reps, int64_t stride,
+                                                        int wave, int nwaves, int lane64) {
+    const int n = cols / E::kEPV;
+    const int rpw = 64 / n;
+    const int sub = lane64 / n;
+    const int i = lane64 - sub * n;
+    const bool on = sub < rpw;
+    const int gb = sub * n;
+    const int step = nwaves * rpw;
+    uint32_t done = 0;
+    for (int k = 0; k < reps; ++k) {
+        const int64_t b = base + k * stride;
+        int r0 = wave * rpw;
+        for (; r0 + (U - 1) * step < nrows; r0 += U * step) {
+            rows_packed_bwd<E, U>(y, dy, dx, b, n, nrows, r0 + sub, step, i, gb, on);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int left = nrows - (r0 + u * step);
+                done += left < rpw ? left : rpw;
+            }
+        }
+        for (; r0 < nrows; r0 += step) {
+            rows_packed_bwd<E, 1>(y, dy, dx, b, n, nrows, r0 + sub, step, i, gb, on);
+            const int left = nrows - r0;
+            done += left < rpw ? left : rpw;
+        }
+    }
+    return done;
+}
+
 template <class E, int G, int V, int U, bool VEC, bool SHIFT>
 __device__ __forceinline__ uint32_t run_item_bwd(const typename E::T* y, const typename E::T* dy,
                                                  typename E::T* dx, int64_t base, int cols,
@@ -1350,8 +1420,14 @@ __device__ __forceinline__ uint32_t dispatch_item_bwd(const typename E::T* y,
         // two input streams the forward pass's 32 x 2 tile measured 3% slower on 384 x 512 x
         // 512 bf16)
         constexpr bool F = E::kBytes == 4;
-        const bsm::Tile t = bsm::tile_for_bwd(nvec, KCLASS < 3 ? KCLASS : 3, E::kBytes);
+        const bsm::Tile t = bsm::tile_for_bwd(nvec, KCLASS < 3 ? KCLASS : 3, E::kBytes, !SHIFT);
+        if constexpr (!SHIFT && KCLASS == 0) {
+            if ((t.G & (t.G - 1)) != 0)  // packed tile
+                return run_item_packed_bwd<E, 2>(y, dy, dx, base, cols, nrows, reps, stride, wave,
+                                                 nwaves, lane64);
+        }
 #define BSM_TILE(g, v, u) if (t.G == g && t.V == v && t.U == u) return BSM_RUN_BWD(g, v, u)
+        if constexpr (KCLASS == 0) BSM_TILE(8, 1, 2);
         BSM_TILE(16, 1, 2);
         if constexpr (F) BSM_TILE(32, 1, 4);
         BSM_TILE(32, 1, 2);

@@ -81,8 +81,12 @@ constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes, bool packed = 
 // per wave in flight where a power-of-two tile is partly empty, and rows of 257-512 vectors
 // keep a 64 x 8 register tile (the one-wave path, staging y and dy in LDS, ran them at
 // 3.7 TB/s).
-constexpr Tile tile_for_bwd(int64_t nvec, int kclass, int elem_bytes) {
+constexpr Tile tile_for_bwd(int64_t nvec, int kclass, int elem_bytes, bool packed = true) {
     const bool f = elem_bytes == 4;
+    // plans of kernel class 0: rows of 5-7 vectors in packed groups, of 8 in 8-lane groups (as
+    // in the forward pass)
+    if (packed && kclass == 0 && nvec >= 5 && nvec <= 7) return Tile{static_cast<int>(nvec), 1, 2};
+    if (kclass == 0 && nvec == 8) return Tile{8, 1, 2};
     if (nvec <= 16) return Tile{16, 1, 2};
     if (f && nvec <= 24) return Tile{32, 1, 4};
     if (nvec <= 32) return Tile{32, 1, 2};

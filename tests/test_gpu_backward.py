@@ -58,6 +58,25 @@ def test_backward_ragged_odd_cols_with_gaps(dtype, schedule):
     _check(w, schedule, y, dy)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_packed_tile_widths_all_schedules(dtype):
+    """Rows of 5-7 vectors in packed groups and of 8 vectors in 8-lane groups (plans of kernel
+    class 0), with row counts that leave partly filled waves, a 16-vector slice and an unaligned
+    one in the same plan: every schedule matches the oracle and all three give the same bits."""
+    cols = {"f32": [20, 24, 28, 32, 64, 21], "bf16": [40, 48, 56, 64, 128, 41]}[dtype]
+    rng = np.random.default_rng(43)
+    rows = [int(r) for r in rng.integers(1, 200, size=len(cols))]
+    w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=44, gap=4 if dtype == "f32" else 8)
+    y, dy = backward_inputs(w)
+    results = []
+    for schedule in SCHEDULES:
+        print(f"[backward packed {dtype} {schedule}] cols {cols} rows {rows}", flush=True)
+        bits, st, _ = _check(w, schedule, y, dy)
+        assert st["kernel_class"] == 0
+        results.append(bits)
+    assert np.array_equal(results[0], results[1]) and np.array_equal(results[0], results[2])
+
+
 # Rows past the backward register tile (256 vectors): 16-byte aligned rows first, then
 # unaligned ones (which make the plan count one more vector per row for its kernel class).
 # Class 3: one wave per row, staged in LDS or read twice.  Class 4: a workgroup holds y and
