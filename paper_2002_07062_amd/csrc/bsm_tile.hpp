@@ -83,9 +83,12 @@ constexpr Tile tile_for(int64_t nvec, int kclass, int elem_bytes, bool packed = 
 // 3.7 TB/s).
 constexpr Tile tile_for_bwd(int64_t nvec, int kclass, int elem_bytes, bool packed = true) {
     const bool f = elem_bytes == 4;
-    // plans of kernel class 0: rows of 5-7 vectors in packed groups, of 8 in 8-lane groups (as
-    // in the forward pass)
-    if (packed && kclass == 0 && nvec >= 5 && nvec <= 7) return Tile{static_cast<int>(nvec), 1, 2};
+    // plans of kernel class 0: rows of 5-7 vectors (fp32 also 9-10 and 17-21) in packed
+    // groups, of 8 in 8-lane groups, as in the forward pass (bf16 rows of 9 and 18 vectors lost
+    // 3% packed: their 16- and 32-lane tiles already keep twice the elements per lane busy)
+    if (packed && kclass == 0 &&
+        ((nvec >= 5 && nvec <= 7) || (f && ((nvec >= 9 && nvec <= 10) || (nvec >= 17 && nvec <= 21)))))
+        return Tile{static_cast<int>(nvec), 1, 2};
     if (kclass == 0 && nvec == 8) return Tile{8, 1, 2};
     if (nvec <= 16) return Tile{16, 1, 2};
     if (f && nvec <= 24) return Tile{32, 1, 4};

@@ -60,10 +60,11 @@ def test_backward_ragged_odd_cols_with_gaps(dtype, schedule):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_backward_packed_tile_widths_all_schedules(dtype):
-    """Rows of 5-7 vectors in packed groups and of 8 vectors in 8-lane groups (plans of kernel
-    class 0), with row counts that leave partly filled waves, a 16-vector slice and an unaligned
+    """Rows of 5-7 vectors (fp32 also 9-10 and 17-21) in packed groups and of 8 vectors in
+    8-lane groups (plans of kernel class 0), with row counts that leave partly filled waves, a 16-vector slice and an unaligned
     one in the same plan: every schedule matches the oracle and all three give the same bits."""
-    cols = {"f32": [20, 24, 28, 32, 64, 21], "bf16": [40, 48, 56, 64, 128, 41]}[dtype]
+    cols = {"f32": [20, 24, 28, 32, 36, 40, 68, 72, 84, 64, 21],
+            "bf16": [40, 48, 56, 64, 72, 128, 41]}[dtype]
     rng = np.random.default_rng(43)
     rows = [int(r) for r in rng.integers(1, 200, size=len(cols))]
     w = workloads.custom(rows, cols, dtype=dtype, sigma=3.0, seed=44, gap=4 if dtype == "f32" else 8)
