@@ -93,7 +93,9 @@ typedef struct bsm_topology {
     int32_t wg_threads;  /* threads per workgroup, a multiple of 64 in [64, 1024]; plans with
                             rows longer than 2048 fp32 / 4096 bf16 elements run 256 (512 when
                             a row spans more than 16384 elements) whatever is asked: the
-                            workgroup's waves share each such row */
+                            workgroup's waves share each such row; bf16 plans whose longest
+                            row has 2049-4096 elements run at most 256 (their kernel needs
+                            more registers than 1024-thread workgroups leave) */
     int32_t piece_bytes; /* BALANCED / XCD: traffic of one worker's piece of a round */
     float item_cost;     /* planner cost of one work item, in byte equivalents (<= 0: default) */
     float row_cost;      /* planner cost of one row on top of its bytes (<= 0: default) */

@@ -324,6 +324,13 @@ bsm_status create_plan(bsm_plan* out_plan, const int64_t* offs, const int32_t* r
             tu.wg_threads = bsm::team_threads(p->kernel_class);
             topology = &tu;
         }
+        // bf16 plans of class 3 run in instances compiled for workgroups of up to 256 threads
+        if (!product && dtype == BSM_BF16 && p->kernel_class == 3 && topology &&
+            topology->wg_threads > 256) {
+            tu = *topology;
+            tu.wg_threads = 256;
+            topology = &tu;
+        }
         bsm_status st = resolve_topology(topology, device, dtype, p->kernel_class, p->shifted,
                                          &p->topo);
         if (st != BSM_OK) return st;

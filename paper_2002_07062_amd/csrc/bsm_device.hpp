@@ -1535,18 +1535,22 @@ __device__ __forceinline__ void worker_loop(const typename E::T* a, const typena
 
 extern __shared__ float bsm_lds[];  // lds_floats_per_wave floats per wave (long rows only)
 
-// Launch bounds: any workgroup size up to 1024 threads; long-row plans run workgroups of
-// bsm::team_threads(class) threads (classes 4 and 5: 256, two or more per CU; class 6: 512, one
-// per CU), so their rows may hold up to 256 VGPRs per lane.
-template <int KCLASS>
-constexpr int kMaxThreads = KCLASS >= 4 ? bsm::team_threads(KCLASS) : 1024;
-template <int KCLASS>
-constexpr int kMinWavesPerSimd = KCLASS >= 4 ? 2 : 1;
+// Launch bounds: any workgroup size up to 1024 threads (128 VGPRs per lane); long-row plans run
+// workgroups of bsm::team_threads(class) threads (classes 4 and 5: 256, two or more per CU;
+// class 6: 512, one per CU), so their rows may hold up to 256 VGPRs per lane.  bf16 plans of
+// class 3 run workgroups of at most 256 threads: their 64 x 8 tile needs about 160 VGPRs (at
+// 128 it spilled, 4.7-4.8 TB/s on 2304-4096-element rows; at 163 it runs three waves per SIMD,
+// 5.0-5.2 TB/s).
+template <class E, int KCLASS>
+constexpr int kMaxThreads = KCLASS >= 4 ? bsm::team_threads(KCLASS)
+                                        : (E::kBytes == 2 && KCLASS == 3 ? 256 : 1024);
+template <class E, int KCLASS>
+constexpr int kMinWavesPerSimd = (KCLASS >= 4 || (E::kBytes == 2 && KCLASS == 3)) ? 2 : 1;
 
 // SHIFTED: the instance for plans with slices whose rows do not start and end on 16-byte
 // vectors (kept apart so that the other plans' instances carry none of its registers).
 template <class E, int KCLASS, bool SHIFTED>
-__global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
+__global__ void __launch_bounds__((kMaxThreads<E, KCLASS>), (kMinWavesPerSimd<E, KCLASS>))
 bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* __restrict__ worker_ptr,
                    const bsm_item* __restrict__ items, int base_aligned, int per_wave,
                    int lds_floats_per_wave, bsm_trace_rec* __restrict__ trace) {
@@ -1556,7 +1560,7 @@ bsm_softmax_kernel(const typename E::T* in, typename E::T* out, const int32_t* _
 
 // dx = softmax backward of (y, dy) under the same work table.
 template <class E, int KCLASS, bool SHIFTED>
-__global__ void __launch_bounds__(kMaxThreads<KCLASS>, kMinWavesPerSimd<KCLASS>)
+__global__ void __launch_bounds__((kMaxThreads<E, KCLASS>), (kMinWavesPerSimd<E, KCLASS>))
 bsm_softmax_bwd_kernel(const typename E::T* y, const typename E::T* dy, typename E::T* dx,
                        const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                        int base_aligned, int per_wave, int lds_floats_per_wave,

@@ -581,6 +581,18 @@ def test_weighted_xcd_plan_skewed_weights_uniform_batch():
         assert rows_x * row_bytes == int(xb[x]), (x, rows_x)
 
 
+@pytest.mark.parametrize("threads", [64, 256, 512, 1024])
+def test_bf16_class3_plans_run_at_most_256_thread_workgroups(threads):
+    """bf16 rows of 2049-4096 elements (kernel class 3) run in an instance compiled for
+    workgroups of up to 256 threads: a larger request runs 256, a smaller one as asked; every
+    size matches the oracle."""
+    cols = [2304, 4096, 3000, 2056]
+    w = workloads.custom([9, 4, 7, 5], cols, dtype="bf16", sigma=3.0, seed=13, gap=8)
+    print(f"[bf16 class 3 asked {threads}]", flush=True)
+    bits, st = _check_ragged(w, "balanced", topology=dict(wg_threads=threads))
+    assert st["kernel_class"] == 3 and st["wg_threads"] == min(threads, 256)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_long_row_plans_run_256_thread_workgroups(dtype):
     """A plan with rows beyond the register tile runs 256-thread workgroups whatever workgroup
