@@ -314,13 +314,18 @@ typedef enum {
     /* C_b = row softmax of alpha * A_b * B_b^T (A_b m x k, B_b n x k): Section 6's score
      * product followed by Section 2's softmax of every score row (each row of C_b sums to 1
      * over its n columns), in one kernel: the scores are never stored.  k == 0 gives rows
-     * of 1/n. */
+     * of 1/n.  For 0 < k <= 64 and 64 < n <= 512 (16-byte rows and operands, alpha != 0) each
+     * product is formed once and held in registers until its row's sum is known; such plans
+     * default to 2 workgroups per CU and take rounds of 64 rows (a topology asking for 3 or
+     * more workgroups per CU keeps the two-pass form, whose rounds are 128 rows).  Otherwise
+     * each round forms its products twice (row maximum and sum, then the probabilities). */
     BSM_GEMM_NT_SOFTMAX = 2,
     BSM_GEMM_LAYOUT_MAX_ENUM = 0x7FFFFFFF
 } bsm_gemm_layout;
 
 /* Build a matrix-product plan (out_dtype is C's type; home_xcd, topology and device as for
- * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 3).  A plan
+ * bsm_plan_create; topology->wg_threads must be 0 or 256, wg_per_cu defaults to 3, or to
+ * 2 for the one-pass form of BSM_GEMM_NT_SOFTMAX).  A plan
  * made here runs only with bsm_gemm_execute.  Its stats report per_wave 0 (worker =
  * workgroup). */
 bsm_status bsm_gemm_plan_create(bsm_plan* out_plan, int64_t batch, int32_t m, int32_t n,

@@ -37,6 +37,7 @@ struct bsm_plan_s {
     // 2 = NT with the row softmax of the products.
     bool gemm = false;
     int gemm_m = 0, gemm_n = 0, gemm_k = 0, gemm_layout = 0;
+    bool gemm_single = false;  // layout 2 in one pass (products held in registers)
     int64_t gemm_batch = 0;
     int lds_floats_per_wave = 0;  // one-wave long-row staging (kernel classes 4, 5 on a device)
     int32_t flags = 0;            // BSM_FLAG_* bits
@@ -468,14 +469,18 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
     if (static_cast<double>(batch) * std::max({m, n, k}) * std::max({m, n, k}) > 1.0e18)
         return fail(BSM_ERR_INVALID_ARG, "operands too large");
     // The kernel runs workgroups of gemm_wg_threads() threads whose waves share staged operands,
-    // gemm_waves_per_simd() per CU by default; each workgroup is one worker of the table.
+    // gemm_waves_per_simd() per CU by default; each workgroup is one worker of the table.  The
+    // score softmax of k <= 64 and 64 < n <= 512 runs in one pass, two workgroups per CU (its
+    // LDS does not fit three), unless the topology asks for more.
     bsm_topology t{};
     if (topology) t = *topology;
     const int wg_threads = bsm::gemm_wg_threads();
     if (t.wg_threads != 0 && t.wg_threads != wg_threads)
         return fail(BSM_ERR_INVALID_ARG, "matrix-product plans run %d-thread workgroups (got %d)",
                     wg_threads, t.wg_threads);
-    if (t.wg_per_cu == 0) t.wg_per_cu = bsm::gemm_waves_per_simd();
+    const bool single = layout == BSM_GEMM_NT_SOFTMAX && bsm::gemm_single_pass_shape(n, k) &&
+                        (t.wg_per_cu == 0 || t.wg_per_cu <= bsm::gemm_waves_per_simd(true));
+    if (t.wg_per_cu == 0) t.wg_per_cu = bsm::gemm_waves_per_simd(single);
     const bool bf16_out = out_dtype == BSM_BF16;
     if (device >= 0) {
         DeviceGuard g;
@@ -483,7 +488,7 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
         hipDeviceProp_t prop;
         if (e == hipSuccess) e = hipGetDeviceProperties(&prop, device);
         if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
-        const int64_t per_wg = bsm::gemm_lds_bytes_per_wg(bf16_out);
+        const int64_t per_wg = bsm::gemm_lds_bytes_per_wg(bf16_out, single);
         if (per_wg > static_cast<int64_t>(prop.sharedMemPerBlock) ||
             per_wg * t.wg_per_cu > static_cast<int64_t>(prop.maxSharedMemoryPerMultiProcessor))
             return fail(BSM_ERR_INVALID_ARG, "wg_per_cu %d: %lld bytes of LDS per workgroup do not fit",
@@ -495,7 +500,7 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
     const int32_t rows[1] = {m}, cols[1] = {n};
     bsm_plan p = nullptr;
     bsm_status st = create_plan(&p, nullptr, rows, cols, m == 0 || n == 0 ? 0 : batch, out_dtype,
-                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg(), true,
+                                schedule, home_xcd, nullptr, &t, device, bsm::gemm_rows_per_wg(single), true,
                                 upload);
     if (st != BSM_OK) return st;
     p->topo.wg_threads = wg_threads;
@@ -509,6 +514,7 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
     p->gemm_n = n;
     p->gemm_k = k;
     p->gemm_layout = layout;
+    p->gemm_single = single;
     p->gemm_batch = batch;
     p->table.stats.algorithmic_bytes =
         batch * (2 * (static_cast<int64_t>(m) * k + static_cast<int64_t>(n) * k) +
@@ -544,7 +550,7 @@ bsm_status execute_gemm(bsm_plan p, const void* a, const void* b, void* c, float
     hipStream_t s = static_cast<hipStream_t>(stream);
     // k == 0 runs the same kernel: an empty reduction stores zeros
     e = bsm::launch_gemm(p->gemm_layout, p->dtype == BSM_BF16, (p->flags & BSM_FLAG_TEMPORAL) != 0,
-                         a, b, c, p->gemm_m, p->gemm_n,
+                         p->gemm_single, a, b, c, p->gemm_m, p->gemm_n,
                          p->gemm_k, alpha, p->d_worker_ptr, p->d_items, p->topo.n_wg(), trace, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     p->used = true;

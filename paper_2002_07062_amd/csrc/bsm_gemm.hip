@@ -20,7 +20,8 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &a_trace};
-    const size_t lds = static_cast<size_t>(bsm_mm::wg_lds_bytes(BF16OUT));
+    const size_t lds = static_cast<size_t>(MODE == bsm_mm::kModeNtSoftmax1 ? bsm_mm::s1_lds_bytes(BF16OUT)
+                                                                         : bsm_mm::wg_lds_bytes(BF16OUT));
     return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC, TEMPORAL, AREG>),
                            dim3(n_wg), dim3(bsm_mm::kGemmThreads), args, lds, stream);
 }
@@ -30,13 +31,21 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
 namespace bsm {
 
 int gemm_wg_threads() { return bsm_mm::kGemmThreads; }
-int gemm_lds_bytes_per_wg(bool bf16_out) { return bsm_mm::wg_lds_bytes(bf16_out); }
-int gemm_waves_per_simd() { return bsm_mm::kWavesPerSimd; }
-int gemm_rows_per_wg() { return bsm_mm::kWaves * bsm_mm::kTileM; }
+bool gemm_single_pass_shape(int n, int k) { return bsm_mm::single_pass_shape(n, k); }
+int gemm_lds_bytes_per_wg(bool bf16_out, bool single_pass) {
+    return single_pass ? bsm_mm::s1_lds_bytes(bf16_out) : bsm_mm::wg_lds_bytes(bf16_out);
+}
+int gemm_waves_per_simd(bool single_pass) {
+    return single_pass ? bsm_mm::kS1WavesPerSimd : bsm_mm::kWavesPerSimd;
+}
+int gemm_rows_per_wg(bool single_pass) {
+    return single_pass ? bsm_mm::kS1Rows : bsm_mm::kWaves * bsm_mm::kTileM;
+}
 
-hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, const void* b,
-                       void* c, int m, int n, int k, float alpha, const int32_t* d_worker_ptr,
-                       const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream) {
+hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, bool single_pass, const void* a,
+                       const void* b, void* c, int m, int n, int k, float alpha,
+                       const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg, void* trace,
+                       hipStream_t stream) {
     Shape s;
     s.m = m;
     s.n = n;
@@ -58,6 +67,16 @@ hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, 
                               : (areg ? BSM_G(M, O, true, T, true) : BSM_G(M, O, true, T, false)))
 #define BSM_G1(M, T) (bf16_out ? BSM_GV(M, true, T) : BSM_GV(M, false, T))
 #define BSM_G2(M) (temporal ? BSM_G1(M, true) : BSM_G1(M, false))
+    // the one-pass softmax takes alpha != 0 only (with alpha = 0 every logit is 0, which the
+    // two-pass form handles)
+    if (layout == bsm_mm::kModeNtSoftmax && single_pass && vec && alpha != 0.0f &&
+        bsm_mm::single_pass_shape(n, k)) {
+        if (bf16_out)
+            return temporal ? BSM_G(bsm_mm::kModeNtSoftmax1, true, true, true, false)
+                            : BSM_G(bsm_mm::kModeNtSoftmax1, true, true, false, false);
+        return temporal ? BSM_G(bsm_mm::kModeNtSoftmax1, false, true, true, false)
+                        : BSM_G(bsm_mm::kModeNtSoftmax1, false, true, false, false);
+    }
     if (layout == bsm_mm::kNN) return BSM_G2(bsm_mm::kModeNn);
     if (layout == bsm_mm::kModeNtSoftmax) return BSM_G2(bsm_mm::kModeNtSoftmax);
     return BSM_G2(bsm_mm::kModeNt);

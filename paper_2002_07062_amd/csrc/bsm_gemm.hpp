@@ -559,6 +559,10 @@ __device__ __forceinline__ void round_rows(const uint16_t* a, const uint16_t* b,
     using P0 = std::integral_constant<int, 0>;
     using P1 = std::integral_constant<int, 1>;
     using P2 = std::integral_constant<int, 2>;
+    // Step 0 writes buffer 0, which the previous round's last step read when a round has an odd
+    // number of steps (every round of a launch has the same number): then one more barrier, so
+    // that no wave still reads it.
+    if (nall & 1) __syncthreads();
     int st = 0;
     auto run = [&](auto pass, int end, bool odd_start) {
         if (!odd_start) {
@@ -600,12 +604,252 @@ __device__ __forceinline__ void zero_rows(void* c, const Shape& s, int64_t bidx,
     }
 }
 
-// Kernel modes (one compiled instance each): NT, NN and NT with the row softmax.
-enum { kModeNt = 0, kModeNn = 1, kModeNtSoftmax = 2 };
+// ----------------------------------------------------------- single-pass score softmax
+// NT + softmax for k <= 64 and 64 < n <= 512 (Section 6's score shape, d = 64 over sequences of
+// up to 512): each product is formed once and held in registers until its row is done.  The
+// two waves of a pair share 32 output rows; wave q of the pair takes the column blocks 2s + q
+// (s = 0 .. 3), so a step stages 128 rows of B (two 64-column blocks) and each wave holds at
+// most four blocks, 128 values per lane.  A row's maximum and sum are combined between the two
+// lanes of its row (half_pair) and the two waves of its pair (LDS), then the held values are
+// turned into probabilities and stored block by block.  Two waves per SIMD (the held values
+// take 128 registers); a workgroup round covers 64 rows.
+constexpr int kS1Rows = 2 * kTileM;                                // rows per workgroup round
+constexpr int kS1BlockN = 2 * kBlockN;                             // B rows staged per step
+constexpr int kS1MaxSteps = 4;                                     // n <= 4 * 128
+constexpr int kS1BBufElems = kS1BlockN * kLdk;
+constexpr int kS1BPieces = kS1BlockN * kChunkK / 8 / 64 / kWaves;  // 16-byte pieces per lane
+constexpr int kS1WavesPerSimd = 2;
+constexpr int s1_lds_bytes(bool bf16_out) {
+    return kWaves * wave_lds_bytes(bf16_out) + kDepth * kS1BBufElems * 2 + 2 * kWaves * kTileM * 4;
+}
+constexpr bool single_pass_shape(int n, int k) {
+    return k > 0 && k <= kChunkK && n > kBlockN && n <= kS1MaxSteps * kS1BlockN;
+}
+
+struct S1Pieces {
+    u16x8 b[kS1BPieces];
+};
+
+// The wave's quarter of B's rows [j0, j0 + 128) (the whole reduction, k <= 64), and its LDS
+// write (rows past n and columns past k zeroed).
+__device__ __forceinline__ void s1_load(const uint16_t* b_blk, const Shape& s, int j0, int wave,
+                                        int lane, S1Pieces& p) {
+#pragma unroll
+    for (int q = 0; q < kS1BPieces; ++q) {
+        const int qg = kS1BPieces * wave + q;
+        const int j = j0 + piece_row(lane, qg);
+        p.b[q] = load8<true>(b_blk + static_cast<int64_t>(j < s.n ? j : s.n - 1) * s.k,
+                             piece_col(lane, qg), s.k);
+    }
+}
+
+__device__ __forceinline__ void s1_write(const S1Pieces& p, const Shape& s, int j0, int wave,
+                                         int lane, uint16_t* lb) {
+#pragma unroll
+    for (int q = 0; q < kS1BPieces; ++q) {
+        const int qg = kS1BPieces * wave + q;
+        const int r = piece_row(lane, qg), c = piece_col(lane, qg);
+        *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8<true>(p.b[q], c, s.k, j0 + r < s.n);
+    }
+}
+
+// Stages one output block (two 32 x 32 tiles, times `scale`) in the wave's LDS region and
+// stores it as whole rows.
+template <bool BF16OUT, bool TEMPORAL>
+__device__ __forceinline__ void s1_store_block(const f32x16 (&v)[kBlockTiles], float scale, void* c,
+                                               const Shape& s, int64_t bidx, int i0, int rows,
+                                               int j0, int jn, int lane, uint16_t* lw) {
+    const int li = lane & 31, h = lane >> 5;
+    if constexpr (BF16OUT) {
+#pragma unroll
+        for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<u32x2*>(lw + li * kLdh + t * kTileN + 8 * g + 4 * h) =
+                    u32x2{pack_bf16(scale * v[t][4 * g], scale * v[t][4 * g + 1]),
+                          pack_bf16(scale * v[t][4 * g + 2], scale * v[t][4 * g + 3])};
+        wave_lds_sync();
+        store_block_bf16<true, TEMPORAL>(static_cast<uint16_t*>(c), s, bidx, i0, rows, j0, jn, lane, lw);
+    } else {
+        float* const lc = reinterpret_cast<float*>(lw);
+#pragma unroll
+        for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<f32x4*>(lc + li * kLdc + t * kTileN + 8 * g + 4 * h) =
+                    f32x4{scale * v[t][4 * g], scale * v[t][4 * g + 1], scale * v[t][4 * g + 2],
+                          scale * v[t][4 * g + 3]};
+        wave_lds_sync();
+        store_block_f32<true, TEMPORAL>(static_cast<float*>(c), s, bidx, i0, rows, j0, jn, lane, lc);
+    }
+    wave_lds_sync();  // the next block rewrites the region
+}
+
+// One round of a wave: output rows [i0, i0 + rows) of batch bidx (rows <= 32; 0 for a wave
+// past the round's end, which still loads its part of B and meets every barrier).  lstat:
+// [2][kWaves][32] floats, the waves' row maxima and sums for their partners.
+template <bool BF16OUT, bool TEMPORAL>
+__device__ __forceinline__ void round_rows_s1(const uint16_t* a, const uint16_t* b, void* c,
+                                              const Shape& s, int64_t bidx, int i0, int rows,
+                                              int wave, int lane, uint16_t* lw, uint16_t* lbs,
+                                              float* lstat) {
+    const int li = lane & 31;
+    const int h = lane >> 5;
+    const int q = wave & 1;
+    const uint16_t* a_blk = rows > 0 ? a + bidx * s.a_batch + static_cast<int64_t>(i0) * s.k : a;
+    const uint16_t* b_blk = b + bidx * s.b_batch;
+    const int nj = (s.n + kBlockN - 1) / kBlockN;  // 2 .. 8
+    const int ns = (nj + 1) / 2;                   // steps: 1 .. 4
+    // A's rows and B's first two steps.  Both waves of a pair read the same A rows: ordinary
+    // loads, so that the second finds them in cache.
+    u16x8 pa[kAPieces];
+    load_a<true>(a_blk, s, rows, 0, lane, false, pa);
+    S1Pieces p[kDepth];
+    s1_load(b_blk, s, 0, wave, lane, p[0]);
+    s1_load(b_blk, s, (ns > 1 ? 1 : 0) * kS1BlockN, wave, lane, p[1]);
+    // A once, through the wave's LDS into its MFMA layout
+    u16x8 a_reg[kChunkK / kTileK];
+    write_a<true>(pa, s, rows, 0, lane, lw);
+    wave_lds_sync();
+#pragma unroll
+    for (int kq = 0; kq < kChunkK / kTileK; ++kq)
+        a_reg[kq] = *reinterpret_cast<const u16x8*>(lw + li * kLdk + kq * kTileK + 8 * h);
+    wave_lds_sync();
+    f32x16 held[kS1MaxSteps][kBlockTiles];
+#pragma unroll
+    for (int st = 0; st < kS1MaxSteps; ++st) {
+        if (st >= ns) break;  // wave-uniform
+        uint16_t* const lb = lbs + (st & 1) * kS1BBufElems;
+        // Buffer st % 2 was last read at step st - 2, which every wave finished before the
+        // barrier of step st - 1.  Step 0 writes buffer 0, which the previous round's last
+        // step read when that round had an odd number of steps: then one more barrier.
+        if (st == 0 && (ns & 1)) __syncthreads();
+        s1_write(p[st & 1], s, st * kS1BlockN, wave, lane, lb);
+        __syncthreads();
+        // step st + 2's operands (none past the last step: the registers then take the next
+        // round's first loads)
+        if (st + 2 < ns) s1_load(b_blk, s, (st + 2) * kS1BlockN, wave, lane, p[st & 1]);
+#pragma unroll
+        for (int kk = 0; kk < kChunkK; kk += kTileK) {
+            const bf16x8 av = __builtin_bit_cast(bf16x8, a_reg[kk / kTileK]);
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
+                const bf16x8 bv = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u16x8*>(lb + (q * kBlockN + t * kTileN + li) * kLdk + kk + 8 * h));
+                held[st][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, kk == 0 ? f32x16{} : held[st][t], 0, 0, 0);
+            }
+        }
+    }
+    // Tile t of step st, lane (li, h): row li, columns 64 (2 st + q) + 32 t + 8 g + 4 h + 0..3
+    // (value 4 g + e).  Blocks past n (st >= ns, or wave 1 of a pair past an odd block count)
+    // take no part.
+    auto block_cols = [&](int st) {
+        const int j0 = (2 * st + q) * kBlockN;
+        return st < ns && j0 < s.n ? (s.n - j0 < kBlockN ? s.n - j0 : kBlockN) : 0;
+    };
+    auto col_ok = [&](int jn, int t, int i) { return t * kTileN + 8 * (i / 4) + 4 * h + (i % 4) < jn; };
+    // Logits in base-2 units, y = c2 * product (alpha != 0: the host sends alpha = 0 to the
+    // two-pass form).  Columns past n inside a partial block get a product whose y is -inf,
+    // once, so that the maximum, the exponentials and the sums below take every held value as
+    // it is.
+    const float c2 = s.alpha * kLog2eF;
+    const float none = c2 > 0.0f ? kNegInfF : -kNegInfF;
+#pragma unroll
+    for (int st = 0; st < kS1MaxSteps; ++st) {
+        const int jn = block_cols(st);
+        if (jn > 0 && jn < kBlockN) {
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) held[st][t][i] = col_ok(jn, t, i) ? held[st][t][i] : none;
+        }
+    }
+    // the row's largest y: c2 times its largest (c2 < 0: smallest) product, pairwise (16 -> 1
+    // per tile, then the tiles) rather than one chain of 128
+    auto extreme = [&](auto pick, float none) {
+        float part[kS1MaxSteps * kBlockTiles];
+#pragma unroll
+        for (int st = 0; st < kS1MaxSteps; ++st) {
+#pragma unroll
+            for (int t = 0; t < kBlockTiles; ++t) {
+                part[st * kBlockTiles + t] = none;
+                if (block_cols(st) > 0) {
+                    float f[16];
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) f[i] = held[st][t][i];
+#pragma unroll
+                    for (int w = 8; w >= 1; w /= 2)
+#pragma unroll
+                        for (int i = 0; i < w; ++i) f[i] = pick(f[2 * i], f[2 * i + 1]);
+                    part[st * kBlockTiles + t] = f[0];
+                }
+            }
+        }
+#pragma unroll
+        for (int w = kS1MaxSteps * kBlockTiles / 2; w >= 1; w /= 2)
+#pragma unroll
+            for (int i = 0; i < w; ++i) part[i] = pick(part[2 * i], part[2 * i + 1]);
+        return part[0];
+    };
+    float bm = c2 > 0.0f
+                   ? extreme([](float u, float v) { return __builtin_elementwise_maximum(u, v); }, kNegInfF)
+                   : extreme([](float u, float v) { return __builtin_elementwise_minimum(u, v); }, -kNegInfF);
+    bm = c2 * bm;
+    bm = half_pair(bm, lane, [](float u, float v) { return __builtin_elementwise_maximum(u, v); });
+    float* const lmax = lstat;
+    float* const lsum = lstat + kWaves * kTileM;
+    if (h == 0) lmax[wave * kTileM + li] = bm;
+    __syncthreads();
+    const float mx = __builtin_elementwise_maximum(bm, lmax[(wave ^ 1) * kTileM + li]);
+    const float ms = mx == kNegInfF ? 0.0f : mx;
+    // 2^(y - M) in place (0 past n), and the lane's sum: 16 -> 1 per tile, then the tiles
+    float part[kS1MaxSteps * kBlockTiles];
+#pragma unroll
+    for (int st = 0; st < kS1MaxSteps; ++st) {
+#pragma unroll
+        for (int t = 0; t < kBlockTiles; ++t) {
+            part[st * kBlockTiles + t] = 0.0f;
+            if (block_cols(st) > 0) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    held[st][t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(held[st][t][i], c2, -ms));
+                float f[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) f[i] = held[st][t][i];
+#pragma unroll
+                for (int w = 8; w >= 1; w /= 2)
+#pragma unroll
+                    for (int i = 0; i < w; ++i) f[i] = f[2 * i] + f[2 * i + 1];
+                part[st * kBlockTiles + t] = f[0];
+            }
+        }
+    }
+#pragma unroll
+    for (int w = kS1MaxSteps * kBlockTiles / 2; w >= 1; w /= 2)
+#pragma unroll
+        for (int i = 0; i < w; ++i) part[i] = part[2 * i] + part[2 * i + 1];
+    const float bs = half_pair(part[0], lane, [](float u, float v) { return u + v; });
+    if (h == 0) lsum[wave * kTileM + li] = bs;
+    __syncthreads();
+    const float tot = bs + lsum[(wave ^ 1) * kTileM + li];
+    const float inv = tot == 0.0f ? 0.0f : __builtin_amdgcn_rcpf(tot);
+    if (rows == 0) return;  // wave-uniform; every barrier of the round is behind
+#pragma unroll
+    for (int st = 0; st < kS1MaxSteps; ++st) {
+        const int jn = block_cols(st);
+        if (jn > 0)
+            s1_store_block<BF16OUT, TEMPORAL>(held[st], inv, c, s, bidx, i0, rows, (2 * st + q) * kBlockN,
+                                              jn, lane, lw);
+    }
+}
+
+// Kernel modes (one compiled instance each): NT, NN, NT with the row softmax in two passes,
+// and in one pass (single_pass_shape).
+enum { kModeNt = 0, kModeNn = 1, kModeNtSoftmax = 2, kModeNtSoftmax1 = 3 };
 constexpr int kWavesPerSimd = 3;
 
 // Worker loop: workgroup w runs its items; an item's rows are taken up to 128 at a time (cut
-// where a batch ends), 32 per wave.  Every bound of these loops is the same for the four
+// where a batch ends), 32 per wave (single-pass softmax: 64 at a time, 32 per wave pair).  Every bound of these loops is the same for the four
 // waves, so they meet the same barriers.
 template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
 __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b, void* c,
@@ -614,12 +858,17 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                                             bsm_trace_rec* __restrict__ trace, uint16_t* lds_base) {
     constexpr int kLayout = MODE == kModeNn ? kNN : kNT;
     constexpr bool kSoftmax = MODE == kModeNtSoftmax;
+    constexpr bool kS1 = MODE == kModeNtSoftmax1;
+    static_assert(!kS1 || (VEC && !AREG), "the single-pass form is one 16-byte instance");
+    constexpr int kRoundRows = kS1 ? kS1Rows : kWaves * kTileM;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int lane = static_cast<int>(threadIdx.x) & 63;
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
     uint16_t* const lw = lds_base + wave * (wave_lds_bytes(BF16OUT) / 2);
     uint16_t* const lbs = lds_base + kWaves * (wave_lds_bytes(BF16OUT) / 2);
+    float* const lstat = reinterpret_cast<float*>(lbs + kDepth * kS1BBufElems);  // kS1 only
+    const int row0 = kS1 ? (wave >> 1) * kTileM : wave * kTileM;  // the wave's first row of a round
     uint32_t done = 0;
     const int i_begin = worker_ptr[w];
     const int i_end = worker_ptr[w + 1];
@@ -639,14 +888,19 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 const int64_t bidx = g / s.m;
                 const int i = static_cast<int>(g - bidx * s.m);
                 int seg = s.m - i < left ? s.m - i : left;
-                if (seg > kWaves * kTileM) seg = kWaves * kTileM;
-                int mine = seg - wave * kTileM;
+                if (seg > kRoundRows) seg = kRoundRows;
+                int mine = seg - row0;
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
-                if (s.k == 0)
-                    zero_rows<BF16OUT, kSoftmax>(c, s, bidx, i + wave * kTileM, mine, lane);
-                else
-                    round_rows<kLayout, BF16OUT, VEC, AREG, TEMPORAL, kSoftmax>(a, b, c, s, bidx, i + wave * kTileM, mine,
-                                                            wave, lane, lw, lbs, wg_done, seg, total_rows);
+                if constexpr (kS1) {  // k > 0 and alpha != 0 (the host picks this form only then)
+                    round_rows_s1<BF16OUT, TEMPORAL>(a, b, c, s, bidx, i + row0, mine, wave, lane, lw,
+                                                     lbs, lstat);
+                } else {
+                    if (s.k == 0)
+                        zero_rows<BF16OUT, kSoftmax>(c, s, bidx, i + row0, mine, lane);
+                    else
+                        round_rows<kLayout, BF16OUT, VEC, AREG, TEMPORAL, kSoftmax>(
+                            a, b, c, s, bidx, i + row0, mine, wave, lane, lw, lbs, wg_done, seg, total_rows);
+                }
                 wg_done += seg;
                 done += static_cast<uint32_t>(mine);
                 g += seg;
@@ -671,14 +925,14 @@ extern __shared__ uint16_t bsm_gemm_lds[];  // wg_lds_bytes() per workgroup
 constexpr int kGemmThreads = 64 * kWaves;
 
 // The element-wise (unaligned / odd-size) form is compiled for two waves per SIMD: its
-// registers do not fit three.
+// registers do not fit three; so is the single-pass softmax, whose held products take 128.
 // TEMPORAL: ordinary stores of C and loads of A (a consumer finds C in the Infinity Cache)
 // instead of nontemporal ones; a compile-time choice, so the default instance carries no
 // branch for it.  AREG (A's operands held in registers, k <= 64 < n, 16-byte form only): a
 // separate instance too, so that neither form's registers are allocated for the other's.
 constexpr bool use_areg(bool vec, int n, int k) { return vec && k <= kChunkK && n > kBlockN; }
 template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
-__global__ void __launch_bounds__(kGemmThreads, VEC ? kWavesPerSimd : 2)
+__global__ void __launch_bounds__(kGemmThreads, (MODE == kModeNtSoftmax1 || !VEC) ? kS1WavesPerSimd : kWavesPerSimd)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 bsm_trace_rec* __restrict__ trace) {

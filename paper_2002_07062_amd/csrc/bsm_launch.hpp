@@ -44,17 +44,22 @@ hipError_t launch_softmax_backward(bsm_dtype dtype, int kernel_class, bool shift
 // after batch): layout 0 (NT) C_b = alpha A_b B_b^T, layout 1 (NN) C_b = alpha A_b B_b; bf16
 // A and B, fp32 or bf16 C.
 // Matrix-product launches: threads per workgroup, LDS bytes per workgroup, the waves per SIMD
-// the kernel is compiled for, and the output rows a workgroup takes per round.
+// the kernel is compiled for, and the output rows a workgroup takes per round; single_pass:
+// the one-pass score softmax (layout 2, shapes for which gemm_single_pass_shape holds).
 int gemm_wg_threads();
-int gemm_lds_bytes_per_wg(bool bf16_out);
-int gemm_waves_per_simd();
-int gemm_rows_per_wg();
+bool gemm_single_pass_shape(int n, int k);
+int gemm_lds_bytes_per_wg(bool bf16_out, bool single_pass);
+int gemm_waves_per_simd(bool single_pass);
+int gemm_rows_per_wg(bool single_pass);
 
 // Worker w of the table is workgroup w (gemm_wg_threads() threads, gemm_rows_per_wg() rows
 // per round).  temporal: ordinary instead of nontemporal stores of C and loads of A.
-hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, const void* a, const void* b,
-                       void* c, int m, int n, int k, float alpha, const int32_t* d_worker_ptr,
-                       const bsm_item* d_items, int n_wg, void* trace, hipStream_t stream);
+// single_pass (layout 2): the one-pass form where the shape and 16-byte operands allow it,
+// else the two-pass form.
+hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, bool single_pass, const void* a,
+                       const void* b, void* c, int m, int n, int k, float alpha,
+                       const int32_t* d_worker_ptr, const bsm_item* d_items, int n_wg, void* trace,
+                       hipStream_t stream);
 
 // Largest static LDS (bytes per workgroup) of a plan's instances, forward and backward.
 hipError_t static_lds_bytes(bsm_dtype dtype, int kernel_class, bool shifted, int* bytes);

@@ -175,3 +175,35 @@ def test_scores_softmax_one_shot():
     bsm.bsm_gemm(_dev_bf16(a), _dev_bf16(b), c, batch, m, n, k, "nt_softmax", alpha=0.125)
     torch.cuda.synchronize()
     _check(to_host_bits(c), a, b, batch, m, n, k, 0.125, "bf16")
+
+
+@pytest.mark.parametrize("out", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", [(2, 200, 72, 64), (3, 131, 264, 16), (2, 96, 512, 40),
+                                   (1, 65, 392, 8), (2, 64, 128, 64)],
+                         ids=["n72", "n264", "n512k40", "n392k8", "n128"])
+def test_scores_softmax_one_pass_form(shape, out):
+    """Shapes of the one-pass form (k <= 64, 64 < n <= 512, 16-byte rows): an odd number of
+    128-column steps (72, 264, 392: the pair's second wave has no block in the last step, and
+    the next round waits for the last step's buffer), partial blocks, ragged row rounds. The
+    two-pass form (forced by three workgroups per CU) gives results within the same bound."""
+    batch, m, n, k = shape
+    print(f"[nt_softmax one-pass {shape} {out}]", flush=True)
+    a, b = _operands(batch, m, n, k, seed=70 + n)
+    a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+    alpha = 1.0 / np.sqrt(k)
+    first = None
+    for schedule in SCHEDULES:
+        got = _run(batch, m, n, k, out, schedule, a_d, b_d, alpha)
+        if first is None:
+            first = got
+            _check(got, a, b, batch, m, n, k, alpha, out)
+        else:
+            assert np.array_equal(got, first), f"{schedule} differs from rr"
+    tdt = torch.float32 if out == "f32" else torch.bfloat16
+    c = torch.full((batch * m * n,), float("nan"), dtype=tdt, device="cuda")
+    p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt_softmax", out, "balanced",
+                                 topology={"wg_per_cu": 3}, device=0)
+    bsm.bsm_gemm_execute(p, a_d, b_d, c, alpha)
+    torch.cuda.synchronize()
+    p.destroy()
+    _check(to_host_bits(c), a, b, batch, m, n, k, alpha, out)
