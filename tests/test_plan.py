@@ -403,6 +403,31 @@ def test_gemm_plans_cover_every_output_row_in_128_row_blocks(schedule, shape):
         assert np.all(np.asarray(rows) == 384)
 
 
+@pytest.mark.parametrize("layout,n,k,wg_per_cu,one_pass", [
+    ("nt_softmax", 512, 64, 0, True), ("nt_softmax", 72, 8, 0, True), ("nt_softmax", 520, 64, 0, False),
+    ("nt_softmax", 64, 64, 0, False), ("nt_softmax", 512, 72, 0, False), ("nt_softmax", 512, 0, 0, False),
+    ("nt_softmax", 512, 64, 3, False), ("nt_softmax", 512, 64, 1, True), ("nt", 512, 64, 0, False)])
+def test_score_softmax_plans_pick_the_one_pass_form(layout, n, k, wg_per_cu, one_pass):
+    """The score product with the row softmax runs in one pass for 0 < k <= 64 and
+    64 < n <= 512 unless the topology asks for three or more workgroups per CU: such plans
+    default to two workgroups per CU and cut BALANCED pieces at 64-row blocks (the rows a
+    workgroup takes per round); the others default to three per CU and 128-row blocks."""
+    batch, m = 6, 512
+    topo = dict(n_cu=256, n_xcd=8, wg_per_cu=wg_per_cu, wg_threads=256)
+    p = bsm.bsm_gemm_plan_create(batch, m, n, k, layout, "bf16", "balanced", topology=topo, device=-1)
+    d = bsm.bsm_plan_describe(p)
+    ptr, items, _, _ = bsm.bsm_plan_export(p)
+    p.destroy()
+    assert d["n_wg"] == 256 * (wg_per_cu or (2 if one_pass else 3))
+    if n == 0:
+        return
+    unit = 64 if one_pass else 128
+    g0 = items["elem_offset"] // n
+    assert np.all(g0 % unit == 0)
+    assert np.all((items["nrows"] % unit == 0) | (g0 + items["nrows"] == batch * m))
+    assert np.any(items["nrows"] % 128 != 0) == one_pass
+
+
 def test_gemm_plan_rejects_bad_arguments():
     for args in [(-1, 4, 4, 4, 0), (1, -4, 4, 4, 0), (1, 4, 4, 4, 3)]:
         with pytest.raises(bsm.BsmError) as e:
