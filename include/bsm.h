@@ -176,7 +176,8 @@ typedef struct bsm_trace_rec {
     uint32_t wg;      /* workgroup index in the grid */
     uint32_t xcc_id;  /* XCD the wave ran on, from the hardware XCC_ID register */
     uint32_t hw_id;   /* raw hardware HW_ID register (wave, SIMD, CU, shader engine) */
-    uint32_t rows;    /* rows this wave processed */
+    uint32_t rows;    /* rows this wave processed (the one-pass score softmax of
+                       * BSM_GEMM_NT_SOFTMAX: two waves share each row, the first counts it) */
     uint64_t t_start; /* constant-rate (100 MHz) real-time counter when the wave started */
     uint64_t t_end;   /* ... when it finished its last row */
 } bsm_trace_rec;

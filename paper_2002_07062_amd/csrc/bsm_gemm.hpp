@@ -902,7 +902,8 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                             a, b, c, s, bidx, i + row0, mine, wave, lane, lw, lbs, wg_done, seg, total_rows);
                 }
                 wg_done += seg;
-                done += static_cast<uint32_t>(mine);
+                // one-pass softmax: the two waves of a pair share rows; the first counts them
+                if (!kS1 || (wave & 1) == 0) done += static_cast<uint32_t>(mine);
                 g += seg;
                 left -= seg;
             }

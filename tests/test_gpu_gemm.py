@@ -116,15 +116,18 @@ def test_one_shot_equals_plan_and_rejects_overlap():
     assert e.value.status == bsm.BSM_ERR_ALIAS
 
 
-def test_trace_counts_every_output_row():
+@pytest.mark.parametrize("layout", ["nt", "nt_softmax"])
+def test_trace_counts_every_output_row(layout):
+    """The trace's row counts add up to the output rows (the one-pass score softmax, whose
+    wave pairs share rows, counts each row once)."""
     batch, m, n, k = 96, 512, 512, 64
     a, b = _operands(batch, m, n, k, seed=74)
     a_d, b_d = _dev_bf16(a), _dev_bf16(b)
     c = torch.empty(batch * m * n, device="cuda")
-    p = bsm.bsm_gemm_plan_create(batch, m, n, k, "nt", "f32", "balanced", device=0)
+    p = bsm.bsm_gemm_plan_create(batch, m, n, k, layout, "f32", "balanced", device=0)
     st = bsm.bsm_plan_describe(p)
     trace = torch.zeros(st["trace_bytes"], dtype=torch.uint8, device="cuda")
-    bsm.bsm_gemm_execute(p, a_d, b_d, c, trace=trace)
+    bsm.bsm_gemm_execute(p, a_d, b_d, c, 0.125, trace=trace)
     torch.cuda.synchronize()
     p.destroy()
     rec = trace.cpu().numpy().view(bsm.TRACE_DTYPE)
