@@ -754,8 +754,8 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not "
-              "supported: the batched softmax needs no exchange between GPUs and this build "
-              "runs on a single MI355X", file=sys.stderr)
+              "supported: the batched softmax needs no exchange between GPUs, and the library "
+              "runs on one MI355X at a time", file=sys.stderr)
         return 2
 
     import torch

@@ -54,7 +54,7 @@ extern "C" {
 typedef enum bsm_status {
     BSM_OK = 0,
     BSM_ERR_INVALID_ARG = 1, /* bad pointer, size, enum, geometry or overlapping slices */
-    BSM_ERR_UNSUPPORTED = 2, /* valid request this build cannot serve (e.g. host-only plan) */
+    BSM_ERR_UNSUPPORTED = 2, /* valid request the library cannot serve (e.g. host-only plan) */
     BSM_ERR_ALIAS = 3,       /* in and out overlap without being equal */
     BSM_ERR_OOM = 4,         /* host or device allocation failed */
     BSM_ERR_HIP = 5,         /* a HIP runtime call failed; bsm_last_error() has its string */
