@@ -207,3 +207,23 @@ def test_scores_softmax_one_pass_form(shape, out):
     torch.cuda.synchronize()
     p.destroy()
     _check(to_host_bits(c), a, b, batch, m, n, k, alpha, out)
+
+
+def test_scores_softmax_one_pass_random_shapes():
+    """Seeded random shapes of the one-pass form (64 < n <= 512 in steps of 8, k a multiple of
+    8 up to 64, ragged m, alpha of either sign, both output types) against the oracle, and
+    RR against BALANCED bit for bit."""
+    rng = np.random.default_rng(2002)
+    for case in range(10):
+        batch = int(rng.integers(1, 4))
+        m = int(rng.integers(1, 230))
+        n = 8 * int(rng.integers(9, 65))
+        k = 8 * int(rng.integers(1, 9))
+        alpha = float(rng.choice([-1.0, 1.0]) * rng.uniform(0.05, 0.5))
+        out = "bf16" if case % 2 == 0 else "f32"
+        print(f"[nt_softmax one-pass random {case}: {batch} {m} {n} {k} {alpha:.3f} {out}]", flush=True)
+        a, b = _operands(batch, m, n, k, seed=3000 + case)
+        a_d, b_d = _dev_bf16(a), _dev_bf16(b)
+        got = _run(batch, m, n, k, out, "balanced", a_d, b_d, alpha)
+        _check(got, a, b, batch, m, n, k, alpha, out)
+        assert np.array_equal(_run(batch, m, n, k, out, "rr", a_d, b_d, alpha), got)
