@@ -721,9 +721,8 @@ __device__ __forceinline__ void round_rows_s1(const uint16_t* a, const uint16_t*
         if (st >= ns) break;  // wave-uniform
         uint16_t* const lb = lbs + (st & 1) * kS1BBufElems;
         // Buffer st % 2 was last read at step st - 2, which every wave finished before the
-        // barrier of step st - 1.  Step 0 writes buffer 0, which the previous round's last
-        // step read when that round had an odd number of steps: then one more barrier.
-        if (st == 0 && (ns & 1)) __syncthreads();
+        // barrier of step st - 1; the previous round's last reads came before its
+        // row-statistics barriers.
         s1_write(p[st & 1], s, st * kS1BlockN, wave, lane, lb);
         __syncthreads();
         // step st + 2's operands (none past the last step: the registers then take the next
