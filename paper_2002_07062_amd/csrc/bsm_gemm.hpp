@@ -925,14 +925,18 @@ extern __shared__ uint16_t bsm_gemm_lds[];  // wg_lds_bytes() per workgroup
 constexpr int kGemmThreads = 64 * kWaves;
 
 // The element-wise (unaligned / odd-size) form is compiled for two waves per SIMD: its
-// registers do not fit three; so is the single-pass softmax, whose held products take 128.
+// registers do not fit three; so is the single-pass softmax, whose held products take 128, and
+// the two-pass softmax with A staged through LDS (k > 64): capped at three waves it spilled 149
+// registers and took 157 us at 192 x 512 x 512 x 128, against 83 us at two.
 // TEMPORAL: ordinary stores of C and loads of A (a consumer finds C in the Infinity Cache)
 // instead of nontemporal ones; a compile-time choice, so the default instance carries no
 // branch for it.  AREG (A's operands held in registers, k <= 64 < n, 16-byte form only): a
 // separate instance too, so that neither form's registers are allocated for the other's.
 constexpr bool use_areg(bool vec, int n, int k) { return vec && k <= kChunkK && n > kBlockN; }
 template <int MODE, bool BF16OUT, bool VEC, bool TEMPORAL, bool AREG>
-__global__ void __launch_bounds__(kGemmThreads, (MODE == kModeNtSoftmax1 || !VEC) ? kS1WavesPerSimd : kWavesPerSimd)
+__global__ void __launch_bounds__(kGemmThreads,
+                                  (MODE == kModeNtSoftmax1 || !VEC || (MODE == kModeNtSoftmax && !AREG))
+                                      ? kS1WavesPerSimd : kWavesPerSimd)
 bsm_gemm_kernel(const uint16_t* a, const uint16_t* b, void* c, Shape s,
                 const int32_t* __restrict__ worker_ptr, const bsm_item* __restrict__ items,
                 bsm_trace_rec* __restrict__ trace) {
