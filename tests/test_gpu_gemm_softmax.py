@@ -179,13 +179,16 @@ def test_scores_softmax_one_shot():
 
 @pytest.mark.parametrize("out", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", [(2, 200, 72, 64), (3, 131, 264, 16), (2, 96, 512, 40),
-                                   (1, 65, 392, 8), (2, 64, 128, 64)],
-                         ids=["n72", "n264", "n512k40", "n392k8", "n128"])
+                                   (1, 65, 392, 8), (2, 64, 128, 64), (1, 1, 72, 8), (5, 1, 512, 64),
+                                   (3, 33, 136, 24)],
+                         ids=["n72", "n264", "n512k40", "n392k8", "n128", "one_row", "rows_of_one",
+                              "m33"])
 def test_scores_softmax_one_pass_form(shape, out):
     """Shapes of the one-pass form (k <= 64, 64 < n <= 512, 16-byte rows): an odd number of
-    128-column steps (72, 264, 392: the pair's second wave has no block in the last step, and
-    the next round waits for the last step's buffer), partial blocks, ragged row rounds. The
-    two-pass form (forced by three workgroups per CU) gives results within the same bound."""
+    128-column steps (72, 264, 392: the pair's second wave has no block in the last step),
+    partial blocks, ragged row rounds, batches of a single row (the second wave pair of every
+    workgroup has no rows and still meets every barrier). The two-pass form (forced by three
+    workgroups per CU) gives results within the same bound."""
     batch, m, n, k = shape
     print(f"[nt_softmax one-pass {shape} {out}]", flush=True)
     a, b = _operands(batch, m, n, k, seed=70 + n)
