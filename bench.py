@@ -208,7 +208,7 @@ GEMM_SHAPES = {  # Section 6's two batch products of BERT attention (batch, m, n
     "context_384x512x64x512": (384, 512, 64, 512, "nn"),
     # the score product with the row softmax in the same kernel (P = softmax(Q K^T / 8))
     "scores_softmax_384x512x512x64": (384, 512, 512, 64, "nt_softmax"),
-    # the same with a head dimension of 128 (the two-pass form: products formed twice)
+    # the same with a head dimension of 128 (one pass, A kept in LDS, two 64-deep chunks per step)
     "scores_softmax_192x512x512x128": (192, 512, 512, 128, "nt_softmax"),
 }
 

@@ -315,7 +315,7 @@ typedef enum {
     /* C_b = row softmax of alpha * A_b * B_b^T (A_b m x k, B_b n x k): Section 6's score
      * product followed by Section 2's softmax of every score row (each row of C_b sums to 1
      * over its n columns), in one kernel: the scores are never stored.  k == 0 gives rows
-     * of 1/n.  For 0 < k <= 64 and 64 < n <= 512 (16-byte rows and operands, alpha != 0) each
+     * of 1/n.  For 0 < k <= 128 and 64 < n <= 512 (16-byte rows and operands, alpha != 0) each
      * product is formed once and held in registers until its row's sum is known; such plans
      * default to 2 workgroups per CU and take rounds of 64 rows (a topology asking for 3 or
      * more workgroups per CU keeps the two-pass form, whose rounds are 128 rows).  Otherwise

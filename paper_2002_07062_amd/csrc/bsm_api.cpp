@@ -470,7 +470,7 @@ bsm_status create_gemm_plan(bsm_plan* out_plan, int64_t batch, int32_t m, int32_
         return fail(BSM_ERR_INVALID_ARG, "operands too large");
     // The kernel runs workgroups of gemm_wg_threads() threads whose waves share staged operands,
     // gemm_waves_per_simd() per CU by default; each workgroup is one worker of the table.  The
-    // score softmax of k <= 64 and 64 < n <= 512 runs in one pass, two workgroups per CU (its
+    // score softmax of k <= 128 and 64 < n <= 512 runs in one pass, two workgroups per CU (its
     // LDS does not fit three), unless the topology asks for more.
     bsm_topology t{};
     if (topology) t = *topology;

@@ -20,7 +20,7 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &a_trace};
-    const size_t lds = static_cast<size_t>(MODE == bsm_mm::kModeNtSoftmax1 ? bsm_mm::s1_lds_bytes(BF16OUT)
+    const size_t lds = static_cast<size_t>(MODE == bsm_mm::kModeNtSoftmax1 ? bsm_mm::s1_lds_bytes(BF16OUT, AREG)
                                                                          : bsm_mm::wg_lds_bytes(BF16OUT));
     return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC, TEMPORAL, AREG>),
                            dim3(n_wg), dim3(bsm_mm::kGemmThreads), args, lds, stream);
@@ -33,7 +33,7 @@ namespace bsm {
 int gemm_wg_threads() { return bsm_mm::kGemmThreads; }
 bool gemm_single_pass_shape(int n, int k) { return bsm_mm::single_pass_shape(n, k); }
 int gemm_lds_bytes_per_wg(bool bf16_out, bool single_pass) {
-    return single_pass ? bsm_mm::s1_lds_bytes(bf16_out) : bsm_mm::wg_lds_bytes(bf16_out);
+    return single_pass ? bsm_mm::s1_lds_bytes(bf16_out, true) : bsm_mm::wg_lds_bytes(bf16_out);
 }
 int gemm_waves_per_simd(bool single_pass) {
     return single_pass ? bsm_mm::kS1WavesPerSimd : bsm_mm::kWavesPerSimd;
@@ -71,11 +71,12 @@ hipError_t launch_gemm(int layout, bool bf16_out, bool temporal, bool single_pas
     // two-pass form handles)
     if (layout == bsm_mm::kModeNtSoftmax && single_pass && vec && alpha != 0.0f &&
         bsm_mm::single_pass_shape(n, k)) {
-        if (bf16_out)
-            return temporal ? BSM_G(bsm_mm::kModeNtSoftmax1, true, true, true, false)
-                            : BSM_G(bsm_mm::kModeNtSoftmax1, true, true, false, false);
-        return temporal ? BSM_G(bsm_mm::kModeNtSoftmax1, false, true, true, false)
-                        : BSM_G(bsm_mm::kModeNtSoftmax1, false, true, false, false);
+        // the last flag of the single-pass instance: 64 < k <= 128 (A kept in LDS)
+#define BSM_G1P(O, T) (k > bsm_mm::kChunkK ? BSM_G(bsm_mm::kModeNtSoftmax1, O, true, T, true) \
+                                           : BSM_G(bsm_mm::kModeNtSoftmax1, O, true, T, false))
+        if (bf16_out) return temporal ? BSM_G1P(true, true) : BSM_G1P(true, false);
+        return temporal ? BSM_G1P(false, true) : BSM_G1P(false, false);
+#undef BSM_G1P
     }
     if (layout == bsm_mm::kNN) return BSM_G2(bsm_mm::kModeNn);
     if (layout == bsm_mm::kModeNtSoftmax) return BSM_G2(bsm_mm::kModeNtSoftmax);

@@ -605,7 +605,7 @@ __device__ __forceinline__ void zero_rows(void* c, const Shape& s, int64_t bidx,
 }
 
 // ----------------------------------------------------------- single-pass score softmax
-// NT + softmax for k <= 64 and 64 < n <= 512 (Section 6's score shape, d = 64 over sequences of
+// NT + softmax for k <= 128 and 64 < n <= 512 (Section 6's score shape, d = 64 over sequences of
 // up to 512): each product is formed once and held in registers until its row is done.  The
 // two waves of a pair share 32 output rows; wave q of the pair takes the column blocks 2s + q
 // (s = 0 .. 3), so a step stages 128 rows of B (two 64-column blocks) and each wave holds at
@@ -619,37 +619,43 @@ constexpr int kS1MaxSteps = 4;                                     // n <= 4 * 1
 constexpr int kS1BBufElems = kS1BlockN * kLdk;
 constexpr int kS1BPieces = kS1BlockN * kChunkK / 8 / 64 / kWaves;  // 16-byte pieces per lane
 constexpr int kS1WavesPerSimd = 2;
-constexpr int s1_lds_bytes(bool bf16_out) {
-    return kWaves * wave_lds_bytes(bf16_out) + kDepth * kS1BBufElems * 2 + 2 * kWaves * kTileM * 4;
+// DEEP (64 < k <= 128): the wave's 32 A rows stay in its LDS region for the round (pitch
+// kLdA) and each 128-column step takes two 64-deep chunks of B through the shared buffers.
+constexpr int kLdA = 2 * kChunkK + 8;
+constexpr int s1_wave_bytes(bool bf16_out, bool deep) {
+    return deep && kTileM * kLdA * 2 > wave_lds_bytes(bf16_out) ? kTileM * kLdA * 2 : wave_lds_bytes(bf16_out);
+}
+constexpr int s1_lds_bytes(bool bf16_out, bool deep = false) {
+    return kWaves * s1_wave_bytes(bf16_out, deep) + kDepth * kS1BBufElems * 2 + 2 * kWaves * kTileM * 4;
 }
 constexpr bool single_pass_shape(int n, int k) {
-    return k > 0 && k <= kChunkK && n > kBlockN && n <= kS1MaxSteps * kS1BlockN;
+    return k > 0 && k <= 2 * kChunkK && n > kBlockN && n <= kS1MaxSteps * kS1BlockN;
 }
 
 struct S1Pieces {
     u16x8 b[kS1BPieces];
 };
 
-// The wave's quarter of B's rows [j0, j0 + 128) (the whole reduction, k <= 64), and its LDS
+// The wave's quarter of B's rows [j0, j0 + 128), reduction slice [k0, k0 + 64), and its LDS
 // write (rows past n and columns past k zeroed).
-__device__ __forceinline__ void s1_load(const uint16_t* b_blk, const Shape& s, int j0, int wave,
+__device__ __forceinline__ void s1_load(const uint16_t* b_blk, const Shape& s, int j0, int k0, int wave,
                                         int lane, S1Pieces& p) {
 #pragma unroll
     for (int q = 0; q < kS1BPieces; ++q) {
         const int qg = kS1BPieces * wave + q;
         const int j = j0 + piece_row(lane, qg);
         p.b[q] = load8<true>(b_blk + static_cast<int64_t>(j < s.n ? j : s.n - 1) * s.k,
-                             piece_col(lane, qg), s.k);
+                             k0 + piece_col(lane, qg), s.k);
     }
 }
 
-__device__ __forceinline__ void s1_write(const S1Pieces& p, const Shape& s, int j0, int wave,
+__device__ __forceinline__ void s1_write(const S1Pieces& p, const Shape& s, int j0, int k0, int wave,
                                          int lane, uint16_t* lb) {
 #pragma unroll
     for (int q = 0; q < kS1BPieces; ++q) {
         const int qg = kS1BPieces * wave + q;
         const int r = piece_row(lane, qg), c = piece_col(lane, qg);
-        *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8<true>(p.b[q], c, s.k, j0 + r < s.n);
+        *reinterpret_cast<u16x8*>(lb + r * kLdk + c) = keep8<true>(p.b[q], k0 + c, s.k, j0 + r < s.n);
     }
 }
 
@@ -688,7 +694,7 @@ __device__ __forceinline__ void s1_store_block(const f32x16 (&v)[kBlockTiles], f
 // One round of a wave: output rows [i0, i0 + rows) of batch bidx (rows <= 32; 0 for a wave
 // past the round's end, which still loads its part of B and meets every barrier).  lstat:
 // [2][kWaves][32] floats, the waves' row maxima and sums for their partners.
-template <bool BF16OUT, bool TEMPORAL>
+template <bool BF16OUT, bool TEMPORAL, bool DEEP>
 __device__ __forceinline__ void round_rows_s1(const uint16_t* a, const uint16_t* b, void* c,
                                               const Shape& s, int64_t bidx, int i0, int rows,
                                               int wave, int lane, uint16_t* lw, uint16_t* lbs,
@@ -700,45 +706,73 @@ __device__ __forceinline__ void round_rows_s1(const uint16_t* a, const uint16_t*
     const uint16_t* b_blk = b + bidx * s.b_batch;
     const int nj = (s.n + kBlockN - 1) / kBlockN;  // 2 .. 8
     const int ns = (nj + 1) / 2;                   // steps: 1 .. 4
-    // A's rows and B's first two steps.  Both waves of a pair read the same A rows: ordinary
-    // loads, so that the second finds them in cache.
-    u16x8 pa[kAPieces];
-    load_a<true>(a_blk, s, rows, 0, lane, false, pa);
-    S1Pieces p[kDepth];
-    s1_load(b_blk, s, 0, wave, lane, p[0]);
-    s1_load(b_blk, s, (ns > 1 ? 1 : 0) * kS1BlockN, wave, lane, p[1]);
-    // A once, through the wave's LDS into its MFMA layout
-    u16x8 a_reg[kChunkK / kTileK];
-    write_a<true>(pa, s, rows, 0, lane, lw);
-    wave_lds_sync();
+    // Sub-steps: chunk kc (64 deep) of step st is sub-step NK st + kc (NK = 2 with DEEP).
+    constexpr int NK = DEEP ? 2 : 1;
+    const int nu = NK * ns;
+    auto sub_j0 = [](int u) { return (u / NK) * kS1BlockN; };
+    auto sub_k0 = [](int u) { return (u % NK) * kChunkK; };
+    // A's rows and B's first two sub-steps.  Both waves of a pair read the same A rows:
+    // ordinary loads, so that the second finds them in cache.
+    u16x8 pa[NK][kAPieces];
 #pragma unroll
-    for (int kq = 0; kq < kChunkK / kTileK; ++kq)
-        a_reg[kq] = *reinterpret_cast<const u16x8*>(lw + li * kLdk + kq * kTileK + 8 * h);
+    for (int kc = 0; kc < NK; ++kc) load_a<true>(a_blk, s, rows, kc * kChunkK, lane, false, pa[kc]);
+    S1Pieces p[kDepth];
+    s1_load(b_blk, s, sub_j0(0), sub_k0(0), wave, lane, p[0]);
+    s1_load(b_blk, s, sub_j0(nu > 1 ? 1 : 0), sub_k0(nu > 1 ? 1 : 0), wave, lane, p[1]);
+    // A through the wave's LDS into its MFMA layout: into registers (k <= 64), or kept there
+    // for the round (DEEP, row pitch kLdA)
+    constexpr int LDA = DEEP ? kLdA : kLdk;
+#pragma unroll
+    for (int kc = 0; kc < NK; ++kc) {
+#pragma unroll
+        for (int qq = 0; qq < kAPieces; ++qq) {
+            const int r = piece_row(lane, qq), cc = piece_col(lane, qq);
+            *reinterpret_cast<u16x8*>(lw + r * LDA + kc * kChunkK + cc) =
+                keep8<true>(pa[kc][qq], kc * kChunkK + cc, s.k, r < rows);
+        }
+    }
     wave_lds_sync();
+    u16x8 a_reg[DEEP ? 1 : kChunkK / kTileK];
+    if constexpr (!DEEP) {
+#pragma unroll
+        for (int kq = 0; kq < kChunkK / kTileK; ++kq)
+            a_reg[kq] = *reinterpret_cast<const u16x8*>(lw + li * kLdk + kq * kTileK + 8 * h);
+        wave_lds_sync();
+    }
     f32x16 held[kS1MaxSteps][kBlockTiles];
 #pragma unroll
     for (int st = 0; st < kS1MaxSteps; ++st) {
         if (st >= ns) break;  // wave-uniform
-        uint16_t* const lb = lbs + (st & 1) * kS1BBufElems;
-        // Buffer st % 2 was last read at step st - 2, which every wave finished before the
-        // barrier of step st - 1; the previous round's last reads came before its
-        // row-statistics barriers.
-        s1_write(p[st & 1], s, st * kS1BlockN, wave, lane, lb);
-        __syncthreads();
-        // step st + 2's operands (none past the last step: the registers then take the next
-        // round's first loads)
-        if (st + 2 < ns) s1_load(b_blk, s, (st + 2) * kS1BlockN, wave, lane, p[st & 1]);
 #pragma unroll
-        for (int kk = 0; kk < kChunkK; kk += kTileK) {
-            const bf16x8 av = __builtin_bit_cast(bf16x8, a_reg[kk / kTileK]);
+        for (int kc = 0; kc < NK; ++kc) {
+            const int u = NK * st + kc;
+            uint16_t* const lb = lbs + (u & 1) * kS1BBufElems;
+            // Buffer u % 2 was last read at sub-step u - 2, which every wave finished before the
+            // barrier of sub-step u - 1; the previous round's last reads came before its
+            // row-statistics barriers.
+            s1_write(p[u & 1], s, sub_j0(u), sub_k0(u), wave, lane, lb);
+            __syncthreads();
+            // sub-step u + 2's operands (none past the last)
+            if (u + 2 < nu) s1_load(b_blk, s, sub_j0(u + 2), sub_k0(u + 2), wave, lane, p[u & 1]);
 #pragma unroll
-            for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
-                const bf16x8 bv = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u16x8*>(lb + (q * kBlockN + t * kTileN + li) * kLdk + kk + 8 * h));
-                held[st][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, kk == 0 ? f32x16{} : held[st][t], 0, 0, 0);
+            for (int kk = 0; kk < kChunkK; kk += kTileK) {
+                bf16x8 av;
+                if constexpr (DEEP)
+                    av = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u16x8*>(lw + li * kLdA + kc * kChunkK + kk + 8 * h));
+                else
+                    av = __builtin_bit_cast(bf16x8, a_reg[DEEP ? 0 : kk / kTileK]);
+#pragma unroll
+                for (int t = 0; t < kBlockTiles; ++t) {  // a tile past n multiplies zeros
+                    const bf16x8 bv = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u16x8*>(lb + (q * kBlockN + t * kTileN + li) * kLdk + kk + 8 * h));
+                    held[st][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        bv, av, (kc == 0 && kk == 0) ? f32x16{} : held[st][t], 0, 0, 0);
+                }
             }
         }
     }
+    if constexpr (DEEP) wave_lds_sync();  // the wave's A consumed before its output staging
     // Tile t of step st, lane (li, h): row li, columns 64 (2 st + q) + 32 t + 8 g + 4 h + 0..3
     // (value 4 g + e).  Blocks past n (st >= ns, or wave 1 of a pair past an odd block count)
     // take no part.
@@ -858,14 +892,16 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     constexpr int kLayout = MODE == kModeNn ? kNN : kNT;
     constexpr bool kSoftmax = MODE == kModeNtSoftmax;
     constexpr bool kS1 = MODE == kModeNtSoftmax1;
-    static_assert(!kS1 || (VEC && !AREG), "the single-pass form is one 16-byte instance");
+    static_assert(!kS1 || VEC, "the single-pass form is a 16-byte instance");
+    // AREG in the single-pass instance: the deep form (64 < k <= 128, A kept in LDS)
     constexpr int kRoundRows = kS1 ? kS1Rows : kWaves * kTileM;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int lane = static_cast<int>(threadIdx.x) & 63;
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
-    uint16_t* const lw = lds_base + wave * (wave_lds_bytes(BF16OUT) / 2);
-    uint16_t* const lbs = lds_base + kWaves * (wave_lds_bytes(BF16OUT) / 2);
+    constexpr int kWaveBytes = kS1 ? s1_wave_bytes(BF16OUT, AREG) : wave_lds_bytes(BF16OUT);
+    uint16_t* const lw = lds_base + wave * (kWaveBytes / 2);
+    uint16_t* const lbs = lds_base + kWaves * (kWaveBytes / 2);
     float* const lstat = reinterpret_cast<float*>(lbs + kDepth * kS1BBufElems);  // kS1 only
     const int row0 = kS1 ? (wave >> 1) * kTileM : wave * kTileM;  // the wave's first row of a round
     uint32_t done = 0;
@@ -891,7 +927,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 int mine = seg - row0;
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
                 if constexpr (kS1) {  // k > 0 and alpha != 0 (the host picks this form only then)
-                    round_rows_s1<BF16OUT, TEMPORAL>(a, b, c, s, bidx, i + row0, mine, wave, lane, lw,
+                    round_rows_s1<BF16OUT, TEMPORAL, AREG>(a, b, c, s, bidx, i + row0, mine, wave, lane, lw,
                                                      lbs, lstat);
                 } else {
                     if (s.k == 0)

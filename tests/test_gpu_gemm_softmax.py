@@ -180,11 +180,12 @@ def test_scores_softmax_one_shot():
 @pytest.mark.parametrize("out", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", [(2, 200, 72, 64), (3, 131, 264, 16), (2, 96, 512, 40),
                                    (1, 65, 392, 8), (2, 64, 128, 64), (1, 1, 72, 8), (5, 1, 512, 64),
-                                   (3, 33, 136, 24)],
+                                   (3, 33, 136, 24), (2, 80, 200, 72), (2, 130, 512, 128), (1, 97, 264, 104)],
                          ids=["n72", "n264", "n512k40", "n392k8", "n128", "one_row", "rows_of_one",
-                              "m33"])
+                              "m33", "k72", "k128", "k104"])
 def test_scores_softmax_one_pass_form(shape, out):
-    """Shapes of the one-pass form (k <= 64, 64 < n <= 512, 16-byte rows): an odd number of
+    """Shapes of the one-pass form (k <= 128, 64 < n <= 512, 16-byte rows; past k = 64 the A
+    rows stay in LDS and each step takes two 64-deep chunks of B): an odd number of
     128-column steps (72, 264, 392: the pair's second wave has no block in the last step),
     partial blocks, ragged row rounds, batches of a single row (the second wave pair of every
     workgroup has no rows and still meets every barrier). The two-pass form (forced by three
@@ -214,14 +215,14 @@ def test_scores_softmax_one_pass_form(shape, out):
 
 def test_scores_softmax_one_pass_random_shapes():
     """Seeded random shapes of the one-pass form (64 < n <= 512 in steps of 8, k a multiple of
-    8 up to 64, ragged m, alpha of either sign, both output types) against the oracle, and
+    8 up to 128, ragged m, alpha of either sign, both output types) against the oracle, and
     RR against BALANCED bit for bit."""
     rng = np.random.default_rng(2002)
     for case in range(10):
         batch = int(rng.integers(1, 4))
         m = int(rng.integers(1, 230))
         n = 8 * int(rng.integers(9, 65))
-        k = 8 * int(rng.integers(1, 9))
+        k = 8 * int(rng.integers(1, 17))
         alpha = float(rng.choice([-1.0, 1.0]) * rng.uniform(0.05, 0.5))
         out = "bf16" if case % 2 == 0 else "f32"
         print(f"[nt_softmax one-pass random {case}: {batch} {m} {n} {k} {alpha:.3f} {out}]", flush=True)

@@ -405,10 +405,11 @@ def test_gemm_plans_cover_every_output_row_in_128_row_blocks(schedule, shape):
 
 @pytest.mark.parametrize("layout,n,k,wg_per_cu,one_pass", [
     ("nt_softmax", 512, 64, 0, True), ("nt_softmax", 72, 8, 0, True), ("nt_softmax", 520, 64, 0, False),
-    ("nt_softmax", 64, 64, 0, False), ("nt_softmax", 512, 72, 0, False), ("nt_softmax", 512, 0, 0, False),
+    ("nt_softmax", 64, 64, 0, False), ("nt_softmax", 512, 72, 0, True), ("nt_softmax", 512, 128, 0, True),
+    ("nt_softmax", 512, 136, 0, False), ("nt_softmax", 512, 0, 0, False),
     ("nt_softmax", 512, 64, 3, False), ("nt_softmax", 512, 64, 1, True), ("nt", 512, 64, 0, False)])
 def test_score_softmax_plans_pick_the_one_pass_form(layout, n, k, wg_per_cu, one_pass):
-    """The score product with the row softmax runs in one pass for 0 < k <= 64 and
+    """The score product with the row softmax runs in one pass for 0 < k <= 128 and
     64 < n <= 512 unless the topology asks for three or more workgroups per CU: such plans
     default to two workgroups per CU and cut BALANCED pieces at 64-row blocks (the rows a
     workgroup takes per round); the others default to three per CU and 128-row blocks."""
