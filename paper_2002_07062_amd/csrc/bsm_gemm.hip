@@ -20,6 +20,7 @@ hipError_t launch_g(const void* a, const void* b, void* c, const Shape& s, const
     Shape a_s = s;
     bsm_trace_rec* a_trace = static_cast<bsm_trace_rec*>(trace);
     void* args[] = {&a_a, &a_b, &a_c, &a_s, &worker_ptr, &items, &a_trace};
+    // single-pass instances: the last flag selects the deep form (64 < k <= 128)
     const size_t lds = static_cast<size_t>(MODE == bsm_mm::kModeNtSoftmax1 ? bsm_mm::s1_lds_bytes(BF16OUT, AREG)
                                                                          : bsm_mm::wg_lds_bytes(BF16OUT));
     return hipLaunchKernel(reinterpret_cast<const void*>(&bsm_mm::bsm_gemm_kernel<MODE, BF16OUT, VEC, TEMPORAL, AREG>),

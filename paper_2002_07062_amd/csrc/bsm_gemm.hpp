@@ -893,13 +893,15 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
     constexpr bool kSoftmax = MODE == kModeNtSoftmax;
     constexpr bool kS1 = MODE == kModeNtSoftmax1;
     static_assert(!kS1 || VEC, "the single-pass form is a 16-byte instance");
-    // AREG in the single-pass instance: the deep form (64 < k <= 128, A kept in LDS)
+    // The single-pass instances take their last template flag as the deep form (64 < k <= 128,
+    // A kept in LDS), not as A in registers, which their k <= 64 form always does.
+    constexpr bool kDeep = kS1 && AREG;
     constexpr int kRoundRows = kS1 ? kS1Rows : kWaves * kTileM;
     const int w = blockIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int lane = static_cast<int>(threadIdx.x) & 63;
     const uint64_t t0 = trace ? __builtin_amdgcn_s_memrealtime() : 0;
-    constexpr int kWaveBytes = kS1 ? s1_wave_bytes(BF16OUT, AREG) : wave_lds_bytes(BF16OUT);
+    constexpr int kWaveBytes = kS1 ? s1_wave_bytes(BF16OUT, kDeep) : wave_lds_bytes(BF16OUT);
     uint16_t* const lw = lds_base + wave * (kWaveBytes / 2);
     uint16_t* const lbs = lds_base + kWaves * (kWaveBytes / 2);
     float* const lstat = reinterpret_cast<float*>(lbs + kDepth * kS1BBufElems);  // kS1 only
@@ -927,7 +929,7 @@ __device__ __forceinline__ void gemm_worker(const uint16_t* a, const uint16_t* b
                 int mine = seg - row0;
                 mine = mine < 0 ? 0 : (mine > kTileM ? kTileM : mine);
                 if constexpr (kS1) {  // k > 0 and alpha != 0 (the host picks this form only then)
-                    round_rows_s1<BF16OUT, TEMPORAL, AREG>(a, b, c, s, bidx, i + row0, mine, wave, lane, lw,
+                    round_rows_s1<BF16OUT, TEMPORAL, kDeep>(a, b, c, s, bidx, i + row0, mine, wave, lane, lw,
                                                      lbs, lstat);
                 } else {
                     if (s.k == 0)
